@@ -1,0 +1,20 @@
+"""Oracle: a plain, slow, obviously correct CPU reference of the batched
+dynamic-dataflow-graph forward pass (ED-Batch, arXiv 2302.03851).
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports, calls or
+links this package; only the tests, the smoke check and the CPU-baseline leg
+of the benchmark do.  It shares no code with the HIP path or its host
+library.  It is written in numpy float64 (the paper fixes no precision).
+
+Contents
+  cells     the cell equations of the evaluated models (Section 5.1, Table 2)
+  evaluate  node-at-a-time evaluation in topological order (the unbatched
+            semantics that batching must not change, Section 2.1)
+  schedule  Algorithm 1 (FSM-based dynamic batching) with table / agenda /
+            depth policies, the state encodings of Section 2.3, the lower
+            bound of Appendix A.3, the Eq. 1 frontier ratio and a brute-force
+            optimum (Appendix A.1)
+  plan      the batching-aware memory plan (Section 3.1 constraints; slot
+            assignment by a reverse consumer-first pass) and its hazard check
+  compare   the normwise relative error used by the parity tests
+"""
