@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Benchmark: batched forward pass of 64 binary TreeLSTMs (N-ary, N = 2,
+leaves U[10, 50], E = H = 256, fp32) on one MI355X.
+
+A step is one pass of the whole hot path over one mini-batch: graph ingest,
+batching schedule (Algorithm 1), memory plan, launch preparation and the
+device execution (x staging, then per batch the fused gather -> MFMA cell GEMM
+-> gate epilogue -> scatter kernel).  Inputs (x, packed weights) are resident
+in HBM before the timed region.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--config 2]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "node-cells/sec on 1 MI355X + % of MFMA/HBM roofline, TreeLSTM h=256"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # dense MFMA peaks (fp32, bf16)
+PEAK_HBM_GBS = 8000.0
+
+WORKLOAD_TEXT = {
+    1: "chain LSTM forward fp32: 8 sequences, lengths U[5,20], E=H=64",
+    2: "binary TreeLSTM (N=2) forward fp32: 64 trees, leaves U[10,50], E=H=256",
+    3: "lattice LSTM forward fp32: 32 lattices, lengths U[20,60], word p=0.3 span 2-4, E=100, H=200",
+    4: "2-D grid RNN forward fp32: 32 grids 16x16, E=128, H=256",
+    5: "child-sum TreeLSTM forward bf16 (fp32 accumulate): 256 trees, leaves U[20,200], arity U{1..4}, E=H=512",
+}
+
+
+def algorithmic_work(w, f):
+    """Per batch (flops, bytes) of the work the method must do: 2*K*N flops
+    per node over the present operands (x, present children) and N = gates*H,
+    plus the per-child GEMMs of child-sum forget gates and lattice link
+    gates; bytes = x rows, present children's h and c read, own h and c
+    written (weights are counted once per forward, separately)."""
+    from paper_2302_03851_amd import workloads as WL
+    H, E = w.hidden, w.in_dim
+    esz = 2 if w.dtype == "bf16" else 4
+    G = {WL.LSTM_CHAIN: 4, WL.NARY_LEAF: 3, WL.NARY_INTERNAL: 5, WL.GRID: 5, WL.CS_LEAF: 3,
+         WL.CS_INTERNAL: 3, WL.LAT_CHAR: 4, WL.LAT_WORD: 3}
+    out = []
+    for b in range(f.sched.n_batches):
+        t = int(f.sched.batch_type[b])
+        k = w.kinds[t]
+        nf = w.shapes()[t][0]
+        fl = by = 0
+        for v in f.sched.batch_nodes[f.sched.batch_ptr[b]:f.sched.batch_ptr[b + 1]]:
+            ch = w.children(int(v))
+            fixed = [c for c in ch[:nf] if c >= 0]
+            rag = [c for c in ch[nf:] if c >= 0]
+            hasx = w.x_row[v] >= 0 and WL.KIND_SHAPE[k][2]
+            Kp = (E if hasx else 0) + H * len(fixed)
+            if k == WL.CS_INTERNAL:
+                Kp = H
+                fl += 2 * H * H * len(rag)                 # h_k U_f
+            if k == WL.LAT_CHAR and rag:
+                fl += 2 * E * H + 2 * H * H * len(rag)     # x W_lx, c_w W_lc
+            fl += 2 * Kp * G[k] * H
+            by += (E * esz if hasx else 0) + len(fixed) * H * (esz + 4) + len(rag) * H * (esz + 4)
+            by += H * (esz + 4)
+        out.append((fl, by))
+    return out
+
+
+def weight_bytes(w):
+    esz = 2 if w.dtype == "bf16" else 4
+    return sum(int(np.prod(m.shape)) * (esz if m.ndim == 2 else 4) for d in w.weights for m in d.values())
+
+
+def cpu_baseline(w, budget_s=12.0):
+    """The oracle (numpy float64, node at a time, one BLAS thread) on the same
+    workload: repeated full forwards until the time budget is spent."""
+    from threadpoolctl import threadpool_limits
+    from oracle.evaluate import evaluate
+    reps, t_total = 0, 0.0
+    with threadpool_limits(limits=1):
+        while t_total < budget_s and reps < 20:
+            t0 = time.perf_counter()
+            evaluate(w.kinds, w.op_type, w.child_ptr, w.child_idx, w.x_row, w.x, w.weights, w.hidden,
+                     n_fixed=w.n_children, dtype=w.dtype)
+            t_total += time.perf_counter() - t0
+            reps += 1
+    return {"value": round(w.n_nodes * reps / t_total, 1), "unit": "node-cells/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} full forward passes of the same {w.n_nodes}-node workload, "
+                      f"{t_total:.1f} s, numpy float64 with BLAS limited to 1 thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--replays", type=int, default=200)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); the path shards by "
+              "instance with no exchange, see the design notes", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2302_03851_amd import _lib as L
+    from paper_2302_03851_amd import edb, workloads as WL
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = WL.make_config(args.config)
+    V = w.n_nodes
+
+    # resident inputs: packed weights, x, arena
+    base = edb.Forward(w, flags=L.USE_GRAPH)
+    stream = base.stream.cuda_stream
+    wptrs = [b.data_ptr() for b in base.weights]
+    xp, ahp, acp = base.x.data_ptr(), base.arena_h.data_ptr(), base.arena_c.data_ptr()
+    shapes = edb.operand_shapes(w)
+    table = edb.LATTICE_TABLE if args.config == 3 else None
+    dt = base.dtype
+
+    def step(keep):
+        g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)      # a1
+        s = edb.Schedule(g, L.POLICY_TABLE, L.ENC_SORT, table)                       # a2
+        p = edb.Plan(g, s, shapes, L.PLAN_RC)                                          # a3
+        ex = edb.Exec(g, s, p, base.cells, 0)                                          # descriptors
+        ex.execute(wptrs, xp, ahp, acp, stream)                                        # a4..a8
+        keep.append(ex)
+
+    keep = []
+    for _ in range(args.warmup):
+        step(keep)
+    torch.cuda.synchronize()
+    keep.clear()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(keep)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    keep.clear()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    # device-only rate: the captured HIP graph of the same batch sequence replayed
+    for _ in range(10):
+        base.run()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.replays):
+        base.run()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_replay = ev0.elapsed_time(ev1) / args.replays
+
+    # host part of a step (a1-a3 + descriptor upload), measured alone
+    th = time.perf_counter()
+    nh = 20
+    for _ in range(nh):
+        g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+        s = edb.Schedule(g, L.POLICY_TABLE, L.ENC_SORT, table)
+        p = edb.Plan(g, s, shapes, L.PLAN_RC)
+        ex = edb.Exec(g, s, p, base.cells, 0)
+    ms_host = (time.perf_counter() - th) * 1e3 / nh
+
+    # per-launch durations with HIP events on the execution stream
+    prof = edb.Exec(base.graph, base.sched, base.plan, base.cells, L.PROFILE)
+    reps = 20
+    times = np.zeros(prof.launches())
+    for _ in range(reps):
+        prof.execute(wptrs, xp, ahp, acp, stream)
+        times += prof.launch_times()
+    times /= reps
+    work = algorithmic_work(w, base)
+    infos = [prof.launch_info(i) for i in range(prof.launches())]
+    groups = {}
+    for i, inf in enumerate(infos[1:], start=1):
+        key = (inf["kind"], inf["variant"])
+        gsum = groups.setdefault(key, [0.0, 0, 0, 0])
+        gsum[0] += times[i]
+        gsum[1] += 1
+        gsum[2] += work[inf["batch"]][0]
+        gsum[3] += work[inf["batch"]][1]
+    dom = max(groups, key=lambda k: groups[k][0])
+    tot_ms, nl, fl, by = groups[dom]
+    avg_ms = tot_ms / nl
+    tflops = (fl / nl) / (avg_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+    kname = {0: "LSTM_CHAIN", 1: "NARY_LEAF", 2: "NARY_INTERNAL", 3: "GRID", 4: "CS_LEAF",
+             5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD"}[dom[0]]
+    tot_flops = sum(x[0] for x in work)
+    tot_bytes = sum(x[1] for x in work) + weight_bytes(w)
+
+    result = {
+        "metric": METRIC,
+        "value": round(V / (ms_step * 1e-3), 1),
+        "unit": "node-cells/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.config], "nodes": V, "batches": base.sched.n_batches,
+                   "launches_per_step": base.exec.launches(),
+                   "step": "graph ingest + schedule + memory plan + launch prep + device execution"},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(tflops / peak, 4), "traffic": None,
+                     "kernel": f"cell_kernel<{kname}, {w.dtype}, variant {dom[1]}>",
+                     "launches": nl, "avg_launch_us": round(avg_ms * 1e3, 2),
+                     "alg_flops_per_launch": int(fl / nl)},
+        "device_replay": {"ms_per_forward": round(ms_replay, 4),
+                          "node_cells_per_s": round(V / (ms_replay * 1e-3), 1),
+                          "alg_tflops": round(tot_flops / (ms_replay * 1e-3) / 1e12, 3),
+                          "alg_hbm_gbs": round(tot_bytes / (ms_replay * 1e-3) / 1e9, 1)},
+        "host_ms_per_graph": round(ms_host, 4),
+        "launch_us": [round(t * 1e3, 2) for t in times],
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,277 @@
+/*
+ * edb.h -- C ABI of the batched dynamic-dataflow-graph executor for AMD
+ * MI355X (gfx950).
+ *
+ * The library executes the forward pass of a mini-batch of per-instance
+ * dataflow graphs (chain LSTM, N-ary and child-sum TreeLSTM, lattice LSTM,
+ * 2-D grid RNN) the way ED-Batch (arXiv 2302.03851) batches them:
+ *
+ *   edb_build_graph   typed graph ingest (Section 2.1: every operation has a
+ *                     type; the mini-batch is the union of instance graphs)
+ *   edb_schedule      Algorithm 1: repeatedly pick a type through a policy
+ *                     table keyed by the frontier's state encoding
+ *                     (Sections 2.2-2.3) and batch every ready node of it
+ *   edb_plan_memory   batching-aware arena layout (Section 3.1: source and
+ *                     result operands of a batch contiguous and aligned)
+ *   edb_pack_weights  gate-interleaved weight layout for the fused cell kernels
+ *   edb_prepare /     per batch one fused kernel on the GPU: operand gather ->
+ *   edb_execute       cell GEMM on the matrix cores -> gate epilogue ->
+ *                     scatter into the planned slots, the whole batch
+ *                     sequence replayed from one HIP graph
+ *
+ * Conventions
+ *   - Every call returns an edb_status.  On failure no output handle is
+ *     created (*out is set to NULL) and edb_last_error() describes the error.
+ *     No C++ exception crosses this interface.
+ *   - Pointers documented as "host" are read during the call only; the
+ *     library deep-copies what it keeps.  Pointers documented as "device"
+ *     are caller-owned GPU memory the library never frees.
+ *   - Handles are immutable after creation (except edb_exec_t, which caches
+ *     its HIP graph) and may be read from several threads at once.
+ */
+#ifndef EDB_H
+#define EDB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status ------------------------------------------------------------ */
+typedef int32_t edb_status;
+#define EDB_OK               0
+#define EDB_ERR_INVALID     -1  /* bad argument: NULL, out of range, size mismatch */
+#define EDB_ERR_CYCLE       -2  /* the graph is not a DAG */
+#define EDB_ERR_OOM         -3  /* host or device allocation failed */
+#define EDB_ERR_UNSUPPORTED -4  /* shape or cell configuration the kernels do not handle */
+#define EDB_ERR_TABLE       -5  /* malformed policy table */
+#define EDB_ERR_HIP         -6  /* a HIP runtime call failed (message holds the HIP error) */
+
+/* Text of the last error on the calling thread; valid until the next call
+ * into the library on that thread.  Never NULL. */
+const char* edb_last_error(void);
+/* Library version, major * 10000 + minor * 100 + patch. */
+int32_t edb_version(void);
+
+/* ---- graph (Section 2.1) ------------------------------------------------ */
+typedef struct edb_graph edb_graph_t;
+
+/* Typed dataflow graph in CSR form.
+ *   n_nodes, n_types   V >= 0 nodes with types in [0, n_types), n_types >= 1
+ *   op_type   host int32[V]      type of every node
+ *   child_ptr host int64[V+1]    CSR offsets, child_ptr[0] == 0, non-decreasing
+ *   child_idx host int32[E]      children of v: child_idx[child_ptr[v] .. child_ptr[v+1]);
+ *                                positional children first, then ragged ones;
+ *                                -1 = absent child (reads a zero state)
+ *   x_row     host int32[V]      row of the caller's input matrix x holding v's
+ *                                input vector, or -1 when v has none
+ * Errors: EDB_ERR_INVALID for NULL arrays, ids out of range, a non-monotone
+ * child_ptr or a self edge; EDB_ERR_CYCLE when the present edges contain a
+ * cycle (checked with Kahn's algorithm). */
+edb_status edb_build_graph(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
+                           const int64_t* child_ptr, const int32_t* child_idx,
+                           const int32_t* x_row, edb_graph_t** out);
+void edb_graph_free(edb_graph_t* g);
+edb_status edb_graph_info(const edb_graph_t* g, int32_t* n_nodes, int32_t* n_types,
+                          int64_t* n_edges);
+
+/* ---- schedule (Algorithm 1, Sections 2.2-2.3) --------------------------- */
+#define EDB_POLICY_TABLE  0  /* FSM policy table keyed by the state encoding */
+#define EDB_POLICY_AGENDA 1  /* type of minimal mean topological depth (DyNet agenda) */
+#define EDB_POLICY_DEPTH  2  /* groups of equal (depth, type) (TensorFlow Fold) */
+
+#define EDB_ENC_SORT 0  /* frontier types sorted by frontier count desc, ties by id */
+#define EDB_ENC_BASE 1  /* set of frontier types, ascending id */
+#define EDB_ENC_MAX  2  /* E_base followed by the most common frontier type */
+
+/* Batching policy.  `table` (host, may be NULL when table_len == 0) is a flat
+ * int32 list [n_entries, {key_len, key[0..key_len), action} x n_entries]:
+ * the state key (type ids in the encoding's order) maps to the next type.
+ * A key that is missing, or an action that is not on the frontier, falls
+ * back to the most common frontier type (ties to the lowest id).  Keys that
+ * name types outside [0, n_types) never match.  A later entry with the same
+ * key replaces an earlier one. */
+typedef struct {
+    int32_t kind;          /* EDB_POLICY_* */
+    int32_t encoding;      /* EDB_ENC_* (table policy only) */
+    const int32_t* table;  /* host */
+    int64_t table_len;
+} edb_policy;
+
+typedef struct edb_schedule edb_schedule_t;
+
+/* Runs the batching loop on the host.  Every batch holds all ready nodes of
+ * the chosen type in ascending node id (Algorithm 1's frontier batch).
+ * Errors: EDB_ERR_INVALID (NULL, unknown kind/encoding), EDB_ERR_TABLE. */
+edb_status edb_schedule(const edb_graph_t* g, const edb_policy* policy, edb_schedule_t** out);
+/* Borrowed views, valid until edb_schedule_free:
+ *   batch_ptr int32[n_batches+1], batch_nodes int32[V], batch_type int32[n_batches]. */
+edb_status edb_schedule_view(const edb_schedule_t* s, int32_t* n_batches,
+                             const int32_t** batch_ptr, const int32_t** batch_nodes,
+                             const int32_t** batch_type);
+void edb_schedule_free(edb_schedule_t* s);
+
+/* ---- memory plan (Section 3.1) ------------------------------------------ */
+/* Operand shape of a type: exactly n_fixed positional children (-1 allowed),
+ * then ragged children only when `ragged` is non-zero; has_x != 0 when the
+ * type's cell reads an input row (then every node of it needs x_row >= 0). */
+typedef struct {
+    int32_t n_fixed;
+    int32_t ragged;
+    int32_t has_x;
+} edb_operand_shape;
+
+#define EDB_PLAN_RC       0  /* reverse consumer-first contiguous slot plan */
+#define EDB_PLAN_IDENTITY 1  /* slot[v] = v + 1, every operand indexed (ablation) */
+
+#define EDB_SEG_NONE    0  /* operand absent in every row: nothing to load */
+#define EDB_SEG_CONTIG  1  /* rows base, base+1, ... */
+#define EDB_SEG_GATHER  2  /* source rows listed in the index pool */
+#define EDB_SEG_SCATTER 3  /* result rows listed in the index pool */
+
+/* One operand list of a batch.  Rows are slot numbers of the node-state
+ * arena (slot 0 is the all-zero row; pad slots are zero and never written). */
+typedef struct {
+    int32_t kind;     /* EDB_SEG_* */
+    int32_t base;     /* CONTIG: first slot */
+    int64_t idx_off;  /* GATHER/SCATTER: offset of the slot list in idx_pool */
+    int32_t len;      /* number of entries (rows) */
+    int32_t reserved;
+} edb_seg;
+
+typedef struct edb_plan edb_plan_t;
+
+/* Plan the arena.  shapes: host [n_types].  Segment layout per batch b:
+ * segs[seg_ptr[b]] is the result list (CONTIG or SCATTER), followed by one
+ * source list per positional child, followed by the ragged list when the
+ * type is ragged.  Ragged lists hold only present children; ragged_ptr gives
+ * each row's entries.
+ * Errors: EDB_ERR_INVALID (NULL, flags, a node of a has_x type without x),
+ * EDB_ERR_UNSUPPORTED (a node's child count does not fit its type's shape). */
+edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t* s,
+                           const edb_operand_shape* shapes, int32_t flags, edb_plan_t** out);
+
+typedef struct {
+    int32_t n_nodes, n_batches, n_slots, n_pads;
+    const int32_t* slot;        /* [V] arena row of each node */
+    const int32_t* order;       /* [V] rows of batch b: order[batch_ptr[b] .. batch_ptr[b+1]) */
+    const int32_t* x_slot;      /* [V] row of the node's input in the staged x buffer, -1 if none */
+    const int32_t* seg_ptr;     /* [n_batches+1] */
+    const edb_seg* segs;        /* [seg_ptr[n_batches]] */
+    const int32_t* idx_pool;    /* [idx_len] */
+    int64_t idx_len;
+    const int64_t* ragged_off;  /* [n_batches] offset of the batch's m+1 row offsets in ragged_pool, -1 if none */
+    const int32_t* ragged_pool;
+    int64_t ragged_len;
+    const int32_t* pads;        /* [n_pads] pad slots */
+} edb_plan_view_t;
+
+/* Borrowed view, valid until edb_plan_free. */
+edb_status edb_plan_view(const edb_plan_t* p, edb_plan_view_t* view);
+void edb_plan_free(edb_plan_t* p);
+
+/* ---- cells and weights ---------------------------------------------------- */
+#define EDB_CELL_LSTM_CHAIN    0  /* children [prev];            gates [i,f,g,o]          */
+#define EDB_CELL_NARY_LEAF     1  /* no children, x;             gates [i,o,u]            */
+#define EDB_CELL_NARY_INTERNAL 2  /* children [h_0, h_1], no x;  gates [i,f_0,f_1,o,u]    */
+#define EDB_CELL_GRID          3  /* children [left, top], x;    gates [i,f_l,f_t,o,u]    */
+#define EDB_CELL_CS_LEAF       4  /* no children, x;             gates [i,o,u]            */
+#define EDB_CELL_CS_INTERNAL   5  /* ragged children, no x;      [i,o,u] on sum h, f per child */
+#define EDB_CELL_LAT_CHAR      6  /* [prev char] + ragged words; gates [i,f,o,u] + link gates */
+#define EDB_CELL_LAT_WORD      7  /* [first char], x;            gates [i,f,u], no h output */
+
+#define EDB_F32  0  /* W, x, h fp32 */
+#define EDB_BF16 1  /* W, x, h bf16 (round to nearest even); c fp32; fp32 accumulation */
+
+typedef struct {
+    int32_t kind;        /* EDB_CELL_* */
+    int32_t in_dim;      /* E (ignored by kinds without x) */
+    int32_t hidden;      /* H, equal for every type of a graph */
+    int32_t n_children;  /* N of NARY_INTERNAL (only 2 is supported); 0 otherwise */
+    int32_t dtype;       /* EDB_F32 or EDB_BF16 */
+} edb_cell;
+
+/* Bytes of the packed weight buffer of one cell type. */
+edb_status edb_packed_weight_bytes(const edb_cell* cell, int64_t* bytes);
+
+/* Pack the logical weights of one cell type into the gate-interleaved,
+ * zero-padded device layout the kernels read.  `logical` is a host array of
+ * float32 row-major matrices in this order (K x N, rows [x ; child h ...],
+ * columns gate-major in the kind's gate order):
+ *   LSTM_CHAIN     W[(E+H) x 4H], b[4H]
+ *   NARY_LEAF      W[E x 3H], b[3H]          (CS_LEAF alike)
+ *   NARY_INTERNAL  U[2H x 5H], b[5H]
+ *   GRID           W[(E+2H) x 5H], b[5H]
+ *   CS_INTERNAL    U_iou[H x 3H], U_f[H x H], b_iou[3H], b_f[H]
+ *   LAT_WORD       W[(E+H) x 3H], b[3H]
+ *   LAT_CHAR       W[(E+H) x 4H], W_lx[E x H], W_lc[H x H], b[4H], b_l[H]
+ * bf16 cells round the matrices to bf16 (ties to even); biases stay fp32.
+ * packed_dev: device buffer of edb_packed_weight_bytes bytes (caller-owned).
+ * The copy is enqueued on `stream` (hipStream_t, NULL = default stream) and
+ * has completed when the call returns. */
+edb_status edb_pack_weights(const edb_cell* cell, const float* const* logical,
+                            void* packed_dev, void* stream);
+
+/* ---- execution ------------------------------------------------------------ */
+#define EDB_USE_GRAPH    1  /* capture the batch sequence once, replay it per call */
+#define EDB_DRYRUN       2  /* record the launch list only; no HIP call (CPU testing) */
+#define EDB_FORCE_GATHER 4  /* treat every CONTIG operand as indexed (ablation) */
+#define EDB_X_DIRECT     8  /* read x rows in place by x_row instead of staging them */
+#define EDB_PROFILE     16  /* eager launches, each bracketed by HIP events (edb_exec_launch_times) */
+
+typedef struct edb_exec edb_exec_t;
+
+/* Bind a graph, schedule and plan to cell kernels.  cells: host [n_types].
+ * Uploads the batch descriptors and index lists to the current HIP device
+ * and allocates the staged-x buffer; both are owned by the handle.
+ * Errors: EDB_ERR_INVALID, EDB_ERR_UNSUPPORTED (dimension or kind mix the
+ * kernels do not handle), EDB_ERR_OOM, EDB_ERR_HIP. */
+edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
+                       const edb_cell* cells, int32_t flags, edb_exec_t** out);
+
+/* Run one forward pass, asynchronously on `stream` (hipStream_t).
+ *   packed_weights host array [n_types] of device pointers (edb_pack_weights output)
+ *   x        device [n_x_rows x in_dim] of the cells' dtype, rows addressed by x_row
+ *   arena_h  device [n_slots x H] of the cells' dtype; node v's h is row slot[v]
+ *   arena_c  device [n_slots x H] fp32;               node v's c is row slot[v]
+ * The call zeroes the arena's zero row and pad rows, stages x (unless
+ * EDB_X_DIRECT), then runs every batch in schedule order.  With
+ * EDB_USE_GRAPH the sequence is captured into a HIP graph on the first call
+ * and whenever a pointer differs from the captured ones, and replayed with a
+ * single graph launch otherwise.  Kernel faults surface at the caller's next
+ * synchronisation.  One edb_exec_t must not run on two streams at once. */
+edb_status edb_execute(edb_exec_t* e, const void* const* packed_weights, const void* x,
+                       void* arena_h, void* arena_c, void* stream);
+
+/* Number of kernel launches one edb_execute issues (launches per graph). */
+edb_status edb_exec_launches(const edb_exec_t* e, int32_t* n_kernels);
+
+/* Description of launch i (for tests and profiling). */
+typedef struct {
+    int32_t batch;     /* batch index, -1 for the staging / zero-fill kernel */
+    int32_t kind;      /* EDB_CELL_* of the batch, -1 for staging */
+    int32_t m;         /* rows */
+    int32_t k;         /* padded reduction length of the main GEMM */
+    int32_t n;         /* padded output columns (gates x padded hidden) */
+    int32_t variant;   /* tile variant id */
+    int32_t grid;      /* work-groups */
+    int32_t block;     /* threads per work-group */
+    int32_t seg_kind[4]; /* kinds of result, child 0, child 1, ragged lists */
+} edb_launch_info;
+edb_status edb_exec_launch_info(const edb_exec_t* e, int32_t i, edb_launch_info* info);
+
+/* Per-launch GPU durations of the last edb_execute of an EDB_PROFILE handle,
+ * in milliseconds, measured with HIP events recorded on the execution stream
+ * between consecutive launches.  ms: host float[n], n = edb_exec_launches.
+ * Waits for that execution to finish.  EDB_ERR_INVALID without EDB_PROFILE
+ * or before the first execute. */
+edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
+
+void edb_exec_free(edb_exec_t* e);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EDB_H */

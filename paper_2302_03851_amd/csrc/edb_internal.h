@@ -1,0 +1,40 @@
+// Internal structures shared by the host-side parts of the library.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "edb.h"
+
+struct edb_graph {
+    int32_t V = 0, T = 0;
+    std::vector<int32_t> op_type;
+    std::vector<int64_t> child_ptr;
+    std::vector<int32_t> child_idx;
+    std::vector<int32_t> x_row;
+};
+
+struct edb_schedule {
+    int32_t V = 0, T = 0;
+    std::vector<int32_t> batch_ptr;    // [B+1]
+    std::vector<int32_t> batch_nodes;  // [V]
+    std::vector<int32_t> batch_type;   // [B]
+};
+
+struct edb_plan {
+    int32_t V = 0, B = 0, n_slots = 0;
+    std::vector<int32_t> slot, order, x_slot, seg_ptr, idx_pool, ragged_pool, pads;
+    std::vector<int64_t> ragged_off;
+    std::vector<edb_seg> segs;
+    std::vector<edb_operand_shape> shapes;
+    int32_t mode = EDB_PLAN_RC;
+};
+
+namespace edb {
+
+// Thread-local last-error message; returns the status for `return fail(...)`.
+edb_status fail(edb_status st, const std::string& msg);
+void clear_error();
+
+}  // namespace edb

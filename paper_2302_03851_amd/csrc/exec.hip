@@ -1,0 +1,615 @@
+// Device executor: weight packing, per-batch launch records, HIP graph
+// capture and replay of the whole batch sequence.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <functional>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "cell_kernels.h"
+#include "edb_internal.h"
+
+using edb::fail;
+using namespace edbk;
+
+namespace {
+
+constexpr int NUM_VARIANTS = 4;
+// tile variants (rows per work-group = 16*RT, units per work-group = 16*WU)
+constexpr int VAR_RT[NUM_VARIANTS] = {2, 1, 1, 1};
+constexpr int VAR_WU[NUM_VARIANTS] = {4, 4, 2, 1};
+
+struct KindInfo {
+    int G, nfix;
+    bool x, rag;
+};
+
+KindInfo kind_info(int kind) {
+    switch (kind) {
+        case EDB_CELL_LSTM_CHAIN: return {4, 1, true, false};
+        case EDB_CELL_NARY_LEAF: return {3, 0, true, false};
+        case EDB_CELL_NARY_INTERNAL: return {5, 2, false, false};
+        case EDB_CELL_GRID: return {5, 2, true, false};
+        case EDB_CELL_CS_LEAF: return {3, 0, true, false};
+        case EDB_CELL_CS_INTERNAL: return {3, 0, false, true};
+        case EDB_CELL_LAT_CHAR: return {5, 1, true, true};
+        case EDB_CELL_LAT_WORD: return {3, 1, true, false};
+        default: return {0, 0, false, false};
+    }
+}
+
+int round_up(int v, int m) { return (v + m - 1) / m * m; }
+
+// Derived dimensions of a cell type's packed layout.
+struct Dims {
+    int G, KG, esz, E, Ep, H, Hk, Hu, K;
+    bool x, rag;
+    int64_t off_W, off_b, off_Wr, off_br, bytes;
+};
+
+edb_status cell_dims(const edb_cell* c, Dims& d) {
+    if (!c) return fail(EDB_ERR_INVALID, "cell is NULL");
+    KindInfo ki = kind_info(c->kind);
+    if (ki.G == 0) return fail(EDB_ERR_INVALID, "unknown cell kind " + std::to_string(c->kind));
+    if (c->dtype != EDB_F32 && c->dtype != EDB_BF16) return fail(EDB_ERR_INVALID, "unknown cell dtype");
+    if (c->hidden <= 0) return fail(EDB_ERR_INVALID, "hidden must be positive");
+    if (ki.x && c->in_dim <= 0) return fail(EDB_ERR_INVALID, "in_dim must be positive for this cell kind");
+    if (c->kind == EDB_CELL_NARY_INTERNAL && c->n_children != 2)
+        return fail(EDB_ERR_UNSUPPORTED, "NARY_INTERNAL supports n_children == 2 only");
+    d.G = ki.G;
+    d.x = ki.x;
+    d.rag = ki.rag;
+    d.KG = c->dtype == EDB_F32 ? 16 : 32;
+    d.esz = c->dtype == EDB_F32 ? 4 : 2;
+    const int vec = 16 / d.esz;
+    d.H = c->hidden;
+    d.E = ki.x ? c->in_dim : 0;
+    if (d.H % vec != 0 || d.E % vec != 0)
+        return fail(EDB_ERR_UNSUPPORTED, "hidden and in_dim must be multiples of " + std::to_string(vec) +
+                                             " (16-byte rows)");
+    if (d.H > 4096 || d.E > 4096) return fail(EDB_ERR_UNSUPPORTED, "hidden / in_dim above 4096");
+    d.Hk = round_up(d.H, d.KG);
+    d.Ep = ki.x ? round_up(d.E, d.KG) : 0;
+    d.Hu = round_up(d.H, 64);
+    if (c->kind == EDB_CELL_CS_INTERNAL) d.K = d.Hk;
+    else d.K = d.Ep + ki.nfix * d.Hk;
+    const int64_t wmain = (int64_t)(d.Hu / 16) * d.G * (d.K / d.KG) * 64 * 16;
+    const int64_t bmain = (int64_t)d.G * d.Hu * 4;
+    const int64_t wr = ki.rag ? (int64_t)(d.Hu / 16) * (d.Hk / d.KG) * 64 * 16 : 0;
+    const int64_t brr = ki.rag ? (int64_t)d.Hu * 4 : 0;
+    auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
+    d.off_W = 0;
+    d.off_b = al(wmain);
+    d.off_Wr = d.off_b + al(bmain);
+    d.off_br = d.off_Wr + al(wr);
+    d.bytes = d.off_br + al(brr);
+    return EDB_OK;
+}
+
+uint16_t bf16_rne(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// Logical row of main-GEMM K position k (padded layout), or -1 for padding.
+int main_row(int kind, const Dims& d, int k) {
+    int seg_start = 0, logical_start = 0;
+    if (d.x) {
+        if (k < d.Ep) return k < d.E ? k : -1;
+        seg_start = d.Ep;
+        logical_start = d.E;
+    }
+    const int s = (k - seg_start) / d.Hk, o = (k - seg_start) % d.Hk;
+    (void)kind;
+    return o < d.H ? logical_start + s * d.H + o : -1;
+}
+
+// Pack one GEMM operand [K x (G x H)] into the lane layout of cell_kernels.h.
+void pack_gemm(std::vector<uint8_t>& out, int64_t off, const Dims& d, int G, int K,
+               const std::function<float(int k, int g, int j)>& val) {
+    const int nkg = K / d.KG, per = d.KG / 4;
+    for (int ub = 0; ub < d.Hu / 16; ++ub)
+        for (int g = 0; g < G; ++g)
+            for (int kg = 0; kg < nkg; ++kg)
+                for (int l = 0; l < 64; ++l)
+                    for (int i = 0; i < per; ++i) {
+                        const int k = kg * d.KG + (l / 16) * per + i;
+                        const int j = ub * 16 + (l % 16);
+                        const float v = j < d.H ? val(k, g, j) : 0.f;
+                        const int64_t e = ((((int64_t)ub * G + g) * nkg + kg) * 64 + l) * per + i;
+                        if (d.esz == 4) std::memcpy(out.data() + off + e * 4, &v, 4);
+                        else {
+                            uint16_t b = bf16_rne(v);
+                            std::memcpy(out.data() + off + e * 2, &b, 2);
+                        }
+                    }
+}
+
+}  // namespace
+
+extern "C" edb_status edb_packed_weight_bytes(const edb_cell* cell, int64_t* bytes) {
+    if (!bytes) return fail(EDB_ERR_INVALID, "edb_packed_weight_bytes: bytes is NULL");
+    Dims d;
+    edb_status st = cell_dims(cell, d);
+    if (st != EDB_OK) return st;
+    *bytes = d.bytes;
+    return EDB_OK;
+}
+
+extern "C" edb_status edb_pack_weights(const edb_cell* cell, const float* const* lg, void* packed_dev,
+                                       void* stream) {
+    Dims d;
+    edb_status st = cell_dims(cell, d);
+    if (st != EDB_OK) return st;
+    if (!lg || !packed_dev) return fail(EDB_ERR_INVALID, "edb_pack_weights: NULL argument");
+    const int nmat = cell->kind == EDB_CELL_CS_INTERNAL ? 4 : cell->kind == EDB_CELL_LAT_CHAR ? 5 : 2;
+    for (int i = 0; i < nmat; ++i)
+        if (!lg[i]) return fail(EDB_ERR_INVALID, "edb_pack_weights: NULL logical matrix");
+    std::vector<uint8_t> buf;
+    try {
+        buf.assign((size_t)d.bytes, 0);
+    } catch (const std::bad_alloc&) {
+        return fail(EDB_ERR_OOM, "edb_pack_weights: out of host memory");
+    }
+    const int kind = cell->kind, H = d.H, G = d.G;
+    const float *W = lg[0], *b = nullptr, *Wr = nullptr, *br = nullptr, *Wlx = nullptr;
+    int ncol = 0;  // logical columns of W
+    switch (kind) {
+        case EDB_CELL_CS_INTERNAL: ncol = 3 * H; Wr = lg[1]; b = lg[2]; br = lg[3]; break;
+        case EDB_CELL_LAT_CHAR: ncol = 4 * H; Wlx = lg[1]; Wr = lg[2]; b = lg[3]; br = lg[4]; break;
+        default: ncol = G * H; b = lg[1]; break;
+    }
+    pack_gemm(buf, d.off_W, d, G, d.K, [&](int k, int g, int j) -> float {
+        const int row = main_row(kind, d, k);
+        if (row < 0) return 0.f;
+        if (kind == EDB_CELL_LAT_CHAR && g == 4) return row < d.E ? Wlx[(int64_t)row * H + j] : 0.f;
+        return W[(int64_t)row * ncol + g * H + j];
+    });
+    float* bias = reinterpret_cast<float*>(buf.data() + d.off_b);
+    for (int g = 0; g < G; ++g)
+        for (int j = 0; j < H; ++j)
+            bias[g * d.Hu + j] = (kind == EDB_CELL_LAT_CHAR && g == 4) ? 0.f : b[g * H + j];
+    if (d.rag) {
+        pack_gemm(buf, d.off_Wr, d, 1, d.Hk, [&](int k, int, int j) -> float {
+            return k < H ? Wr[(int64_t)k * H + j] : 0.f;
+        });
+        float* brp = reinterpret_cast<float*>(buf.data() + d.off_br);
+        for (int j = 0; j < H; ++j) brp[j] = br[j];
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(packed_dev, buf.data(), (size_t)d.bytes, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_pack_weights: ") + hipGetErrorString(e));
+    return EDB_OK;
+}
+
+// ---------------------------------------------------------------------------
+// kernel dispatch
+
+namespace {
+
+using LaunchFn = void (*)(const BatchArgs&, int grid, int lds, hipStream_t);
+using AttrFn = hipError_t (*)(int lds);
+
+template <int KIND, typename T, int RT, int WU>
+void launch_cell(const BatchArgs& a, int grid, int lds, hipStream_t st) {
+    hipLaunchKernelGGL((cell_kernel<KIND, T, RT, WU>), dim3(grid), dim3(256), lds, st, a);
+}
+template <int KIND, typename T, int RT, int WU>
+hipError_t attr_cell(int lds) {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&cell_kernel<KIND, T, RT, WU>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+}
+template <int KIND, typename T, int RT, int WU>
+int lds_cell(int K) { return lds_bytes<KIND, T, RT, WU>(K); }
+
+struct Entry {
+    LaunchFn launch;
+    AttrFn attr;
+    int (*lds)(int);
+};
+
+template <int KIND, typename T>
+void fill_kind(Entry* e) {
+    e[0] = {launch_cell<KIND, T, 2, 4>, attr_cell<KIND, T, 2, 4>, lds_cell<KIND, T, 2, 4>};
+    e[1] = {launch_cell<KIND, T, 1, 4>, attr_cell<KIND, T, 1, 4>, lds_cell<KIND, T, 1, 4>};
+    e[2] = {launch_cell<KIND, T, 1, 2>, attr_cell<KIND, T, 1, 2>, lds_cell<KIND, T, 1, 2>};
+    e[3] = {launch_cell<KIND, T, 1, 1>, attr_cell<KIND, T, 1, 1>, lds_cell<KIND, T, 1, 1>};
+}
+
+struct Table {
+    Entry e[8][2][NUM_VARIANTS];
+    Table() {
+        fill_kind<K_CHAIN, float>(e[0][0]);        fill_kind<K_CHAIN, __bf16>(e[0][1]);
+        fill_kind<K_NARY_LEAF, float>(e[1][0]);    fill_kind<K_NARY_LEAF, __bf16>(e[1][1]);
+        fill_kind<K_NARY_INT, float>(e[2][0]);     fill_kind<K_NARY_INT, __bf16>(e[2][1]);
+        fill_kind<K_GRID, float>(e[3][0]);         fill_kind<K_GRID, __bf16>(e[3][1]);
+        fill_kind<K_CS_LEAF, float>(e[4][0]);      fill_kind<K_CS_LEAF, __bf16>(e[4][1]);
+        fill_kind<K_CS_INT, float>(e[5][0]);       fill_kind<K_CS_INT, __bf16>(e[5][1]);
+        fill_kind<K_LAT_CHAR, float>(e[6][0]);     fill_kind<K_LAT_CHAR, __bf16>(e[6][1]);
+        fill_kind<K_LAT_WORD, float>(e[7][0]);     fill_kind<K_LAT_WORD, __bf16>(e[7][1]);
+    }
+};
+
+const Table& table() {
+    static Table t;
+    return t;
+}
+
+// One kernel launch of the forward pass.
+struct Launch {
+    edb_launch_info info;
+    int type;      // cell type (batches)
+    BatchArgs args;  // pointer fields to data buffers are filled at execute time
+    // offsets into the device int buffer (-1 = none)
+    int64_t off_x, off_f0, off_f1, off_rag, off_rptr, off_res;
+    int x_base;
+    int lds;
+};
+
+}  // namespace
+
+struct edb_exec {
+    int32_t flags = 0;
+    int32_t T = 0, B = 0, dtype = 0;
+    int32_t n_slots = 0, n_x = 0, E = 0, H = 0;
+    std::vector<Dims> dims;
+    std::vector<edb_cell> cells;
+    std::vector<Launch> launches;     // [0] = staging, then one per batch
+    int32_t n_zero = 0;
+    int64_t off_xsrc = 0, off_zero = 0;
+    std::vector<int32_t> hbuf;        // host copy of the device int buffer
+    int* dbuf = nullptr;
+    void* xstaged = nullptr;
+    hipStream_t cap_stream = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t gexec = nullptr;
+    std::vector<const void*> cap_ptrs;  // pointers the captured graph was built with
+    std::vector<hipEvent_t> events;     // EDB_PROFILE: launches + 1 events
+    bool profiled = false;
+    int device = -1;
+
+    ~edb_exec() {
+        for (hipEvent_t ev : events) (void)hipEventDestroy(ev);
+        if (gexec) (void)hipGraphExecDestroy(gexec);
+        if (graph) (void)hipGraphDestroy(graph);
+        if (cap_stream) (void)hipStreamDestroy(cap_stream);
+        if (dbuf) (void)hipFree(dbuf);
+        if (xstaged) (void)hipFree(xstaged);
+    }
+};
+
+extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
+                                  const edb_cell* cells, int32_t flags, edb_exec_t** out) {
+    if (!out) return fail(EDB_ERR_INVALID, "edb_prepare: out is NULL");
+    *out = nullptr;
+    if (!g || !s || !p || !cells) return fail(EDB_ERR_INVALID, "edb_prepare: NULL argument");
+    if (flags & ~(EDB_USE_GRAPH | EDB_DRYRUN | EDB_FORCE_GATHER | EDB_X_DIRECT | EDB_PROFILE))
+        return fail(EDB_ERR_INVALID, "edb_prepare: unknown flags");
+    if (s->V != g->V || p->V != g->V || p->B != (int32_t)s->batch_type.size())
+        return fail(EDB_ERR_INVALID, "edb_prepare: graph, schedule and plan do not match");
+    const int32_t T = g->T, B = p->B;
+    std::vector<Dims> dims(T);
+    int H = -1, E = -1, dtype = -1;
+    for (int32_t t = 0; t < T; ++t) {
+        edb_status st = cell_dims(&cells[t], dims[t]);
+        if (st != EDB_OK) return fail(st, "edb_prepare: type " + std::to_string(t) + ": " + edb_last_error());
+        if (H < 0) H = cells[t].hidden;
+        if (cells[t].hidden != H) return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: all types must share hidden");
+        if (dtype < 0) dtype = cells[t].dtype;
+        if (cells[t].dtype != dtype) return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: all types must share dtype");
+        if (dims[t].x) {
+            if (E < 0) E = dims[t].E;
+            if (dims[t].E != E) return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: all input types must share in_dim");
+        }
+        const KindInfo ki = kind_info(cells[t].kind);
+        const edb_operand_shape& sh = p->shapes[t];
+        if (sh.n_fixed != ki.nfix || (sh.ragged != 0) != ki.rag || (sh.has_x != 0) != ki.x)
+            return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: operand shape of type " + std::to_string(t) +
+                                                 " does not match its cell kind");
+    }
+    if (E < 0) E = 0;
+
+    edb_exec* e = new (std::nothrow) edb_exec;
+    if (!e) return fail(EDB_ERR_OOM, "edb_prepare: out of host memory");
+    try {
+        e->flags = flags;
+        e->T = T;
+        e->B = B;
+        e->dtype = dtype;
+        e->n_slots = p->n_slots;
+        e->E = E;
+        e->H = H;
+        e->dims = dims;
+        e->cells.assign(cells, cells + T);
+        int n_x = 0;
+        for (int32_t v = 0; v < g->V; ++v) n_x += p->x_slot[v] >= 0;
+        e->n_x = n_x;
+
+        // device int buffer: plan idx pool | ragged pool | x source rows | zero rows
+        std::vector<int32_t>& hb = e->hbuf;
+        hb.insert(hb.end(), p->idx_pool.begin(), p->idx_pool.end());
+        const int64_t off_rag = (int64_t)hb.size();
+        hb.insert(hb.end(), p->ragged_pool.begin(), p->ragged_pool.end());
+        e->off_xsrc = (int64_t)hb.size();
+        hb.resize(hb.size() + n_x, 0);
+        for (int32_t v = 0; v < g->V; ++v)
+            if (p->x_slot[v] >= 0) hb[e->off_xsrc + p->x_slot[v]] = g->x_row[v];
+        e->off_zero = (int64_t)hb.size();
+        hb.push_back(0);
+        hb.insert(hb.end(), p->pads.begin(), p->pads.end());
+        e->n_zero = 1 + (int32_t)p->pads.size();
+        if (hb.empty()) hb.push_back(0);
+
+        int max_lds = 160 * 1024;
+        if (!(flags & EDB_DRYRUN)) {
+            int dev = 0;
+            hipError_t he = hipGetDevice(&dev);
+            if (he == hipSuccess) he = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+            if (he != hipSuccess) {
+                delete e;
+                return fail(EDB_ERR_HIP, std::string("edb_prepare: ") + hipGetErrorString(he));
+            }
+            e->device = dev;
+        }
+        int min_wg = 512;
+        if (const char* env = std::getenv("EDB_MIN_WG")) min_wg = std::max(1, std::atoi(env));
+        const int force_var = std::getenv("EDB_VARIANT") ? std::atoi(std::getenv("EDB_VARIANT")) : -1;
+
+        // launch 0: x staging + zero rows
+        {
+            Launch L{};
+            L.info.batch = -1;
+            L.info.kind = -1;
+            L.info.m = n_x;
+            L.info.grid = ((flags & EDB_X_DIRECT) ? 0 : n_x) + e->n_zero;
+            L.info.block = 256;
+            L.info.variant = -1;
+            e->launches.push_back(L);
+        }
+        const bool force_gather = (flags & EDB_FORCE_GATHER) != 0;
+        for (int32_t b = 0; b < B; ++b) {
+            const int32_t t = s->batch_type[b];
+            const Dims& d = dims[t];
+            const int32_t m = s->batch_ptr[b + 1] - s->batch_ptr[b];
+            const int32_t* ord = p->order.data() + s->batch_ptr[b];
+            Launch L{};
+            L.type = t;
+            L.info.batch = b;
+            L.info.kind = cells[t].kind;
+            L.info.m = m;
+            L.info.k = d.K;
+            L.info.n = d.G * d.Hu;
+            L.info.block = 256;
+            L.off_x = L.off_f0 = L.off_f1 = L.off_rag = L.off_rptr = L.off_res = -1;
+            BatchArgs& a = L.args;
+            a.m = m;
+            a.H = d.H;
+            a.Hk = d.Hk;
+            a.Hu = d.Hu;
+            a.E = d.E;
+            a.Ep = d.Ep;
+            a.K = d.K;
+            // segments of this batch: result, positional lists, ragged list
+            const edb_seg* sg = p->segs.data() + p->seg_ptr[b];
+            auto conv = [&](const edb_seg& q, Seg& out_seg, int64_t& off) {
+                off = -1;
+                out_seg = Seg{S_NONE, 0, nullptr};
+                if (q.kind == EDB_SEG_NONE) return;
+                if (q.kind == EDB_SEG_CONTIG && !force_gather) {
+                    out_seg.kind = S_CONTIG;
+                    out_seg.base = q.base;
+                } else {
+                    out_seg.kind = S_INDEXED;
+                    off = q.idx_off;
+                }
+            };
+            conv(sg[0], a.res, L.off_res);
+            L.info.seg_kind[0] = sg[0].kind;
+            const KindInfo ki = kind_info(cells[t].kind);
+            if (ki.nfix >= 1) { conv(sg[1], a.fix[0], L.off_f0); L.info.seg_kind[1] = sg[1].kind; }
+            if (ki.nfix >= 2) { conv(sg[2], a.fix[1], L.off_f1); L.info.seg_kind[2] = sg[2].kind; }
+            if (ki.rag) {
+                conv(sg[1 + ki.nfix], a.rag, L.off_rag);
+                L.info.seg_kind[3] = sg[1 + ki.nfix].kind;
+                L.off_rptr = off_rag + p->ragged_off[b];
+                // rag_ptr entries are offsets into this batch's ragged list
+            }
+            if (ki.x) {
+                const int xb = p->x_slot[ord[0]];
+                if (flags & EDB_X_DIRECT) {
+                    a.x = Seg{S_INDEXED, 0, nullptr};
+                    L.off_x = e->off_xsrc + xb;
+                } else {
+                    a.x = Seg{S_CONTIG, xb, nullptr};
+                }
+            }
+            // tile variant: the largest tile that still gives min_wg work-groups
+            const int esz_kind = cells[t].kind;
+            int var = NUM_VARIANTS - 1;
+            for (int vi = 0; vi < NUM_VARIANTS; ++vi) {
+                const int TM = 16 * VAR_RT[vi], TU = 16 * VAR_WU[vi];
+                const int wgs = (m + TM - 1) / TM * (d.Hu / TU);
+                const int lds = table().e[esz_kind][dtype][vi].lds(d.K);
+                if (lds > max_lds) continue;
+                var = vi;
+                if (wgs >= min_wg) break;
+            }
+            if (force_var >= 0 && force_var < NUM_VARIANTS) var = force_var;
+            L.lds = table().e[esz_kind][dtype][var].lds(d.K);
+            if (L.lds > max_lds) {
+                delete e;
+                return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: LDS need of batch " + std::to_string(b) +
+                                                     " exceeds the device limit");
+            }
+            L.info.variant = var;
+            const int TM = 16 * VAR_RT[var], TU = 16 * VAR_WU[var];
+            L.info.grid = (m + TM - 1) / TM * (d.Hu / TU);
+            e->launches.push_back(L);
+        }
+        if (!(flags & EDB_DRYRUN)) {
+            hipError_t he = hipMalloc(&e->dbuf, hb.size() * sizeof(int32_t));
+            if (he == hipSuccess)
+                he = hipMemcpy(e->dbuf, hb.data(), hb.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+            if (he == hipSuccess && n_x > 0 && !(flags & EDB_X_DIRECT))
+                he = hipMalloc(&e->xstaged, (size_t)n_x * E * (dtype == EDB_F32 ? 4 : 2));
+            if (he == hipSuccess) he = hipStreamCreateWithFlags(&e->cap_stream, hipStreamNonBlocking);
+            if (flags & EDB_PROFILE) {
+                e->events.assign(e->launches.size() + 1, nullptr);
+                for (size_t i = 0; he == hipSuccess && i < e->events.size(); ++i)
+                    he = hipEventCreate(&e->events[i]);
+            }
+            for (size_t i = 1; he == hipSuccess && i < e->launches.size(); ++i) {
+                const Launch& L = e->launches[i];
+                if (L.lds > 64 * 1024)
+                    he = table().e[L.info.kind][dtype][L.info.variant].attr(L.lds);
+            }
+            if (he != hipSuccess) {
+                const bool oom = he == hipErrorOutOfMemory;
+                delete e;
+                return fail(oom ? EDB_ERR_OOM : EDB_ERR_HIP, std::string("edb_prepare: ") + hipGetErrorString(he));
+            }
+        }
+    } catch (const std::bad_alloc&) {
+        delete e;
+        return fail(EDB_ERR_OOM, "edb_prepare: out of host memory");
+    }
+    edb::clear_error();
+    *out = e;
+    return EDB_OK;
+}
+
+namespace {
+
+hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* arena_h, void* arena_c,
+                      hipStream_t st) {
+    const int esz = e->dtype == EDB_F32 ? 4 : 2;
+    const int* db = e->dbuf;
+    const bool prof = !e->events.empty();
+    if (prof) (void)hipEventRecord(e->events[0], st);
+    // launch 0: stage x rows and clear the zero / pad rows
+    {
+        const Launch& L = e->launches[0];
+        const bool direct = (e->flags & EDB_X_DIRECT) != 0;
+        const int nx = direct ? 0 : e->n_x;
+        if (L.info.grid > 0) {
+            if (e->dtype == EDB_F32)
+                hipLaunchKernelGGL(stage_kernel<float>, dim3(L.info.grid), dim3(256), 0, st,
+                                   reinterpret_cast<const float*>(x), reinterpret_cast<float*>(e->xstaged),
+                                   db + e->off_xsrc, nx, e->E, db + e->off_zero, e->n_zero,
+                                   reinterpret_cast<float*>(arena_h), reinterpret_cast<float*>(arena_c), e->H);
+            else
+                hipLaunchKernelGGL(stage_kernel<__bf16>, dim3(L.info.grid), dim3(256), 0, st,
+                                   reinterpret_cast<const __bf16*>(x), reinterpret_cast<__bf16*>(e->xstaged),
+                                   db + e->off_xsrc, nx, e->E, db + e->off_zero, e->n_zero,
+                                   reinterpret_cast<__bf16*>(arena_h), reinterpret_cast<float*>(arena_c), e->H);
+        }
+        if (prof) (void)hipEventRecord(e->events[1], st);
+    }
+    (void)esz;
+    for (size_t i = 1; i < e->launches.size(); ++i) {
+        const Launch& L = e->launches[i];
+        BatchArgs a = L.args;
+        const Dims& d = e->dims[L.type];
+        const uint8_t* wb = reinterpret_cast<const uint8_t*>(w[L.type]);
+        a.W = wb + d.off_W;
+        a.bias = reinterpret_cast<const float*>(wb + d.off_b);
+        a.Wr = d.rag ? wb + d.off_Wr : nullptr;
+        a.br = d.rag ? reinterpret_cast<const float*>(wb + d.off_br) : nullptr;
+        a.arena_h = arena_h;
+        a.arena_c = reinterpret_cast<float*>(arena_c);
+        a.xmat = (e->flags & EDB_X_DIRECT) ? x : e->xstaged;
+        if (L.off_x >= 0) a.x.idx = db + L.off_x;
+        if (L.off_f0 >= 0) a.fix[0].idx = db + L.off_f0;
+        if (L.off_f1 >= 0) a.fix[1].idx = db + L.off_f1;
+        if (L.off_rag >= 0) a.rag.idx = db + L.off_rag;
+        if (L.off_rptr >= 0) a.rag_ptr = db + L.off_rptr;
+        if (L.off_res >= 0) a.res.idx = db + L.off_res;
+        table().e[L.info.kind][e->dtype][L.info.variant].launch(a, L.info.grid, L.lds, st);
+        if (prof) (void)hipEventRecord(e->events[i + 1], st);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" edb_status edb_execute(edb_exec_t* e, const void* const* w, const void* x, void* arena_h,
+                                  void* arena_c, void* stream) {
+    if (!e) return fail(EDB_ERR_INVALID, "edb_execute: exec is NULL");
+    if (e->flags & EDB_DRYRUN) return EDB_OK;
+    if (!w || !arena_h || !arena_c) return fail(EDB_ERR_INVALID, "edb_execute: NULL argument");
+    if (e->n_x > 0 && !x) return fail(EDB_ERR_INVALID, "edb_execute: x is NULL");
+    for (int32_t t = 0; t < e->T; ++t)
+        if (!w[t]) return fail(EDB_ERR_INVALID, "edb_execute: packed weights of type " + std::to_string(t) + " are NULL");
+    auto misaligned = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) != 0; };
+    if (misaligned(x) || misaligned(arena_h) || misaligned(arena_c))
+        return fail(EDB_ERR_INVALID, "edb_execute: device buffers must be 16-byte aligned");
+    for (int32_t t = 0; t < e->T; ++t)
+        if (reinterpret_cast<uintptr_t>(w[t]) & 255u)
+            return fail(EDB_ERR_INVALID, "edb_execute: packed weights must be 256-byte aligned");
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    hipError_t he;
+    if (!(e->flags & EDB_USE_GRAPH) || (e->flags & EDB_PROFILE)) {
+        he = launch_all(e, w, x, arena_h, arena_c, st);
+        if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_execute: ") + hipGetErrorString(he));
+        e->profiled = !e->events.empty();
+        return EDB_OK;
+    }
+    std::vector<const void*> ptrs(w, w + e->T);
+    ptrs.push_back(x);
+    ptrs.push_back(arena_h);
+    ptrs.push_back(arena_c);
+    if (!e->gexec || ptrs != e->cap_ptrs) {
+        if (e->gexec) { (void)hipGraphExecDestroy(e->gexec); e->gexec = nullptr; }
+        if (e->graph) { (void)hipGraphDestroy(e->graph); e->graph = nullptr; }
+        he = hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal);
+        if (he == hipSuccess) {
+            hipError_t le = launch_all(e, w, x, arena_h, arena_c, e->cap_stream);
+            he = hipStreamEndCapture(e->cap_stream, &e->graph);
+            if (le != hipSuccess) he = le;
+        }
+        if (he == hipSuccess) he = hipGraphInstantiate(&e->gexec, e->graph, nullptr, nullptr, 0);
+        if (he != hipSuccess) {
+            if (e->graph) { (void)hipGraphDestroy(e->graph); e->graph = nullptr; }
+            e->gexec = nullptr;
+            return fail(EDB_ERR_HIP, std::string("edb_execute: graph capture: ") + hipGetErrorString(he));
+        }
+        e->cap_ptrs = ptrs;
+    }
+    he = hipGraphLaunch(e->gexec, st);
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_execute: ") + hipGetErrorString(he));
+    return EDB_OK;
+}
+
+extern "C" edb_status edb_exec_launches(const edb_exec_t* e, int32_t* n) {
+    if (!e || !n) return fail(EDB_ERR_INVALID, "edb_exec_launches: NULL argument");
+    *n = (int32_t)e->launches.size();
+    return EDB_OK;
+}
+
+extern "C" edb_status edb_exec_launch_info(const edb_exec_t* e, int32_t i, edb_launch_info* info) {
+    if (!e || !info) return fail(EDB_ERR_INVALID, "edb_exec_launch_info: NULL argument");
+    if (i < 0 || i >= (int32_t)e->launches.size()) return fail(EDB_ERR_INVALID, "edb_exec_launch_info: index out of range");
+    *info = e->launches[i].info;
+    return EDB_OK;
+}
+
+extern "C" edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n) {
+    if (!e || !ms) return fail(EDB_ERR_INVALID, "edb_exec_launch_times: NULL argument");
+    if (e->events.empty() || !e->profiled)
+        return fail(EDB_ERR_INVALID, "edb_exec_launch_times: no profiled execution");
+    if (n != (int32_t)e->launches.size()) return fail(EDB_ERR_INVALID, "edb_exec_launch_times: n != launches");
+    hipError_t he = hipEventSynchronize(e->events.back());
+    for (int32_t i = 0; he == hipSuccess && i < n; ++i) he = hipEventElapsedTime(&ms[i], e->events[i], e->events[i + 1]);
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_exec_launch_times: ") + hipGetErrorString(he));
+    return EDB_OK;
+}
+
+extern "C" void edb_exec_free(edb_exec_t* e) { delete e; }

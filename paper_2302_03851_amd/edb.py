@@ -1,0 +1,245 @@
+"""Python front end of libedb: handles for the graph, schedule, plan and
+executor, plus a `Forward` helper that owns the device buffers of one
+mini-batch.  PyTorch provides device memory and the stream only; all work is
+done by libedb's host code and HIP kernels."""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from . import _lib as L
+from .workloads import KIND_SHAPE, NARY_INTERNAL, weight_shapes
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _ptr(a, ctype):
+    return a.ctypes.data_as(C.POINTER(ctype))
+
+
+class Graph:
+    def __init__(self, op_type, child_ptr, child_idx, x_row, n_types):
+        lib = L.load()
+        self._op = _i32(op_type)
+        self._ptr = np.ascontiguousarray(child_ptr, dtype=np.int64)
+        self._idx = _i32(child_idx) if len(child_idx) else np.zeros(1, dtype=np.int32)
+        self._xr = _i32(x_row)
+        self.n_nodes = int(self._op.shape[0])
+        self.n_types = int(n_types)
+        h = C.c_void_p()
+        L.check(lib.edb_build_graph(self.n_nodes, self.n_types, _ptr(self._op, C.c_int32),
+                                    _ptr(self._ptr, C.c_int64), _ptr(self._idx, C.c_int32),
+                                    _ptr(self._xr, C.c_int32), C.byref(h)), "edb_build_graph")
+        self.handle = h
+
+    def __del__(self):
+        if getattr(self, "handle", None) and L._lib is not None:
+            L._lib.edb_graph_free(self.handle)
+            self.handle = None
+
+
+class Schedule:
+    def __init__(self, graph: Graph, kind=L.POLICY_TABLE, encoding=L.ENC_SORT, table=None):
+        lib = L.load()
+        self.graph = graph
+        flat = None
+        if table:
+            if isinstance(table, dict):
+                flat = [len(table)]
+                for key, action in table.items():
+                    flat += [len(key)] + list(key) + [action]
+            else:
+                flat = list(table)
+        self._tab = _i32(flat) if flat else None
+        pol = L.Policy(kind, encoding, _ptr(self._tab, C.c_int32) if flat else None,
+                       len(flat) if flat else 0)
+        h = C.c_void_p()
+        L.check(lib.edb_schedule(graph.handle, C.byref(pol), C.byref(h)), "edb_schedule")
+        self.handle = h
+        nb = C.c_int32()
+        bp, bn, bt = C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)()
+        L.check(lib.edb_schedule_view(h, C.byref(nb), C.byref(bp), C.byref(bn), C.byref(bt)))
+        B = nb.value
+        self.batch_ptr = np.ctypeslib.as_array(bp, shape=(B + 1,)).copy()
+        self.batch_nodes = np.ctypeslib.as_array(bn, shape=(graph.n_nodes,)).copy() if graph.n_nodes else \
+            np.zeros(0, dtype=np.int32)
+        self.batch_type = np.ctypeslib.as_array(bt, shape=(B,)).copy() if B else np.zeros(0, dtype=np.int32)
+
+    @property
+    def n_batches(self):
+        return int(self.batch_type.shape[0])
+
+    def batches(self) -> List[List[int]]:
+        return [self.batch_nodes[self.batch_ptr[b]:self.batch_ptr[b + 1]].tolist()
+                for b in range(self.n_batches)]
+
+    def __del__(self):
+        if getattr(self, "handle", None) and L._lib is not None:
+            L._lib.edb_schedule_free(self.handle)
+            self.handle = None
+
+
+class Plan:
+    def __init__(self, graph: Graph, sched: Schedule, shapes: Sequence[Tuple[int, int, int]], mode=L.PLAN_RC):
+        lib = L.load()
+        self.graph, self.sched = graph, sched
+        arr = (L.OperandShape * len(shapes))(*[L.OperandShape(*s) for s in shapes])
+        h = C.c_void_p()
+        L.check(lib.edb_plan_memory(graph.handle, sched.handle, arr, mode, C.byref(h)), "edb_plan_memory")
+        self.handle = h
+        v = L.PlanView()
+        L.check(lib.edb_plan_view(h, C.byref(v)))
+        V, B = v.n_nodes, v.n_batches
+        asarr = lambda p, n, dt=np.int32: np.ctypeslib.as_array(p, shape=(n,)).copy() if n else np.zeros(0, dt)
+        self.n_slots = v.n_slots
+        self.slot = asarr(v.slot, V)
+        self.order = asarr(v.order, V)
+        self.x_slot = asarr(v.x_slot, V)
+        self.seg_ptr = asarr(v.seg_ptr, B + 1)
+        nseg = int(self.seg_ptr[-1]) if B else 0
+        self.segs = [(v.segs[i].kind, v.segs[i].base, v.segs[i].idx_off, v.segs[i].len) for i in range(nseg)]
+        self.idx_pool = asarr(v.idx_pool, v.idx_len)
+        self.ragged_off = asarr(v.ragged_off, B, np.int64)
+        self.ragged_pool = asarr(v.ragged_pool, v.ragged_len)
+        self.pads = asarr(v.pads, v.n_pads)
+
+    def batch_segments(self, b):
+        """[(kind, slot list)] for batch b: result first, then the operand lists."""
+        out = []
+        for kind, base, off, n in self.segs[self.seg_ptr[b]:self.seg_ptr[b + 1]]:
+            out.append((kind, [] if kind == L.SEG_NONE else self.idx_pool[off:off + n].tolist()))
+        return out
+
+    def __del__(self):
+        if getattr(self, "handle", None) and L._lib is not None:
+            L._lib.edb_plan_free(self.handle)
+            self.handle = None
+
+
+def cell_struct(kind, in_dim, hidden, n_children, dtype) -> L.Cell:
+    return L.Cell(kind, in_dim, hidden, n_children, dtype)
+
+
+def packed_bytes(cell: L.Cell) -> int:
+    n = C.c_int64()
+    L.check(L.load().edb_packed_weight_bytes(C.byref(cell), C.byref(n)), "edb_packed_weight_bytes")
+    return int(n.value)
+
+
+def pack_weights(cell: L.Cell, logical: Sequence[np.ndarray], dest_ptr: int, stream: int = 0):
+    mats = [np.ascontiguousarray(m, dtype=np.float32) for m in logical]
+    arr = (C.POINTER(C.c_float) * len(mats))(*[_ptr(m, C.c_float) for m in mats])
+    L.check(L.load().edb_pack_weights(C.byref(cell), arr, C.c_void_p(dest_ptr), C.c_void_p(stream)),
+            "edb_pack_weights")
+
+
+class Exec:
+    def __init__(self, graph: Graph, sched: Schedule, plan: Plan, cells: Sequence[L.Cell], flags=L.USE_GRAPH):
+        lib = L.load()
+        self.graph, self.sched, self.plan = graph, sched, plan
+        self._cells = (L.Cell * len(cells))(*cells)
+        h = C.c_void_p()
+        L.check(lib.edb_prepare(graph.handle, sched.handle, plan.handle, self._cells, flags, C.byref(h)),
+                "edb_prepare")
+        self.handle = h
+        self.flags = flags
+
+    def launches(self) -> int:
+        n = C.c_int32()
+        L.check(L.load().edb_exec_launches(self.handle, C.byref(n)))
+        return n.value
+
+    def launch_info(self, i) -> Dict:
+        info = L.LaunchInfo()
+        L.check(L.load().edb_exec_launch_info(self.handle, i, C.byref(info)))
+        return {f: (list(getattr(info, f)) if f == "seg_kind" else getattr(info, f)) for f, _ in info._fields_}
+
+    def launch_times(self) -> np.ndarray:
+        """Per-launch milliseconds of the last profiled execution."""
+        n = self.launches()
+        out = (C.c_float * n)()
+        L.check(L.load().edb_exec_launch_times(self.handle, out, n), "edb_exec_launch_times")
+        return np.array(out[:], dtype=np.float64)
+
+    def execute(self, weight_ptrs: Sequence[int], x_ptr: int, arena_h_ptr: int, arena_c_ptr: int, stream: int):
+        arr = (C.c_void_p * len(weight_ptrs))(*weight_ptrs)
+        L.check(L.load().edb_execute(self.handle, arr, C.c_void_p(x_ptr), C.c_void_p(arena_h_ptr),
+                                     C.c_void_p(arena_c_ptr), C.c_void_p(stream)), "edb_execute")
+
+    def __del__(self):
+        if getattr(self, "handle", None) and L._lib is not None:
+            L._lib.edb_exec_free(self.handle)
+            self.handle = None
+
+
+def operand_shapes(w) -> List[Tuple[int, int, int]]:
+    return [(nf, rg, int(KIND_SHAPE[k][2])) for (nf, rg), k in zip(w.shapes(), w.kinds)]
+
+
+def logical_weights(w, t) -> List[np.ndarray]:
+    k = w.kinds[t]
+    names = [n for n, _ in weight_shapes(k, w.in_dim, w.hidden, w.n_children[t] or 2)]
+    return [w.weights[t][n] for n in names]
+
+
+LATTICE_TABLE = {(0,): 0, (1,): 1, (0, 1): 0, (1, 0): 1}
+
+
+class Forward:
+    """Everything needed to run the batched forward pass of one workload on
+    the current GPU: graph, schedule, plan, packed weights, x, arena."""
+
+    def __init__(self, w, policy=L.POLICY_TABLE, table=None, plan_mode=L.PLAN_RC, flags=L.USE_GRAPH,
+                 device="cuda", encoding=L.ENC_SORT):
+        import torch
+        self.w = w
+        self.torch = torch
+        if table is None and policy == L.POLICY_TABLE and w.kinds == [6, 7]:
+            table = LATTICE_TABLE
+        self.graph = Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+        self.sched = Schedule(self.graph, policy, encoding, table)
+        self.plan = Plan(self.graph, self.sched, operand_shapes(w), plan_mode)
+        dt = L.BF16 if w.dtype == "bf16" else L.F32
+        self.dtype = dt
+        self.cells = [cell_struct(k, w.in_dim, w.hidden, w.n_children[t] if k == NARY_INTERNAL else 0, dt)
+                      for t, k in enumerate(w.kinds)]
+        self.exec = Exec(self.graph, self.sched, self.plan, self.cells, flags)
+        self.flags = flags
+        if flags & L.DRYRUN:
+            return
+        tdt = torch.bfloat16 if dt == L.BF16 else torch.float32
+        self.tdt = tdt
+        dev = torch.device(device)
+        self.stream = torch.cuda.current_stream(dev)
+        self.weights = []
+        for t in range(w.n_types):
+            nb = packed_bytes(self.cells[t])
+            buf = torch.empty(nb, dtype=torch.uint8, device=dev)
+            pack_weights(self.cells[t], logical_weights(w, t), buf.data_ptr(), self.stream.cuda_stream)
+            self.weights.append(buf)
+        n_x = max(1, int(w.x.shape[0]))
+        if w.x.shape[0] and int(w.x_row.max()) >= w.x.shape[0]:
+            raise ValueError("x_row points past the end of x")
+        xt = torch.zeros((n_x, max(1, w.in_dim)), dtype=torch.float32)
+        if w.x.shape[0]:
+            xt[: w.x.shape[0], : w.in_dim] = torch.from_numpy(w.x)
+        self.x = xt.to(dev).to(tdt).contiguous()
+        H = w.hidden
+        self.arena_h = torch.empty((self.plan.n_slots, H), dtype=tdt, device=dev)
+        self.arena_c = torch.empty((self.plan.n_slots, H), dtype=torch.float32, device=dev)
+
+    def run(self):
+        self.exec.execute([b.data_ptr() for b in self.weights], self.x.data_ptr(), self.arena_h.data_ptr(),
+                          self.arena_c.data_ptr(), self.stream.cuda_stream)
+
+    def states(self):
+        """Node-ordered (h, c) as float64 numpy arrays (synchronises)."""
+        self.torch.cuda.synchronize()
+        ah = self.arena_h.float().cpu().numpy().astype(np.float64)
+        ac = self.arena_c.cpu().numpy().astype(np.float64)
+        s = self.plan.slot
+        return ah[s], ac[s]

@@ -1,0 +1,229 @@
+"""GPU parity: the HIP path through the C ABI against the oracle.
+
+Bounds (normwise relative error per state vector, max over nodes and h/c):
+1e-4 for the fp32 configurations, 2e-2 for the bf16 child-sum configuration.
+Small instances compare every node; the full-size configurations run in the
+benchmark's launch configuration (HIP graph, planned layout) and compare
+whole sampled instances, which the oracle evaluates on their own (instances
+are independent graphs)."""
+import numpy as np
+import pytest
+
+from oracle.compare import normwise_rel_err, state_rel_err
+from oracle.evaluate import evaluate
+from paper_2302_03851_amd import _lib as L
+from paper_2302_03851_amd import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+SMALL = {1: 8, 2: 6, 3: 6, 4: 2, 5: 4}
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _fwd(w, **kw):
+    from paper_2302_03851_amd import edb
+    return edb.Forward(w, **kw)
+
+
+def _oracle(w):
+    return evaluate(w.kinds, w.op_type, w.child_ptr, w.child_idx, w.x_row, w.x, w.weights, w.hidden,
+                    n_fixed=w.n_children, dtype=w.dtype)
+
+
+def _h_rows(w):
+    """Nodes that have an h output (lattice word cells have none)."""
+    return np.array([w.kinds[t] != WL.LAT_WORD for t in w.op_type])
+
+
+def _check(w, h, c, hr, cr, label):
+    err = state_rel_err(h, c, hr, cr, h_rows=_h_rows(w))
+    print(f"{label}: {w.name} V={w.n_nodes} max normwise rel err {err:.3e}", flush=True)
+    assert np.isfinite(h).all() and np.isfinite(c).all()
+    assert err <= TOL[w.dtype], err
+    return err
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_parity_small(k):
+    _torch()
+    w = WL.make_config(k, instances=SMALL[k])
+    f = _fwd(w)
+    f.run()
+    h, c = f.states()
+    hr, cr = _oracle(w)
+    _check(w, h, c, hr, cr, f"small k={k}")
+    # lattice words keep h == 0
+    if k == 3:
+        words = np.array([w.kinds[t] == WL.LAT_WORD for t in w.op_type])
+        assert (h[words] == 0).all()
+
+
+def _components(w):
+    """Instance id of every node (connected components over present edges)."""
+    parent = np.arange(w.n_nodes)
+
+    def find(a):
+        while parent[a] != a:
+            parent[a] = parent[parent[a]]
+            a = parent[a]
+        return a
+    for v in range(w.n_nodes):
+        for c in w.children(v):
+            if c >= 0:
+                ra, rb = find(v), find(int(c))
+                if ra != rb:
+                    parent[ra] = rb
+    return np.array([find(v) for v in range(w.n_nodes)])
+
+
+def _subgraph(w, nodes):
+    """Workload restricted to `nodes` (closed under children), ids remapped."""
+    nodes = np.sort(nodes)
+    remap = {int(v): i for i, v in enumerate(nodes)}
+    ptr = [0]
+    idx = []
+    for v in nodes:
+        for c in w.children(int(v)):
+            idx.append(remap[int(c)] if c >= 0 else -1)
+        ptr.append(len(idx))
+    return dict(op_type=w.op_type[nodes], child_ptr=np.array(ptr, dtype=np.int64),
+                child_idx=np.array(idx, dtype=np.int32), x_row=w.x_row[nodes])
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_parity_full_size_sampled_instances(k):
+    _torch()
+    w = WL.make_config(k)
+    f = _fwd(w)           # the benchmark's configuration: HIP graph, planned layout
+    f.run()
+    f.run()               # a replay of the captured graph
+    h, c = f.states()
+    comp = _components(w)
+    roots = np.unique(comp)
+    rng = np.random.default_rng(k)
+    pick = rng.choice(roots, size=min(len(roots), 3), replace=False)
+    # always include the largest instance
+    sizes = {r: int((comp == r).sum()) for r in roots}
+    pick = set(pick.tolist()) | {max(sizes, key=sizes.get)}
+    nodes = np.nonzero(np.isin(comp, list(pick)))[0]
+    sg = _subgraph(w, nodes)
+    hr, cr = evaluate(w.kinds, sg["op_type"], sg["child_ptr"], sg["child_idx"], sg["x_row"], w.x,
+                      w.weights, w.hidden, n_fixed=w.n_children, dtype=w.dtype)
+    hrows = _h_rows(w)[nodes]
+    err = max(normwise_rel_err(h[nodes], hr, rows=hrows), normwise_rel_err(c[nodes], cr))
+    print(f"full k={k}: {w.name} V={w.n_nodes}, checked {len(nodes)} nodes of {len(pick)} instances, "
+          f"err {err:.3e}", flush=True)
+    assert np.isfinite(h).all() and np.isfinite(c).all()
+    assert err <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("k", [2, 3, 4, 5])
+def test_layout_and_launch_mode_bitwise(k):
+    """The planned layout, the identity layout with every operand indexed,
+    forced gathers, x read in place and eager launches all give bitwise the
+    same node states: only the addressing differs."""
+    _torch()
+    w = WL.make_config(k, instances=SMALL[k])
+    ref = _fwd(w)
+    ref.run()
+    h0, c0 = ref.states()
+    for kw in (dict(plan_mode=L.PLAN_IDENTITY), dict(flags=L.USE_GRAPH | L.FORCE_GATHER),
+               dict(flags=L.USE_GRAPH | L.X_DIRECT), dict(flags=0)):
+        f = _fwd(w, **kw)
+        f.run()
+        h, c = f.states()
+        np.testing.assert_array_equal(h, h0, err_msg=str(kw))
+        np.testing.assert_array_equal(c, c0, err_msg=str(kw))
+
+
+def test_graph_replays_match_eager():
+    """Replays of the captured graph, with eager work and synchronisations in
+    between, all equal the eager result."""
+    torch = _torch()
+    w = WL.make_config(2, instances=8)
+    eager = _fwd(w, flags=0)
+    eager.run()
+    he, ce = eager.states()
+    f = _fwd(w)
+    for i in range(4):
+        f.arena_h.fill_(7.0)
+        f.arena_c.fill_(-3.0)
+        torch.cuda.synchronize()
+        f.run()
+        h, c = f.states()
+        np.testing.assert_array_equal(h, he, err_msg=f"replay {i}")
+        np.testing.assert_array_equal(c, ce, err_msg=f"replay {i}")
+
+
+def test_policies_give_same_states():
+    """Agenda and depth schedules change the batches, not the results."""
+    _torch()
+    w = WL.make_config(3, instances=4)
+    hr, cr = _oracle(w)
+    for pol in (L.POLICY_AGENDA, L.POLICY_DEPTH):
+        f = _fwd(w, policy=pol)
+        f.run()
+        h, c = f.states()
+        _check(w, h, c, hr, cr, f"policy {pol}")
+
+
+def test_edge_cases():
+    _torch()
+    # single leaf; single chain node; a batch of one row per kind
+    w = WL.make_graph([WL.NARY_LEAF, WL.NARY_INTERNAL], 256, 256, [0], [[]], [True], seed=3)
+    f = _fwd(w)
+    f.run()
+    h, c = f.states()
+    hr, cr = _oracle(w)
+    _check(w, h, c, hr, cr, "single leaf")
+    # internal nodes with one or both children absent, non-zero biases
+    w = WL.make_graph([WL.NARY_LEAF, WL.NARY_INTERNAL], 64, 64, [0, 0, 1, 1, 1],
+                      [[], [], [0, -1], [-1, 1], [2, 3]], [True, True, False, False, False],
+                      seed=4, bias_scale=0.5)
+    f = _fwd(w)
+    f.run()
+    h, c = f.states()
+    hr, cr = _oracle(w)
+    _check(w, h, c, hr, cr, "absent children")
+    # odd sizes: H = 200 with E = 100 (padded K and units), ragged row tail
+    w = WL.make_config(3, instances=1)
+    f = _fwd(w)
+    f.run()
+    h, c = f.states()
+    hr, cr = _oracle(w)
+    _check(w, h, c, hr, cr, "one lattice")
+    # child-sum in fp32 and chain in bf16 (the other dtype of each kind)
+    for kinds, E, H, dt in (([WL.CS_LEAF, WL.CS_INTERNAL], 64, 64, "f32"),):
+        ch = [[], [], [], [0, 1, 2], [3], [3, 4]]
+        w = WL.make_graph(kinds, E, H, [0, 0, 0, 1, 1, 1], ch, [True] * 3 + [False] * 3, seed=5,
+                          dtype=dt, bias_scale=0.3)
+        f = _fwd(w)
+        f.run()
+        h, c = f.states()
+        hr, cr = _oracle(w)
+        _check(w, h, c, hr, cr, "child-sum f32")
+    op = [0] * 12
+    ch = [[-1]] + [[i] for i in range(11)]
+    w = WL.make_graph([WL.LSTM_CHAIN], 64, 64, op, ch, [True] * 12, seed=6, dtype="bf16", bias_scale=0.2)
+    f = _fwd(w)
+    f.run()
+    h, c = f.states()
+    hr, cr = _oracle(w)
+    _check(w, h, c, hr, cr, "chain bf16")
+
+
+def test_empty_graph():
+    _torch()
+    w = WL.make_graph([WL.NARY_LEAF, WL.NARY_INTERNAL], 64, 64, [], [], [], seed=1)
+    f = _fwd(w)
+    assert f.sched.n_batches == 0 and f.exec.launches() == 1
+    f.run()
+    h, c = f.states()
+    assert h.shape == (0, 64)

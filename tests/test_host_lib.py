@@ -1,0 +1,235 @@
+"""The C-ABI host library on the CPU: every declared symbol is exported; the
+C++ schedule and memory plan are bit-exact against the oracle's on all five
+configurations and on random graphs; error conventions; dry-run launch
+lists (no GPU call)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import plan as OP
+from oracle import schedule as OS
+from paper_2302_03851_amd import _lib as L
+from paper_2302_03851_amd import edb
+from paper_2302_03851_amd import workloads as WL
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.load()
+
+
+def test_header_symbols_exported(lib):
+    with open(os.path.join(ROOT, "include", "edb.h")) as f:
+        text = f.read()
+    declared = set(re.findall(r"\b(edb_[a-z_]+)\s*\(", text))
+    assert declared == set(L.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.edb_version() >= 10000
+
+
+def _oracle_schedule(w, policy=OS.POLICY_TABLE, table=None, encoding=OS.ENC_SORT):
+    return OS.schedule(w.op_type, w.child_ptr, w.child_idx, w.n_types, policy, table, encoding)
+
+
+CFG_INSTANCES = {1: None, 2: None, 3: None, 4: None, 5: 48}
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("policy", [OS.POLICY_TABLE, OS.POLICY_AGENDA, OS.POLICY_DEPTH])
+def test_schedule_bit_exact_configs(k, policy):
+    w = WL.make_config(k, instances=CFG_INSTANCES[k])
+    table = edb.LATTICE_TABLE if k == 3 else None
+    g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+    s = edb.Schedule(g, policy, L.ENC_SORT, table)
+    batches, bt = _oracle_schedule(w, policy, table)
+    assert s.batches() == batches
+    assert s.batch_type.tolist() == bt
+
+
+def _compare_plan(pl, ref, batches):
+    assert pl.n_slots == ref.n_slots
+    np.testing.assert_array_equal(pl.slot, ref.slot)
+    np.testing.assert_array_equal(pl.x_slot, ref.x_slot)
+    assert pl.order.tolist() == [v for o in ref.order for v in o]
+    assert sorted(pl.pads.tolist()) == sorted(ref.pads)
+    for b in range(len(batches)):
+        segs = pl.batch_segments(b)
+        assert segs[0] == ref.results[b]
+        assert segs[1:] == [(k, s) for k, s in ref.segments[b]]
+        if ref.ragged_ptr[b] is not None:
+            off = int(pl.ragged_off[b])
+            assert pl.ragged_pool[off:off + len(ref.ragged_ptr[b])].tolist() == ref.ragged_ptr[b]
+        else:
+            assert pl.ragged_off[b] == -1
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("mode", [OP.PLAN_RC, OP.PLAN_IDENTITY])
+def test_plan_bit_exact_configs(k, mode):
+    w = WL.make_config(k, instances=CFG_INSTANCES[k])
+    table = edb.LATTICE_TABLE if k == 3 else None
+    g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+    s = edb.Schedule(g, L.POLICY_TABLE, L.ENC_SORT, table)
+    shapes = edb.operand_shapes(w)
+    pl = edb.Plan(g, s, shapes, mode)
+    batches, _ = _oracle_schedule(w, OS.POLICY_TABLE, table)
+    ref = OP.plan_memory(w.op_type, w.child_ptr, w.child_idx, batches, shapes, mode)
+    _compare_plan(pl, ref, batches)
+
+
+@st.composite
+def random_graphs(draw):
+    n = draw(st.integers(1, 40))
+    T = draw(st.integers(1, 3))
+    # per type: n_fixed in 0..2, ragged flag
+    nfix = [draw(st.integers(0, 2)) for _ in range(T)]
+    rag = [draw(st.booleans()) for _ in range(T)]
+    op, children = [], []
+    for v in range(n):
+        t = draw(st.integers(0, T - 1))
+        op.append(t)
+        kids = []
+        for _ in range(nfix[t]):
+            kids.append(draw(st.integers(-1, v - 1)) if v else -1)
+        if rag[t] and v:
+            kids += draw(st.lists(st.integers(-1, v - 1), max_size=4))
+        children.append(kids)
+    return np.array(op, dtype=np.int32), children, T, [(nfix[t], int(rag[t]), 0) for t in range(T)]
+
+
+@settings(max_examples=80, deadline=None)
+@given(random_graphs(), st.sampled_from([OS.ENC_SORT, OS.ENC_BASE, OS.ENC_MAX]),
+       st.sampled_from([OS.POLICY_TABLE, OS.POLICY_AGENDA, OS.POLICY_DEPTH]),
+       st.sampled_from([OP.PLAN_RC, OP.PLAN_IDENTITY]))
+def test_random_graphs_bit_exact(g, enc, policy, mode):
+    op, children, T, shapes = g
+    ptr = np.zeros(len(children) + 1, dtype=np.int64)
+    for v, ch in enumerate(children):
+        ptr[v + 1] = ptr[v] + len(ch)
+    idx = np.array([c for ch in children for c in ch], dtype=np.int32)
+    x_row = np.full(len(op), -1, dtype=np.int32)
+    table = {(0,): 0, (1, 0): 1, (0, 1): 1, (2, 1, 0): 2, (0, 1, 2): 1}
+    gr = edb.Graph(op, ptr, idx, x_row, T)
+    s = edb.Schedule(gr, policy, enc, table)
+    batches, bt = OS.schedule(op, ptr, idx, T, policy, table, enc)
+    assert s.batches() == batches
+    assert s.batch_type.tolist() == bt
+    pl = edb.Plan(gr, s, shapes, mode)
+    ref = OP.plan_memory(op, ptr, idx, batches, shapes, mode)
+    _compare_plan(pl, ref, batches)
+    OP.hazard_check(op, ptr, idx, batches, ref)
+
+
+def _status(lib, fn, *args):
+    st_ = fn(*args)
+    msg = lib.edb_last_error().decode()
+    return st_, msg
+
+
+def test_abi_errors(lib):
+    P = C.POINTER
+    h = C.c_void_p()
+    op = np.array([0, 0], dtype=np.int32)
+    ptr = np.array([0, 1, 2], dtype=np.int64)
+    xr = np.array([-1, -1], dtype=np.int32)
+    cyc = np.array([1, 0], dtype=np.int32)
+    p_ = lambda a, t: a.ctypes.data_as(P(t))
+    st_, msg = _status(lib, lib.edb_build_graph, 2, 1, p_(op, C.c_int32), p_(ptr, C.c_int64),
+                       p_(cyc, C.c_int32), p_(xr, C.c_int32), C.byref(h))
+    assert st_ == L.EDB_ERR_CYCLE and "cycle" in msg and not h.value
+    bad = np.array([5, -1], dtype=np.int32)
+    st_, _ = _status(lib, lib.edb_build_graph, 2, 1, p_(op, C.c_int32), p_(ptr, C.c_int64),
+                     p_(bad, C.c_int32), p_(xr, C.c_int32), C.byref(h))
+    assert st_ == L.EDB_ERR_INVALID and not h.value
+    selfe = np.array([0, -1], dtype=np.int32)
+    st_, _ = _status(lib, lib.edb_build_graph, 2, 1, p_(op, C.c_int32), p_(ptr, C.c_int64),
+                     p_(selfe, C.c_int32), p_(xr, C.c_int32), C.byref(h))
+    assert st_ == L.EDB_ERR_INVALID
+    badt = np.array([0, 3], dtype=np.int32)
+    ok_idx = np.array([-1, 0], dtype=np.int32)
+    st_, _ = _status(lib, lib.edb_build_graph, 2, 1, p_(badt, C.c_int32), p_(ptr, C.c_int64),
+                     p_(ok_idx, C.c_int32), p_(xr, C.c_int32), C.byref(h))
+    assert st_ == L.EDB_ERR_INVALID
+    nonmono = np.array([0, 2, 1], dtype=np.int64)
+    st_, _ = _status(lib, lib.edb_build_graph, 2, 1, p_(op, C.c_int32), p_(nonmono, C.c_int64),
+                     p_(ok_idx, C.c_int32), p_(xr, C.c_int32), C.byref(h))
+    assert st_ == L.EDB_ERR_INVALID
+    st_, _ = _status(lib, lib.edb_build_graph, -1, 1, None, p_(ptr, C.c_int64), None, None, C.byref(h))
+    assert st_ == L.EDB_ERR_INVALID
+    st_, _ = _status(lib, lib.edb_build_graph, 2, 1, p_(op, C.c_int32), p_(ptr, C.c_int64),
+                     p_(ok_idx, C.c_int32), p_(xr, C.c_int32), None)
+    assert st_ == L.EDB_ERR_INVALID
+
+    g = edb.Graph(op, ptr, ok_idx, xr, 1)
+    # malformed tables
+    for flat in ([2, 1, 0, 0], [1, 5, 0, 0], [1, -1, 0], [1, 1, 0, 0, 9], [-1]):
+        with pytest.raises(L.EdbError) as ei:
+            edb.Schedule(g, L.POLICY_TABLE, L.ENC_SORT, flat)
+        assert ei.value.status == L.EDB_ERR_TABLE
+    with pytest.raises(L.EdbError) as ei:
+        edb.Schedule(g, 7)
+    assert ei.value.status == L.EDB_ERR_INVALID
+    s = edb.Schedule(g)
+    # shape mismatch: the second node has 1 child but the type declares 2 fixed
+    with pytest.raises(L.EdbError) as ei:
+        edb.Plan(g, s, [(2, 0, 0)])
+    assert ei.value.status == L.EDB_ERR_UNSUPPORTED
+    # has_x without an x row
+    with pytest.raises(L.EdbError) as ei:
+        edb.Plan(g, s, [(1, 0, 1)])
+    assert ei.value.status == L.EDB_ERR_INVALID
+    pl = edb.Plan(g, s, [(1, 0, 0)])
+    # cell kind vs operand shape mismatch, unsupported N, bad dtype
+    cells = [edb.cell_struct(WL.GRID, 8, 8, 0, L.F32)]
+    with pytest.raises(L.EdbError) as ei:
+        edb.Exec(g, s, pl, cells, L.DRYRUN)
+    assert ei.value.status == L.EDB_ERR_UNSUPPORTED
+    with pytest.raises(L.EdbError) as ei:
+        edb.packed_bytes(edb.cell_struct(WL.NARY_INTERNAL, 0, 8, 3, L.F32))
+    assert ei.value.status == L.EDB_ERR_UNSUPPORTED
+    with pytest.raises(L.EdbError) as ei:
+        edb.packed_bytes(edb.cell_struct(WL.NARY_LEAF, 8, 8, 0, 5))
+    assert ei.value.status == L.EDB_ERR_INVALID
+    with pytest.raises(L.EdbError) as ei:
+        edb.packed_bytes(edb.cell_struct(WL.NARY_LEAF, 8, 6, 0, L.F32))   # 24-byte rows
+    assert ei.value.status == L.EDB_ERR_UNSUPPORTED
+    n = C.c_int32()
+    assert lib.edb_exec_launches(None, C.byref(n)) == L.EDB_ERR_INVALID
+    assert lib.edb_execute(None, None, None, None, None, None) == L.EDB_ERR_INVALID
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_dryrun_launch_list(k):
+    w = WL.make_config(k, instances=CFG_INSTANCES[k])
+    f = edb.Forward(w, flags=L.DRYRUN | L.USE_GRAPH)
+    n = f.exec.launches()
+    assert n == 1 + f.sched.n_batches
+    info0 = f.exec.launch_info(0)
+    assert info0["batch"] == -1 and info0["grid"] == int((w.x_row >= 0).sum()) + 1 + len(f.plan.pads)
+    for i in range(1, n):
+        info = f.exec.launch_info(i)
+        b = info["batch"]
+        assert b == i - 1
+        t = int(f.sched.batch_type[b])
+        assert info["kind"] == w.kinds[t]
+        assert info["m"] == f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b]
+        assert 0 <= info["variant"] < 4 and info["grid"] >= 1 and info["block"] == 256
+        segs = f.plan.batch_segments(b)
+        assert info["seg_kind"][0] == segs[0][0]
+    with pytest.raises(L.EdbError):
+        f.exec.launch_info(n)
+
+
+def test_packed_weight_bytes_layout():
+    # main [Hu/16][G][K/KG][64][16 B] + bias, 256-byte aligned
+    c = edb.cell_struct(WL.NARY_INTERNAL, 0, 256, 2, L.F32)
+    assert edb.packed_bytes(c) == 256 // 16 * 5 * (512 // 16) * 64 * 16 + 5 * 256 * 4
+    c = edb.cell_struct(WL.CS_INTERNAL, 0, 512, 0, L.BF16)
+    assert edb.packed_bytes(c) == (512 // 16 * 3 * 16 * 1024 + 3 * 512 * 4 + 512 // 16 * 16 * 1024 + 2048)
