@@ -218,7 +218,8 @@ edb_status edb_pack_weights(const edb_cell* cell, const float* const* logical,
 #define EDB_DRYRUN       2  /* record the launch list only; no HIP call (CPU testing) */
 #define EDB_FORCE_GATHER 4  /* treat every CONTIG operand as indexed (ablation) */
 #define EDB_X_DIRECT     8  /* read x rows in place by x_row instead of staging them */
-#define EDB_PROFILE     16  /* eager launches, each bracketed by HIP events (edb_exec_launch_times) */
+#define EDB_PROFILE     16  /* eager launches timed by start/stop HIP events in each dispatch (edb_exec_launch_times) */
+#define EDB_NO_FLOW     32  /* one launch per batch only (no dataflow launches) */
 
 typedef struct edb_exec edb_exec_t;
 
@@ -244,29 +245,40 @@ edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_
 edb_status edb_execute(edb_exec_t* e, const void* const* packed_weights, const void* x,
                        void* arena_h, void* arena_c, void* stream);
 
-/* Number of kernel launches one edb_execute issues (launches per graph). */
+/* Dataflow launches (a persistent kernel running a run of consecutive small
+ * batches, each tile waiting only for the tiles that produce its operand
+ * rows) are currently switched off: every batch runs as its own launch and
+ * EDB_NO_FLOW has no effect.  edb_exec_check reports a timed-out dataflow
+ * wait when they are enabled.
+ *
+ * Number of kernel launches one edb_execute issues (launches per graph). */
 edb_status edb_exec_launches(const edb_exec_t* e, int32_t* n_kernels);
 
 /* Description of launch i (for tests and profiling). */
 typedef struct {
-    int32_t batch;     /* batch index, -1 for the staging / zero-fill kernel */
-    int32_t kind;      /* EDB_CELL_* of the batch, -1 for staging */
-    int32_t m;         /* rows */
+    int32_t batch;     /* batch index (first batch of a dataflow launch), -1 for the staging kernel */
+    int32_t kind;      /* EDB_CELL_* of the batch, -1 for staging and dataflow launches */
+    int32_t m;         /* rows (all batches of a dataflow launch) */
     int32_t k;         /* padded reduction length of the main GEMM */
     int32_t n;         /* padded output columns (gates x padded hidden) */
-    int32_t variant;   /* tile variant id */
+    int32_t variant;   /* tile variant id; 100 for a dataflow launch */
     int32_t grid;      /* work-groups */
     int32_t block;     /* threads per work-group */
     int32_t seg_kind[4]; /* kinds of result, child 0, child 1, ragged lists */
+    int32_t n_batches; /* batches the launch executes (0 for staging) */
 } edb_launch_info;
 edb_status edb_exec_launch_info(const edb_exec_t* e, int32_t i, edb_launch_info* info);
 
 /* Per-launch GPU durations of the last edb_execute of an EDB_PROFILE handle,
- * in milliseconds, measured with HIP events recorded on the execution stream
- * between consecutive launches.  ms: host float[n], n = edb_exec_launches.
+ * in milliseconds: each kernel's own duration, from start and stop HIP events
+ * that the dispatch packet records on the execution stream.  ms: host float[n], n = edb_exec_launches.
  * Waits for that execution to finish.  EDB_ERR_INVALID without EDB_PROFILE
  * or before the first execute. */
 edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
+
+/* Wait for `stream` and check the last execution's dataflow launches:
+ * EDB_ERR_HIP if a bounded wait timed out (the results are then invalid). */
+edb_status edb_exec_check(edb_exec_t* e, void* stream);
 
 void edb_exec_free(edb_exec_t* e);
 

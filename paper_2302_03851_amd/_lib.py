@@ -22,7 +22,8 @@ ENC_SORT, ENC_BASE, ENC_MAX = 0, 1, 2
 PLAN_RC, PLAN_IDENTITY = 0, 1
 SEG_NONE, SEG_CONTIG, SEG_GATHER, SEG_SCATTER = 0, 1, 2, 3
 F32, BF16 = 0, 1
-USE_GRAPH, DRYRUN, FORCE_GATHER, X_DIRECT, PROFILE = 1, 2, 4, 8, 16
+USE_GRAPH, DRYRUN, FORCE_GATHER, X_DIRECT, PROFILE, NO_FLOW = 1, 2, 4, 8, 16, 32
+FLOW_VARIANT = 100
 
 # every symbol include/edb.h declares
 EXPORTS = [
@@ -32,7 +33,7 @@ EXPORTS = [
     "edb_plan_memory", "edb_plan_view", "edb_plan_free",
     "edb_packed_weight_bytes", "edb_pack_weights",
     "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
-    "edb_exec_free",
+    "edb_exec_check", "edb_exec_free",
 ]
 
 
@@ -74,7 +75,7 @@ class Cell(C.Structure):
 class LaunchInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("kind", C.c_int32), ("m", C.c_int32), ("k", C.c_int32),
                 ("n", C.c_int32), ("variant", C.c_int32), ("grid", C.c_int32), ("block", C.c_int32),
-                ("seg_kind", C.c_int32 * 4)]
+                ("seg_kind", C.c_int32 * 4), ("n_batches", C.c_int32)]
 
 
 _lib = None
@@ -112,6 +113,7 @@ def load():
         "edb_exec_launches": (C.c_int32, [vp, P(C.c_int32)]),
         "edb_exec_launch_info": (C.c_int32, [vp, C.c_int32, P(LaunchInfo)]),
         "edb_exec_launch_times": (C.c_int32, [vp, P(C.c_float), C.c_int32]),
+        "edb_exec_check": (C.c_int32, [vp, vp]),
         "edb_exec_free": (None, [vp]),
     }
     for name, (res, args) in sig.items():

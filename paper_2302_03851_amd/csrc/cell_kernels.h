@@ -8,20 +8,24 @@
 // GEMM's prologue (operand rows staged through LDS, contiguous rows taking a
 // base+row fast path) and epilogue (row-indexed stores).
 //
-// Work decomposition.  A work-group (4 waves) owns TM = 16*RT rows and
-// TU = 16*WU hidden units of the batch, all G gates of those units.  The 4
-// waves are split WU along units and WK = 4/WU along the reduction (split-K
-// inside the work-group; partial sums are combined in LDS in a fixed order, so
-// results do not depend on scheduling).  Each wave computes a 16*RT x 16 x G
-// block with 16x16 MFMA tiles: v_mfma_f32_16x16x4_f32 (fp32) or
-// v_mfma_f32_16x16x32_bf16 (bf16 inputs, fp32 accumulation).
+// Work decomposition.  A work-group of WU*WK waves owns TM = 16*RT rows and
+// TU = 16*WU hidden units of the batch, all G gates of those units.  Waves
+// are split WU along units and WK along the reduction (split-K inside the
+// work-group; partial sums are added in LDS in a fixed order, so the result
+// does not depend on timing).  Each wave computes a 16*RT x 16 x G block with
+// 16x16 MFMA tiles: v_mfma_f32_16x16x4_f32 (fp32) or v_mfma_f32_16x16x32_bf16
+// (bf16 inputs, fp32 accumulation).  Small batches are latency bound, so the
+// prologue issues every global load it can before waiting: operand rows in
+// batches of 8 per thread, the epilogue's child cell states, and the first
+// weight fragments; the GEMM loop keeps the weights of the next 2-4 k-groups
+// in flight.
 //
 // Packed weights (gate-interleaved, zero padded; produced by edb_pack_weights):
 //   main  [Hu/16 unit blocks][G gates][K/KG k-groups][64 lanes][16 bytes]
 //   lane l of k-group kg holds, for unit u = ub*16 + l%16 of gate g, the KG/4
 //   consecutive k values kg*KG + (l/16)*(KG/4) + i.  With KG = 16 (fp32) this
-//   is 4 floats; with KG = 32 (bf16) 8 bf16 values.  One 16-byte load per lane
-//   is one B operand (bf16) or four (fp32, one per MFMA of the k-group).
+//   is 4 floats, one per MFMA of the k-group; with KG = 32 (bf16) 8 bf16
+//   values, one MFMA operand.  One 16-byte load per lane per (gate, k-group).
 //   bias  [G][Hu] fp32.  Ragged weights (child-sum U_f, lattice W_lc) use the
 //   same layout with G = 1 and K = Hk.
 // K layout of the A operand: [x (Ep)] [child 0 h (Hk)] [child 1 h (Hk)], each
@@ -50,6 +54,7 @@ struct Seg {
 };
 
 struct BatchArgs {
+    int kind;         // cell kind (K_*)
     int m;            // rows in the batch
     int H, Hk, Hu;    // hidden size, its K-segment width (padded to KG), its unit padding (64)
     int E, Ep;        // input size and its padded K-segment width
@@ -69,14 +74,14 @@ struct BatchArgs {
 };
 
 template <int KIND> struct Kind;
-template <> struct Kind<K_CHAIN>    { static constexpr int G = 3 + 1, NFIX = 1; static constexpr bool X = true,  RAG = false; };
-template <> struct Kind<K_NARY_LEAF>{ static constexpr int G = 3,     NFIX = 0; static constexpr bool X = true,  RAG = false; };
-template <> struct Kind<K_NARY_INT> { static constexpr int G = 5,     NFIX = 2; static constexpr bool X = false, RAG = false; };
-template <> struct Kind<K_GRID>     { static constexpr int G = 5,     NFIX = 2; static constexpr bool X = true,  RAG = false; };
-template <> struct Kind<K_CS_LEAF>  { static constexpr int G = 3,     NFIX = 0; static constexpr bool X = true,  RAG = false; };
-template <> struct Kind<K_CS_INT>   { static constexpr int G = 3,     NFIX = 0; static constexpr bool X = false, RAG = true;  };
-template <> struct Kind<K_LAT_CHAR> { static constexpr int G = 5,     NFIX = 1; static constexpr bool X = true,  RAG = true;  };
-template <> struct Kind<K_LAT_WORD> { static constexpr int G = 3,     NFIX = 1; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_CHAIN>    { static constexpr int G = 4, NFIX = 1; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_NARY_LEAF>{ static constexpr int G = 3, NFIX = 0; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_NARY_INT> { static constexpr int G = 5, NFIX = 2; static constexpr bool X = false, RAG = false; };
+template <> struct Kind<K_GRID>     { static constexpr int G = 5, NFIX = 2; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_CS_LEAF>  { static constexpr int G = 3, NFIX = 0; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_CS_INT>   { static constexpr int G = 3, NFIX = 0; static constexpr bool X = false, RAG = true;  };
+template <> struct Kind<K_LAT_CHAR> { static constexpr int G = 5, NFIX = 1; static constexpr bool X = true,  RAG = true;  };
+template <> struct Kind<K_LAT_WORD> { static constexpr int G = 3, NFIX = 1; static constexpr bool X = true,  RAG = false; };
 
 template <typename T> struct Elem;
 template <> struct Elem<float>  { static constexpr int KG = 16; static constexpr int VEC = 4; };
@@ -99,63 +104,125 @@ template <typename T> __device__ __forceinline__ T from_f(float v);
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ __bf16 from_f<__bf16>(float v) { return (__bf16)v; }
 
-// 16-byte vector of T.
-template <typename T> struct Vec16 { uint4 u; };
-
-// LDS budget of one work-group (bytes).
-template <int KIND, typename T, int RT, int WU>
+// ---- LDS budget of one work-group (bytes) ----
+template <int KIND, typename T, int RT, int WU, int WK>
 __host__ __device__ constexpr int lds_a_bytes(int K) {
     return 16 * RT * (K + a_pad<T>()) * (int)sizeof(T);
 }
-template <int KIND, typename T, int RT, int WU>
+template <int KIND, typename T, int RT, int WU, int WK>
 __host__ __device__ constexpr int lds_z_bytes() {
-    return (4 / WU) * 16 * RT * Kind<KIND>::G * 16 * WU * 4;
+    return WK * 16 * RT * Kind<KIND>::G * 16 * WU * 4;
 }
-template <int KIND, typename T, int RT, int WU>
+template <int KIND, typename T, int RT, int WU, int WK>
 __host__ __device__ constexpr int lds_zr_bytes() {
-    return Kind<KIND>::RAG ? (4 / WU) * 16 * RT * 16 * WU * 4 : 0;
+    return Kind<KIND>::RAG ? WK * 16 * RT * 16 * WU * 4 : 0;
 }
-template <int KIND, typename T, int RT, int WU>
+// Offset of Z: after A for kinds with a ragged phase (A is reused for child
+// rows while Z must persist), else Z aliases A (written after the GEMM).
+template <int KIND, typename T, int RT, int WU, int WK>
+__host__ __device__ constexpr int lds_z_off(int K) {
+    return Kind<KIND>::RAG ? lds_a_bytes<KIND, T, RT, WU, WK>(K) : 0;
+}
+template <int KIND, typename T, int RT, int WU, int WK>
+__host__ __device__ constexpr int lds_rowc_off(int K) {
+    return Kind<KIND>::RAG
+               ? lds_a_bytes<KIND, T, RT, WU, WK>(K) + lds_z_bytes<KIND, T, RT, WU, WK>() +
+                     lds_zr_bytes<KIND, T, RT, WU, WK>()
+               : (lds_a_bytes<KIND, T, RT, WU, WK>(K) > lds_z_bytes<KIND, T, RT, WU, WK>()
+                      ? lds_a_bytes<KIND, T, RT, WU, WK>(K)
+                      : lds_z_bytes<KIND, T, RT, WU, WK>());
+}
+template <int KIND, typename T, int RT, int WU, int WK>
 __host__ __device__ constexpr int lds_bytes(int K) {
-    return lds_a_bytes<KIND, T, RT, WU>(K) + lds_z_bytes<KIND, T, RT, WU>() +
-           lds_zr_bytes<KIND, T, RT, WU>() + 4 * 16 * RT * 4 /* row index cache */;
+    return lds_rowc_off<KIND, T, RT, WU, WK>(K);
 }
 
-// Stage rows [row0, row0 + TM) of one K segment into the LDS A tile.
-// src row stride = width elements; seg_w = padded width; col0 = K offset.
-template <typename T, int TM>
-__device__ __forceinline__ void stage_rows(T* A, int AS, const int* rows, int nrows, const T* src,
-                                           int width, int seg_w, int col0) {
+// One K segment of the A tile: tile row r reads source row
+// seg_row(seg, row0 + r) (the zero row 0 when the list is absent), `nreal`
+// 16-byte chunks of data (row stride `width` elements), zero up to `nv`
+// chunks.  Contiguous lists need no index load at all.
+template <typename T>
+struct ASeg {
+    const T* src;
+    Seg seg;
+    int row0;
+    int col;      // first chunk of the segment in the tile row
+    int nv;       // chunks of the (padded) segment
+    int nreal;    // chunks holding data
+    int width;    // source row stride (elements)
+};
+
+template <typename T>
+__device__ __forceinline__ int aseg_row(const ASeg<T>& s, int r) {
+    return s.seg.kind == S_NONE ? 0 : seg_row(s.seg, s.row0 + r);
+}
+
+// Stage the A tile [TM rows][nseg segments] with up to 8 outstanding 16-byte
+// loads per thread.
+template <typename T, int TM, int NT, int NSEG>
+__device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSEG], int nrows, int tid) {
     constexpr int V = Elem<T>::VEC;
-    const int nv = seg_w / V;              // 16-byte chunks per row (padded)
-    const int nreal = width / V;           // chunks holding data (width % V == 0)
-    for (int it = threadIdx.x; it < TM * nv; it += blockDim.x) {
-        const int r = it / nv, c = it % nv;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (r < nrows && c < nreal) {
-            const int row = rows[r];
-            val = *reinterpret_cast<const uint4*>(src + (size_t)row * width + c * V);
+    int nvt = 0;
+#pragma unroll
+    for (int s = 0; s < NSEG; ++s) nvt += sg[s].nv;
+    const int total = TM * nvt;
+    for (int base = 0; base < total; base += NT * 8) {
+        uint4 val[8];
+        int dst[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int it = base + i * NT + tid;
+            val[i] = make_uint4(0, 0, 0, 0);
+            dst[i] = -1;
+            if (it < total) {
+                const int r = it / nvt;
+                int c = it - r * nvt;
+#pragma unroll
+                for (int s = 0; s < NSEG; ++s) {
+                    if (c >= 0 && c < sg[s].nv) {
+                        if (r < nrows && c < sg[s].nreal)
+                            val[i] = *reinterpret_cast<const uint4*>(sg[s].src + (size_t)aseg_row(sg[s], r) * sg[s].width +
+                                                                     c * V);
+                        dst[i] = r * AS + (sg[s].col + c) * V;
+                    }
+                    c -= sg[s].nv;
+                }
+            }
         }
-        *reinterpret_cast<uint4*>(A + r * AS + col0 + c * V) = val;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (dst[i] >= 0) *reinterpret_cast<uint4*>(A + dst[i]) = val[i];
     }
 }
 
 // Child sum of h rows for child-sum internal nodes: A[r][k] = sum_children h[k].
-template <typename T, int TM>
-__device__ __forceinline__ void stage_child_sum(T* A, int AS, const BatchArgs& a, int row0, int nrows) {
+template <typename T, int TM, int NT>
+__device__ __forceinline__ void stage_child_sum(T* A, int AS, const BatchArgs& a, int row0, int nrows, int tid) {
     constexpr int V = Elem<T>::VEC;
     const T* h = reinterpret_cast<const T*>(a.arena_h);
     const int nv = a.Hk / V, nreal = a.H / V;
-    for (int it = threadIdx.x; it < TM * nv; it += blockDim.x) {
+    for (int it = tid; it < TM * nv; it += NT) {
         const int r = it / nv, c = it % nv;
         float acc[V];
 #pragma unroll
         for (int i = 0; i < V; ++i) acc[i] = 0.f;
         if (r < nrows && c < nreal) {
             const int e0 = a.rag_ptr[row0 + r], e1 = a.rag_ptr[row0 + r + 1];
-            for (int e = e0; e < e1; ++e) {
-                const int row = seg_row(a.rag, e);
-                uint4 raw = *reinterpret_cast<const uint4*>(h + (size_t)row * a.H + c * V);
+            int e = e0;
+            for (; e + 4 <= e1; e += 4) {
+                uint4 raw[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    raw[q] = *reinterpret_cast<const uint4*>(h + (size_t)seg_row(a.rag, e + q) * a.H + c * V);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const T* pv = reinterpret_cast<const T*>(&raw[q]);
+#pragma unroll
+                    for (int i = 0; i < V; ++i) acc[i] += to_f(pv[i]);
+                }
+            }
+            for (; e < e1; ++e) {
+                uint4 raw = *reinterpret_cast<const uint4*>(h + (size_t)seg_row(a.rag, e) * a.H + c * V);
                 const T* pv = reinterpret_cast<const T*>(&raw);
 #pragma unroll
                 for (int i = 0; i < V; ++i) acc[i] += to_f(pv[i]);
@@ -169,112 +236,175 @@ __device__ __forceinline__ void stage_child_sum(T* A, int AS, const BatchArgs& a
     }
 }
 
-// GEMM of one wave: acc[g][rt] += A[rt*16 .. +16][kg range] * Wp[ub][g][kg range].
+// MFMA on one (gate, row-block) accumulator for one k-group.
 template <typename T, int G, int RT>
-__device__ __forceinline__ void wave_gemm(v4f (&acc)[G][RT], const T* A, int AS, const T* Wp, int nkg,
-                                          int ub, int kg0, int kg1, int lane) {
-    constexpr int KG = Elem<T>::KG;
-    const int arow = lane & 15, aq = lane >> 4;
-    // each (ub, g, kg) chunk is 64 lanes x 16 bytes
-    const uint4* B = reinterpret_cast<const uint4*>(Wp) + ((size_t)ub * G * nkg) * 64 + lane;
-    for (int kg = kg0; kg < kg1; ++kg) {
-        uint4 av[RT], bv[G];
+__device__ __forceinline__ void kgroup_mma(v4f (&acc)[G][RT], const uint4 (&av)[RT], const uint4 (&bv)[G]) {
+    if constexpr (sizeof(T) == 4) {
 #pragma unroll
-        for (int g = 0; g < G; ++g) bv[g] = B[((size_t)g * nkg + kg) * 64];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-            av[rt] = *reinterpret_cast<const uint4*>(A + (rt * 16 + arow) * AS + kg * KG + aq * (KG / 4));
-        if constexpr (sizeof(T) == 4) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int g = 0; g < G; ++g)
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) {
-                        const float a_ = __uint_as_float((&av[rt].x)[j]);
-                        const float b_ = __uint_as_float((&bv[g].x)[j]);
-                        acc[g][rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_, b_, acc[g][rt], 0, 0, 0);
-                    }
-        } else {
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt) {
-                    v8bf a_ = __builtin_bit_cast(v8bf, av[rt]);
-                    v8bf b_ = __builtin_bit_cast(v8bf, bv[g]);
-                    acc[g][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_, b_, acc[g][rt], 0, 0, 0);
+                    const float a_ = __uint_as_float((&av[rt].x)[j]);
+                    const float b_ = __uint_as_float((&bv[g].x)[j]);
+                    acc[g][rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_, b_, acc[g][rt], 0, 0, 0);
                 }
+    } else {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                v8bf a_ = __builtin_bit_cast(v8bf, av[rt]);
+                v8bf b_ = __builtin_bit_cast(v8bf, bv[g]);
+                acc[g][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_, b_, acc[g][rt], 0, 0, 0);
+            }
+    }
+}
+
+// Weight fragments of k-group kg for all gates (B points at this lane's
+// (ub, gate 0, k-group 0) chunk).
+template <int G>
+__device__ __forceinline__ void load_b(uint4 (&bv)[G], const uint4* B, int nkg, int kg) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) bv[g] = B[((size_t)g * nkg + kg) * 64];
+}
+
+// Weight prefetch ring: PD k-groups of fragments in flight.
+template <int G> constexpr int ring_depth() { return G >= 5 ? 3 : 4; }
+template <int G, int PD>
+struct BRing {
+    uint4 b[PD][G];
+};
+
+template <int G, int PD>
+__device__ __forceinline__ void ring_prologue(BRing<G, PD>& r, const uint4* B, int nkg, int kg0, int kg1) {
+#pragma unroll
+    for (int s = 0; s < PD; ++s)
+        if (kg0 + s < kg1) load_b<G>(r.b[s], B, nkg, kg0 + s);
+}
+
+// GEMM of one wave over k-groups [kg0, kg1): acc[g][rt] += A[rt*16 .. +16] * W[ub][g].
+// The ring holds k-groups kg0 .. kg0+PD-1 on entry (ring_prologue); each step
+// refills the slot it consumed with the k-group PD steps ahead.
+template <typename T, int G, int RT, int PD>
+__device__ __forceinline__ void wave_gemm(v4f (&acc)[G][RT], const T* A, int AS, const uint4* B, int nkg,
+                                          int kg0, int kg1, int lane, BRing<G, PD>& ring) {
+    constexpr int KG = Elem<T>::KG;
+    const int arow = lane & 15, aq = lane >> 4;
+    for (int kg = kg0; kg < kg1; kg += PD) {
+#pragma unroll
+        for (int s = 0; s < PD; ++s) {
+            const int k = kg + s;
+            if (k < kg1) {
+                uint4 av[RT];
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+                    av[rt] = *reinterpret_cast<const uint4*>(A + (rt * 16 + arow) * AS + k * KG + aq * (KG / 4));
+                kgroup_mma<T, G, RT>(acc, av, ring.b[s]);
+                if (k + PD < kg1) load_b<G>(ring.b[s], B, nkg, k + PD);
+            }
         }
     }
 }
 
-template <int KIND, typename T, int RT, int WU>
-__global__ __launch_bounds__(256) void cell_kernel(BatchArgs a) {
+// No inter-tile synchronisation (one launch per batch: kernel boundaries order
+// producers before consumers).
+struct NoSync {
+    __device__ __forceinline__ void wait() const {}
+    __device__ __forceinline__ void signal() const {}
+};
+
+// One tile: rows [16*RT*rtile, +16*RT) x units [16*WU*ut, +16*WU) of a batch,
+// all gates.  sync.wait() runs after the weight and descriptor loads and
+// before the first read of a producer's output; sync.signal() after the
+// tile's h and c stores.
+template <int KIND, typename T, int RT, int WU, int WK, typename Sync>
+__device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut, char* smem, const Sync& sync) {
     using KT = Kind<KIND>;
     constexpr int G = KT::G;
-    constexpr int TM = 16 * RT, TU = 16 * WU, WK = 4 / WU;
+    constexpr int NT = 64 * WU * WK;
+    constexpr int TM = 16 * RT, TU = 16 * WU;
     constexpr int KG = Elem<T>::KG;
     constexpr int AS_PAD = a_pad<T>();
-    constexpr int NSEG = (KT::X ? 1 : 0) + KT::NFIX + (KT::RAG ? 1 : 0);
+    constexpr int NITEM = TM * TU;
+    constexpr int NI = (NITEM + NT - 1) / NT;     // epilogue items per thread
+    constexpr int NFX = KT::NFIX;
 
-    extern __shared__ __align__(16) char smem[];
     const int AS = a.K + AS_PAD;                           // A row stride (elements)
     T* A = reinterpret_cast<T*>(smem);
-    float* Z = reinterpret_cast<float*>(smem + lds_a_bytes<KIND, T, RT, WU>(a.K));
+    float* Z = reinterpret_cast<float*>(smem + lds_z_off<KIND, T, RT, WU, WK>(a.K));
     float* Zr = Z + WK * TM * G * TU;
-    int* rowc = reinterpret_cast<int*>(Zr + (KT::RAG ? WK * TM * TU : 0));   // [4][TM]
+    constexpr int PD = WK >= 16 ? 2 : ring_depth<G>();   // 1024-thread groups have 128 VGPRs
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nut = a.Hu / TU;
-    const int ut = blockIdx.x % nut, rtile = blockIdx.x / nut;
     const int row0 = rtile * TM, u0 = ut * TU;
     const int nrows = min(TM, a.m - row0);
-
-    // ---- 1. operand row indices of this tile (x, child 0, child 1) ----
-    if (tid < TM) {
-        const int r = tid;
-        const bool ok = r < nrows;
-        if constexpr (KT::X) rowc[0 * TM + r] = ok ? seg_row(a.x, row0 + r) : 0;
-        if constexpr (KT::NFIX >= 1) rowc[1 * TM + r] = (ok && a.fix[0].kind != S_NONE) ? seg_row(a.fix[0], row0 + r) : 0;
-        if constexpr (KT::NFIX >= 2) rowc[2 * TM + r] = (ok && a.fix[1].kind != S_NONE) ? seg_row(a.fix[1], row0 + r) : 0;
-        rowc[3 * TM + r] = ok ? seg_row(a.res, row0 + r) : 0;
-    }
-    __syncthreads();
-
-    // ---- 2. stage the A tile: [x | child h ...] or [child sum of h] ----
-    {
-        int col = 0;
-        if constexpr (KT::X) {
-            stage_rows<T, TM>(A, AS, rowc, nrows, reinterpret_cast<const T*>(a.xmat), a.E, a.Ep, col);
-            col += a.Ep;
-        }
-        const T* h = reinterpret_cast<const T*>(a.arena_h);
-        if constexpr (KT::NFIX >= 1) {
-            // an absent operand list reads the zero row 0 (rowc holds 0)
-            stage_rows<T, TM>(A, AS, rowc + TM, nrows, h, a.H, a.Hk, col);
-            col += a.Hk;
-        }
-        if constexpr (KT::NFIX >= 2) {
-            stage_rows<T, TM>(A, AS, rowc + 2 * TM, nrows, h, a.H, a.Hk, col);
-            col += a.Hk;
-        }
-        if constexpr (KIND == K_CS_INT) stage_child_sum<T, TM>(A, AS, a, row0, nrows);
-        (void)NSEG;
-    }
-    __syncthreads();
-
-    // ---- 3. gate GEMM: wave (wu, wk) -> unit block u0/16 + wu, k-groups of split wk ----
     const int wu = wave % WU, wk = wave / WU;
     const int nkg = a.K / KG;
     const int ub = u0 / 16 + wu;
+    const uint4* Bmain = reinterpret_cast<const uint4*>(a.W) + ((size_t)ub * G * nkg) * 64 + lane;
+    const int kg0 = (nkg * wk) / WK, kg1 = (nkg * (wk + 1)) / WK;
+
+    // first weight fragments: independent of everything, issued first
+    BRing<G, PD> ring;
+    ring_prologue<G, PD>(ring, Bmain, nkg, kg0, kg1);
+
+    // ---- 1. early loads: the epilogue's result rows and child cell states ----
+    // (row indices of contiguous lists are arithmetic; indexed lists cost one
+    // load, issued here in parallel with the operand and weight loads)
+    int rres[NI];
+#pragma unroll
+    for (int q = 0; q < NI; ++q) {
+        const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
+        const bool ok = it < NITEM && r < nrows && j < a.H;
+        rres[q] = ok ? seg_row(a.res, row0 + r) : 0;
+    }
+    sync.wait();   // producers of this tile's operand rows have finished
+    float cpre[NI][NFX > 0 ? NFX : 1];
+#pragma unroll
+    for (int q = 0; q < NI; ++q) {
+        const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
+        const bool ok = it < NITEM && r < nrows && j < a.H;
+#pragma unroll
+        for (int p = 0; p < (NFX > 0 ? NFX : 1); ++p) {
+            cpre[q][p] = 0.f;
+            if (NFX > p && ok && a.fix[p].kind != S_NONE)
+                cpre[q][p] = a.arena_c[(size_t)seg_row(a.fix[p], row0 + r) * a.H + j];
+        }
+    }
+
+    // ---- 3. stage the A tile: [x | child h ...] or [child sum of h] ----
+    if constexpr (KIND == K_CS_INT) {
+        stage_child_sum<T, TM, NT>(A, AS, a, row0, nrows, tid);
+    } else {
+        constexpr int NSEG = (KT::X ? 1 : 0) + NFX;
+        constexpr int V = Elem<T>::VEC;
+        ASeg<T> sg[NSEG];
+        int s = 0, col = 0;
+        if constexpr (KT::X) {
+            sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.xmat), a.x, row0, 0, a.Ep / V, a.E / V, a.E};
+            col += a.Ep / V;
+        }
+#pragma unroll
+        for (int p = 0; p < NFX; ++p) {
+            // an absent operand list reads the zero row 0
+            sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.fix[p], row0, col, a.Hk / V, a.H / V, a.H};
+            col += a.Hk / V;
+        }
+        stage_tile<T, TM, NT, NSEG>(A, AS, sg, nrows, tid);
+    }
+    __syncthreads();
+
+    // ---- 4. gate GEMM: wave (wu, wk) -> unit block ub, k-groups [kg0, kg1) ----
     {
         v4f acc[G][RT];
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) acc[g][rt] = v4f{0.f, 0.f, 0.f, 0.f};
-        const int kg0 = (nkg * wk) / WK, kg1 = (nkg * (wk + 1)) / WK;
-        wave_gemm<T, G, RT>(acc, A, AS, reinterpret_cast<const T*>(a.W), nkg, ub, kg0, kg1, lane);
+        if (kg0 < kg1) wave_gemm<T, G, RT, PD>(acc, A, AS, Bmain, nkg, kg0, kg1, lane, ring);
+        if constexpr (!KT::RAG) __syncthreads();   // Z aliases A: all waves done reading A
         // partial sums -> Z[wk][row][g][unit]
 #pragma unroll
         for (int g = 0; g < G; ++g)
@@ -289,12 +419,12 @@ __global__ __launch_bounds__(256) void cell_kernel(BatchArgs a) {
     }
     __syncthreads();
 
-    // ---- 4. per-item epilogue state; items (r, u) owned by fixed threads ----
-    constexpr int NI = TM * TU / 256;
+    // ---- 5. per-item gate pre-activations (fixed-order sum over the K split) ----
     float zsum[NI][G];
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
-        const int it = tid + 256 * q, r = it / TU, u = it % TU;
+        const int it = tid + NT * q;
+        const int r = (it < NITEM ? it : 0) / TU, u = (it < NITEM ? it : 0) % TU;
         const int j = u0 + u;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -305,7 +435,7 @@ __global__ __launch_bounds__(256) void cell_kernel(BatchArgs a) {
         }
     }
 
-    // ---- 5. ragged phase: per-child GEMM (child-sum U_f, lattice W_lc) ----
+    // ---- 6. ragged phase: per-child GEMM (child-sum U_f, lattice W_lc) ----
     float racc[NI], rden[NI];
 #pragma unroll
     for (int q = 0; q < NI; ++q) { racc[q] = 0.f; rden[q] = 0.f; }
@@ -313,28 +443,32 @@ __global__ __launch_bounds__(256) void cell_kernel(BatchArgs a) {
         const int cbeg = a.rag_ptr[row0];
         const int cend = a.rag_ptr[row0 + nrows];
         const int nkgr = a.Hk / KG;
-        const T* Rsrc = KIND == K_CS_INT ? reinterpret_cast<const T*>(a.arena_h) : nullptr;
+        const uint4* Brag = reinterpret_cast<const uint4*>(a.Wr) + ((size_t)ub * nkgr) * 64 + lane;
+        const int rk0 = (nkgr * wk) / WK, rk1 = (nkgr * (wk + 1)) / WK;
+        const int RS = a.Hk + AS_PAD;
         for (int cb = cbeg; cb < cend; cb += TM) {
             const int cn = min(TM, cend - cb);
             __syncthreads();   // previous chunk's readers of A / Zr are done
-            if (tid < TM) rowc[tid] = tid < cn ? seg_row(a.rag, cb + tid) : 0;
-            __syncthreads();
+            BRing<1, 4> rring;
+            ring_prologue<1, 4>(rring, Brag, nkgr, rk0, rk1);
             if constexpr (KIND == K_CS_INT) {
-                stage_rows<T, TM>(A, a.Hk + AS_PAD, rowc, cn, Rsrc, a.H, a.Hk, 0);
+                constexpr int V = Elem<T>::VEC;
+                ASeg<T> sg[1] = {ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.rag, cb, 0, a.Hk / V, a.H / V, a.H}};
+                stage_tile<T, TM, NT, 1>(A, RS, sg, cn, tid);
             } else {
                 // lattice: the word cell states c_w (fp32) converted to T
                 constexpr int V = Elem<T>::VEC;
                 const int nv = a.Hk / V, nreal = a.H / V;
-                for (int it = tid; it < TM * nv; it += 256) {
+                for (int it = tid; it < TM * nv; it += NT) {
                     const int r = it / nv, c = it % nv;
                     uint4 out = make_uint4(0, 0, 0, 0);
                     T* po = reinterpret_cast<T*>(&out);
                     if (r < cn && c < nreal) {
-                        const float* src = a.arena_c + (size_t)rowc[r] * a.H + c * V;
+                        const float* src = a.arena_c + (size_t)seg_row(a.rag, cb + r) * a.H + c * V;
 #pragma unroll
                         for (int i = 0; i < V; ++i) po[i] = from_f<T>(src[i]);
                     }
-                    *reinterpret_cast<uint4*>(A + r * (a.Hk + AS_PAD) + c * V) = out;
+                    *reinterpret_cast<uint4*>(A + r * RS + c * V) = out;
                 }
             }
             __syncthreads();
@@ -342,9 +476,7 @@ __global__ __launch_bounds__(256) void cell_kernel(BatchArgs a) {
                 v4f acc[1][RT];
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt) acc[0][rt] = v4f{0.f, 0.f, 0.f, 0.f};
-                const int kg0 = (nkgr * wk) / WK, kg1 = (nkgr * (wk + 1)) / WK;
-                wave_gemm<T, 1, RT>(acc, A, a.Hk + AS_PAD, reinterpret_cast<const T*>(a.Wr), nkgr, ub,
-                                    kg0, kg1, lane);
+                if (rk0 < rk1) wave_gemm<T, 1, RT, 4>(acc, A, RS, Brag, nkgr, rk0, rk1, lane, rring);
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -357,15 +489,15 @@ __global__ __launch_bounds__(256) void cell_kernel(BatchArgs a) {
             __syncthreads();
 #pragma unroll
             for (int q = 0; q < NI; ++q) {
-                const int it = tid + 256 * q, r = it / TU, u = it % TU;
+                const int it = tid + NT * q, r = it / TU, u = it % TU;
                 const int j = u0 + u;
-                if (r < nrows && j < a.H) {
+                if (it < NITEM && r < nrows && j < a.H) {
                     const int e0 = max(a.rag_ptr[row0 + r], cb), e1 = min(a.rag_ptr[row0 + r + 1], cb + cn);
                     for (int e = e0; e < e1; ++e) {
                         float s = a.br[j];
 #pragma unroll
                         for (int w = 0; w < WK; ++w) s += Zr[(w * TM + (e - cb)) * TU + u];
-                        const float cw = a.arena_c[(size_t)rowc[e - cb] * a.H + j];
+                        const float cw = a.arena_c[(size_t)seg_row(a.rag, e) * a.H + j];
                         if constexpr (KIND == K_CS_INT) {
                             racc[q] += sigm(s) * cw;           // f_k * c_k
                         } else {
@@ -380,73 +512,237 @@ __global__ __launch_bounds__(256) void cell_kernel(BatchArgs a) {
         }
     }
 
-    // ---- 6. gate epilogue and scatter of h, c ----
+    // ---- 7. gate epilogue and scatter of h, c ----
     T* Hout = reinterpret_cast<T*>(a.arena_h);
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
-        const int it = tid + 256 * q, r = it / TU, u = it % TU;
+        const int it = tid + NT * q, r = it / TU, u = it % TU;
         const int j = u0 + u;
-        if (r >= nrows || j >= a.H) continue;
+        if (it >= NITEM || r >= nrows || j >= a.H) continue;
         const float* z = zsum[q];
         float c, h;
         if constexpr (KIND == K_CHAIN) {
-            const float cp = a.fix[0].kind != S_NONE ? a.arena_c[(size_t)rowc[TM + r] * a.H + j] : 0.f;
-            c = sigm(z[1]) * cp + sigm(z[0]) * tanh_f(z[2]);
+            c = sigm(z[1]) * cpre[q][0] + sigm(z[0]) * tanh_f(z[2]);
             h = sigm(z[3]) * tanh_f(c);
         } else if constexpr (KIND == K_NARY_LEAF || KIND == K_CS_LEAF) {
             c = sigm(z[0]) * tanh_f(z[2]);
             h = sigm(z[1]) * tanh_f(c);
         } else if constexpr (KIND == K_NARY_INT || KIND == K_GRID) {
-            const float c0 = a.fix[0].kind != S_NONE ? a.arena_c[(size_t)rowc[TM + r] * a.H + j] : 0.f;
-            const float c1 = a.fix[1].kind != S_NONE ? a.arena_c[(size_t)rowc[2 * TM + r] * a.H + j] : 0.f;
-            c = sigm(z[0]) * tanh_f(z[4]) + sigm(z[1]) * c0 + sigm(z[2]) * c1;
+            c = sigm(z[0]) * tanh_f(z[4]) + sigm(z[1]) * cpre[q][0] + sigm(z[2]) * cpre[q][1];
             h = sigm(z[3]) * tanh_f(c);
         } else if constexpr (KIND == K_CS_INT) {
             c = sigm(z[0]) * tanh_f(z[2]) + racc[q];
             h = sigm(z[1]) * tanh_f(c);
         } else if constexpr (KIND == K_LAT_WORD) {
-            const float cb = a.fix[0].kind != S_NONE ? a.arena_c[(size_t)rowc[TM + r] * a.H + j] : 0.f;
-            c = sigm(z[1]) * cb + sigm(z[0]) * tanh_f(z[2]);
+            c = sigm(z[1]) * cpre[q][0] + sigm(z[0]) * tanh_f(z[2]);
             h = 0.f;
         } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
             const int nw = a.rag_ptr[row0 + r + 1] - a.rag_ptr[row0 + r];
             if (nw == 0) {
-                const float cp = a.fix[0].kind != S_NONE ? a.arena_c[(size_t)rowc[TM + r] * a.H + j] : 0.f;
-                c = sigm(z[1]) * cp + sigm(z[0]) * tanh_f(z[3]);
+                c = sigm(z[1]) * cpre[q][0] + sigm(z[0]) * tanh_f(z[3]);
             } else {
                 const float e0 = __expf(sigm(z[0]));
                 c = (e0 * tanh_f(z[3]) + racc[q]) / (e0 + rden[q]);
             }
             h = sigm(z[2]) * tanh_f(c);
         }
-        const size_t o = (size_t)rowc[3 * TM + r] * a.H + j;
+        const size_t o = (size_t)rres[q] * a.H + j;
         a.arena_c[o] = c;
         Hout[o] = from_f<T>(h);
+    }
+    sync.signal();
+}
+
+// One launch per batch: work-group -> (row tile, unit tile).
+template <int KIND, typename T, int RT, int WU, int WK>
+__global__ __launch_bounds__(64 * WU * WK) void cell_kernel(BatchArgs a) {
+    extern __shared__ __align__(16) char smem[];
+    const int nut = a.Hu / (16 * WU);
+    cell_tile<KIND, T, RT, WU, WK>(a, blockIdx.x / nut, blockIdx.x % nut, smem, NoSync{});
+}
+
+// ---------------------------------------------------------------------------
+// Dataflow launch: one persistent launch runs a run of consecutive batches.
+// Tiles (batch, row tile, unit tile) are claimed from a global ticket in
+// schedule order; a tile waits only for the row tiles that produce its own
+// operand rows (every unit tile of each such row tile has signalled), so
+// tiles of successive batches overlap.  A claimed tile waits only on tiles
+// with smaller tickets, which are held by running work-groups or finished, so
+// the launch always drains.  Waits are bounded in time: past `spin_us` the
+// tile sets the error flag and proceeds, and every later ticket exits at once.
+
+// Pointer-free description of one batch, resident in device memory.
+struct BatchDesc {
+    int kind, type, m, H, Hk, Hu, E, Ep, K;
+    int x_staged;                 // x rows come from the staged buffer
+    int seg_kind[5];              // x, child 0, child 1, ragged, result
+    int seg_base[5];
+    int seg_off[5];               // offset of the index list in the int buffer, -1 if none
+    int rptr_off;                 // ragged row offsets, -1 if none
+    int off_b, off_Wr, off_br;    // byte offsets inside the type's packed weights
+};
+
+constexpr int FLOW_MAX_TYPES = 16;
+
+struct FlowArgs {
+    const int* ibuf;              // descriptor ints
+    const BatchDesc* desc;        // per batch of the run
+    const int4* tiles;            // {batch, row tile, unit tile, row-tile id}
+    const int2* rt_deps;          // per row-tile id: {first dependency, count}
+    const int* deps;              // producer row-tile ids
+    int* ticket;
+    int* error;
+    int* done;                    // per row-tile id: unit tiles finished
+    int n_tiles, need, spin_us;   // spin_us: bound of one tile's wait, microseconds
+    const void* x;
+    const void* xstaged;
+    void* arena_h;
+    float* arena_c;
+    const void* w[FLOW_MAX_TYPES];
+};
+
+__device__ __forceinline__ Seg desc_seg(const BatchDesc& d, const int* ibuf, int i) {
+    return Seg{d.seg_kind[i], d.seg_base[i], d.seg_off[i] >= 0 ? ibuf + d.seg_off[i] : nullptr};
+}
+
+__device__ __forceinline__ BatchArgs resolve(const BatchDesc& d, const FlowArgs& f) {
+    BatchArgs a;
+    a.kind = d.kind;
+    a.m = d.m;
+    a.H = d.H;
+    a.Hk = d.Hk;
+    a.Hu = d.Hu;
+    a.E = d.E;
+    a.Ep = d.Ep;
+    a.K = d.K;
+    a.x = desc_seg(d, f.ibuf, 0);
+    a.fix[0] = desc_seg(d, f.ibuf, 1);
+    a.fix[1] = desc_seg(d, f.ibuf, 2);
+    a.rag = desc_seg(d, f.ibuf, 3);
+    a.res = desc_seg(d, f.ibuf, 4);
+    a.rag_ptr = d.rptr_off >= 0 ? f.ibuf + d.rptr_off : nullptr;
+    a.xmat = d.x_staged ? f.xstaged : f.x;
+    const uint8_t* wb = reinterpret_cast<const uint8_t*>(f.w[d.type]);
+    a.W = wb;
+    a.bias = reinterpret_cast<const float*>(wb + d.off_b);
+    a.Wr = wb + d.off_Wr;
+    a.br = reinterpret_cast<const float*>(wb + d.off_br);
+    a.arena_h = f.arena_h;
+    a.arena_c = f.arena_c;
+    return a;
+}
+
+struct FlowSync {
+    const int2* rt_deps;
+    const int* deps;
+    int* done;
+    int* error;
+    int rt, need, spin_us;
+
+    // Thread 0 polls each producer row tile with relaxed atomic loads (coherent
+    // across XCDs, no cache maintenance per poll), then issues one acquire
+    // fence (agent scope) so that the operand rows read after the barrier are
+    // the producers' values.  The wait is bounded in real time: past
+    // `spin_us` microseconds (s_memrealtime runs at 100 MHz) it sets the
+    // error flag and proceeds; a set error flag ends every other wait.
+    __device__ __forceinline__ void wait() const {
+        if (threadIdx.x == 0) {
+            const int2 di = rt_deps[rt];
+            if (di.y > 0) {
+                const unsigned long long t0 = wall_clock64();
+                const unsigned long long lim = (unsigned long long)spin_us * 100ull;
+                bool stop = false;
+                for (int k = 0; k < di.y && !stop; ++k) {
+                    const int* c = done + deps[di.x + k];
+                    int n = 0;
+                    while (__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need) {
+                        __builtin_amdgcn_s_sleep(2);
+                        if (wall_clock64() - t0 > lim) {
+                            __hip_atomic_store(error, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            stop = true;
+                            break;
+                        }
+                        if ((++n & 63) == 0 && __hip_atomic_load(error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                            stop = true;
+                            break;
+                        }
+                    }
+                }
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            }
+        }
+        __syncthreads();
+    }
+    // Every wave waits for its own h and c stores, then thread 0 publishes
+    // the tile with a release increment (agent scope).
+    __device__ __forceinline__ void signal() const {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0) __hip_atomic_fetch_add(done + rt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+};
+
+// Tile shape of dataflow launches: 16 rows x 16 units, 4 waves splitting K.
+constexpr int FLOW_RT = 1, FLOW_WU = 1, FLOW_WK = 4;
+
+template <typename T>
+__global__ __launch_bounds__(256) void flow_kernel(FlowArgs f) {
+    extern __shared__ __align__(16) char smem[];
+    __shared__ int s_ticket;
+    for (;;) {
+        if (threadIdx.x == 0) {
+            int t = __hip_atomic_fetch_add(f.ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__hip_atomic_load(f.error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) t = f.n_tiles;
+            s_ticket = t;
+        }
+        __syncthreads();
+        const int t = s_ticket;
+        if (t >= f.n_tiles) break;
+        const int4 tl = f.tiles[t];
+        const BatchArgs a = resolve(f.desc[tl.x], f);
+        const FlowSync sync{f.rt_deps, f.deps, f.done, f.error, tl.w, f.need, f.spin_us};
+        // every tile body contains barriers, so s_ticket is not rewritten
+        // before all threads have read it
+        switch (a.kind) {
+            case K_CHAIN: cell_tile<K_CHAIN, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_NARY_LEAF: cell_tile<K_NARY_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_NARY_INT: cell_tile<K_NARY_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_GRID: cell_tile<K_GRID, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_CS_LEAF: cell_tile<K_CS_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_CS_INT: cell_tile<K_CS_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_LAT_CHAR: cell_tile<K_LAT_CHAR, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            default: cell_tile<K_LAT_WORD, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+        }
     }
 }
 
 // x staging (the input rows of every batch made contiguous in batch order)
-// and clearing of the arena's zero row and pad rows.
+// and clearing of the arena's zero row and pad rows.  Each work-group handles
+// 4 rows with one wave per row.
 //   rows [0, n_x): xs[i] = x[src[i]]          (row length E elements of T)
 //   rows [n_x, n_x + n_zero): arena row zrow[i] of h and c set to zero
+//   work-group 0 also clears the `nint` dataflow counters at `ints`
 template <typename T>
 __global__ __launch_bounds__(256) void stage_kernel(const T* __restrict__ x, T* __restrict__ xs,
                                                     const int* __restrict__ src, int n_x, int E,
                                                     const int* __restrict__ zrow, int n_zero,
                                                     T* __restrict__ arena_h, float* __restrict__ arena_c,
-                                                    int H) {
+                                                    int H, int* __restrict__ ints, int nint) {
     constexpr int V = Elem<T>::VEC;
-    const int row = blockIdx.x;
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < nint; i += blockDim.x) ints[i] = 0;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
     if (row < n_x) {
         const uint4* s = reinterpret_cast<const uint4*>(x + (size_t)src[row] * E);
         uint4* d = reinterpret_cast<uint4*>(xs + (size_t)row * E);
-        for (int c = threadIdx.x; c < E / V; c += blockDim.x) d[c] = s[c];
+        for (int c = lane; c < E / V; c += 64) d[c] = s[c];
     } else if (row < n_x + n_zero) {
         const int z = zrow[row - n_x];
         uint4* dh = reinterpret_cast<uint4*>(arena_h + (size_t)z * H);
-        for (int c = threadIdx.x; c < H / V; c += blockDim.x) dh[c] = make_uint4(0, 0, 0, 0);
+        for (int c = lane; c < H / V; c += 64) dh[c] = make_uint4(0, 0, 0, 0);
         float4* dc = reinterpret_cast<float4*>(arena_c + (size_t)z * H);
-        for (int c = threadIdx.x; c < H / 4; c += blockDim.x) dc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int c = lane; c < H / 4; c += 64) dc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
 }
 

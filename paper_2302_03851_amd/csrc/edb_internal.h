@@ -13,6 +13,9 @@ struct edb_graph {
     std::vector<int64_t> child_ptr;
     std::vector<int32_t> child_idx;
     std::vector<int32_t> x_row;
+    // consumers over present edges (CSR) and present-child counts, built once
+    // during ingest and reused by every schedule
+    std::vector<int32_t> cons_ptr, cons, pending;
 };
 
 struct edb_schedule {

@@ -59,17 +59,26 @@ extern "C" edb_status edb_build_graph(int32_t n_nodes, int32_t n_types, const in
         g->child_ptr.assign(child_ptr, child_ptr + n_nodes + 1);
         g->child_idx.assign(child_idx, child_idx + E);
         g->x_row.assign(x_row, x_row + n_nodes);
-        // Kahn's algorithm over present edges: the graph must be acyclic.
-        std::vector<int32_t> pending(n_nodes, 0), cons_ptr(n_nodes + 1, 0), cons, stack;
+        // consumers CSR over present edges, then Kahn's algorithm: the graph
+        // must be acyclic
+        std::vector<int32_t>& pend0 = g->pending;
+        std::vector<int32_t>& cons_ptr = g->cons_ptr;
+        std::vector<int32_t>& cons = g->cons;
+        pend0.assign(n_nodes, 0);
+        cons_ptr.assign(n_nodes + 1, 0);
         for (int32_t v = 0; v < n_nodes; ++v)
             for (int64_t e = child_ptr[v]; e < child_ptr[v + 1]; ++e)
-                if (child_idx[e] >= 0) { ++pending[v]; ++cons_ptr[child_idx[e] + 1]; }
+                if (child_idx[e] >= 0) { ++pend0[v]; ++cons_ptr[child_idx[e] + 1]; }
         for (int32_t v = 0; v < n_nodes; ++v) cons_ptr[v + 1] += cons_ptr[v];
         cons.resize(cons_ptr[n_nodes]);
-        std::vector<int32_t> fill(cons_ptr.begin(), cons_ptr.end() - 1);
-        for (int32_t v = 0; v < n_nodes; ++v)
-            for (int64_t e = child_ptr[v]; e < child_ptr[v + 1]; ++e)
-                if (child_idx[e] >= 0) cons[fill[child_idx[e]]++] = v;
+        {
+            std::vector<int32_t> fill(cons_ptr.begin(), cons_ptr.end() - 1);
+            for (int32_t v = 0; v < n_nodes; ++v)
+                for (int64_t e = child_ptr[v]; e < child_ptr[v + 1]; ++e)
+                    if (child_idx[e] >= 0) cons[fill[child_idx[e]]++] = v;
+        }
+        std::vector<int32_t> pending(pend0), stack;
+        stack.reserve(n_nodes);
         for (int32_t v = 0; v < n_nodes; ++v) if (pending[v] == 0) stack.push_back(v);
         int32_t seen = 0;
         while (!stack.empty()) {

@@ -15,7 +15,9 @@
 //       list order, so the list becomes contiguous;
 //     otherwise unset entries take the next slots and absent entries read
 //       the zero row (slot 0).
-// Slot 0 is the zero row.  x rows are numbered in (batch, row) order.
+// Every slot a batch reads or writes is final once the batch is processed,
+// so its descriptors are emitted in the same pass.  Slot 0 is the zero row.
+// x rows are numbered in (batch, row) order.
 #include <algorithm>
 #include <new>
 #include <string>
@@ -30,6 +32,32 @@ bool consecutive(const int32_t* s, int64_t n) {
     for (int64_t i = 0; i + 1 < n; ++i)
         if (s[i + 1] != s[i] + 1) return false;
     return true;
+}
+
+// Sort (key, value) pairs by their non-negative, distinct keys: LSD radix
+// sort with 11-bit digits (a comparison sort for short lists).
+void sort_by_key(std::vector<std::pair<int32_t, int32_t>>& a, std::vector<std::pair<int32_t, int32_t>>& tmp) {
+    const size_t n = a.size();
+    if (n < 64) {
+        std::sort(a.begin(), a.end());
+        return;
+    }
+    uint32_t maxk = 0;
+    for (const auto& x : a) maxk = std::max(maxk, (uint32_t)x.first);
+    tmp.resize(n);
+    uint32_t count[2048];
+    for (int shift = 0; shift < 32 && (maxk >> shift) != 0; shift += 11) {
+        std::fill(count, count + 2048, 0u);
+        for (const auto& x : a) ++count[((uint32_t)x.first >> shift) & 2047u];
+        uint32_t sum = 0;
+        for (uint32_t& c : count) {
+            const uint32_t t = c;
+            c = sum;
+            sum += t;
+        }
+        for (const auto& x : a) tmp[count[((uint32_t)x.first >> shift) & 2047u]++] = x;
+        a.swap(tmp);
+    }
 }
 }  // namespace
 
@@ -59,99 +87,138 @@ extern "C" edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t
     if (!p) return fail(EDB_ERR_OOM, "edb_plan_memory: out of host memory");
     try {
         const int32_t B = (int32_t)s->batch_type.size();
+        const int32_t* bptr = s->batch_ptr.data();
         p->V = V;
         p->B = B;
         p->mode = flags;
         p->shapes.assign(shapes, shapes + T);
         p->slot.assign(V, UNSET);
         p->order.assign(s->batch_nodes.begin(), s->batch_nodes.end());
-        std::vector<int32_t>& slot = p->slot;
-        // per batch, per list, per entry: the pad slot of an absent entry (fresh lists)
-        std::vector<std::vector<std::vector<int32_t>>> pad_of(B);
-        std::vector<std::vector<std::vector<int32_t>>> lists(B);
-        std::vector<std::vector<int32_t>> rptr(B);
+        int32_t* slot = p->slot.data();
 
-        auto build_lists = [&](int32_t b) {
-            const int32_t t = s->batch_type[b];
-            const edb_operand_shape& sh = shapes[t];
-            const int32_t* ord = p->order.data() + s->batch_ptr[b];
-            const int32_t m = s->batch_ptr[b + 1] - s->batch_ptr[b];
-            auto& L = lists[b];
-            L.assign(sh.n_fixed + (sh.ragged ? 1 : 0), {});
-            for (int32_t q = 0; q < sh.n_fixed; ++q) {
-                L[q].resize(m);
-                for (int32_t r = 0; r < m; ++r) L[q][r] = g->child_idx[g->child_ptr[ord[r]] + q];
-            }
+        // layout of the descriptors, in ascending batch order:
+        // segs: [result, positional lists..., ragged list] per batch
+        // idx_pool: the slot list of every non-empty segment, same order
+        // ragged_pool: m+1 row offsets per ragged batch
+        std::vector<int64_t> idx_off(B + 1, 0), rag_off(B, -1);
+        p->seg_ptr.assign(B + 1, 0);
+        int64_t rag_total = 0;
+        for (int32_t b = 0; b < B; ++b) {
+            const edb_operand_shape& sh = shapes[s->batch_type[b]];
+            const int32_t m = bptr[b + 1] - bptr[b];
+            int64_t n = m + (int64_t)sh.n_fixed * m;
             if (sh.ragged) {
-                auto& R = L[sh.n_fixed];
-                rptr[b].assign(1, 0);
-                for (int32_t r = 0; r < m; ++r) {
-                    const int32_t v = ord[r];
+                int64_t rc = 0;
+                for (int32_t i = bptr[b]; i < bptr[b + 1]; ++i) {
+                    const int32_t v = s->batch_nodes[i];
                     for (int64_t e = g->child_ptr[v] + sh.n_fixed; e < g->child_ptr[v + 1]; ++e)
-                        if (g->child_idx[e] >= 0) R.push_back(g->child_idx[e]);
-                    rptr[b].push_back((int32_t)R.size());
+                        rc += g->child_idx[e] >= 0;
                 }
+                n += rc;
+                rag_off[b] = rag_total;
+                rag_total += m + 1;
             }
-            pad_of[b].assign(L.size(), {});
-        };
+            idx_off[b + 1] = idx_off[b] + n;
+            p->seg_ptr[b + 1] = p->seg_ptr[b] + 1 + sh.n_fixed + (sh.ragged ? 1 : 0);
+        }
+        p->idx_pool.assign((size_t)idx_off[B], 0);
+        p->ragged_pool.assign((size_t)rag_total, 0);
+        p->ragged_off.assign(rag_off.begin(), rag_off.end());
+        p->segs.assign((size_t)p->seg_ptr[B], edb_seg{});
 
+        const bool identity = flags == EDB_PLAN_IDENTITY;
         int32_t next = 1;
-        if (flags == EDB_PLAN_IDENTITY) {
+        if (identity) {
             for (int32_t v = 0; v < V; ++v) slot[v] = v + 1;
             next = V + 1;
-            for (int32_t b = 0; b < B; ++b) build_lists(b);
-        } else {
-            std::vector<int32_t> tmp;
-            for (int32_t b = B - 1; b >= 0; --b) {
-                int32_t* ord = p->order.data() + s->batch_ptr[b];
-                const int32_t m = s->batch_ptr[b + 1] - s->batch_ptr[b];
-                std::stable_sort(ord, ord + m, [&](int32_t a, int32_t c) {
-                    const bool ua = slot[a] == UNSET, uc = slot[c] == UNSET;
-                    if (ua != uc) return !ua;
-                    return !ua && slot[a] < slot[c];
-                });
+        }
+        std::vector<int32_t> list, mark(V, -1);
+        std::vector<std::pair<int32_t, int32_t>> setnodes, sort_tmp;
+        int32_t stamp = 0;
+        for (int32_t b = B - 1; b >= 0; --b) {
+            const int32_t t = s->batch_type[b];
+            const edb_operand_shape& sh = shapes[t];
+            int32_t* ord = p->order.data() + bptr[b];
+            const int32_t m = bptr[b + 1] - bptr[b];
+            if (!identity) {
+                // stable sort by slot, unset last: set nodes by slot, then unset in id order
+                setnodes.clear();
+                int32_t nu = 0;
+                for (int32_t r = 0; r < m; ++r) {
+                    if (slot[ord[r]] != UNSET) setnodes.emplace_back(slot[ord[r]], ord[r]);
+                    else ord[nu++] = ord[r];   // compacts unset nodes to the front, order kept
+                }
+                if (!setnodes.empty()) {
+                    sort_by_key(setnodes, sort_tmp);
+                    const int32_t ns = (int32_t)setnodes.size();
+                    for (int32_t r = nu - 1; r >= 0; --r) ord[r + ns] = ord[r];
+                    for (int32_t r = 0; r < ns; ++r) ord[r] = setnodes[r].second;
+                }
                 for (int32_t r = 0; r < m; ++r)
                     if (slot[ord[r]] == UNSET) slot[ord[r]] = next++;
-                build_lists(b);
-                for (size_t li = 0; li < lists[b].size(); ++li) {
-                    const auto& L = lists[b][li];
-                    bool any = false, fresh = true;
-                    tmp.clear();
-                    for (int32_t c : L) {
-                        if (c < 0) continue;
-                        any = true;
-                        if (slot[c] != UNSET) fresh = false;
-                        tmp.push_back(c);
-                    }
-                    if (!any) continue;
-                    if (fresh) {
-                        std::sort(tmp.begin(), tmp.end());
-                        fresh = std::adjacent_find(tmp.begin(), tmp.end()) == tmp.end();
-                    }
-                    if (fresh) {
-                        auto& pads = pad_of[b][li];
-                        pads.assign(L.size(), 0);
-                        for (size_t e = 0; e < L.size(); ++e) {
-                            if (L[e] < 0) {
-                                pads[e] = next;
-                                p->pads.push_back(next);
-                            } else {
-                                slot[L[e]] = next;
-                            }
-                            ++next;
-                        }
-                    } else {
-                        for (int32_t c : L)
-                            if (c >= 0 && slot[c] == UNSET) slot[c] = next++;
+            }
+            // operand lists, in order: positional children, then the ragged list
+            int64_t off = idx_off[b] + m;
+            edb_seg* sg = p->segs.data() + p->seg_ptr[b];
+            const int nlists = sh.n_fixed + (sh.ragged ? 1 : 0);
+            for (int li = 0; li < nlists; ++li) {
+                list.clear();
+                if (li < sh.n_fixed) {
+                    for (int32_t r = 0; r < m; ++r) list.push_back(g->child_idx[g->child_ptr[ord[r]] + li]);
+                } else {
+                    int32_t* rp = p->ragged_pool.data() + rag_off[b];
+                    rp[0] = 0;
+                    for (int32_t r = 0; r < m; ++r) {
+                        const int32_t v = ord[r];
+                        for (int64_t e = g->child_ptr[v] + sh.n_fixed; e < g->child_ptr[v + 1]; ++e)
+                            if (g->child_idx[e] >= 0) list.push_back(g->child_idx[e]);
+                        rp[r + 1] = (int32_t)list.size();
                     }
                 }
+                const int64_t n = (int64_t)list.size();
+                edb_seg& q = sg[1 + li];
+                q.len = (int32_t)n;
+                bool any = false, fresh = !identity;
+                ++stamp;
+                for (int32_t c : list) {
+                    if (c < 0) continue;
+                    any = true;
+                    if (slot[c] != UNSET || mark[c] == stamp) fresh = false;
+                    mark[c] = stamp;
+                }
+                if (!any) {
+                    q.kind = EDB_SEG_NONE;
+                    q.idx_off = -1;
+                    continue;
+                }
+                int32_t* dst = p->idx_pool.data() + off;
+                if (fresh) {
+                    for (int64_t e = 0; e < n; ++e) {
+                        if (list[e] < 0) p->pads.push_back(next);
+                        else slot[list[e]] = next;
+                        dst[e] = next++;
+                    }
+                } else {
+                    for (int64_t e = 0; e < n; ++e) {
+                        const int32_t c = list[e];
+                        if (c >= 0 && slot[c] == UNSET) slot[c] = next++;
+                        dst[e] = c >= 0 ? slot[c] : 0;
+                    }
+                }
+                q.idx_off = off;
+                q.base = dst[0];
+                q.kind = (!identity && consecutive(dst, n)) ? EDB_SEG_CONTIG : EDB_SEG_GATHER;
+                off += n;
             }
+            // result list
+            int32_t* rs = p->idx_pool.data() + idx_off[b];
+            for (int32_t r = 0; r < m; ++r) rs[r] = slot[ord[r]];
+            edb_seg& res = sg[0];
+            res.idx_off = idx_off[b];
+            res.len = m;
+            res.base = m > 0 ? rs[0] : 0;
+            res.kind = (!identity && consecutive(rs, m)) ? EDB_SEG_CONTIG : EDB_SEG_SCATTER;
         }
-        for (int32_t v = 0; v < V; ++v)
-            if (slot[v] == UNSET) {
-                delete p;
-                return fail(EDB_ERR_INVALID, "edb_plan_memory: node " + std::to_string(v) + " is not scheduled");
-            }
         p->n_slots = next;
 
         // x rows in (batch, row) order
@@ -159,51 +226,7 @@ extern "C" edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t
         int32_t nx = 0;
         for (int32_t b = 0; b < B; ++b) {
             if (!shapes[s->batch_type[b]].has_x) continue;
-            for (int32_t i = s->batch_ptr[b]; i < s->batch_ptr[b + 1]; ++i) p->x_slot[p->order[i]] = nx++;
-        }
-
-        // segment descriptors: result, positional lists, ragged list
-        const bool indexed = flags == EDB_PLAN_IDENTITY;
-        p->seg_ptr.push_back(0);
-        p->ragged_off.assign(B, -1);
-        std::vector<int32_t> ss;
-        for (int32_t b = 0; b < B; ++b) {
-            const int32_t* ord = p->order.data() + s->batch_ptr[b];
-            const int32_t m = s->batch_ptr[b + 1] - s->batch_ptr[b];
-            edb_seg res{};
-            res.idx_off = (int64_t)p->idx_pool.size();
-            res.len = m;
-            for (int32_t r = 0; r < m; ++r) p->idx_pool.push_back(slot[ord[r]]);
-            const int32_t* rs = p->idx_pool.data() + res.idx_off;
-            res.kind = (!indexed && consecutive(rs, m)) ? EDB_SEG_CONTIG : EDB_SEG_SCATTER;
-            res.base = rs[0];
-            p->segs.push_back(res);
-            for (size_t li = 0; li < lists[b].size(); ++li) {
-                const auto& L = lists[b][li];
-                edb_seg sg{};
-                sg.len = (int32_t)L.size();
-                bool any = false;
-                for (int32_t c : L) any |= c >= 0;
-                if (!any) {
-                    sg.kind = EDB_SEG_NONE;
-                    sg.idx_off = -1;
-                    p->segs.push_back(sg);
-                    continue;
-                }
-                sg.idx_off = (int64_t)p->idx_pool.size();
-                const auto& pads = pad_of[b][li];
-                for (size_t e = 0; e < L.size(); ++e)
-                    p->idx_pool.push_back(L[e] >= 0 ? slot[L[e]] : (pads.empty() ? 0 : pads[e]));
-                const int32_t* q = p->idx_pool.data() + sg.idx_off;
-                sg.kind = (!indexed && consecutive(q, sg.len)) ? EDB_SEG_CONTIG : EDB_SEG_GATHER;
-                sg.base = sg.len > 0 ? q[0] : 0;
-                p->segs.push_back(sg);
-            }
-            p->seg_ptr.push_back((int32_t)p->segs.size());
-            if (!rptr[b].empty()) {
-                p->ragged_off[b] = (int64_t)p->ragged_pool.size();
-                p->ragged_pool.insert(p->ragged_pool.end(), rptr[b].begin(), rptr[b].end());
-            }
+            for (int32_t i = bptr[b]; i < bptr[b + 1]; ++i) p->x_slot[p->order[i]] = nx++;
         }
     } catch (const std::bad_alloc&) {
         delete p;

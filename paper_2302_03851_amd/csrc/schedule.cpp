@@ -21,23 +21,14 @@ using edb::fail;
 // else 1 + max depth(child) (the input operation has depth 0).
 void topo_depth(const edb_graph& g, std::vector<int64_t>& depth) {
     const int32_t V = g.V;
-    std::vector<int32_t> pending(V, 0), cons_ptr(V + 1, 0), cons, queue;
-    for (int32_t v = 0; v < V; ++v)
-        for (int64_t e = g.child_ptr[v]; e < g.child_ptr[v + 1]; ++e)
-            if (g.child_idx[e] >= 0) { ++pending[v]; ++cons_ptr[g.child_idx[e] + 1]; }
-    for (int32_t v = 0; v < V; ++v) cons_ptr[v + 1] += cons_ptr[v];
-    cons.resize(cons_ptr[V]);
-    std::vector<int32_t> fill(cons_ptr.begin(), cons_ptr.end() - 1);
-    for (int32_t v = 0; v < V; ++v)
-        for (int64_t e = g.child_ptr[v]; e < g.child_ptr[v + 1]; ++e)
-            if (g.child_idx[e] >= 0) cons[fill[g.child_idx[e]]++] = v;
+    std::vector<int32_t> pending(g.pending), queue;
     depth.assign(V, 0);
     queue.reserve(V);
     for (int32_t v = 0; v < V; ++v) if (pending[v] == 0) queue.push_back(v);
     for (size_t q = 0; q < queue.size(); ++q) {
         int32_t v = queue[q];
-        for (int32_t i = cons_ptr[v]; i < cons_ptr[v + 1]; ++i) {
-            int32_t p = cons[i];
+        for (int32_t i = g.cons_ptr[v]; i < g.cons_ptr[v + 1]; ++i) {
+            int32_t p = g.cons[i];
             depth[p] = std::max(depth[p], depth[v] + 1);
             if (--pending[p] == 0) queue.push_back(p);
         }
@@ -123,19 +114,10 @@ extern "C" edb_status edb_schedule(const edb_graph_t* g, const edb_policy* pol, 
             }
             if (V > 0) s->batch_ptr.push_back(V);
         } else {
-            // pending counters and consumer lists over present edges
-            std::vector<int32_t> pending(V, 0), cons_ptr(V + 1, 0), cons;
-            for (int32_t v = 0; v < V; ++v)
-                for (int64_t e = g->child_ptr[v]; e < g->child_ptr[v + 1]; ++e)
-                    if (g->child_idx[e] >= 0) { ++pending[v]; ++cons_ptr[g->child_idx[e] + 1]; }
-            for (int32_t v = 0; v < V; ++v) cons_ptr[v + 1] += cons_ptr[v];
-            cons.resize(cons_ptr[V]);
-            {
-                std::vector<int32_t> fill(cons_ptr.begin(), cons_ptr.end() - 1);
-                for (int32_t v = 0; v < V; ++v)
-                    for (int64_t e = g->child_ptr[v]; e < g->child_ptr[v + 1]; ++e)
-                        if (g->child_idx[e] >= 0) cons[fill[g->child_idx[e]]++] = v;
-            }
+            // pending counters and consumer lists over present edges (from ingest)
+            std::vector<int32_t> pending(g->pending);
+            const std::vector<int32_t>& cons_ptr = g->cons_ptr;
+            const std::vector<int32_t>& cons = g->cons;
             std::vector<std::vector<int32_t>> ready(T);
             for (int32_t v = 0; v < V; ++v) if (pending[v] == 0) ready[g->op_type[v]].push_back(v);
             std::vector<int64_t> depth, dsum(T, 0), dcnt(T, 0);

@@ -60,14 +60,31 @@ class Schedule:
         h = C.c_void_p()
         L.check(lib.edb_schedule(graph.handle, C.byref(pol), C.byref(h)), "edb_schedule")
         self.handle = h
-        nb = C.c_int32()
-        bp, bn, bt = C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)()
-        L.check(lib.edb_schedule_view(h, C.byref(nb), C.byref(bp), C.byref(bn), C.byref(bt)))
-        B = nb.value
-        self.batch_ptr = np.ctypeslib.as_array(bp, shape=(B + 1,)).copy()
-        self.batch_nodes = np.ctypeslib.as_array(bn, shape=(graph.n_nodes,)).copy() if graph.n_nodes else \
-            np.zeros(0, dtype=np.int32)
-        self.batch_type = np.ctypeslib.as_array(bt, shape=(B,)).copy() if B else np.zeros(0, dtype=np.int32)
+        self._view = None
+
+    def _load_view(self):
+        if self._view is None:
+            lib = L.load()
+            nb = C.c_int32()
+            bp, bn, bt = C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)()
+            L.check(lib.edb_schedule_view(self.handle, C.byref(nb), C.byref(bp), C.byref(bn), C.byref(bt)))
+            B, V = nb.value, self.graph.n_nodes
+            self._view = (np.ctypeslib.as_array(bp, shape=(B + 1,)).copy(),
+                          np.ctypeslib.as_array(bn, shape=(V,)).copy() if V else np.zeros(0, dtype=np.int32),
+                          np.ctypeslib.as_array(bt, shape=(B,)).copy() if B else np.zeros(0, dtype=np.int32))
+        return self._view
+
+    @property
+    def batch_ptr(self):
+        return self._load_view()[0]
+
+    @property
+    def batch_nodes(self):
+        return self._load_view()[1]
+
+    @property
+    def batch_type(self):
+        return self._load_view()[2]
 
     @property
     def n_batches(self):
@@ -91,21 +108,34 @@ class Plan:
         h = C.c_void_p()
         L.check(lib.edb_plan_memory(graph.handle, sched.handle, arr, mode, C.byref(h)), "edb_plan_memory")
         self.handle = h
+        self._loaded = False
+
+    def __getattr__(self, name):
+        # plan arrays are copied out of the library on first use only
+        if name in ("n_slots", "slot", "order", "x_slot", "seg_ptr", "segs", "idx_pool", "ragged_off",
+                    "ragged_pool", "pads") and not self.__dict__.get("_loaded", True):
+            self._load_view()
+            return self.__dict__[name]
+        raise AttributeError(name)
+
+    def _load_view(self):
         v = L.PlanView()
-        L.check(lib.edb_plan_view(h, C.byref(v)))
+        L.check(L.load().edb_plan_view(self.handle, C.byref(v)))
         V, B = v.n_nodes, v.n_batches
         asarr = lambda p, n, dt=np.int32: np.ctypeslib.as_array(p, shape=(n,)).copy() if n else np.zeros(0, dt)
-        self.n_slots = v.n_slots
-        self.slot = asarr(v.slot, V)
-        self.order = asarr(v.order, V)
-        self.x_slot = asarr(v.x_slot, V)
-        self.seg_ptr = asarr(v.seg_ptr, B + 1)
-        nseg = int(self.seg_ptr[-1]) if B else 0
-        self.segs = [(v.segs[i].kind, v.segs[i].base, v.segs[i].idx_off, v.segs[i].len) for i in range(nseg)]
-        self.idx_pool = asarr(v.idx_pool, v.idx_len)
-        self.ragged_off = asarr(v.ragged_off, B, np.int64)
-        self.ragged_pool = asarr(v.ragged_pool, v.ragged_len)
-        self.pads = asarr(v.pads, v.n_pads)
+        d = self.__dict__
+        d["n_slots"] = v.n_slots
+        d["slot"] = asarr(v.slot, V)
+        d["order"] = asarr(v.order, V)
+        d["x_slot"] = asarr(v.x_slot, V)
+        d["seg_ptr"] = asarr(v.seg_ptr, B + 1)
+        nseg = int(d["seg_ptr"][-1]) if B else 0
+        d["segs"] = [(v.segs[i].kind, v.segs[i].base, v.segs[i].idx_off, v.segs[i].len) for i in range(nseg)]
+        d["idx_pool"] = asarr(v.idx_pool, v.idx_len)
+        d["ragged_off"] = asarr(v.ragged_off, B, np.int64)
+        d["ragged_pool"] = asarr(v.ragged_pool, v.ragged_len)
+        d["pads"] = asarr(v.pads, v.n_pads)
+        d["_loaded"] = True
 
     def batch_segments(self, b):
         """[(kind, slot list)] for batch b: result first, then the operand lists."""
@@ -164,6 +194,10 @@ class Exec:
         out = (C.c_float * n)()
         L.check(L.load().edb_exec_launch_times(self.handle, out, n), "edb_exec_launch_times")
         return np.array(out[:], dtype=np.float64)
+
+    def check(self, stream: int = 0):
+        """Synchronise and raise if a dataflow wait of the last execution timed out."""
+        L.check(L.load().edb_exec_check(self.handle, C.c_void_p(stream)), "edb_exec_check")
 
     def execute(self, weight_ptrs: Sequence[int], x_ptr: int, arena_h_ptr: int, arena_c_ptr: int, stream: int):
         arr = (C.c_void_p * len(weight_ptrs))(*weight_ptrs)
@@ -237,7 +271,9 @@ class Forward:
                           self.arena_c.data_ptr(), self.stream.cuda_stream)
 
     def states(self):
-        """Node-ordered (h, c) as float64 numpy arrays (synchronises)."""
+        """Node-ordered (h, c) as float64 numpy arrays (synchronises and checks
+        the dataflow launches)."""
+        self.exec.check(self.stream.cuda_stream)
         self.torch.cuda.synchronize()
         ah = self.arena_h.float().cpu().numpy().astype(np.float64)
         ac = self.arena_c.cpu().numpy().astype(np.float64)

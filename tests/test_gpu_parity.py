@@ -135,12 +135,79 @@ def test_layout_and_launch_mode_bitwise(k):
     ref.run()
     h0, c0 = ref.states()
     for kw in (dict(plan_mode=L.PLAN_IDENTITY), dict(flags=L.USE_GRAPH | L.FORCE_GATHER),
-               dict(flags=L.USE_GRAPH | L.X_DIRECT), dict(flags=0)):
+               dict(flags=L.USE_GRAPH | L.X_DIRECT), dict(flags=0),
+               dict(flags=L.PROFILE)):
         f = _fwd(w, **kw)
         f.run()
         h, c = f.states()
         np.testing.assert_array_equal(h, h0, err_msg=str(kw))
         np.testing.assert_array_equal(c, c0, err_msg=str(kw))
+
+
+DATAFLOW_OFF = ("dataflow launches are switched off: their first GPU runs did not drain "
+                "(cause not yet shown); every batch runs as its own launch")
+
+
+@pytest.mark.skip(reason=DATAFLOW_OFF)
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_dataflow_matches_per_batch_launches(k):
+    """Dataflow launches (default) against one launch per batch: both within
+    the bound of the oracle, and identical where the tile shapes agree."""
+    _torch()
+    w = WL.make_config(k, instances=SMALL[k])
+    hr, cr = _oracle(w)
+    flow = _fwd(w)
+    n_flow = sum(1 for i in range(flow.exec.launches())
+                 if flow.exec.launch_info(i)["variant"] == L.FLOW_VARIANT)
+    assert n_flow >= 1
+    flow.run()
+    h1, c1 = flow.states()
+    _check(w, h1, c1, hr, cr, f"dataflow k={k}")
+    per = _fwd(w, flags=L.USE_GRAPH | L.NO_FLOW)
+    per.run()
+    h2, c2 = per.states()
+    _check(w, h2, c2, hr, cr, f"per-batch k={k}")
+
+
+@pytest.mark.skip(reason=DATAFLOW_OFF)
+def test_dataflow_full_size_replays():
+    """Full-size binary trees through the dataflow launch, replayed several
+    times: every replay bitwise equal to the first (no timing dependence)."""
+    _torch()
+    w = WL.make_config(2)
+    f = _fwd(w)
+    f.run()
+    h0, c0 = f.states()
+    for i in range(5):
+        f.run()
+        h, c = f.states()
+        np.testing.assert_array_equal(h, h0, err_msg=f"replay {i}")
+        np.testing.assert_array_equal(c, c0, err_msg=f"replay {i}")
+
+
+@pytest.mark.skip(reason=DATAFLOW_OFF)
+def test_dataflow_wait_timeout_is_reported(monkeypatch):
+    """A wait bound of one microsecond forces the bounded-wait path from the
+    host: every kernel still exits normally and edb_exec_check reports it."""
+    _torch()
+    monkeypatch.setenv("EDB_SPIN_US", "1")
+    w = WL.make_config(2, instances=16)
+    f = _fwd(w, flags=0)
+    f.run()
+    try:
+        f.exec.check(f.stream.cuda_stream)
+        timed_out = False
+    except L.EdbError as e:
+        timed_out = True
+        assert e.status == L.EDB_ERR_HIP and "timed out" in str(e)
+    # with a 1 us bound a timeout is all but certain; either way the launch
+    # drained and a fresh executor with the default bound is correct
+    monkeypatch.delenv("EDB_SPIN_US")
+    g = _fwd(w, flags=0)
+    g.run()
+    h, c = g.states()
+    hr, cr = _oracle(w)
+    _check(w, h, c, hr, cr, f"after forced timeout (timed_out={timed_out})")
 
 
 def test_graph_replays_match_eager():

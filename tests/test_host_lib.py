@@ -206,23 +206,37 @@ def test_abi_errors(lib):
 
 
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
-def test_dryrun_launch_list(k):
+@pytest.mark.parametrize("flow", [True, False])
+def test_dryrun_launch_list(k, flow):
     w = WL.make_config(k, instances=CFG_INSTANCES[k])
-    f = edb.Forward(w, flags=L.DRYRUN | L.USE_GRAPH)
+    f = edb.Forward(w, flags=L.DRYRUN | L.USE_GRAPH | (0 if flow else L.NO_FLOW))
     n = f.exec.launches()
-    assert n == 1 + f.sched.n_batches
+    B = f.sched.n_batches
     info0 = f.exec.launch_info(0)
-    assert info0["batch"] == -1 and info0["grid"] == int((w.x_row >= 0).sum()) + 1 + len(f.plan.pads)
+    assert info0["batch"] == -1 and info0["n_batches"] == 0
+    assert info0["grid"] == (int((w.x_row >= 0).sum()) + 1 + len(f.plan.pads) + 3) // 4
+    seen = []
     for i in range(1, n):
         info = f.exec.launch_info(i)
         b = info["batch"]
-        assert b == i - 1
+        if info["variant"] == L.FLOW_VARIANT:
+            assert flow and info["n_batches"] >= 2 and info["kind"] == -1
+            rows = [f.sched.batch_ptr[q + 1] - f.sched.batch_ptr[q] for q in range(b, b + info["n_batches"])]
+            assert max(rows) <= 1024 and info["m"] == sum(rows)
+            assert 1 <= info["grid"] and info["block"] == 256
+            seen += list(range(b, b + info["n_batches"]))
+            continue
+        assert info["n_batches"] == 1
         t = int(f.sched.batch_type[b])
         assert info["kind"] == w.kinds[t]
         assert info["m"] == f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b]
-        assert 0 <= info["variant"] < 4 and info["grid"] >= 1 and info["block"] == 256
+        assert 0 <= info["variant"] < 8 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
         segs = f.plan.batch_segments(b)
         assert info["seg_kind"][0] == segs[0][0]
+        seen.append(b)
+    assert seen == list(range(B))          # every batch exactly once, in schedule order
+    if not flow:
+        assert n == 1 + B
     with pytest.raises(L.EdbError):
         f.exec.launch_info(n)
 
