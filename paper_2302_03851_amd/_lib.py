@@ -33,7 +33,7 @@ EXPORTS = [
     "edb_plan_memory", "edb_plan_view", "edb_plan_free",
     "edb_packed_weight_bytes", "edb_pack_weights",
     "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
-    "edb_exec_check", "edb_exec_free",
+    "edb_exec_check", "edb_exec_free", "edb_forward",
 ]
 
 
@@ -115,6 +115,9 @@ def load():
         "edb_exec_launch_times": (C.c_int32, [vp, P(C.c_float), C.c_int32]),
         "edb_exec_check": (C.c_int32, [vp, vp]),
         "edb_exec_free": (None, [vp]),
+        "edb_forward": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32), P(C.c_int32),
+                                    P(Policy), P(OperandShape), C.c_int32, P(Cell), C.c_int32, P(vp), vp, vp, vp,
+                                    C.c_int64, vp, P(C.c_int32)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libedb.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
-HOST_SRC = ["graph.cpp", "schedule.cpp", "plan.cpp"]
+HOST_SRC = ["graph.cpp", "schedule.cpp", "plan.cpp", "forward.cpp"]
 HIP_SRC = ["exec.hip"]
 
 CXXFLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include")]

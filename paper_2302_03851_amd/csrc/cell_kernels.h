@@ -279,33 +279,48 @@ struct BRing {
 
 template <int G, int PD>
 __device__ __forceinline__ void ring_prologue(BRing<G, PD>& r, const uint4* B, int nkg, int kg0, int kg1) {
+    if (kg0 >= kg1) return;
 #pragma unroll
-    for (int s = 0; s < PD; ++s)
-        if (kg0 + s < kg1) load_b<G>(r.b[s], B, nkg, kg0 + s);
+    for (int s = 0; s < PD; ++s) load_b<G>(r.b[s], B, nkg, min(kg0 + s, kg1 - 1));
+}
+
+// A fragments of k-group k for all row blocks of the wave.
+template <typename T, int RT>
+__device__ __forceinline__ void load_a(uint4 (&av)[RT], const T* A, int AS, int k, int lane) {
+    constexpr int KG = Elem<T>::KG;
+    const int arow = lane & 15, aq = lane >> 4;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+        av[rt] = *reinterpret_cast<const uint4*>(A + (rt * 16 + arow) * AS + k * KG + aq * (KG / 4));
 }
 
 // GEMM of one wave over k-groups [kg0, kg1): acc[g][rt] += A[rt*16 .. +16] * W[ub][g].
-// The ring holds k-groups kg0 .. kg0+PD-1 on entry (ring_prologue); each step
-// refills the slot it consumed with the k-group PD steps ahead.
+// The ring holds k-groups kg0 .. kg0+PD-1 on entry (ring_prologue; indices
+// past the end repeat the last k-group).  In the steady state every slot is
+// refilled, unconditionally, with the k-group PD steps ahead (clamped to the
+// last one), so the compiler can wait for exactly the load a slot needs; the
+// remaining k-groups drain the ring without loads.
 template <typename T, int G, int RT, int PD>
 __device__ __forceinline__ void wave_gemm(v4f (&acc)[G][RT], const T* A, int AS, const uint4* B, int nkg,
                                           int kg0, int kg1, int lane, BRing<G, PD>& ring) {
-    constexpr int KG = Elem<T>::KG;
-    const int arow = lane & 15, aq = lane >> 4;
-    for (int kg = kg0; kg < kg1; kg += PD) {
+    int kg = kg0;
+    for (; kg + PD < kg1; kg += PD) {
+        uint4 av[PD][RT];
+#pragma unroll
+        for (int s = 0; s < PD; ++s) load_a<T, RT>(av[s], A, AS, kg + s, lane);
 #pragma unroll
         for (int s = 0; s < PD; ++s) {
-            const int k = kg + s;
-            if (k < kg1) {
-                uint4 av[RT];
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
-                    av[rt] = *reinterpret_cast<const uint4*>(A + (rt * 16 + arow) * AS + k * KG + aq * (KG / 4));
-                kgroup_mma<T, G, RT>(acc, av, ring.b[s]);
-                if (k + PD < kg1) load_b<G>(ring.b[s], B, nkg, k + PD);
-            }
+            kgroup_mma<T, G, RT>(acc, av[s], ring.b[s]);
+            load_b<G>(ring.b[s], B, nkg, min(kg + s + PD, kg1 - 1));
         }
     }
+    uint4 av[PD][RT];
+#pragma unroll
+    for (int s = 0; s < PD; ++s)
+        if (kg + s < kg1) load_a<T, RT>(av[s], A, AS, kg + s, lane);
+#pragma unroll
+    for (int s = 0; s < PD; ++s)
+        if (kg + s < kg1) kgroup_mma<T, G, RT>(acc, av[s], ring.b[s]);
 }
 
 // No inter-tile synchronisation (one launch per batch: kernel boundaries order

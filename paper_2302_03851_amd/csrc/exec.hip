@@ -329,6 +329,7 @@ struct DeviceCtx {
     int max_lds = 0;
     int n_cu = 0;
     hipStream_t upload = nullptr;
+    hipStream_t release = nullptr;   // stream-ordered frees wait here, off the upload path
     std::map<int, int> lds_granted;
 };
 std::mutex g_ctx_mu;
@@ -345,6 +346,7 @@ hipError_t device_ctx(int dev, DeviceCtx** out) {
     hipError_t he = hipDeviceGetAttribute(&c.max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (he == hipSuccess) he = hipDeviceGetAttribute(&c.n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (he == hipSuccess) he = hipStreamCreateWithFlags(&c.upload, hipStreamNonBlocking);
+    if (he == hipSuccess) he = hipStreamCreateWithFlags(&c.release, hipStreamNonBlocking);
     if (he != hipSuccess) return he;
     *out = &(g_ctx[dev] = c);
     return hipSuccess;
@@ -366,6 +368,7 @@ struct edb_exec {
     int* dbuf = nullptr;
     void* xstaged = nullptr;
     hipStream_t upload = nullptr;     // the device's upload stream
+    hipStream_t release = nullptr;    // the device's stream for stream-ordered frees
     hipEvent_t ready = nullptr;       // descriptors uploaded
     hipEvent_t done = nullptr;        // last execution enqueued
     bool ran = false;
@@ -383,10 +386,13 @@ struct edb_exec {
         if (graph) (void)hipGraphDestroy(graph);
         if (cap_stream) (void)hipStreamDestroy(cap_stream);
         if (dmem) {
-            // free in stream order after the last execution (and the upload)
+            // free in stream order after the upload and the last execution, on a
+            // stream of its own so that later uploads do not queue behind this
+            // executor's kernels
             if (dmem_async) {
-                if (ran && done) (void)hipStreamWaitEvent(upload, done, 0);
-                (void)hipFreeAsync(dmem, upload);
+                (void)hipStreamWaitEvent(release, ready, 0);
+                if (ran && done) (void)hipStreamWaitEvent(release, done, 0);
+                (void)hipFreeAsync(dmem, release);
             } else {
                 (void)hipFree(dmem);
             }
@@ -774,6 +780,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             const size_t ibytes = (hb.size() * sizeof(int32_t) + 255) / 256 * 256;
             const size_t xbytes = (n_x > 0 && !(flags & EDB_X_DIRECT)) ? (size_t)n_x * E * (dtype == EDB_F32 ? 4 : 2) : 0;
             e->upload = ctx->upload;
+            e->release = ctx->release;
             hipError_t he = hipMallocAsync(&e->dmem, ibytes + xbytes, ctx->upload);
             if (he != hipSuccess) {
                 (void)hipGetLastError();

@@ -1,0 +1,40 @@
+// One call for one mini-batch: graph ingest, schedule, memory plan, launch
+// preparation and asynchronous execution (the whole hot path, Algorithm 1 and
+// Section 3.1 of ED-Batch), with every host object released before return.
+// Device buffers owned by the executor are freed in stream order after the
+// work completes, so the call never waits for the GPU.
+#include <string>
+
+#include "edb_internal.h"
+
+extern "C" edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
+                                  const int64_t* child_ptr, const int32_t* child_idx, const int32_t* x_row,
+                                  const edb_policy* policy, const edb_operand_shape* shapes, int32_t plan_flags,
+                                  const edb_cell* cells, int32_t exec_flags, const void* const* packed_weights,
+                                  const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
+                                  int32_t* n_slots) {
+    if (exec_flags & EDB_DRYRUN) return edb::fail(EDB_ERR_INVALID, "edb_forward: EDB_DRYRUN is not allowed");
+    edb_graph_t* g = nullptr;
+    edb_schedule_t* s = nullptr;
+    edb_plan_t* p = nullptr;
+    edb_exec_t* e = nullptr;
+    edb_status st = edb_build_graph(n_nodes, n_types, op_type, child_ptr, child_idx, x_row, &g);
+    if (st == EDB_OK) st = edb_schedule(g, policy, &s);
+    if (st == EDB_OK) st = edb_plan_memory(g, s, shapes, plan_flags, &p);
+    if (st == EDB_OK) {
+        if (n_slots) *n_slots = p->n_slots;
+        if (arena_rows < p->n_slots)
+            st = edb::fail(EDB_ERR_INVALID, "edb_forward: the arena has " + std::to_string(arena_rows) +
+                                                " rows, the plan needs " + std::to_string(p->n_slots));
+    }
+    if (st == EDB_OK) st = edb_prepare(g, s, p, cells, exec_flags & ~EDB_USE_GRAPH, &e);
+    if (st == EDB_OK) st = edb_execute(e, packed_weights, x, arena_h, arena_c, stream);
+    // keep the error text of the failing step across the frees below
+    const std::string err = st == EDB_OK ? std::string() : std::string(edb_last_error());
+    edb_exec_free(e);
+    edb_plan_free(p);
+    edb_schedule_free(s);
+    edb_graph_free(g);
+    if (st != EDB_OK) return edb::fail(st, err);
+    return EDB_OK;
+}

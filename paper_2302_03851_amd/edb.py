@@ -210,6 +210,39 @@ class Exec:
             self.handle = None
 
 
+class ForwardCall:
+    """Argument block of edb_forward for one graph, marshalled once; call()
+    then runs the whole path for that mini-batch in a single C call."""
+
+    def __init__(self, op_type, child_ptr, child_idx, x_row, n_types, shapes, cells, policy=L.POLICY_TABLE,
+                 encoding=L.ENC_SORT, table=None, plan_mode=L.PLAN_RC, flags=0):
+        self._op = _i32(op_type)
+        self._ptr = np.ascontiguousarray(child_ptr, dtype=np.int64)
+        self._idx = _i32(child_idx) if len(child_idx) else np.zeros(1, dtype=np.int32)
+        self._xr = _i32(x_row)
+        flat = None
+        if table:
+            flat = [len(table)]
+            for key, action in table.items():
+                flat += [len(key)] + list(key) + [action]
+        self._tab = _i32(flat) if flat else None
+        self._pol = L.Policy(policy, encoding, _ptr(self._tab, C.c_int32) if flat else None, len(flat) if flat else 0)
+        self._shapes = (L.OperandShape * len(shapes))(*[L.OperandShape(*s) for s in shapes])
+        self._cells = (L.Cell * len(cells))(*cells)
+        self.n_nodes, self.n_types = int(self._op.shape[0]), int(n_types)
+        self.plan_mode, self.flags = plan_mode, flags
+        self._args = (self.n_nodes, self.n_types, _ptr(self._op, C.c_int32), _ptr(self._ptr, C.c_int64),
+                      _ptr(self._idx, C.c_int32), _ptr(self._xr, C.c_int32), C.byref(self._pol), self._shapes,
+                      plan_mode, self._cells, flags)
+        self.n_slots = C.c_int32()
+
+    def call(self, weight_ptrs, x_ptr, arena_h_ptr, arena_c_ptr, arena_rows, stream):
+        arr = (C.c_void_p * len(weight_ptrs))(*weight_ptrs)
+        L.check(L.load().edb_forward(*self._args, arr, C.c_void_p(x_ptr), C.c_void_p(arena_h_ptr),
+                                     C.c_void_p(arena_c_ptr), arena_rows, C.c_void_p(stream),
+                                     C.byref(self.n_slots)), "edb_forward")
+
+
 def operand_shapes(w) -> List[Tuple[int, int, int]]:
     return [(nf, rg, int(KIND_SHAPE[k][2])) for (nf, rg), k in zip(w.shapes(), w.kinds)]
 

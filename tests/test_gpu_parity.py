@@ -229,6 +229,29 @@ def test_graph_replays_match_eager():
         np.testing.assert_array_equal(c, ce, err_msg=f"replay {i}")
 
 
+@pytest.mark.parametrize("k", [2, 5])
+def test_forward_call_matches_handles(k):
+    """edb_forward (the whole path in one call) writes bitwise the same arena
+    as the separate calls with eager launches."""
+    torch = _torch()
+    from paper_2302_03851_amd import edb
+    w = WL.make_config(k, instances=SMALL[k])
+    ref = _fwd(w, flags=0)
+    ref.run()
+    h0, c0 = ref.states()
+    table = edb.LATTICE_TABLE if k == 3 else None
+    fc = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w),
+                         ref.cells, table=table)
+    ah = torch.full_like(ref.arena_h, 5.0)
+    ac = torch.full_like(ref.arena_c, 5.0)
+    fc.call([b.data_ptr() for b in ref.weights], ref.x.data_ptr(), ah.data_ptr(), ac.data_ptr(),
+            ah.shape[0], ref.stream.cuda_stream)
+    torch.cuda.synchronize()
+    s = ref.plan.slot
+    np.testing.assert_array_equal(ah.float().cpu().numpy()[s], h0)
+    np.testing.assert_array_equal(ac.cpu().numpy()[s], c0)
+
+
 def test_policies_give_same_states():
     """Agenda and depth schedules change the batches, not the results."""
     _torch()

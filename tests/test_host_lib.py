@@ -247,3 +247,23 @@ def test_packed_weight_bytes_layout():
     assert edb.packed_bytes(c) == 256 // 16 * 5 * (512 // 16) * 64 * 16 + 5 * 256 * 4
     c = edb.cell_struct(WL.CS_INTERNAL, 0, 512, 0, L.BF16)
     assert edb.packed_bytes(c) == (512 // 16 * 3 * 16 * 1024 + 3 * 512 * 4 + 512 // 16 * 16 * 1024 + 2048)
+
+
+def test_forward_call_validates_before_any_device_work():
+    """edb_forward: an arena smaller than the plan fails with EDB_ERR_INVALID
+    (and reports the rows needed) before any HIP call; EDB_DRYRUN is rejected."""
+    w = WL.make_config(2, instances=3)
+    cells = [edb.cell_struct(k, w.in_dim, w.hidden, w.n_children[t] if k == WL.NARY_INTERNAL else 0, L.F32)
+             for t, k in enumerate(w.kinds)]
+    fc = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w), cells)
+    with pytest.raises(L.EdbError) as ei:
+        fc.call([256, 256], 256, 256, 256, 3, 0)
+    assert ei.value.status == L.EDB_ERR_INVALID and "arena" in str(ei.value)
+    g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+    pl = edb.Plan(g, edb.Schedule(g), edb.operand_shapes(w))
+    assert fc.n_slots.value == pl.n_slots
+    bad = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w), cells,
+                          flags=L.DRYRUN)
+    with pytest.raises(L.EdbError) as ei:
+        bad.call([256, 256], 256, 256, 256, 10 ** 6, 0)
+    assert ei.value.status == L.EDB_ERR_INVALID
