@@ -220,12 +220,23 @@ edb_status edb_pack_weights(const edb_cell* cell, const float* const* logical,
 #define EDB_X_DIRECT     8  /* read x rows in place by x_row instead of staging them */
 #define EDB_PROFILE     16  /* eager launches timed by start/stop HIP events in each dispatch (edb_exec_launch_times) */
 #define EDB_NO_FLOW     32  /* one launch per batch only (no dataflow launches) */
+#define EDB_NO_SPLIT_K  64  /* small tiles without split-K only (each accumulator sums its k-groups in order) */
+#define EDB_TILE_LARGE 128  /* the large bf16 tile for every batch it supports, whatever the batch size */
+#define EDB_NO_LARGE   256  /* never the large tile (ablation) */
 
 typedef struct edb_exec edb_exec_t;
 
 /* Bind a graph, schedule and plan to cell kernels.  cells: host [n_types].
  * Uploads the batch descriptors and index lists to the current HIP device
  * and allocates the staged-x buffer; both are owned by the handle.
+ * Each batch gets the tile variant of smallest estimated time: small tiles
+ * (16-32 rows per work-group, optional split-K) for the many small batches,
+ * the large bf16 tile (64-256 rows, both operands through LDS) for batches
+ * of thousands of rows.  Without split-K (EDB_NO_SPLIT_K, and always in the
+ * large tile) a batch's results do not depend on the variant: they are
+ * bitwise equal across variants, layouts and launch modes.  For sweeps and
+ * tests, the environment variable EDB_VARIANT=v (read at each call) forces
+ * variant v on every batch whose cell kind has it.
  * Errors: EDB_ERR_INVALID, EDB_ERR_UNSUPPORTED (dimension or kind mix the
  * kernels do not handle), EDB_ERR_OOM, EDB_ERR_HIP. */
 edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
@@ -261,7 +272,8 @@ typedef struct {
     int32_t m;         /* rows (all batches of a dataflow launch) */
     int32_t k;         /* padded reduction length of the main GEMM */
     int32_t n;         /* padded output columns (gates x padded hidden) */
-    int32_t variant;   /* tile variant id; 100 for a dataflow launch */
+    int32_t variant;   /* tile variant id: 0-7 small tiles, 8-10 the large bf16 tile (largest rows
+                          per work-group first), 100 a dataflow launch */
     int32_t grid;      /* work-groups */
     int32_t block;     /* threads per work-group */
     int32_t seg_kind[4]; /* kinds of result, child 0, child 1, ragged lists */

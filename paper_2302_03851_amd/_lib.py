@@ -23,6 +23,8 @@ PLAN_RC, PLAN_IDENTITY = 0, 1
 SEG_NONE, SEG_CONTIG, SEG_GATHER, SEG_SCATTER = 0, 1, 2, 3
 F32, BF16 = 0, 1
 USE_GRAPH, DRYRUN, FORCE_GATHER, X_DIRECT, PROFILE, NO_FLOW = 1, 2, 4, 8, 16, 32
+NO_SPLIT_K, TILE_LARGE, NO_LARGE = 64, 128, 256
+LARGE_VARIANTS = (8, 9, 10)
 FLOW_VARIANT = 100
 
 # every symbol include/edb.h declares

@@ -25,7 +25,10 @@ HIP_SRC = ["exec.hip"]
 
 CXXFLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include")]
 # Packed fp32 instructions are disabled for all device code.
-HIPFLAGS = ["-O3", "-fPIC", "-std=c++17", "--offload-arch=gfx950",
+# -ffp-contract=off: every kernel rounds the same expression the same way
+# (fused multiply-adds are written out where they are wanted), which keeps
+# results bitwise equal across tile variants.
+HIPFLAGS = ["-O3", "-fPIC", "-std=c++17", "--offload-arch=gfx950", "-ffp-contract=off",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
             "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 

@@ -1,0 +1,263 @@
+// Large-batch tile for bf16 cells on gfx950.
+//
+// The first batches of a schedule can hold thousands of nodes (all leaves of
+// a mini-batch form one batch under Algorithm 1), and there the cell GEMM is a
+// dense contraction large enough to be bound by the matrix cores.  This tile
+// raises the reuse of every operand fetched from L2: a work-group of 4 waves
+// (2 along rows x 2 along units) owns TM = 32*RB rows and TU = 32*CU hidden
+// units with all G gates, and both operands pass through LDS in chunks of 64
+// k values, double buffered so that the global loads of chunk c+1 are in
+// flight while the matrix cores work on chunk c.  Each wave holds a
+// 16*RB x 16*CU x G block of accumulators (v_mfma_f32_16x16x32_bf16, fp32
+// accumulation), so the gate epilogue finds all G pre-activations of an
+// element in one lane.
+//
+// The operand rows are gathered through the batch's segment descriptors
+// exactly as in the small tile (contiguous lists as base + row, indexed lists
+// through their slot list), and the k-groups of every accumulator are added
+// in ascending order with the same instruction, so a batch computed here is
+// bitwise equal to the small tile without split-K.
+//
+// Work-groups are dispatched round-robin over the 8 XCDs; the tile order is
+// remapped so that each XCD owns a contiguous range of tiles, unit tiles
+// fastest: the work-groups sharing a row tile's operand rows run on one XCD
+// and hit in its L2.
+#pragma once
+
+#include "cell_kernels.h"
+
+namespace edbk {
+
+constexpr int BIG_BK = 64;            // k values per LDS stage (two k-groups of 32)
+
+// Rows blocks per wave for gate count G and size class vb (0 largest): the
+// accumulators (4 * CU * G * RB registers) stay within 192.
+__host__ __device__ constexpr int big_rb(int G, int vb) {
+    const int want = vb == 0 ? 8 : vb == 1 ? 4 : 2;
+    const int cap = 192 / (8 * G);
+    return want < cap ? want : cap;
+}
+constexpr int BIG_CU = 2;
+
+// One LDS stage: A [TM rows][64 k] bf16 (128 bytes a row, 16-byte pieces
+// XOR-swizzled by row: piece q of row r sits in slot q ^ (r & 7), so that the
+// 16 rows one MFMA operand read touches fall in distinct banks), then the
+// weight blocks [2 CU unit blocks][G][2 k-groups][64 lanes][16 bytes].
+template <int G, int RB, int CU>
+__host__ __device__ constexpr int big_stage_bytes() {
+    return 32 * RB * 128 + 2 * CU * G * 2 * 1024;
+}
+template <int KIND, int VB>
+__host__ __device__ constexpr int big_lds_bytes() {
+    return 2 * big_stage_bytes<Kind<KIND>::G, big_rb(Kind<KIND>::G, VB), BIG_CU>();
+}
+
+// Raw buffer resource over `bytes` bytes at p (gfx9 resource word 3).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// Direct global -> LDS copy of 16 bytes per lane: lane l's bytes at byte
+// offset off land at lds + 16 l (lds is wave-uniform).  Offsets past the end
+// of the buffer read as zero.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t off, char* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
+}
+
+// Copies of one k chunk into an LDS stage.  The chunk lies in one operand
+// segment (uniform sg: 0 = x when the kind has x, then child positions); lane
+// column col of that segment's source rows, zero where col >= lim.
+template <int RB, int NSEG, int NBW, bool HAS_X>
+__device__ __forceinline__ void big_copy(const uint32_t (&soff)[NSEG][RB], const uint32_t (&woff)[NBW],
+                                         __amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rh,
+                                         __amdgpu_buffer_rsrc_t rw, int c, int sg, int col, int lim, char* As,
+                                         char* Bs, int wave) {
+    constexpr uint32_t OOB = 0x80000000u;
+    const bool have = col < lim;
+    const bool xs = HAS_X && sg == 0;
+#pragma unroll
+    for (int j = 0; j < RB; ++j) {
+        uint32_t ro = soff[0][j];
+#pragma unroll
+        for (int s = 1; s < NSEG; ++s)
+            if (sg == s) ro = soff[s][j];
+        const uint32_t off = have ? ro + (uint32_t)col * 2u : OOB;
+        if (xs) dma16(rx, off, As + (4 * j + wave) * 1024);
+        else dma16(rh, off, As + (4 * j + wave) * 1024);
+    }
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) dma16(rw, woff[j] + (uint32_t)c * 2048u, Bs + (4 * j + wave) * 1024);
+}
+
+// k-group pair of one LDS stage on the matrix cores.
+template <int RB, int CU, int G>
+__device__ __forceinline__ void big_compute(v4f (&acc)[CU][G][RB], const char* As, const uint4* Bs, int wr, int wc,
+                                            int lane) {
+#pragma unroll
+    for (int kgi = 0; kgi < 2; ++kgi) {
+        uint4 af[RB], bf[CU][G];
+        // row wr*16RB + rb*16 + (lane & 15), piece kgi*4 + lane/16, swizzled by row & 7 = lane & 7
+        const int slot = ((kgi * 4 + (lane >> 4)) ^ (lane & 7)) * 16;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+            af[rb] = *reinterpret_cast<const uint4*>(As + (wr * 16 * RB + rb * 16 + (lane & 15)) * 128 + slot);
+#pragma unroll
+        for (int cu = 0; cu < CU; ++cu)
+#pragma unroll
+            for (int g = 0; g < G; ++g) bf[cu][g] = Bs[(((wc * CU + cu) * G + g) * 2 + kgi) * 64 + lane];
+#pragma unroll
+        for (int cu = 0; cu < CU; ++cu)
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+                    acc[cu][g][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(v8bf, af[rb]), __builtin_bit_cast(v8bf, bf[cu][g]), acc[cu][g][rb], 0, 0, 0);
+    }
+}
+
+template <int KIND, int VB>
+__global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
+    using KT = Kind<KIND>;
+    using T = __bf16;
+    constexpr int G = KT::G, NFX = KT::NFIX;
+    constexpr int RB = big_rb(G, VB), CU = BIG_CU;
+    constexpr int TM = 32 * RB, TU = 32 * CU;
+    constexpr int NSEG = (KT::X ? 1 : 0) + NFX;
+    constexpr int NBW = CU * G;                      // weight blocks per wave per chunk
+    constexpr int SB = big_stage_bytes<G, RB, CU>();
+    constexpr int A_BYTES = TM * 128;
+    static_assert(!KT::RAG, "ragged kinds use the small tile");
+    static_assert(NSEG >= 1, "a cell has at least one operand segment");
+    // two stages as distinct objects: the compiler can then tell that the
+    // copies into one stage do not alias the reads of the other and does not
+    // wait for the copies before the reads
+    __shared__ __align__(16) char st0[SB];
+    __shared__ __align__(16) char st1[SB];
+
+    // ---- XCD-aware tile order ----
+    const int nut = a.Hu / TU;
+    const int ntile = ((a.m + TM - 1) / TM) * nut;
+    const int per = (ntile + 7) / 8;
+    const int tile = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    if (tile >= ntile) return;
+    const int row0 = (tile / nut) * TM, u0 = (tile % nut) * TU;
+    const int nrows = min(TM, a.m - row0);
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = wave >> 1, wc = wave & 1;
+    const int E = a.E, Ep = a.Ep, H = a.H, Hk = a.Hk;
+    const int nkg = a.K / 32;
+    const int nch = a.K / BIG_BK;    // segments are whole chunks (checked by the host)
+
+    // ---- operand copies: buffer -> LDS, 32-bit byte offsets; a masked piece
+    // uses an offset past the buffer and arrives as zero, so the copies carry
+    // no branches.  Buffers stay below 2^31 bytes (checked by the host); the
+    // offsets are unsigned so that OOB plus a column stays out of range ----
+    constexpr uint32_t OOB = 0x80000000u;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.xmat, KT::X ? (uint32_t)a.n_xrows * (uint32_t)E * 2u : 0u);
+    const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.arena_h, (uint32_t)a.n_slots * (uint32_t)H * 2u);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.W, (uint32_t)(a.Hu / 16) * G * nkg * 1024u);
+
+    // A copies: wave w's j-th copy fills rows (4 j + w) * 8 .. + 8 of the stage;
+    // lane l writes slot l & 7 of row (4 j + w) * 8 + l / 8, which holds piece
+    // q = (l & 7) ^ (l / 8) of that row.
+    const int q = (lane & 7) ^ (lane >> 3);
+    uint32_t soff[NSEG][RB];   // byte offset of each segment's source row (OOB: zero)
+#pragma unroll
+    for (int j = 0; j < RB; ++j) {
+        const int r = (4 * j + wave) * 8 + (lane >> 3);
+        const bool ok = r < nrows;
+        int s = 0;
+        if constexpr (KT::X) soff[s++][j] = ok ? (uint32_t)seg_row(a.x, row0 + r) * (uint32_t)E * 2u : OOB;
+#pragma unroll
+        for (int p = 0; p < NFX; ++p)
+            soff[s++][j] = !ok ? OOB
+                               : (a.fix[p].kind == S_NONE ? 0u
+                                                          : (uint32_t)seg_row(a.fix[p], row0 + r) * (uint32_t)H * 2u);
+    }
+    // weight copies: wave w's j-th copy is block b = 4 j + w = ((ubi * G + g) * 2 + kgi)
+    uint32_t woff[NBW];
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+        const int b = 4 * j + wave;
+        const int kgi = b & 1, g = (b >> 1) % G, ubi = (b >> 1) / G;
+        woff[j] = (uint32_t)((((u0 / 16 + ubi) * G + g) * nkg + kgi) * 1024 + lane * 16);
+    }
+
+    v4f acc[CU][G][RB];
+#pragma unroll
+    for (int cu = 0; cu < CU; ++cu)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) acc[cu][g][rb] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    // ---- double-buffered chunk pipeline: the copies of chunk c+1 run while
+    // the matrix cores work on chunk c; the barrier waits for them.  The
+    // chunk's segment is tracked incrementally (uniform scalars).  Even
+    // chunks live in st0, odd chunks in st1 ----
+    int sg = 0, scol = 0, slim = KT::X ? E : H, send = KT::X ? Ep : Hk;
+    auto next_seg = [&]() {
+        scol += BIG_BK;
+        if (scol >= send) { ++sg; scol = 0; slim = H; send = Hk; }
+    };
+    big_copy<RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, 0, sg, scol + q * 8, slim, st0, st0 + A_BYTES, wave);
+    __syncthreads();
+    int c = 0;
+    for (; c + 1 < nch; c += 2) {
+        next_seg();
+        big_copy<RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, c + 1, sg, scol + q * 8, slim, st1, st1 + A_BYTES,
+                                      wave);
+        big_compute<RB, CU, G>(acc, st0, reinterpret_cast<const uint4*>(st0 + A_BYTES), wr, wc, lane);
+        __syncthreads();
+        if (c + 2 < nch) {
+            next_seg();
+            big_copy<RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, c + 2, sg, scol + q * 8, slim, st0,
+                                          st0 + A_BYTES, wave);
+        }
+        big_compute<RB, CU, G>(acc, st1, reinterpret_cast<const uint4*>(st1 + A_BYTES), wr, wc, lane);
+        __syncthreads();
+    }
+    if (c < nch) big_compute<RB, CU, G>(acc, st0, reinterpret_cast<const uint4*>(st0 + A_BYTES), wr, wc, lane);
+
+    // ---- gate epilogue and scatter of h, c ----
+    T* Hout = reinterpret_cast<T*>(a.arena_h);
+    float bz[CU][G];   // bias of this lane's units (the packed bias is zero-padded to Hu)
+#pragma unroll
+    for (int cu = 0; cu < CU; ++cu)
+#pragma unroll
+        for (int g = 0; g < G; ++g) bz[cu][g] = a.bias[g * a.Hu + u0 + (wc * CU + cu) * 16 + (lane & 15)];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = wr * 16 * RB + rb * 16 + (lane >> 4) * 4 + i;
+            if (r >= nrows) continue;
+            const int rres = seg_row(a.res, row0 + r);
+            int crow[NFX > 0 ? NFX : 1];
+#pragma unroll
+            for (int p = 0; p < NFX; ++p) crow[p] = a.fix[p].kind == S_NONE ? -1 : seg_row(a.fix[p], row0 + r);
+#pragma unroll
+            for (int cu = 0; cu < CU; ++cu) {
+                const int j = u0 + (wc * CU + cu) * 16 + (lane & 15);
+                if (j >= a.H) continue;
+                float z[G], cp[NFX > 0 ? NFX : 1];
+#pragma unroll
+                for (int g = 0; g < G; ++g) z[g] = acc[cu][g][rb][i] + bz[cu][g];
+                cp[0] = 0.f;
+#pragma unroll
+                for (int p = 0; p < NFX; ++p) cp[p] = crow[p] >= 0 ? a.arena_c[(size_t)crow[p] * a.H + j] : 0.f;
+                float c, h;
+                cell_update<KIND>(z, cp, 0.f, 0.f, 0, c, h);
+                const size_t o = (size_t)rres * a.H + j;
+                a.arena_c[o] = c;
+                Hout[o] = from_f<T>(h);
+            }
+            // one row at a time: keeps the unrolled epilogue's live registers
+            // (and the pressure on the chunk loop's allocation) small
+            __builtin_amdgcn_sched_barrier(0);
+        }
+}
+
+}  // namespace edbk

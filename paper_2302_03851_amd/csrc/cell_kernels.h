@@ -71,6 +71,8 @@ struct BatchArgs {
     const float* br;      // ragged bias [Hu]
     void* arena_h;        // [n_slots][H] of T
     float* arena_c;       // [n_slots][H]
+    int n_slots;          // arena rows
+    int n_xrows;          // rows of the x matrix xmat points to
 };
 
 template <int KIND> struct Kind;
@@ -95,14 +97,59 @@ __device__ __forceinline__ int seg_row(const Seg& s, int r) {
     return s.kind == S_CONTIG ? s.base + r : s.idx[r];
 }
 
-__device__ __forceinline__ float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
-__device__ __forceinline__ float tanh_f(float z) { return tanhf(z); }
+// Gate nonlinearities from the hardware exponential (v_exp_f32) and
+// reciprocal (v_rcp_f32), each about 1 ulp: the logistic function as
+// 1 / (1 + e^-z), and tanh z = 1 - 2 / (1 + e^{2z}) (exact limits +-1 when the
+// exponential overflows or vanishes).  Below |z| = 2^-9 tanh z = z to within
+// z^3/3, under half an fp32 ulp of z, which also avoids the cancellation
+// of the formula there.
+__device__ __forceinline__ float sigm(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
+__device__ __forceinline__ float tanh_f(float z) {
+    const float t = fmaf(-2.0f, __builtin_amdgcn_rcpf(1.0f + __expf(2.0f * z)), 1.0f);
+    return fabsf(z) < 0x1p-9f ? z : t;
+}
 
 __device__ __forceinline__ float to_f(float v) { return v; }
 __device__ __forceinline__ float to_f(__bf16 v) { return (float)v; }
 template <typename T> __device__ __forceinline__ T from_f(float v);
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ __bf16 from_f<__bf16>(float v) { return (__bf16)v; }
+
+// Gate nonlinearities and cell-state update of one (node, unit) element.
+// z: the G gate pre-activations (bias included), cp: child cell states of the
+// positional children, racc / rden: the ragged phase's sums (child-sum:
+// sum_k f_k c_k; lattice: sum_k e^{l_k} c_w^k and sum_k e^{l_k}), nw: number
+// of words ending at a lattice character.  Every multiply-add is an explicit
+// fmaf (the library is compiled without floating-point contraction), so the
+// update rounds identically in every kernel that uses it.
+template <int KIND>
+__device__ __forceinline__ void cell_update(const float* z, const float* cp, float racc, float rden, int nw,
+                                            float& c, float& h) {
+    if constexpr (KIND == K_CHAIN) {
+        c = fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[2]));
+        h = sigm(z[3]) * tanh_f(c);
+    } else if constexpr (KIND == K_NARY_LEAF || KIND == K_CS_LEAF) {
+        c = sigm(z[0]) * tanh_f(z[2]);
+        h = sigm(z[1]) * tanh_f(c);
+    } else if constexpr (KIND == K_NARY_INT || KIND == K_GRID) {
+        c = fmaf(sigm(z[2]), cp[1], fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[4])));
+        h = sigm(z[3]) * tanh_f(c);
+    } else if constexpr (KIND == K_CS_INT) {
+        c = fmaf(sigm(z[0]), tanh_f(z[2]), racc);
+        h = sigm(z[1]) * tanh_f(c);
+    } else if constexpr (KIND == K_LAT_WORD) {
+        c = fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[2]));
+        h = 0.f;
+    } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
+        if (nw == 0) {
+            c = fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[3]));
+        } else {
+            const float e0 = __expf(sigm(z[0]));
+            c = fmaf(e0, tanh_f(z[3]), racc) / (e0 + rden);
+        }
+        h = sigm(z[2]) * tanh_f(c);
+    }
+}
 
 // ---- LDS budget of one work-group (bytes) ----
 template <int KIND, typename T, int RT, int WU, int WK>
@@ -514,11 +561,11 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
                         for (int w = 0; w < WK; ++w) s += Zr[(w * TM + (e - cb)) * TU + u];
                         const float cw = a.arena_c[(size_t)seg_row(a.rag, e) * a.H + j];
                         if constexpr (KIND == K_CS_INT) {
-                            racc[q] += sigm(s) * cw;           // f_k * c_k
+                            racc[q] = fmaf(sigm(s), cw, racc[q]);   // f_k * c_k
                         } else {
                             const float l = sigm(zsum[q][4] + s);  // link gate of word k
                             const float ek = __expf(l);
-                            racc[q] += ek * cw;
+                            racc[q] = fmaf(ek, cw, racc[q]);
                             rden[q] += ek;
                         }
                     }
@@ -534,33 +581,9 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
         const int it = tid + NT * q, r = it / TU, u = it % TU;
         const int j = u0 + u;
         if (it >= NITEM || r >= nrows || j >= a.H) continue;
-        const float* z = zsum[q];
         float c, h;
-        if constexpr (KIND == K_CHAIN) {
-            c = sigm(z[1]) * cpre[q][0] + sigm(z[0]) * tanh_f(z[2]);
-            h = sigm(z[3]) * tanh_f(c);
-        } else if constexpr (KIND == K_NARY_LEAF || KIND == K_CS_LEAF) {
-            c = sigm(z[0]) * tanh_f(z[2]);
-            h = sigm(z[1]) * tanh_f(c);
-        } else if constexpr (KIND == K_NARY_INT || KIND == K_GRID) {
-            c = sigm(z[0]) * tanh_f(z[4]) + sigm(z[1]) * cpre[q][0] + sigm(z[2]) * cpre[q][1];
-            h = sigm(z[3]) * tanh_f(c);
-        } else if constexpr (KIND == K_CS_INT) {
-            c = sigm(z[0]) * tanh_f(z[2]) + racc[q];
-            h = sigm(z[1]) * tanh_f(c);
-        } else if constexpr (KIND == K_LAT_WORD) {
-            c = sigm(z[1]) * cpre[q][0] + sigm(z[0]) * tanh_f(z[2]);
-            h = 0.f;
-        } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
-            const int nw = a.rag_ptr[row0 + r + 1] - a.rag_ptr[row0 + r];
-            if (nw == 0) {
-                c = sigm(z[1]) * cpre[q][0] + sigm(z[0]) * tanh_f(z[3]);
-            } else {
-                const float e0 = __expf(sigm(z[0]));
-                c = (e0 * tanh_f(z[3]) + racc[q]) / (e0 + rden[q]);
-            }
-            h = sigm(z[2]) * tanh_f(c);
-        }
+        cell_update<KIND>(zsum[q], cpre[q], racc[q], rden[q],
+                          KIND == K_LAT_CHAR ? a.rag_ptr[row0 + r + 1] - a.rag_ptr[row0 + r] : 0, c, h);
         const size_t o = (size_t)rres[q] * a.H + j;
         a.arena_c[o] = c;
         Hout[o] = from_f<T>(h);

@@ -14,6 +14,7 @@
 #include <string>
 #include <vector>
 
+#include "big_tile.h"
 #include "cell_kernels.h"
 #include "edb_internal.h"
 
@@ -22,12 +23,16 @@ using namespace edbk;
 
 namespace {
 
-constexpr int NUM_VARIANTS = 8;
-// tile variants: rows per work-group 16*RT, units per work-group 16*WU,
+constexpr int NUM_SMALL = 8;
+constexpr int NUM_LARGE = 3;
+constexpr int NUM_VARIANTS = NUM_SMALL + NUM_LARGE;
+// small tile variants: rows per work-group 16*RT, units per work-group 16*WU,
 // WK waves splitting the reduction (threads per work-group 64*WU*WK)
-constexpr int VAR_RT[NUM_VARIANTS] = {2, 1, 1, 1, 1, 1, 2, 2};
-constexpr int VAR_WU[NUM_VARIANTS] = {4, 4, 2, 1, 1, 1, 1, 2};
-constexpr int VAR_WK[NUM_VARIANTS] = {1, 1, 2, 4, 8, 16, 4, 2};
+constexpr int VAR_RT[NUM_SMALL] = {2, 1, 1, 1, 1, 1, 2, 2};
+constexpr int VAR_WU[NUM_SMALL] = {4, 4, 2, 1, 1, 1, 1, 2};
+constexpr int VAR_WK[NUM_SMALL] = {1, 1, 2, 4, 8, 16, 4, 2};
+// large tile variants NUM_SMALL + vb: 32*big_rb(G, vb) rows x 64 units, 256 threads
+bool is_large(int v) { return v >= NUM_SMALL && v < NUM_VARIANTS; }
 
 struct KindInfo {
     int G, nfix;
@@ -233,6 +238,25 @@ Entry entry() {
     return {launch_cell<KIND, T, RT, WU, WK>, attr_cell<KIND, T, RT, WU, WK>, lds_cell<KIND, T, RT, WU, WK>};
 }
 
+// the large tile's LDS is static (its two stages are distinct objects)
+template <int KIND, int VB>
+void launch_big(const BatchArgs& a, int grid, int, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+    if (ev0)
+        hipExtLaunchKernelGGL((big_kernel<KIND, VB>), dim3(grid), dim3(256), 0, st, ev0, ev1, 0, a);
+    else
+        hipLaunchKernelGGL((big_kernel<KIND, VB>), dim3(grid), dim3(256), 0, st, a);
+}
+template <int KIND, int VB>
+hipError_t attr_big(int) { return hipSuccess; }
+template <int KIND, int VB>
+int lds_big(int) { return big_lds_bytes<KIND, VB>(); }
+
+template <int KIND, typename T, int VB>
+Entry big_entry() {
+    if constexpr (sizeof(T) == 2 && !Kind<KIND>::RAG) return {launch_big<KIND, VB>, attr_big<KIND, VB>, lds_big<KIND, VB>};
+    else return {nullptr, nullptr, nullptr};
+}
+
 template <int KIND, typename T>
 void fill_kind(Entry* e) {
     e[0] = entry<KIND, T, 2, 4, 1>();
@@ -243,6 +267,9 @@ void fill_kind(Entry* e) {
     e[5] = entry<KIND, T, 1, 1, 16>();
     e[6] = entry<KIND, T, 2, 1, 4>();
     e[7] = entry<KIND, T, 2, 2, 2>();
+    e[8] = big_entry<KIND, T, 0>();
+    e[9] = big_entry<KIND, T, 1>();
+    e[10] = big_entry<KIND, T, 2>();
 }
 
 struct Table {
@@ -320,6 +347,21 @@ double variant_cost(int v, int m, const Dims& d, int dtype) {
     return rounds * per_wave + 2500.0;
 }
 
+// Estimated cycles of one batch under large tile variant NUM_SMALL + vb: work-
+// groups of 4 waves (one per SIMD) resident lds-limited per CU, each running
+// its 64-wide k chunks (matrix-core cycles of a wave plus a per-chunk
+// synchronisation cost) after a fixed prologue.
+double large_cost(int vb, int m, const Dims& d, int lds, int n_cu, int max_lds) {
+    const int RB = big_rb(d.G, vb);
+    const int TM = 32 * RB;
+    const double tiles = (double)((m + TM - 1) / TM) * (d.Hu / (32 * BIG_CU));
+    const int per_cu = std::max(1, std::min(2, max_lds / std::max(lds, 1)));
+    const double rounds = std::ceil(tiles / (double)(n_cu * per_cu));
+    const int nch = (d.K / d.KG + 1) / 2;
+    const double per_wg = nch * (2.0 * BIG_CU * d.G * RB * 16.0 * 1.25 + 250.0) + 2000.0;
+    return rounds * per_wg + 2500.0;
+}
+
 }  // namespace
 
 // Per-device state shared by all executors: the LDS limit, a non-blocking
@@ -356,6 +398,7 @@ struct edb_exec {
     int32_t flags = 0;
     int32_t T = 0, B = 0, dtype = 0;
     int32_t n_slots = 0, n_x = 0, E = 0, H = 0;
+    int32_t x_direct_rows = 0;        // rows of the caller's x the plan addresses (max x_row + 1)
     std::vector<Dims> dims;
     std::vector<edb_cell> cells;
     std::vector<Launch> launches;     // [0] = staging, then one per batch
@@ -407,8 +450,11 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
     if (!out) return fail(EDB_ERR_INVALID, "edb_prepare: out is NULL");
     *out = nullptr;
     if (!g || !s || !p || !cells) return fail(EDB_ERR_INVALID, "edb_prepare: NULL argument");
-    if (flags & ~(EDB_USE_GRAPH | EDB_DRYRUN | EDB_FORCE_GATHER | EDB_X_DIRECT | EDB_PROFILE | EDB_NO_FLOW))
+    if (flags & ~(EDB_USE_GRAPH | EDB_DRYRUN | EDB_FORCE_GATHER | EDB_X_DIRECT | EDB_PROFILE | EDB_NO_FLOW |
+                  EDB_NO_SPLIT_K | EDB_TILE_LARGE | EDB_NO_LARGE))
         return fail(EDB_ERR_INVALID, "edb_prepare: unknown flags");
+    if ((flags & EDB_TILE_LARGE) && (flags & EDB_NO_LARGE))
+        return fail(EDB_ERR_INVALID, "edb_prepare: EDB_TILE_LARGE and EDB_NO_LARGE exclude each other");
     if (s->V != g->V || p->V != g->V || p->B != (int32_t)s->batch_type.size())
         return fail(EDB_ERR_INVALID, "edb_prepare: graph, schedule and plan do not match");
     const int32_t T = g->T, B = p->B;
@@ -446,8 +492,16 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
         e->dims = dims;
         e->cells.assign(cells, cells + T);
         int n_x = 0;
-        for (int32_t v = 0; v < g->V; ++v) n_x += p->x_slot[v] >= 0;
+        for (int32_t v = 0; v < g->V; ++v) {
+            n_x += p->x_slot[v] >= 0;
+            if (p->x_slot[v] >= 0) e->x_direct_rows = std::max(e->x_direct_rows, g->x_row[v] + 1);
+        }
         e->n_x = n_x;
+        // the large tile addresses x and the arena with 32-bit byte offsets
+        const int64_t esz_b = dtype == EDB_F32 ? 4 : 2;
+        const int64_t off_limit = (int64_t)1 << 31;
+        const bool large_fits = (int64_t)p->n_slots * H * esz_b + (1 << 20) < off_limit &&
+                                (int64_t)std::max(n_x, e->x_direct_rows) * std::max(E, 1) * esz_b + (1 << 20) < off_limit;
 
         // device int buffer: plan idx pool | ragged pool | x source rows | zero rows
         std::vector<int32_t>& hb = e->hbuf;
@@ -464,7 +518,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
         e->n_zero = 1 + (int32_t)p->pads.size();
         if (hb.empty()) hb.push_back(0);
 
-        int max_lds = 160 * 1024;
+        int max_lds = 160 * 1024, n_cu = 256;
         DeviceCtx* ctx = nullptr;
         if (!(flags & EDB_DRYRUN)) {
             int dev = 0;
@@ -476,6 +530,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             }
             e->device = dev;
             max_lds = ctx->max_lds;
+            n_cu = ctx->n_cu;
         }
         const int force_var = std::getenv("EDB_VARIANT") ? std::atoi(std::getenv("EDB_VARIANT")) : -1;
 
@@ -558,14 +613,28 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             const int kind_id = cells[t].kind;
             int var = -1;
             double best = 1e300;
+            // the large tile reads whole 64-wide k chunks of one operand segment
+            const bool large_ok = large_fits && d.Ep % 64 == 0 && d.Hk % 64 == 0;
+            const bool large_only = (flags & EDB_TILE_LARGE) && large_ok && table().e[kind_id][dtype][NUM_SMALL].launch;
             for (int vi = 0; vi < NUM_VARIANTS; ++vi) {
-                const int lds = table().e[kind_id][dtype][vi].lds(d.K);
+                const Entry& en = table().e[kind_id][dtype][vi];
+                if (!en.launch) continue;
+                const int lds = en.lds(d.K);
                 if (lds > max_lds) continue;
-                if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
-                const double est = variant_cost(vi, m, d, dtype);
+                double est;
+                if (is_large(vi)) {
+                    if ((flags & EDB_NO_LARGE) || !large_ok) continue;
+                    est = large_cost(vi - NUM_SMALL, m, d, lds, n_cu, max_lds);
+                } else {
+                    if (large_only) continue;
+                    if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
+                    if ((flags & EDB_NO_SPLIT_K) && VAR_WK[vi] != 1) continue;
+                    est = variant_cost(vi, m, d, dtype);
+                }
                 if (est < best * 0.97) { best = est; var = vi; }
             }
-            if (force_var >= 0 && force_var < NUM_VARIANTS) var = force_var;
+            if (force_var >= 0 && force_var < NUM_VARIANTS && table().e[kind_id][dtype][force_var].launch)
+                var = force_var;
             if (var < 0) {
                 delete e;
                 return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: no tile variant fits the LDS of batch " +
@@ -579,9 +648,16 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             }
             L.info.variant = var;
             L.info.n_batches = 1;
-            const int TM = 16 * VAR_RT[var], TU = 16 * VAR_WU[var];
-            L.info.grid = (m + TM - 1) / TM * (d.Hu / TU);
-            L.info.block = 64 * VAR_WU[var] * VAR_WK[var];
+            if (is_large(var)) {
+                const int TM = 32 * big_rb(d.G, var - NUM_SMALL);
+                const int tiles = (m + TM - 1) / TM * (d.Hu / (32 * BIG_CU));
+                L.info.grid = (tiles + 7) / 8 * 8;   // XCD-aware order: 8 equal tile ranges
+                L.info.block = 256;
+            } else {
+                const int TM = 16 * VAR_RT[var], TU = 16 * VAR_WU[var];
+                L.info.grid = (m + TM - 1) / TM * (d.Hu / TU);
+                L.info.block = 64 * VAR_WU[var] * VAR_WK[var];
+            }
             blaunch.push_back(L);
         }
 
@@ -913,6 +989,8 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
         a.arena_h = arena_h;
         a.arena_c = reinterpret_cast<float*>(arena_c);
         a.xmat = (e->flags & EDB_X_DIRECT) ? x : e->xstaged;
+        a.n_slots = e->n_slots;
+        a.n_xrows = (e->flags & EDB_X_DIRECT) ? e->x_direct_rows : e->n_x;
         if (L.off_x >= 0) a.x.idx = db + L.off_x;
         if (L.off_f0 >= 0) a.fix[0].idx = db + L.off_f0;
         if (L.off_f1 >= 0) a.fix[1].idx = db + L.off_f1;

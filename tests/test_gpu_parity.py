@@ -144,6 +144,65 @@ def test_layout_and_launch_mode_bitwise(k):
         np.testing.assert_array_equal(c, c0, err_msg=str(kw))
 
 
+def _grid_graph(n_grids, R, C, E, H, seed, dtype):
+    """n_grids independent R x C grids of GRID cells (children: left, top)."""
+    op, ch = [], []
+    for gi in range(n_grids):
+        base = gi * R * C
+        for i in range(R):
+            for j in range(C):
+                op.append(0)
+                ch.append([base + i * C + j - 1 if j > 0 else -1, base + (i - 1) * C + j if i > 0 else -1])
+    return WL.make_graph([WL.GRID], E, H, op, ch, [True] * len(op), seed=seed, dtype=dtype, bias_scale=0.2)
+
+
+def _large_tile_workloads():
+    """bf16 workloads whose batches span several large tiles with a ragged row
+    tail: the child-sum configuration (its leaf batch), grids with a
+    zero-padded x segment (E = 120 in a 128-wide segment) and padded units
+    (H = 192 of 256), chains, binary trees."""
+    out = [WL.make_config(5, instances=12), _grid_graph(24, 12, 12, 120, 192, seed=11, dtype="bf16")]
+    n = 300   # chains of length 3
+    op = [0] * (3 * n)
+    ch = [[-1] if i % 3 == 0 else [i - 1] for i in range(3 * n)]
+    out.append(WL.make_graph([WL.LSTM_CHAIN], 64, 128, op, ch, [True] * (3 * n), seed=12, dtype="bf16",
+                             bias_scale=0.2))
+    # binary trees: 200 two-leaf trees
+    op, ch, hx = [], [], []
+    for t in range(200):
+        op += [0, 0, 1]
+        ch += [[], [], [3 * t, 3 * t + 1]]
+        hx += [True, True, False]
+    out.append(WL.make_graph([WL.NARY_LEAF, WL.NARY_INTERNAL], 128, 256, op, ch, hx, seed=13, dtype="bf16",
+                             bias_scale=0.2))
+    return out
+
+
+@pytest.mark.parametrize("variant", [None, 8, 9, 10])
+def test_large_tile_bitwise_and_parity(variant, monkeypatch):
+    """The large bf16 tile (every supported batch forced onto it, or one size
+    class for all) is bitwise equal to the small tile without split-K, and
+    within the bf16 bound of the oracle."""
+    _torch()
+    for w in _large_tile_workloads():
+        monkeypatch.delenv("EDB_VARIANT", raising=False)
+        small = _fwd(w, flags=L.USE_GRAPH | L.NO_SPLIT_K | L.NO_LARGE)
+        small.run()
+        h0, c0 = small.states()
+        if variant is not None:
+            monkeypatch.setenv("EDB_VARIANT", str(variant))
+        f = _fwd(w, flags=L.USE_GRAPH | L.NO_SPLIT_K | L.TILE_LARGE)
+        used = {f.exec.launch_info(i)["variant"] for i in range(1, f.exec.launches())}
+        assert used & set(L.LARGE_VARIANTS), used
+        f.run()
+        h, c = f.states()
+        np.testing.assert_array_equal(h, h0, err_msg=f"{w.name} {w.kinds} variant {variant}")
+        np.testing.assert_array_equal(c, c0, err_msg=f"{w.name} {w.kinds} variant {variant}")
+        if variant is None:
+            hr, cr = _oracle(w)
+            _check(w, h, c, hr, cr, f"large tile {w.kinds}")
+
+
 DATAFLOW_OFF = ("dataflow launches are switched off: their first GPU runs did not drain "
                 "(cause not yet shown); every batch runs as its own launch")
 

@@ -230,7 +230,11 @@ def test_dryrun_launch_list(k, flow):
         t = int(f.sched.batch_type[b])
         assert info["kind"] == w.kinds[t]
         assert info["m"] == f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b]
-        assert 0 <= info["variant"] < 8 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
+        assert 0 <= info["variant"] <= 10 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
+        if info["variant"] in L.LARGE_VARIANTS:
+            # large bf16 tile: non-ragged kinds only, 256 threads, grid a multiple of 8
+            assert w.dtype == "bf16" and w.kinds[t] not in (WL.CS_INTERNAL, WL.LAT_CHAR)
+            assert info["block"] == 256 and info["grid"] % 8 == 0
         segs = f.plan.batch_segments(b)
         assert info["seg_kind"][0] == segs[0][0]
         seen.append(b)
@@ -239,6 +243,34 @@ def test_dryrun_launch_list(k, flow):
         assert n == 1 + B
     with pytest.raises(L.EdbError):
         f.exec.launch_info(n)
+
+
+LARGE_TILE_ROWS = {8: 256, 9: 128, 10: 64}   # rows per work-group of the large variants at G = 3
+
+
+def test_tile_flags_select_variants():
+    """EDB_TILE_LARGE puts every batch the large tile supports on it; EDB_NO_LARGE
+    and EDB_NO_SPLIT_K restrict the choice; the two large-tile flags exclude each other."""
+    w = WL.make_config(5, instances=12)
+    base = L.DRYRUN | L.NO_FLOW
+    f = edb.Forward(w, flags=base | L.TILE_LARGE)
+    for i in range(1, f.exec.launches()):
+        info = f.exec.launch_info(i)
+        if info["kind"] == WL.CS_LEAF:
+            assert info["variant"] in L.LARGE_VARIANTS
+            tm = LARGE_TILE_ROWS[info["variant"]]
+            assert info["grid"] == -(-(-(-info["m"] // tm) * (512 // 64)) // 8) * 8
+        else:
+            assert info["variant"] not in L.LARGE_VARIANTS
+    f = edb.Forward(w, flags=base | L.NO_LARGE | L.NO_SPLIT_K)
+    for i in range(1, f.exec.launches()):
+        assert f.exec.launch_info(i)["variant"] in (0, 1)
+    big = WL.make_config(5)
+    f = edb.Forward(big, flags=base)
+    assert f.exec.launch_info(1)["kind"] == WL.CS_LEAF and f.exec.launch_info(1)["variant"] in L.LARGE_VARIANTS
+    with pytest.raises(L.EdbError) as ei:
+        edb.Forward(w, flags=base | L.TILE_LARGE | L.NO_LARGE)
+    assert ei.value.status == L.EDB_ERR_INVALID
 
 
 def test_packed_weight_bytes_layout():
