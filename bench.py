@@ -37,11 +37,12 @@ WORKLOAD_TEXT = {
 
 
 def algorithmic_work(w, f):
-    """Per batch (flops, bytes) of the work the method must do: 2*K*N flops
-    per node over the present operands (x, present children) and N = gates*H,
-    plus the per-child GEMMs of child-sum forget gates and lattice link
-    gates; bytes = x rows, present children's h and c read, own h and c
-    written (weights are counted once per forward, separately)."""
+    """Per batch (main flops, per-child flops, bytes) of the work the method
+    must do: 2*K*N flops per node over the present operands (x, present
+    children) and N = gates*H; per-child flops are the GEMMs of child-sum
+    forget gates and lattice link gates; bytes = x rows, present children's h
+    and c read, own h and c written (weights are counted once per forward,
+    separately)."""
     from paper_2302_03851_amd import workloads as WL
     H, E = w.hidden, w.in_dim
     esz = 2 if w.dtype == "bf16" else 4
@@ -52,7 +53,7 @@ def algorithmic_work(w, f):
         t = int(f.sched.batch_type[b])
         k = w.kinds[t]
         nf = w.shapes()[t][0]
-        fl = by = 0
+        fl = flr = by = 0
         for v in f.sched.batch_nodes[f.sched.batch_ptr[b]:f.sched.batch_ptr[b + 1]]:
             ch = w.children(int(v))
             fixed = [c for c in ch[:nf] if c >= 0]
@@ -61,14 +62,29 @@ def algorithmic_work(w, f):
             Kp = (E if hasx else 0) + H * len(fixed)
             if k == WL.CS_INTERNAL:
                 Kp = H
-                fl += 2 * H * H * len(rag)                 # h_k U_f
+                flr += 2 * H * H * len(rag)                # h_k U_f
             if k == WL.LAT_CHAR and rag:
-                fl += 2 * E * H + 2 * H * H * len(rag)     # x W_lx, c_w W_lc
+                fl += 2 * E * H
+                flr += 2 * H * H * len(rag)                # x W_lx, c_w W_lc
             fl += 2 * Kp * G[k] * H
             by += (E * esz if hasx else 0) + len(fixed) * H * (esz + 4) + len(rag) * H * (esz + 4)
             by += H * (esz + 4)
-        out.append((fl, by))
+        out.append((fl, flr, by))
     return out
+
+
+def launch_work(info, work, split):
+    """Algorithmic flops of one launch: the whole batch, or for a child-sum
+    batch on the large tile (its batch index in `split`) its parts: part 2 the
+    per-child forget GEMM, part 1 the per-parent sums (no flops), part 0 the
+    parents' main GEMM."""
+    fl, flr, _ = work[info["batch"]]
+    part = info["part"]
+    if part == 2:
+        return flr
+    if part == 1:
+        return 0
+    return fl if info["batch"] in split else fl + flr
 
 
 def weight_bytes(w):
@@ -201,23 +217,32 @@ def main():
     times /= reps
     work = algorithmic_work(w, base)
     infos = [prof.launch_info(i) for i in range(prof.launches())]
+    split = {inf["batch"] for inf in infos[1:] if inf["part"] != 0}
+    # launches grouped by the kernel they run: (cell kind, tile variant, part)
     groups = {}
     for i, inf in enumerate(infos[1:], start=1):
-        key = (inf["kind"], inf["variant"])
-        gsum = groups.setdefault(key, [0.0, 0, 0, 0])
+        key = (inf["kind"], inf["variant"], inf["part"])
+        gsum = groups.setdefault(key, [0.0, 0, 0])
         gsum[0] += times[i]
         gsum[1] += 1
-        gsum[2] += work[inf["batch"]][0]
-        gsum[3] += work[inf["batch"]][1]
+        gsum[2] += launch_work(inf, work, split)
     dom = max(groups, key=lambda k: groups[k][0])
-    tot_ms, nl, fl, by = groups[dom]
+    tot_ms, nl, fl = groups[dom]
     avg_ms = tot_ms / nl
     tflops = (fl / nl) / (avg_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     kname = {0: "LSTM_CHAIN", 1: "NARY_LEAF", 2: "NARY_INTERNAL", 3: "GRID", 4: "CS_LEAF",
              5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD"}[dom[0]]
-    tot_flops = sum(x[0] for x in work)
-    tot_bytes = sum(x[1] for x in work) + weight_bytes(w)
+    kind_v, var_v, part_v = dom
+    if part_v == 1:
+        kernel = "child_reduce_kernel"
+    elif var_v in L.LARGE_VARIANTS:
+        kk = "CS_FORGET" if part_v == 2 else ("CS_PARENT" if kind_v == WL.CS_INTERNAL else kname)
+        kernel = f"big_kernel<{kk}, size class {var_v - 8}>"
+    else:
+        kernel = f"cell_kernel<{kname}, {w.dtype}, variant {var_v}>"
+    tot_flops = sum(x[0] + x[1] for x in work)
+    tot_bytes = sum(x[2] for x in work) + weight_bytes(w)
 
     result = {
         "metric": METRIC,
@@ -237,7 +262,7 @@ def main():
                    "step": "graph ingest + schedule + memory plan + launch prep + device execution"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(tflops / peak, 4), "traffic": None,
-                     "kernel": f"cell_kernel<{kname}, {w.dtype}, variant {dom[1]}>",
+                     "kernel": kernel,
                      "launches": nl, "avg_launch_us": round(avg_ms * 1e3, 2),
                      "alg_flops_per_launch": int(fl / nl)},
         "device_replay": {"ms_per_forward": round(ms_replay, 4),

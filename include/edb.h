@@ -277,7 +277,11 @@ typedef struct {
     int32_t grid;      /* work-groups */
     int32_t block;     /* threads per work-group */
     int32_t seg_kind[4]; /* kinds of result, child 0, child 1, ragged lists */
-    int32_t n_batches; /* batches the launch executes (0 for staging) */
+    int32_t n_batches; /* batches the launch executes (0 for staging and for parts 1, 2) */
+    int32_t part;      /* 0: the batch's cell kernel.  A child-sum batch on the large tile runs
+                          as three launches in this order: 2 the forget GEMM over its children
+                          (m = children), 1 per parent the child sum of h and the sum of the
+                          children's sigma(f_k) c_k, then 0 the parents */
 } edb_launch_info;
 edb_status edb_exec_launch_info(const edb_exec_t* e, int32_t i, edb_launch_info* info);
 

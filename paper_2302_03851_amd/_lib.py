@@ -25,6 +25,7 @@ F32, BF16 = 0, 1
 USE_GRAPH, DRYRUN, FORCE_GATHER, X_DIRECT, PROFILE, NO_FLOW = 1, 2, 4, 8, 16, 32
 NO_SPLIT_K, TILE_LARGE, NO_LARGE = 64, 128, 256
 LARGE_VARIANTS = (8, 9, 10)
+PART_CELL, PART_CHILD_SUM, PART_FORGET = 0, 1, 2
 FLOW_VARIANT = 100
 
 # every symbol include/edb.h declares
@@ -77,7 +78,7 @@ class Cell(C.Structure):
 class LaunchInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("kind", C.c_int32), ("m", C.c_int32), ("k", C.c_int32),
                 ("n", C.c_int32), ("variant", C.c_int32), ("grid", C.c_int32), ("block", C.c_int32),
-                ("seg_kind", C.c_int32 * 4), ("n_batches", C.c_int32)]
+                ("seg_kind", C.c_int32 * 4), ("n_batches", C.c_int32), ("part", C.c_int32)]
 
 
 _lib = None

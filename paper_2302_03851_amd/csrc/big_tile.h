@@ -56,6 +56,10 @@ __host__ __device__ constexpr int big_lds_bytes() {
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
+// 16-byte buffer load at byte offset off; zero past the end of the buffer.
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
 // Direct global -> LDS copy of 16 bytes per lane: lane l's bytes at byte
 // offset off land at lds + 16 l (lds is wave-uniform).  Offsets past the end
 // of the buffer read as zero.
@@ -220,44 +224,145 @@ __global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
         __syncthreads();
     }
     if (c < nch) big_compute<RB, CU, G>(acc, st0, reinterpret_cast<const uint4*>(st0 + A_BYTES), wr, wc, lane);
+    __syncthreads();   // the stages are free for the epilogue's operands
 
-    // ---- gate epilogue and scatter of h, c ----
-    T* Hout = reinterpret_cast<T*>(a.arena_h);
+    // ---- epilogue operands, copied into the stage buffers: rows of 64 fp32
+    // values (this tile's units), the first half of each list in st0 and the
+    // second in st1.  Cell kinds: the positional children's cell states.  The
+    // forget GEMM: the children's own cell states.  The parent GEMM: the sums
+    // of the children's products sigma(f_k) c_k (one row per parent) ----
+    constexpr int HALF = TM / 2;
+    constexpr int NCR = (KIND == K_CS_FORGET || KIND == K_CS_PARENT) ? 1 : NFX;
+    static_assert(NCR * HALF * 256 <= SB, "epilogue rows fit the stages");
+    const __amdgpu_buffer_rsrc_t rc = KIND == K_CS_PARENT
+                                          ? make_rsrc(a.fc, (uint32_t)a.m * (uint32_t)H * 4u)
+                                          : make_rsrc(a.arena_c, (uint32_t)a.n_slots * (uint32_t)H * 4u);
+    auto crow_ptr = [&](int p, int r) -> const float* {
+        const char* base = r < HALF ? st0 : st1;
+        return reinterpret_cast<const float*>(base + (p * HALF + (r < HALF ? r : r - HALF)) * 256);
+    };
+    if constexpr (NCR > 0) {
+#pragma unroll
+        for (int p = 0; p < NCR; ++p)
+#pragma unroll
+            for (int j = 0; j < TM / 16; ++j) {
+                const int r0 = (4 * j + wave) * 4;              // first of the copy's 4 rows (uniform)
+                const int r = r0 + (lane >> 4);
+                int srow = -1;
+                if (r < nrows) {
+                    if constexpr (KIND == K_CS_FORGET) srow = seg_row(a.x, row0 + r);
+                    else if constexpr (KIND == K_CS_PARENT) srow = row0 + r;
+                    else srow = a.fix[p].kind == S_NONE ? -1 : seg_row(a.fix[p], row0 + r);
+                }
+                const uint32_t off = srow >= 0 ? ((uint32_t)srow * (uint32_t)H + (uint32_t)u0) * 4u +
+                                                     (uint32_t)(lane & 15) * 16u
+                                               : OOB;
+                char* dst = (r0 < HALF ? st0 : st1) + (p * HALF + (r0 < HALF ? r0 : r0 - HALF)) * 256;
+                dma16(rc, off, dst);
+            }
+        __syncthreads();
+    }
+
     float bz[CU][G];   // bias of this lane's units (the packed bias is zero-padded to Hu)
 #pragma unroll
     for (int cu = 0; cu < CU; ++cu)
 #pragma unroll
         for (int g = 0; g < G; ++g) bz[cu][g] = a.bias[g * a.Hu + u0 + (wc * CU + cu) * 16 + (lane & 15)];
+
+    // ---- gate epilogue and scatter ----
+    T* Hout = reinterpret_cast<T*>(a.arena_h);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = wr * 16 * RB + rb * 16 + (lane >> 4) * 4 + i;
             if (r >= nrows) continue;
-            const int rres = seg_row(a.res, row0 + r);
-            int crow[NFX > 0 ? NFX : 1];
-#pragma unroll
-            for (int p = 0; p < NFX; ++p) crow[p] = a.fix[p].kind == S_NONE ? -1 : seg_row(a.fix[p], row0 + r);
+            const int rres = KIND == K_CS_FORGET ? row0 + r : seg_row(a.res, row0 + r);
 #pragma unroll
             for (int cu = 0; cu < CU; ++cu) {
-                const int j = u0 + (wc * CU + cu) * 16 + (lane & 15);
+                const int u = (wc * CU + cu) * 16 + (lane & 15), j = u0 + u;
                 if (j >= a.H) continue;
                 float z[G], cp[NFX > 0 ? NFX : 1];
 #pragma unroll
                 for (int g = 0; g < G; ++g) z[g] = acc[cu][g][rb][i] + bz[cu][g];
                 cp[0] = 0.f;
 #pragma unroll
-                for (int p = 0; p < NFX; ++p) cp[p] = crow[p] >= 0 ? a.arena_c[(size_t)crow[p] * a.H + j] : 0.f;
-                float c, h;
-                cell_update<KIND>(z, cp, 0.f, 0.f, 0, c, h);
+                for (int p = 0; p < NCR; ++p) cp[p] = crow_ptr(p, r)[u];
                 const size_t o = (size_t)rres * a.H + j;
-                a.arena_c[o] = c;
-                Hout[o] = from_f<T>(h);
+                if constexpr (KIND == K_CS_FORGET) {
+                    a.fc[o] = sigm(z[0]) * cp[0];   // sigma(f_k) c_k, row = position in the child list
+                } else {
+                    float c, h;
+                    if constexpr (KIND == K_CS_PARENT) cell_update<K_CS_INT>(z, cp, cp[0], 0.f, 0, c, h);
+                    else cell_update<KIND>(z, cp, 0.f, 0.f, 0, c, h);
+                    a.arena_c[o] = c;
+                    Hout[o] = from_f<T>(h);
+                }
             }
             // one row at a time: keeps the unrolled epilogue's live registers
             // (and the pressure on the chunk loop's allocation) small
             __builtin_amdgcn_sched_barrier(0);
         }
+}
+
+// Per parent of a child-sum batch, after the forget GEMM: the child sum of h,
+// hsum[r] = bf16(sum of the children's h rows, fp32, in child order) (the
+// rounding of the small tile's child-sum staging), and the sum of the
+// children's products, racc[r] = sum_k sigma(f_k) c_k in child order.  One
+// thread per 8 units of a row.
+__global__ __launch_bounds__(256) void child_reduce_kernel(BatchArgs a, __bf16* __restrict__ hsum,
+                                                           float* __restrict__ racc) {
+    using T = __bf16;
+    const int nv = a.H / 8;
+    const int it = blockIdx.x * 256 + threadIdx.x;
+    if (it >= a.m * nv) return;
+    const int r = it / nv, c = it - r * nv;
+    const T* h = reinterpret_cast<const T*>(a.arena_h);
+    const int e0 = a.rag_ptr[r], e1 = a.rag_ptr[r + 1];
+    float acc[8], sf[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = sf[i] = 0.f;
+    int e = e0;
+    for (; e + 4 <= e1; e += 4) {
+        uint4 raw[4];
+        float4 f[4][2];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            raw[n] = *reinterpret_cast<const uint4*>(h + (size_t)seg_row(a.rag, e + n) * a.H + c * 8);
+            f[n][0] = *reinterpret_cast<const float4*>(a.fc + (size_t)(e + n) * a.H + c * 8);
+            f[n][1] = *reinterpret_cast<const float4*>(a.fc + (size_t)(e + n) * a.H + c * 8 + 4);
+        }
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            const T* pv = reinterpret_cast<const T*>(&raw[n]);
+            const float* pf = reinterpret_cast<const float*>(&f[n][0]);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                acc[i] += to_f(pv[i]);
+                sf[i] += pf[i];
+            }
+        }
+    }
+    for (; e < e1; ++e) {
+        const uint4 raw = *reinterpret_cast<const uint4*>(h + (size_t)seg_row(a.rag, e) * a.H + c * 8);
+        float4 f[2];
+        f[0] = *reinterpret_cast<const float4*>(a.fc + (size_t)e * a.H + c * 8);
+        f[1] = *reinterpret_cast<const float4*>(a.fc + (size_t)e * a.H + c * 8 + 4);
+        const T* pv = reinterpret_cast<const T*>(&raw);
+        const float* pf = reinterpret_cast<const float*>(&f[0]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            acc[i] += to_f(pv[i]);
+            sf[i] += pf[i];
+        }
+    }
+    uint4 o;
+    T* po = reinterpret_cast<T*>(&o);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) po[i] = from_f<T>(acc[i]);
+    *reinterpret_cast<uint4*>(hsum + (size_t)r * a.H + c * 8) = o;
+    *reinterpret_cast<float4*>(racc + (size_t)r * a.H + c * 8) = make_float4(sf[0], sf[1], sf[2], sf[3]);
+    *reinterpret_cast<float4*>(racc + (size_t)r * a.H + c * 8 + 4) = make_float4(sf[4], sf[5], sf[6], sf[7]);
 }
 
 }  // namespace edbk

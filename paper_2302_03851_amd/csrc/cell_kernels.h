@@ -42,7 +42,10 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 enum { K_CHAIN = 0, K_NARY_LEAF = 1, K_NARY_INT = 2, K_GRID = 3, K_CS_LEAF = 4, K_CS_INT = 5,
-       K_LAT_CHAR = 6, K_LAT_WORD = 7 };
+       K_LAT_CHAR = 6, K_LAT_WORD = 7,
+       // the two GEMMs of a child-sum batch run on the large tile: the forget
+       // gates over the batch's child rows, then the parents on their child sums
+       K_CS_FORGET = 8, K_CS_PARENT = 9 };
 
 enum { S_NONE = 0, S_CONTIG = 1, S_INDEXED = 2 };
 
@@ -73,6 +76,7 @@ struct BatchArgs {
     float* arena_c;       // [n_slots][H]
     int n_slots;          // arena rows
     int n_xrows;          // rows of the x matrix xmat points to
+    float* fc;            // child-sum batches on the large tile: sigma(f_k) * c_k per child, [children][H]
 };
 
 template <int KIND> struct Kind;
@@ -84,6 +88,10 @@ template <> struct Kind<K_CS_LEAF>  { static constexpr int G = 3, NFIX = 0; stat
 template <> struct Kind<K_CS_INT>   { static constexpr int G = 3, NFIX = 0; static constexpr bool X = false, RAG = true;  };
 template <> struct Kind<K_LAT_CHAR> { static constexpr int G = 5, NFIX = 1; static constexpr bool X = true,  RAG = true;  };
 template <> struct Kind<K_LAT_WORD> { static constexpr int G = 3, NFIX = 1; static constexpr bool X = true,  RAG = false; };
+// rows: the batch's children (x = their h rows); one gate
+template <> struct Kind<K_CS_FORGET>{ static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
+// rows: the parents (x = their child sums of h)
+template <> struct Kind<K_CS_PARENT>{ static constexpr int G = 3, NFIX = 0; static constexpr bool X = true,  RAG = false; };
 
 template <typename T> struct Elem;
 template <> struct Elem<float>  { static constexpr int KG = 16; static constexpr int VEC = 4; };
@@ -561,7 +569,7 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
                         for (int w = 0; w < WK; ++w) s += Zr[(w * TM + (e - cb)) * TU + u];
                         const float cw = a.arena_c[(size_t)seg_row(a.rag, e) * a.H + j];
                         if constexpr (KIND == K_CS_INT) {
-                            racc[q] = fmaf(sigm(s), cw, racc[q]);   // f_k * c_k
+                            racc[q] += sigm(s) * cw;   // f_k * c_k, rounded, then added in child order
                         } else {
                             const float l = sigm(zsum[q][4] + s);  // link gate of word k
                             const float ek = __expf(l);

@@ -231,11 +231,13 @@ struct Entry {
     LaunchFn launch;
     AttrFn attr;
     int (*lds)(int);
+    const void* fn;   // the kernel (occupancy queries)
 };
 
 template <int KIND, typename T, int RT, int WU, int WK>
 Entry entry() {
-    return {launch_cell<KIND, T, RT, WU, WK>, attr_cell<KIND, T, RT, WU, WK>, lds_cell<KIND, T, RT, WU, WK>};
+    return {launch_cell<KIND, T, RT, WU, WK>, attr_cell<KIND, T, RT, WU, WK>, lds_cell<KIND, T, RT, WU, WK>,
+            reinterpret_cast<const void*>(&cell_kernel<KIND, T, RT, WU, WK>)};
 }
 
 // the large tile's LDS is static (its two stages are distinct objects)
@@ -253,9 +255,14 @@ int lds_big(int) { return big_lds_bytes<KIND, VB>(); }
 
 template <int KIND, typename T, int VB>
 Entry big_entry() {
-    if constexpr (sizeof(T) == 2 && !Kind<KIND>::RAG) return {launch_big<KIND, VB>, attr_big<KIND, VB>, lds_big<KIND, VB>};
-    else return {nullptr, nullptr, nullptr};
+    if constexpr (sizeof(T) == 2 && !Kind<KIND>::RAG)
+        return {launch_big<KIND, VB>, attr_big<KIND, VB>, lds_big<KIND, VB>,
+                reinterpret_cast<const void*>(&big_kernel<KIND, VB>)};
+    else return {nullptr, nullptr, nullptr, nullptr};
 }
+
+// Rows per work-group of large variant NUM_SMALL + vb for G gates.
+int large_tm(int G, int vb) { return 32 * big_rb(G, vb); }
 
 template <int KIND, typename T>
 void fill_kind(Entry* e) {
@@ -272,8 +279,20 @@ void fill_kind(Entry* e) {
     e[10] = big_entry<KIND, T, 2>();
 }
 
+// The internal kinds of a child-sum batch on the large tile have large bf16 variants only.
+template <int KIND>
+void fill_internal(Entry (&e)[2][NUM_VARIANTS]) {
+    for (int d = 0; d < 2; ++d)
+        for (int v = 0; v < NUM_VARIANTS; ++v) e[d][v] = {nullptr, nullptr, nullptr, nullptr};
+    e[1][8] = big_entry<KIND, __bf16, 0>();
+    e[1][9] = big_entry<KIND, __bf16, 1>();
+    e[1][10] = big_entry<KIND, __bf16, 2>();
+}
+
+constexpr int NUM_KERNEL_KINDS = 10;   // the 8 cell kinds, then K_CS_FORGET, K_CS_PARENT
+
 struct Table {
-    Entry e[8][2][NUM_VARIANTS];
+    Entry e[NUM_KERNEL_KINDS][2][NUM_VARIANTS];
     Table() {
         fill_kind<K_CHAIN, float>(e[0][0]);        fill_kind<K_CHAIN, __bf16>(e[0][1]);
         fill_kind<K_NARY_LEAF, float>(e[1][0]);    fill_kind<K_NARY_LEAF, __bf16>(e[1][1]);
@@ -283,6 +302,8 @@ struct Table {
         fill_kind<K_CS_INT, float>(e[5][0]);       fill_kind<K_CS_INT, __bf16>(e[5][1]);
         fill_kind<K_LAT_CHAR, float>(e[6][0]);     fill_kind<K_LAT_CHAR, __bf16>(e[6][1]);
         fill_kind<K_LAT_WORD, float>(e[7][0]);     fill_kind<K_LAT_WORD, __bf16>(e[7][1]);
+        fill_internal<K_CS_FORGET>(e[K_CS_FORGET]);
+        fill_internal<K_CS_PARENT>(e[K_CS_PARENT]);
     }
 };
 
@@ -295,6 +316,7 @@ const Table& table() {
 struct Launch {
     edb_launch_info info;
     int type;      // cell type (batches)
+    int kk = 0;    // kernel kind (the cell kind, or K_CS_FORGET / K_CS_PARENT)
     BatchArgs args;  // pointer fields to data buffers are filled at execute time
     // offsets into the device int buffer (-1 = none)
     int64_t off_x, off_f0, off_f1, off_rag, off_rptr, off_res;
@@ -334,7 +356,7 @@ int flow_lds(const std::vector<int>& kinds_k) {
 // are spread over the 1024 SIMDs; each wave runs its k-groups back to back
 // (matrix-core cycles plus a fixed per-k-group issue/latency cost) and then
 // the epilogue; plus a fixed launch and prologue latency.
-double variant_cost(int v, int m, const Dims& d, int dtype) {
+double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag = 0) {
     const int RT = VAR_RT[v], WU = VAR_WU[v], WK = VAR_WK[v];
     const int TM = 16 * RT, TU = 16 * WU;
     const double wgs = (double)((m + TM - 1) / TM) * (d.Hu / TU);
@@ -342,7 +364,14 @@ double variant_cost(int v, int m, const Dims& d, int dtype) {
     const int nkg = d.K / d.KG;
     const int kg_per_wave = (nkg + WK - 1) / WK;
     const double mfma_cyc = dtype == EDB_F32 ? 4 * 32.0 : 16.0;   // per gate and row block per k-group
-    const double per_wave = kg_per_wave * (d.G * RT * mfma_cyc + 120.0) + 40.0 * WK * RT * d.G;
+    double per_wave = kg_per_wave * (d.G * RT * mfma_cyc + 120.0) + 40.0 * WK * RT * d.G;
+    if (d.rag && m > 0) {
+        // ragged phase: the work-group's child rows in chunks of TM rows, one
+        // gate each, with a staging and two barriers per chunk
+        const double chunks = std::ceil((double)nrag / m * TM / TM);
+        const int rkg = (d.Hk / d.KG + WK - 1) / WK;
+        per_wave += chunks * (rkg * (RT * mfma_cyc + 120.0) + 3000.0);
+    }
     const double rounds = std::ceil(waves / 1024.0);
     return rounds * per_wave + 2500.0;
 }
@@ -351,15 +380,44 @@ double variant_cost(int v, int m, const Dims& d, int dtype) {
 // groups of 4 waves (one per SIMD) resident lds-limited per CU, each running
 // its 64-wide k chunks (matrix-core cycles of a wave plus a per-chunk
 // synchronisation cost) after a fixed prologue.
-double large_cost(int vb, int m, const Dims& d, int lds, int n_cu, int max_lds) {
-    const int RB = big_rb(d.G, vb);
-    const int TM = 32 * RB;
-    const double tiles = (double)((m + TM - 1) / TM) * (d.Hu / (32 * BIG_CU));
-    const int per_cu = std::max(1, std::min(2, max_lds / std::max(lds, 1)));
-    const double rounds = std::ceil(tiles / (double)(n_cu * per_cu));
-    const int nch = (d.K / d.KG + 1) / 2;
-    const double per_wg = nch * (2.0 * BIG_CU * d.G * RB * 16.0 * 1.25 + 250.0) + 2000.0;
-    return rounds * per_wg + 2500.0;
+// Estimated microseconds of the large tile for G gates over K (padded), m
+// rows, fitted to measurements on MI355X: a 64-wide chunk takes the L2->LDS
+// copy time of the work-groups resident on a CU (about 86 GB/s per CU at full
+// load) or their matrix-core time, whichever is longer (their sum with one
+// work-group per CU, which cannot overlap them), plus 0.3 us; the epilogue
+// about 7 us per 16k elements per CU.  extra_us: work outside the model.
+double large_cost(int G, int vb, int m, int K, int Hu, int per_cu, int n_cu, double extra_us = 0.0) {
+    const int TM = large_tm(G, vb), RB = TM / 32;
+    const double tiles = (double)((m + TM - 1) / TM) * (Hu / (32 * BIG_CU));
+    per_cu = std::max(1, std::min(2, per_cu));
+    const double rounds = std::max(1.0, tiles / (double)(n_cu * per_cu));
+    const int nch = K / BIG_BK;
+    const double bytes = (double)TM * 128 + 2.0 * BIG_CU * G * 2 * 1024;
+    const double t_bw = per_cu * bytes / 86e3;
+    const double t_mma = per_cu * 2.0 * BIG_CU * G * RB * 16 / 2400.0;
+    const double t_chunk = (per_cu >= 2 ? std::max(t_bw, t_mma) : t_bw + t_mma) + 0.3;
+    const double t_epi = 7.0 * (per_cu * TM * 32.0 * BIG_CU) / 16384.0 * std::max(G, 1) / 3.0;
+    return rounds * (nch * t_chunk + t_epi) + 3.0 + extra_us;
+}
+
+// Work-groups of 256 threads of a large-tile kernel resident on one CU: from
+// the runtime (registers and LDS) when a device is bound, else from LDS alone.
+using OccFn = std::function<int(const Entry&, int lds)>;
+
+// Best large variant (NUM_SMALL + vb) of kernel kind kk for m rows, or -1.
+int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max_lds, const OccFn& occ,
+               double& est, double extra_us = 0.0) {
+    int var = -1;
+    est = 1e300;
+    for (int vb = 0; vb < NUM_LARGE; ++vb) {
+        const Entry& en = table().e[kk][dtype][NUM_SMALL + vb];
+        if (!en.launch) continue;
+        const int lds = en.lds(K);
+        if (lds > max_lds) continue;
+        const double c = large_cost(G, vb, m, K, Hu, occ(en, lds), n_cu, extra_us);
+        if (c < est * 0.97) { est = c; var = NUM_SMALL + vb; }
+    }
+    return var;
 }
 
 }  // namespace
@@ -373,6 +431,7 @@ struct DeviceCtx {
     hipStream_t upload = nullptr;
     hipStream_t release = nullptr;   // stream-ordered frees wait here, off the upload path
     std::map<int, int> lds_granted;
+    std::map<const void*, int> occupancy;   // resident 256-thread work-groups per CU of a kernel
 };
 std::mutex g_ctx_mu;
 std::map<int, DeviceCtx> g_ctx;
@@ -399,6 +458,10 @@ struct edb_exec {
     int32_t T = 0, B = 0, dtype = 0;
     int32_t n_slots = 0, n_x = 0, E = 0, H = 0;
     int32_t x_direct_rows = 0;        // rows of the caller's x the plan addresses (max x_row + 1)
+    int64_t hsum_rows = 0, fc_rows = 0;   // scratch rows of child-sum batches on the large tile
+    void* hsum = nullptr;             // [hsum_rows][H] bf16: child sums of h
+    float* racc = nullptr;            // [hsum_rows][H] fp32: per parent, sum of the children's products
+    float* fc = nullptr;              // [fc_rows][H] fp32: sigma(f_k) c_k per child
     std::vector<Dims> dims;
     std::vector<edb_cell> cells;
     std::vector<Launch> launches;     // [0] = staging, then one per batch
@@ -498,9 +561,9 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
         }
         e->n_x = n_x;
         // the large tile addresses x and the arena with 32-bit byte offsets
-        const int64_t esz_b = dtype == EDB_F32 ? 4 : 2;
+        const int64_t esz_b = dtype == EDB_F32 ? 4 : 2;   // x element size
         const int64_t off_limit = (int64_t)1 << 31;
-        const bool large_fits = (int64_t)p->n_slots * H * esz_b + (1 << 20) < off_limit &&
+        const bool large_fits = (int64_t)p->n_slots * H * 4 + (1 << 20) < off_limit &&   // arena_c (and arena_h)
                                 (int64_t)std::max(n_x, e->x_direct_rows) * std::max(E, 1) * esz_b + (1 << 20) < off_limit;
 
         // device int buffer: plan idx pool | ragged pool | x source rows | zero rows
@@ -533,6 +596,20 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             n_cu = ctx->n_cu;
         }
         const int force_var = std::getenv("EDB_VARIANT") ? std::atoi(std::getenv("EDB_VARIANT")) : -1;
+        const OccFn occ = [&](const Entry& en, int lds) -> int {
+            const int by_lds = max_lds / std::max(lds, 1);
+            if (!ctx || !en.fn) return by_lds;
+            std::lock_guard<std::mutex> lk(g_ctx_mu);
+            auto it = ctx->occupancy.find(en.fn);
+            if (it != ctx->occupancy.end()) return it->second;
+            int nb = 0;
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, en.fn, 256, 0) != hipSuccess) {
+                (void)hipGetLastError();
+                nb = by_lds;
+            }
+            ctx->occupancy[en.fn] = nb;
+            return nb;
+        };
 
         // launch 0: x staging + zero rows
         {
@@ -547,7 +624,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             e->launches.push_back(L);
         }
         const bool force_gather = (flags & EDB_FORCE_GATHER) != 0;
-        std::vector<Launch> blaunch;
+        std::vector<std::vector<Launch>> blaunch;   // the launches of each batch, in order
         blaunch.reserve(B);
         for (int32_t b = 0; b < B; ++b) {
             const int32_t t = s->batch_type[b];
@@ -611,36 +688,102 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             // to the larger tile; variants whose LDS need exceeds the device
             // limit are skipped
             const int kind_id = cells[t].kind;
+            L.kk = kind_id;
             int var = -1;
             double best = 1e300;
             // the large tile reads whole 64-wide k chunks of one operand segment
-            const bool large_ok = large_fits && d.Ep % 64 == 0 && d.Hk % 64 == 0;
-            const bool large_only = (flags & EDB_TILE_LARGE) && large_ok && table().e[kind_id][dtype][NUM_SMALL].launch;
-            for (int vi = 0; vi < NUM_VARIANTS; ++vi) {
+            const bool large_ok = large_fits && d.Ep % 64 == 0 && d.Hk % 64 == 0 && !(flags & EDB_NO_LARGE);
+            const bool cs_large = kind_id == EDB_CELL_CS_INTERNAL && dtype == EDB_BF16;
+            const int64_t nrag = d.rag ? p->ragged_pool[p->ragged_off[b] + m] : 0;   // children of the batch
+            // large tile: the cell's own kernel, or for child-sum cells the
+            // child sums, the forget GEMM over the children and the parents
+            int lvar = -1, fvar = -1;
+            double lest = 1e300;
+            if (large_ok && cs_large) {
+                if (nrag > 0 && nrag * (int64_t)d.H * 4 + (1 << 20) < ((int64_t)1 << 31)) {
+                    double ef = 0, ep = 0;
+                    fvar = best_large(K_CS_FORGET, dtype, 1, (int)nrag, d.K, d.Hu, n_cu, max_lds, occ, ef);
+                    lvar = best_large(K_CS_PARENT, dtype, 3, m, d.K, d.Hu, n_cu, max_lds, occ, ep);
+                    if (fvar < 0 || lvar < 0) lvar = fvar = -1;
+                    else lest = ef + ep + 4.0;   // + the child-reduce kernel
+                }
+            } else if (large_ok) {
+                lvar = best_large(kind_id, dtype, d.G, m, d.K, d.Hu, n_cu, max_lds, occ, lest);
+            }
+            const bool large_only = (flags & EDB_TILE_LARGE) && lvar >= 0;
+            for (int vi = 0; vi < NUM_SMALL && !large_only; ++vi) {
                 const Entry& en = table().e[kind_id][dtype][vi];
                 if (!en.launch) continue;
                 const int lds = en.lds(d.K);
                 if (lds > max_lds) continue;
-                double est;
-                if (is_large(vi)) {
-                    if ((flags & EDB_NO_LARGE) || !large_ok) continue;
-                    est = large_cost(vi - NUM_SMALL, m, d, lds, n_cu, max_lds);
-                } else {
-                    if (large_only) continue;
-                    if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
-                    if ((flags & EDB_NO_SPLIT_K) && VAR_WK[vi] != 1) continue;
-                    est = variant_cost(vi, m, d, dtype);
-                }
+                if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
+                if ((flags & EDB_NO_SPLIT_K) && VAR_WK[vi] != 1) continue;
+                const double est = variant_cost(vi, m, d, dtype, nrag);
                 if (est < best * 0.97) { best = est; var = vi; }
             }
-            if (force_var >= 0 && force_var < NUM_VARIANTS && table().e[kind_id][dtype][force_var].launch)
-                var = force_var;
+            // large tile for batches whose main GEMM has at least 4e8 multiply-adds
+            // (measured: from there on it beats the small tiles at bf16, K = 512)
+            (void)lest;
+            const bool big_gemm = (double)m * d.K * d.G * d.Hu >= 4e8;
+            if (lvar >= 0 && (large_only || var < 0 || big_gemm)) var = lvar;
+            if (force_var >= 0 && force_var < NUM_SMALL && table().e[kind_id][dtype][force_var].launch) var = force_var;
+            if (is_large(force_var) && lvar >= 0) {
+                const int fk = cs_large ? K_CS_PARENT : kind_id;
+                if (table().e[fk][dtype][force_var].launch) var = lvar = force_var;
+                if (cs_large && table().e[K_CS_FORGET][dtype][force_var].launch) fvar = force_var;
+            }
             if (var < 0) {
                 delete e;
                 return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: no tile variant fits the LDS of batch " +
                                                      std::to_string(b));
             }
-            L.lds = table().e[kind_id][dtype][var].lds(d.K);
+            std::vector<Launch> parts;
+            if (is_large(var) && cs_large) {
+                // 2: forget GEMM over the batch's children (rows: the child list): sigma(f_k) c_k
+                Launch F = L;
+                F.kk = K_CS_FORGET;
+                F.info.part = 2;
+                F.info.variant = fvar;
+                F.info.n_batches = 0;
+                F.info.m = (int)nrag;
+                F.info.k = d.K;
+                F.info.n = d.Hu;
+                F.args.kind = K_CS_FORGET;
+                F.args.m = (int)nrag;
+                F.args.x = L.args.rag;
+                F.off_x = L.off_rag;
+                F.args.E = d.H;
+                F.args.Ep = d.Hk;
+                F.args.res = Seg{S_NONE, 0, nullptr};
+                F.off_res = -1;
+                F.lds = table().e[K_CS_FORGET][dtype][fvar].lds(d.K);
+                F.info.block = 256;
+                F.info.grid = ((int)((nrag + large_tm(1, fvar - NUM_SMALL) - 1) / large_tm(1, fvar - NUM_SMALL)) *
+                                   (d.Hu / (32 * BIG_CU)) + 7) / 8 * 8;
+                parts.push_back(F);
+                // 1: per parent, the child sum of h (h~) and the sum of the children's products
+                Launch C = L;
+                C.kk = -1;
+                C.lds = 0;
+                C.info.part = 1;
+                C.info.variant = -1;
+                C.info.n_batches = 0;
+                C.info.k = 0;
+                C.info.n = d.H;
+                C.info.block = 256;
+                C.info.grid = (int)(((int64_t)m * (d.H / 8) + 255) / 256);
+                parts.push_back(C);
+                // 0: the parents on their child sums (their children's products summed)
+                L.kk = K_CS_PARENT;
+                L.args.kind = K_CS_PARENT;
+                L.args.x = Seg{S_CONTIG, 0, nullptr};
+                L.off_x = -1;
+                L.args.E = d.H;
+                L.args.Ep = d.Hk;
+                e->hsum_rows = std::max<int64_t>(e->hsum_rows, m);
+                e->fc_rows = std::max<int64_t>(e->fc_rows, nrag);
+            }
+            L.lds = table().e[L.kk][dtype][var].lds(d.K);
             if (L.lds > max_lds) {
                 delete e;
                 return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: LDS need of batch " + std::to_string(b) +
@@ -648,8 +791,9 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             }
             L.info.variant = var;
             L.info.n_batches = 1;
+            L.info.part = 0;
             if (is_large(var)) {
-                const int TM = 32 * big_rb(d.G, var - NUM_SMALL);
+                const int TM = large_tm(d.G, var - NUM_SMALL);
                 const int tiles = (m + TM - 1) / TM * (d.Hu / (32 * BIG_CU));
                 L.info.grid = (tiles + 7) / 8 * 8;   // XCD-aware order: 8 equal tile ranges
                 L.info.block = 256;
@@ -658,7 +802,8 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 L.info.grid = (m + TM - 1) / TM * (d.Hu / TU);
                 L.info.block = 64 * VAR_WU[var] * VAR_WK[var];
             }
-            blaunch.push_back(L);
+            parts.push_back(L);
+            blaunch.push_back(std::move(parts));
         }
 
         // ---- dataflow runs: maximal runs (>= 2) of consecutive batches with at
@@ -678,9 +823,9 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             int b = 0, nrun = 0;
             while (b < B) {
                 const int m0 = s->batch_ptr[b + 1] - s->batch_ptr[b];
-                if (!flow_on || m0 > flow_max_m) { ++b; continue; }
+                if (!flow_on || m0 > flow_max_m || blaunch[b].size() != 1) { ++b; continue; }
                 int b1 = b;
-                while (b1 < B && s->batch_ptr[b1 + 1] - s->batch_ptr[b1] <= flow_max_m) ++b1;
+                while (b1 < B && s->batch_ptr[b1 + 1] - s->batch_ptr[b1] <= flow_max_m && blaunch[b1].size() == 1) ++b1;
                 if (b1 - b >= 2) {
                     for (int q = b; q < b1; ++q) run_of[q] = nrun;
                     ++nrun;
@@ -700,7 +845,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
         int64_t n_counters = 0;
         for (int32_t b = 0; b < B;) {
             if (run_of[b] < 0) {
-                e->launches.push_back(blaunch[b]);
+                for (const Launch& Lp : blaunch[b]) e->launches.push_back(Lp);
                 ++b;
                 continue;
             }
@@ -720,7 +865,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             F.f_desc = (int64_t)hb.size();
             std::vector<int> kinds_k;
             for (int q = b; q < b1; ++q) {
-                const Launch& L = blaunch[q];
+                const Launch& L = blaunch[q].back();
                 const Dims& d = dims[L.type];
                 BatchDesc bd{};
                 bd.kind = L.info.kind;
@@ -747,14 +892,14 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             }
             // row tiles and their producer row tiles inside the run
             std::vector<int> rt_base(b1 - b + 1, 0);
-            const int nut = dims[blaunch[b].type].Hu / (16 * FLOW_WU);
+            const int nut = dims[blaunch[b].back().type].Hu / (16 * FLOW_WU);
             for (int q = b; q < b1; ++q)
-                rt_base[q - b + 1] = rt_base[q - b] + (blaunch[q].args.m + 16 * FLOW_RT - 1) / (16 * FLOW_RT);
+                rt_base[q - b + 1] = rt_base[q - b] + (blaunch[q].back().args.m + 16 * FLOW_RT - 1) / (16 * FLOW_RT);
             const int nrt = rt_base[b1 - b];
             std::vector<int32_t> rtdeps(2 * nrt), deps, tmp;
             for (int q = b; q < b1; ++q) {
                 const int32_t* ord = p->order.data() + s->batch_ptr[q];
-                const int m = blaunch[q].args.m;
+                const int m = blaunch[q].back().args.m;
                 for (int rt = 0; rt * 16 * FLOW_RT < m; ++rt) {
                     tmp.clear();
                     for (int r = rt * 16 * FLOW_RT; r < std::min(m, (rt + 1) * 16 * FLOW_RT); ++r) {
@@ -778,7 +923,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             align_hb(4);
             F.f_tiles = (int64_t)hb.size();
             for (int q = b; q < b1; ++q) {
-                const int m = blaunch[q].args.m;
+                const int m = blaunch[q].back().args.m;
                 for (int rt = 0; rt * 16 * FLOW_RT < m; ++rt)
                     for (int ut = 0; ut < nut; ++ut) {
                         hb.push_back(q - b);
@@ -855,18 +1000,26 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             // the `ready` event instead of the host waiting for the copy
             const size_t ibytes = (hb.size() * sizeof(int32_t) + 255) / 256 * 256;
             const size_t xbytes = (n_x > 0 && !(flags & EDB_X_DIRECT)) ? (size_t)n_x * E * (dtype == EDB_F32 ? 4 : 2) : 0;
+            auto al256 = [](size_t v) { return (v + 255) / 256 * 256; };
+            const size_t hbytes = al256((size_t)e->hsum_rows * H * 2), rbytes = al256((size_t)e->hsum_rows * H * 4);
+            const size_t fbytes = (size_t)e->fc_rows * H * 4;
+            const size_t total = ibytes + al256(xbytes) + hbytes + rbytes + fbytes;
             e->upload = ctx->upload;
             e->release = ctx->release;
-            hipError_t he = hipMallocAsync(&e->dmem, ibytes + xbytes, ctx->upload);
+            hipError_t he = hipMallocAsync(&e->dmem, total, ctx->upload);
             if (he != hipSuccess) {
                 (void)hipGetLastError();
                 e->dmem = nullptr;
                 e->dmem_async = false;
-                he = hipMalloc(&e->dmem, ibytes + xbytes);
+                he = hipMalloc(&e->dmem, total);
             }
             if (he == hipSuccess) {
+                uint8_t* base = reinterpret_cast<uint8_t*>(e->dmem);
                 e->dbuf = reinterpret_cast<int*>(e->dmem);
-                e->xstaged = xbytes ? reinterpret_cast<uint8_t*>(e->dmem) + ibytes : nullptr;
+                e->xstaged = xbytes ? base + ibytes : nullptr;
+                e->hsum = hbytes ? base + ibytes + al256(xbytes) : nullptr;
+                e->racc = rbytes ? reinterpret_cast<float*>(base + ibytes + al256(xbytes) + hbytes) : nullptr;
+                e->fc = fbytes ? reinterpret_cast<float*>(base + ibytes + al256(xbytes) + hbytes + rbytes) : nullptr;
                 he = hipMemcpyAsync(e->dbuf, hb.data(), hb.size() * sizeof(int32_t), hipMemcpyHostToDevice, ctx->upload);
             }
             if (he == hipSuccess) he = hipEventCreateWithFlags(&e->ready, hipEventDisableTiming);
@@ -879,12 +1032,12 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             }
             for (size_t i = 1; he == hipSuccess && i < e->launches.size(); ++i) {
                 const Launch& L = e->launches[i];
-                if (L.lds <= 64 * 1024) continue;
-                const int key = (L.info.kind * 2 + dtype) * NUM_VARIANTS + L.info.variant;
+                if (L.lds <= 64 * 1024 || L.flow || L.kk < 0) continue;
+                const int key = (L.kk * 2 + dtype) * NUM_VARIANTS + L.info.variant;
                 std::lock_guard<std::mutex> lk(g_ctx_mu);
                 int& granted = ctx->lds_granted[key];
                 if (L.lds > granted) {
-                    he = table().e[L.info.kind][dtype][L.info.variant].attr(L.lds);
+                    he = table().e[L.kk][dtype][L.info.variant].attr(L.lds);
                     if (he == hipSuccess) granted = L.lds;
                 }
             }
@@ -991,14 +1144,34 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
         a.xmat = (e->flags & EDB_X_DIRECT) ? x : e->xstaged;
         a.n_slots = e->n_slots;
         a.n_xrows = (e->flags & EDB_X_DIRECT) ? e->x_direct_rows : e->n_x;
+        a.fc = e->fc;
         if (L.off_x >= 0) a.x.idx = db + L.off_x;
         if (L.off_f0 >= 0) a.fix[0].idx = db + L.off_f0;
         if (L.off_f1 >= 0) a.fix[1].idx = db + L.off_f1;
         if (L.off_rag >= 0) a.rag.idx = db + L.off_rag;
         if (L.off_rptr >= 0) a.rag_ptr = db + L.off_rptr;
         if (L.off_res >= 0) a.res.idx = db + L.off_res;
-        table().e[L.info.kind][e->dtype][L.info.variant].launch(a, L.info.grid, L.lds, st, prof ? ev[2 * i] : nullptr,
-                                                                 prof ? ev[2 * i + 1] : nullptr);
+        hipEvent_t e0 = prof ? ev[2 * i] : nullptr, e1 = prof ? ev[2 * i + 1] : nullptr;
+        if (L.kk < 0) {   // child-sum batch on the large tile: child sums and product sums
+            __bf16* out = reinterpret_cast<__bf16*>(e->hsum);
+            if (prof)
+                hipExtLaunchKernelGGL(child_reduce_kernel, dim3(L.info.grid), dim3(256), 0, st, e0, e1, 0, a, out,
+                                      e->racc);
+            else
+                hipLaunchKernelGGL(child_reduce_kernel, dim3(L.info.grid), dim3(256), 0, st, a, out, e->racc);
+            continue;
+        }
+        if (L.kk == K_CS_FORGET) {   // rows: the children's h; weights U_f, b_f
+            a.W = a.Wr;
+            a.bias = a.br;
+            a.xmat = arena_h;
+            a.n_xrows = e->n_slots;
+        } else if (L.kk == K_CS_PARENT) {   // rows: the child sums; epilogue: the product sums
+            a.xmat = e->hsum;
+            a.n_xrows = a.m;
+            a.fc = e->racc;
+        }
+        table().e[L.kk][e->dtype][L.info.variant].launch(a, L.info.grid, L.lds, st, e0, e1);
     }
     return hipGetLastError();
 }

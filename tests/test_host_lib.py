@@ -226,26 +226,41 @@ def test_dryrun_launch_list(k, flow):
             assert 1 <= info["grid"] and info["block"] == 256
             seen += list(range(b, b + info["n_batches"]))
             continue
-        assert info["n_batches"] == 1
         t = int(f.sched.batch_type[b])
         assert info["kind"] == w.kinds[t]
+        if info["part"] != L.PART_CELL:
+            # child-sum batch on the large tile: the forget GEMM over the batch's
+            # children, then the per-parent sums, then (below) the parents
+            assert w.kinds[t] == WL.CS_INTERNAL and w.dtype == "bf16" and info["n_batches"] == 0
+            nxt = f.exec.launch_info(i + 1)
+            assert nxt["batch"] == b and nxt["part"] == info["part"] - 1
+            if info["part"] == L.PART_FORGET:
+                nodes = f.sched.batch_nodes[f.sched.batch_ptr[b]:f.sched.batch_ptr[b + 1]]
+                assert info["m"] == sum(int((w.children(int(v)) >= 0).sum()) for v in nodes)
+                assert info["variant"] in L.LARGE_VARIANTS
+                assert f.exec.launch_info(i + 2)["variant"] in L.LARGE_VARIANTS
+            continue
+        assert info["n_batches"] == 1
         assert info["m"] == f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b]
         assert 0 <= info["variant"] <= 10 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
         if info["variant"] in L.LARGE_VARIANTS:
-            # large bf16 tile: non-ragged kinds only, 256 threads, grid a multiple of 8
-            assert w.dtype == "bf16" and w.kinds[t] not in (WL.CS_INTERNAL, WL.LAT_CHAR)
+            # large bf16 tile: every kind but the lattice character cell, 256 threads,
+            # grid a multiple of 8
+            assert w.dtype == "bf16" and w.kinds[t] != WL.LAT_CHAR
             assert info["block"] == 256 and info["grid"] % 8 == 0
         segs = f.plan.batch_segments(b)
         assert info["seg_kind"][0] == segs[0][0]
         seen.append(b)
     assert seen == list(range(B))          # every batch exactly once, in schedule order
     if not flow:
-        assert n == 1 + B
+        parts = [f.exec.launch_info(i)["part"] for i in range(1, n)]
+        assert n == 1 + B + sum(p != L.PART_CELL for p in parts)
     with pytest.raises(L.EdbError):
         f.exec.launch_info(n)
 
 
-LARGE_TILE_ROWS = {8: 256, 9: 128, 10: 64}   # rows per work-group of the large variants at G = 3
+LARGE_TILE_ROWS = {8: 256, 9: 128, 10: 64}      # rows per work-group of the large variants at G = 3
+LARGE_TILE_ROWS_G1 = {8: 256, 9: 128, 10: 64}   # the one-gate forget GEMM of child-sum cells
 
 
 def test_tile_flags_select_variants():
@@ -256,12 +271,13 @@ def test_tile_flags_select_variants():
     f = edb.Forward(w, flags=base | L.TILE_LARGE)
     for i in range(1, f.exec.launches()):
         info = f.exec.launch_info(i)
-        if info["kind"] == WL.CS_LEAF:
-            assert info["variant"] in L.LARGE_VARIANTS
-            tm = LARGE_TILE_ROWS[info["variant"]]
-            assert info["grid"] == -(-(-(-info["m"] // tm) * (512 // 64)) // 8) * 8
-        else:
-            assert info["variant"] not in L.LARGE_VARIANTS
+        if info["part"] == L.PART_CHILD_SUM:
+            assert info["grid"] == -(-info["m"] * (512 // 8) // 256)
+            continue
+        assert info["variant"] in L.LARGE_VARIANTS
+        rows = LARGE_TILE_ROWS_G1 if info["part"] == L.PART_FORGET else LARGE_TILE_ROWS
+        tm = rows[info["variant"]]
+        assert info["grid"] == -(-(-(-info["m"] // tm) * (512 // 64)) // 8) * 8
     f = edb.Forward(w, flags=base | L.NO_LARGE | L.NO_SPLIT_K)
     for i in range(1, f.exec.launches()):
         assert f.exec.launch_info(i)["variant"] in (0, 1)
