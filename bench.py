@@ -87,6 +87,89 @@ def launch_work(info, work, split):
     return fl if info["batch"] in split else fl + flr
 
 
+# small-tile variants (rows 16*RT, units 16*WU, split-K WK), in the library's order
+SMALL_VARIANTS = [(2, 4, 1), (1, 4, 1), (1, 2, 2), (1, 1, 4), (1, 1, 8), (1, 1, 16), (2, 1, 4), (2, 2, 2)]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def kernel_symbol(kind, dtype, variant, part):
+    """The kernel a launch runs, as rocprofv3 prints its name (prefix)."""
+    if part == 1:
+        return "edbk::child_reduce_kernel"
+    if variant >= 8:
+        kk = 8 if part == 2 else (9 if kind == 5 else kind)
+        return f"edbk::big_kernel<{kk}, {variant - 8}>"
+    rt, wu, wk = SMALL_VARIANTS[variant]
+    return f"edbk::cell_kernel<{kind}, {'float' if dtype == 'f32' else '__bf16'}, {rt}, {wu}, {wk}>"
+
+
+def source_digest():
+    """SHA-256 over the kernel sources (counters taken on other code are stale)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2302_03851_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".h", ".hip", ".cpp")):
+            h.update(f.encode())
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_from(d, workload):
+    """Reduce rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs (KiB per dispatch)
+    to HBM bytes per dispatch per kernel, scaled by what the same counters
+    read for a plain copy of known size, into profiles/traffic.json."""
+    import csv
+    import glob
+
+    def per_kernel(path):
+        acc = {}
+        for r in csv.DictReader(open(path)):
+            acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return acc
+
+    def one(pattern):
+        m = glob.glob(os.path.join(d, pattern))
+        if len(m) != 1:
+            raise SystemExit(f"expected one file for {pattern} under {d}, found {m}")
+        return m[0]
+
+    scale = {}
+    for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+        cp = per_kernel(one(f"copy_{ctr}/*counter_collection.csv"))
+        vals = [v for k, vs in cp.items() if "copyBuffer" in k for v in vs]
+        scale[ctr] = (256 << 10) / (sum(vals) / len(vals))   # 256 MiB per copy, in KiB
+    fetch = per_kernel(one("c2_FETCH_SIZE/*counter_collection.csv"))
+    write = per_kernel(one("c2_WRITE_SIZE/*counter_collection.csv"))
+    out = {"workload": workload, "source_sha256": source_digest(),
+           "fetch_scale": round(scale["FETCH_SIZE"], 4), "write_scale": round(scale["WRITE_SIZE"], 4),
+           "kernels": {}}
+    for k in sorted(set(fetch) & set(write)):
+        f, w_ = fetch[k], write[k]
+        out["kernels"][k] = {"dispatches": len(f),
+                             "fetch_bytes": round(sum(f) / len(f) * 1024 * scale["FETCH_SIZE"]),
+                             "write_bytes": round(sum(w_) / len(w_) * 1024 * scale["WRITE_SIZE"])}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(f"wrote {TRAFFIC_FILE}: {len(out['kernels'])} kernels, scales {scale}")
+
+
+def traffic_of(symbol, workload):
+    """HBM bytes per launch of a kernel from the committed counter record, or
+    None when there is none for this workload or the sources have changed."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("workload") != workload or rec.get("source_sha256") != source_digest():
+        return None
+    for name, v in rec["kernels"].items():
+        if name.startswith("void " + symbol) or name.startswith(symbol):
+            return v["fetch_bytes"] + v["write_bytes"]
+    return None
+
+
 def weight_bytes(w):
     esz = 2 if w.dtype == "bf16" else 4
     return sum(int(np.prod(m.shape)) * (esz if m.ndim == 2 else 4) for d in w.weights for m in d.values())
@@ -120,7 +203,15 @@ def main():
     ap.add_argument("--streams", type=int, default=8,
                     help="mini-batches in flight: host worker threads, each with its own stream and arena")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of 256 MiB, 5 times (to scale HBM byte counters)")
+    ap.add_argument("--traffic-from", metavar="DIR",
+                    help="write profiles/traffic.json from rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR "
+                         "(c2_<counter>/ of this benchmark, copy_<counter>/ of --copy-calibration)")
     args = ap.parse_args()
+    if args.traffic_from:
+        traffic_from(args.traffic_from, WORKLOAD_TEXT[args.config])
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); the path shards by "
               "instance with no exchange, see the design notes", file=sys.stderr)
@@ -133,6 +224,16 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        # a plain copy of known size: each dispatch reads and writes 256 MiB
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": src.numel() * 4, "copy_bytes_written": dst.numel() * 4,
+                          "copies": 5}), flush=True)
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = WL.make_config(args.config)
@@ -154,36 +255,58 @@ def main():
     arenas = [(ahp, acp)] + [(torch.empty_like(base.arena_h), torch.empty_like(base.arena_c)) for _ in range(S - 1)]
     arena_ptrs = [arenas[0]] + [(a.data_ptr(), c.data_ptr()) for a, c in arenas[1:]]
 
+    # the launches of worker stream 0's timed steps record start/stop HIP
+    # events in their dispatch packets (EDB_PROFILE); those executors are kept
+    # until the timed region has ended and are then read.  The other streams
+    # run without events (the events cost host time on every step).
     fwd = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
                           table=table)
+    fwd_prof = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
+                               table=table, flags=L.PROFILE)
     n_rows = base.plan.n_slots
 
-    def step(i):
+    def step(i, keep):
         # a1 graph ingest, a2 schedule, a3 memory plan, descriptor upload and
         # a4..a8 device execution (asynchronous), in one C call
         ah, ac = arena_ptrs[i]
-        fwd.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream)
+        if i == 0:
+            keep.append(fwd_prof.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream, keep=True))
+        else:
+            fwd.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream)
 
     def run_steps(n):
         """n steps spread over S worker threads (each its own stream and arena)."""
+        keeps = [[] for _ in range(S)]
         if S == 1:
             for _ in range(n):
-                step(0)
-            return
+                step(0, keeps[0])
+            return keeps
         counts = [n // S + (1 if i < n % S else 0) for i in range(S)]
-        ths = [threading.Thread(target=lambda i=i: [step(i) for _ in range(counts[i])]) for i in range(S)]
+        ths = [threading.Thread(target=lambda i=i: [step(i, keeps[i]) for _ in range(counts[i])]) for i in range(S)]
         for t in ths:
             t.start()
         for t in ths:
             t.join()
+        return keeps
 
     run_steps(args.warmup)
     torch.cuda.synchronize()
+    # untimed priming pass of as many steps as the timed region: the timed
+    # steps' executors are kept until the region ends, and their timing events
+    # then come from the pool these return to (not created on the host path)
+    primed = run_steps(args.steps)
+    torch.cuda.synchronize()
+    del primed
     t0 = time.perf_counter()
-    run_steps(args.steps)
+    timed = run_steps(args.steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    records = [r for rs in timed for r in rs]
+    n_profiled = len(records)
+    rec_infos = [records[0].launch_info(i) for i in range(records[0].launches())]
+    rec_times = np.array([r.launch_times() for r in records])     # [steps][launches] ms
+    del records, timed
 
     # device-only rate: the captured HIP graph of the same batch sequence replayed
     for _ in range(10):
@@ -207,16 +330,10 @@ def main():
         ex = edb.Exec(g, s, p, base.cells, 0)
     ms_host = (time.perf_counter() - th) * 1e3 / nh
 
-    # per-launch durations with HIP events on the execution stream
-    prof = edb.Exec(base.graph, base.sched, base.plan, base.cells, L.PROFILE)
-    reps = 20
-    times = np.zeros(prof.launches())
-    for _ in range(reps):
-        prof.execute(wptrs, xp, ahp, acp, stream)
-        times += prof.launch_times()
-    times /= reps
+    # per-launch durations: the timed region's own events, averaged over its steps
+    times = rec_times.mean(axis=0)
     work = algorithmic_work(w, base)
-    infos = [prof.launch_info(i) for i in range(prof.launches())]
+    infos = rec_infos
     split = {inf["batch"] for inf in infos[1:] if inf["part"] != 0}
     # launches grouped by the kernel they run: (cell kind, tile variant, part)
     groups = {}
@@ -241,6 +358,8 @@ def main():
         kernel = f"big_kernel<{kk}, size class {var_v - 8}>"
     else:
         kernel = f"cell_kernel<{kname}, {w.dtype}, variant {var_v}>"
+    symbol = kernel_symbol(kind_v, w.dtype, var_v, part_v)
+    traffic = traffic_of(symbol, WORKLOAD_TEXT[args.config])
     tot_flops = sum(x[0] + x[1] for x in work)
     tot_bytes = sum(x[2] for x in work) + weight_bytes(w)
 
@@ -261,9 +380,10 @@ def main():
                    "launches_per_step": base.exec.launches(), "mini_batches_in_flight": S,
                    "step": "graph ingest + schedule + memory plan + launch prep + device execution"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(tflops / peak, 4), "traffic": None,
-                     "kernel": kernel,
+                     "frac": round(tflops / peak, 4), "traffic": traffic,
+                     "kernel": kernel, "symbol": symbol,
                      "launches": nl, "avg_launch_us": round(avg_ms * 1e3, 2),
+                     "timing": f"HIP events in the dispatch packets of the {n_profiled} timed steps on worker stream 0",
                      "alg_flops_per_launch": int(fl / nl)},
         "device_replay": {"ms_per_forward": round(ms_replay, 4),
                           "node_cells_per_s": round(V / (ms_replay * 1e-3), 1),

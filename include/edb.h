@@ -299,13 +299,16 @@ edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
  * after the work.  Arguments are those of the individual calls; arena_h and
  * arena_c must hold at least the plan's n_slots rows (arena_rows), which is
  * returned in *n_slots (may be NULL) also when the arena is too small
- * (EDB_ERR_INVALID).  EDB_DRYRUN is rejected. */
+ * (EDB_ERR_INVALID).  EDB_DRYRUN is rejected.
+ * exec_out (may be NULL): on success receives the executor instead of it
+ * being freed; the caller reads edb_exec_launch_info and, with EDB_PROFILE in
+ * exec_flags, edb_exec_launch_times, and releases it with edb_exec_free. */
 edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
                        const int64_t* child_ptr, const int32_t* child_idx, const int32_t* x_row,
                        const edb_policy* policy, const edb_operand_shape* shapes, int32_t plan_flags,
                        const edb_cell* cells, int32_t exec_flags, const void* const* packed_weights,
                        const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
-                       int32_t* n_slots);
+                       int32_t* n_slots, edb_exec_t** exec_out);
 
 /* Wait for `stream` and check the last execution's dataflow launches:
  * EDB_ERR_HIP if a bounded wait timed out (the results are then invalid). */

@@ -120,7 +120,7 @@ def load():
         "edb_exec_free": (None, [vp]),
         "edb_forward": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32), P(C.c_int32),
                                     P(Policy), P(OperandShape), C.c_int32, P(Cell), C.c_int32, P(vp), vp, vp, vp,
-                                    C.c_int64, vp, P(C.c_int32)]),
+                                    C.c_int64, vp, P(C.c_int32), P(vp)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

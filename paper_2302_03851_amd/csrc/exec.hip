@@ -432,6 +432,7 @@ struct DeviceCtx {
     hipStream_t release = nullptr;   // stream-ordered frees wait here, off the upload path
     std::map<int, int> lds_granted;
     std::map<const void*, int> occupancy;   // resident 256-thread work-groups per CU of a kernel
+    std::vector<hipEvent_t> event_pool;      // timing events of freed EDB_PROFILE executors, for reuse
 };
 std::mutex g_ctx_mu;
 std::map<int, DeviceCtx> g_ctx;
@@ -486,8 +487,18 @@ struct edb_exec {
     bool profiled = false;
     int device = -1;
 
+    DeviceCtx* ctx = nullptr;
+
     ~edb_exec() {
-        for (hipEvent_t ev : events) (void)hipEventDestroy(ev);
+        // timing events go back to the device's pool (creating them costs
+        // host time on every profiled mini-batch)
+        if (ctx && !events.empty()) {
+            std::lock_guard<std::mutex> lk(g_ctx_mu);
+            for (hipEvent_t ev : events)
+                if (ev) ctx->event_pool.push_back(ev);
+        } else {
+            for (hipEvent_t ev : events) (void)hipEventDestroy(ev);
+        }
         if (gexec) (void)hipGraphExecDestroy(gexec);
         if (graph) (void)hipGraphDestroy(graph);
         if (cap_stream) (void)hipStreamDestroy(cap_stream);
@@ -1026,9 +1037,17 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             if (he == hipSuccess) he = hipEventCreateWithFlags(&e->done, hipEventDisableTiming);
             if (he == hipSuccess) he = hipEventRecord(e->ready, ctx->upload);
             if (flags & EDB_PROFILE) {
+                e->ctx = ctx;
                 e->events.assign(2 * e->launches.size(), nullptr);
+                {
+                    std::lock_guard<std::mutex> lk(g_ctx_mu);
+                    for (size_t i = 0; i < e->events.size() && !ctx->event_pool.empty(); ++i) {
+                        e->events[i] = ctx->event_pool.back();
+                        ctx->event_pool.pop_back();
+                    }
+                }
                 for (size_t i = 0; he == hipSuccess && i < e->events.size(); ++i)
-                    he = hipEventCreate(&e->events[i]);
+                    if (!e->events[i]) he = hipEventCreate(&e->events[i]);
             }
             for (size_t i = 1; he == hipSuccess && i < e->launches.size(); ++i) {
                 const Launch& L = e->launches[i];

@@ -2,7 +2,9 @@
 // preparation and asynchronous execution (the whole hot path, Algorithm 1 and
 // Section 3.1 of ED-Batch), with every host object released before return.
 // Device buffers owned by the executor are freed in stream order after the
-// work completes, so the call never waits for the GPU.
+// work completes, so the call never waits for the GPU.  The executor can be
+// handed back instead (exec_out) to read its launch records and, under
+// EDB_PROFILE, the per-launch times.
 #include <string>
 
 #include "edb_internal.h"
@@ -12,7 +14,8 @@ extern "C" edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_
                                   const edb_policy* policy, const edb_operand_shape* shapes, int32_t plan_flags,
                                   const edb_cell* cells, int32_t exec_flags, const void* const* packed_weights,
                                   const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
-                                  int32_t* n_slots) {
+                                  int32_t* n_slots, edb_exec_t** exec_out) {
+    if (exec_out) *exec_out = nullptr;
     if (exec_flags & EDB_DRYRUN) return edb::fail(EDB_ERR_INVALID, "edb_forward: EDB_DRYRUN is not allowed");
     edb_graph_t* g = nullptr;
     edb_schedule_t* s = nullptr;
@@ -31,7 +34,8 @@ extern "C" edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_
     if (st == EDB_OK) st = edb_execute(e, packed_weights, x, arena_h, arena_c, stream);
     // keep the error text of the failing step across the frees below
     const std::string err = st == EDB_OK ? std::string() : std::string(edb_last_error());
-    edb_exec_free(e);
+    if (st == EDB_OK && exec_out) *exec_out = e;
+    else edb_exec_free(e);
     edb_plan_free(p);
     edb_schedule_free(s);
     edb_graph_free(g);

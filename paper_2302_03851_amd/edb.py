@@ -236,11 +236,43 @@ class ForwardCall:
                       plan_mode, self._cells, flags)
         self.n_slots = C.c_int32()
 
-    def call(self, weight_ptrs, x_ptr, arena_h_ptr, arena_c_ptr, arena_rows, stream):
+    def call(self, weight_ptrs, x_ptr, arena_h_ptr, arena_c_ptr, arena_rows, stream, keep=False):
+        """Run the path; with keep=True return the executor (ExecRecord) for its
+        launch records and, under EDB_PROFILE, its per-launch times."""
         arr = (C.c_void_p * len(weight_ptrs))(*weight_ptrs)
+        h = C.c_void_p()
         L.check(L.load().edb_forward(*self._args, arr, C.c_void_p(x_ptr), C.c_void_p(arena_h_ptr),
                                      C.c_void_p(arena_c_ptr), arena_rows, C.c_void_p(stream),
-                                     C.byref(self.n_slots)), "edb_forward")
+                                     C.byref(self.n_slots), C.byref(h) if keep else None), "edb_forward")
+        return ExecRecord(h) if keep else None
+
+
+class ExecRecord:
+    """An executor handed back by edb_forward: launch records and times."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def launches(self) -> int:
+        n = C.c_int32()
+        L.check(L.load().edb_exec_launches(self.handle, C.byref(n)))
+        return n.value
+
+    def launch_info(self, i) -> Dict:
+        info = L.LaunchInfo()
+        L.check(L.load().edb_exec_launch_info(self.handle, i, C.byref(info)))
+        return {f: (list(getattr(info, f)) if f == "seg_kind" else getattr(info, f)) for f, _ in info._fields_}
+
+    def launch_times(self) -> np.ndarray:
+        n = self.launches()
+        out = (C.c_float * n)()
+        L.check(L.load().edb_exec_launch_times(self.handle, out, n), "edb_exec_launch_times")
+        return np.array(out[:], dtype=np.float64)
+
+    def __del__(self):
+        if getattr(self, "handle", None) and L is not None and L._lib is not None:
+            L._lib.edb_exec_free(self.handle)
+            self.handle = None
 
 
 def operand_shapes(w) -> List[Tuple[int, int, int]]:
