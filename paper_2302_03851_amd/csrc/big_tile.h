@@ -119,8 +119,10 @@ __device__ __forceinline__ void big_compute(v4f (&acc)[CU][G][RB], const char* A
     }
 }
 
+// One tile: rows [TM*(tile / nut), +TM) x units [TU*(tile % nut), +TU) of the
+// batch, all gates.  st0 / st1: the kernel's two LDS stages.
 template <int KIND, int VB>
-__global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
+__device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0, char* st1) {
     using KT = Kind<KIND>;
     using T = __bf16;
     constexpr int G = KT::G, NFX = KT::NFIX;
@@ -132,18 +134,8 @@ __global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
     constexpr int A_BYTES = TM * 128;
     static_assert(!KT::RAG, "ragged kinds use the small tile");
     static_assert(NSEG >= 1, "a cell has at least one operand segment");
-    // two stages as distinct objects: the compiler can then tell that the
-    // copies into one stage do not alias the reads of the other and does not
-    // wait for the copies before the reads
-    __shared__ __align__(16) char st0[SB];
-    __shared__ __align__(16) char st1[SB];
 
-    // ---- XCD-aware tile order ----
     const int nut = a.Hu / TU;
-    const int ntile = ((a.m + TM - 1) / TM) * nut;
-    const int per = (ntile + 7) / 8;
-    const int tile = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
-    if (tile >= ntile) return;
     const int row0 = (tile / nut) * TM, u0 = (tile % nut) * TU;
     const int nrows = min(TM, a.m - row0);
 
@@ -303,6 +295,27 @@ __global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
             // (and the pressure on the chunk loop's allocation) small
             __builtin_amdgcn_sched_barrier(0);
         }
+}
+
+// Two stages as distinct objects: the compiler can then tell that the copies
+// into one stage do not alias the reads of the other and does not wait for
+// the copies before the reads.
+#define EDB_BIG_STAGES(KIND, VB)                                                                       \
+    constexpr int SB_ = big_stage_bytes<Kind<KIND>::G, big_rb(Kind<KIND>::G, VB), BIG_CU>();          \
+    __shared__ __align__(16) char st0[SB_];                                                         \
+    __shared__ __align__(16) char st1[SB_]
+
+// One work-group per tile, in XCD-aware order.
+template <int KIND, int VB>
+__global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
+    EDB_BIG_STAGES(KIND, VB);
+    constexpr int TM = 32 * big_rb(Kind<KIND>::G, VB), TU = 32 * BIG_CU;
+    const int nut = a.Hu / TU;
+    const int ntile = ((a.m + TM - 1) / TM) * nut;
+    const int per = (ntile + 7) / 8;
+    const int tile = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    if (tile >= ntile) return;
+    big_tile<KIND, VB>(a, tile, st0, st1);
 }
 
 // Per parent of a child-sum batch, after the forget GEMM: the child sum of h,

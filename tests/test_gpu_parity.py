@@ -203,6 +203,57 @@ def test_large_tile_bitwise_and_parity(variant, monkeypatch):
             _check(w, h, c, hr, cr, f"large tile {w.kinds}")
 
 
+def test_large_tile_indexed_operands_bitwise():
+    """On the large tile, indexed operand lists (forced gathers, x read in place
+    through its row list, the identity layout with every list indexed) give
+    bitwise the states of the planned layout's contiguous lists."""
+    _torch()
+    w = WL.make_config(5, instances=12)
+    base = _fwd(w, flags=L.USE_GRAPH | L.TILE_LARGE)
+    assert any(base.exec.launch_info(i)["part"] == L.PART_FORGET for i in range(1, base.exec.launches()))
+    base.run()
+    h0, c0 = base.states()
+    for kw in (dict(flags=L.USE_GRAPH | L.TILE_LARGE | L.FORCE_GATHER),
+               dict(flags=L.USE_GRAPH | L.TILE_LARGE | L.X_DIRECT),
+               dict(flags=L.USE_GRAPH | L.TILE_LARGE, plan_mode=L.PLAN_IDENTITY)):
+        f = _fwd(w, **kw)
+        f.run()
+        h, c = f.states()
+        np.testing.assert_array_equal(h, h0, err_msg=str(kw))
+        np.testing.assert_array_equal(c, c0, err_msg=str(kw))
+
+
+def test_large_tile_child_sum_many_children():
+    """Child-sum parents with up to 9 children on the large tile (the per-parent
+    reduction's loop beyond 4 children) against the small tile and the oracle."""
+    _torch()
+    rng = np.random.default_rng(21)
+    op, ch, hx = [], [], []
+    for t in range(160):                 # 160 two-level trees, root arity 1..9
+        k = int(rng.integers(1, 10))
+        leaves = list(range(len(op), len(op) + k))
+        op += [0] * k
+        ch += [[]] * k
+        hx += [True] * k
+        op.append(1)
+        ch.append(leaves)
+        hx.append(False)
+    w = WL.make_graph([WL.CS_LEAF, WL.CS_INTERNAL], 512, 512, op, ch, hx, seed=22, dtype="bf16",
+                      scale=0.05, bias_scale=0.2)
+    small = _fwd(w, flags=L.USE_GRAPH | L.NO_SPLIT_K | L.NO_LARGE)
+    small.run()
+    h0, c0 = small.states()
+    f = _fwd(w, flags=L.USE_GRAPH | L.NO_SPLIT_K | L.TILE_LARGE)
+    parts = [f.exec.launch_info(i)["part"] for i in range(1, f.exec.launches())]
+    assert L.PART_CHILD_SUM in parts and L.PART_FORGET in parts
+    f.run()
+    h, c = f.states()
+    np.testing.assert_array_equal(h, h0)
+    np.testing.assert_array_equal(c, c0)
+    hr, cr = _oracle(w)
+    _check(w, h, c, hr, cr, "child-sum up to 9 children, large tile")
+
+
 DATAFLOW_OFF = ("dataflow launches are switched off: their first GPU runs did not drain "
                 "(cause not yet shown); every batch runs as its own launch")
 
