@@ -159,18 +159,28 @@ __device__ __forceinline__ void cell_update(const float* z, const float* cp, flo
     }
 }
 
+// Row blocks per chunk of the ragged phase (child-sum children, lattice
+// words): at least 4 (64 rows), so that the children of a tile's parents
+// usually fit one chunk.
+template <int KIND, int RT>
+__host__ __device__ constexpr int rag_rt() {
+    return Kind<KIND>::RAG ? (RT < 4 ? 4 : RT) : RT;
+}
+
 // ---- LDS budget of one work-group (bytes) ----
 template <int KIND, typename T, int RT, int WU, int WK>
 __host__ __device__ constexpr int lds_a_bytes(int K) {
-    return 16 * RT * (K + a_pad<T>()) * (int)sizeof(T);
+    // ragged kinds reuse A for the chunk's child rows (Hk <= K columns)
+    return 16 * rag_rt<KIND, RT>() * (K + a_pad<T>()) * (int)sizeof(T);
 }
 template <int KIND, typename T, int RT, int WU, int WK>
 __host__ __device__ constexpr int lds_z_bytes() {
     return WK * 16 * RT * Kind<KIND>::G * 16 * WU * 4;
 }
+// Zr (the chunk's per-child GEMM partials) and Crag (its cell states)
 template <int KIND, typename T, int RT, int WU, int WK>
 __host__ __device__ constexpr int lds_zr_bytes() {
-    return Kind<KIND>::RAG ? WK * 16 * RT * 16 * WU * 4 : 0;
+    return Kind<KIND>::RAG ? (WK + 1) * 16 * rag_rt<KIND, RT>() * 16 * WU * 4 : 0;
 }
 // Offset of Z: after A for kinds with a ragged phase (A is reused for child
 // rows while Z must persist), else Z aliases A (written after the GEMM).
@@ -510,26 +520,43 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
 #pragma unroll
     for (int q = 0; q < NI; ++q) { racc[q] = 0.f; rden[q] = 0.f; }
     if constexpr (KT::RAG) {
+        // children (words) of the tile's parents in chunks of TMR rows: their
+        // h rows (child-sum) or cell states (lattice) staged to A, their cell
+        // states for this tile's units to Crag, the per-child GEMM to Zr
+        constexpr int TMR = 16 * rag_rt<KIND, RT>();
+        float* Crag = Zr + WK * TMR * TU;
         const int cbeg = a.rag_ptr[row0];
         const int cend = a.rag_ptr[row0 + nrows];
         const int nkgr = a.Hk / KG;
         const uint4* Brag = reinterpret_cast<const uint4*>(a.Wr) + ((size_t)ub * nkgr) * 64 + lane;
         const int rk0 = (nkgr * wk) / WK, rk1 = (nkgr * (wk + 1)) / WK;
         const int RS = a.Hk + AS_PAD;
-        for (int cb = cbeg; cb < cend; cb += TM) {
-            const int cn = min(TM, cend - cb);
-            __syncthreads();   // previous chunk's readers of A / Zr are done
+        int pe0[NI], pe1[NI];   // child range of each item's parent
+#pragma unroll
+        for (int q = 0; q < NI; ++q) {
+            const int it = tid + NT * q, r = it / TU;
+            const bool ok = it < NITEM && r < nrows;
+            pe0[q] = ok ? a.rag_ptr[row0 + r] : 0;
+            pe1[q] = ok ? a.rag_ptr[row0 + r + 1] : 0;
+        }
+        for (int cb = cbeg; cb < cend; cb += TMR) {
+            const int cn = min(TMR, cend - cb);
+            __syncthreads();   // previous chunk's readers of A / Zr / Crag are done
             BRing<1, 4> rring;
             ring_prologue<1, 4>(rring, Brag, nkgr, rk0, rk1);
+            for (int it = tid; it < TMR * TU; it += NT) {
+                const int r = it / TU, j = u0 + it % TU;
+                Crag[it] = (r < cn && j < a.H) ? a.arena_c[(size_t)seg_row(a.rag, cb + r) * a.H + j] : 0.f;
+            }
             if constexpr (KIND == K_CS_INT) {
                 constexpr int V = Elem<T>::VEC;
                 ASeg<T> sg[1] = {ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.rag, cb, 0, a.Hk / V, a.H / V, a.H}};
-                stage_tile<T, TM, NT, 1>(A, RS, sg, cn, tid);
+                stage_tile<T, TMR, NT, 1>(A, RS, sg, cn, tid);
             } else {
                 // lattice: the word cell states c_w (fp32) converted to T
                 constexpr int V = Elem<T>::VEC;
                 const int nv = a.Hk / V, nreal = a.H / V;
-                for (int it = tid; it < TM * nv; it += NT) {
+                for (int it = tid; it < TMR * nv; it += NT) {
                     const int r = it / nv, c = it % nv;
                     uint4 out = make_uint4(0, 0, 0, 0);
                     T* po = reinterpret_cast<T*>(&out);
@@ -543,39 +570,39 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
             }
             __syncthreads();
             {
-                v4f acc[1][RT];
+                constexpr int RTR = TMR / 16;
+                v4f acc[1][RTR];
 #pragma unroll
-                for (int rt = 0; rt < RT; ++rt) acc[0][rt] = v4f{0.f, 0.f, 0.f, 0.f};
-                if (rk0 < rk1) wave_gemm<T, 1, RT, 4>(acc, A, RS, Brag, nkgr, rk0, rk1, lane, rring);
+                for (int rt = 0; rt < RTR; ++rt) acc[0][rt] = v4f{0.f, 0.f, 0.f, 0.f};
+                if (rk0 < rk1) wave_gemm<T, 1, RTR, 4>(acc, A, RS, Brag, nkgr, rk0, rk1, lane, rring);
 #pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
+                for (int rt = 0; rt < RTR; ++rt)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int r = rt * 16 + (lane >> 4) * 4 + i;
                         const int u = wu * 16 + (lane & 15);
-                        Zr[(wk * TM + r) * TU + u] = acc[0][rt][i];
+                        Zr[(wk * TMR + r) * TU + u] = acc[0][rt][i];
                     }
             }
             __syncthreads();
 #pragma unroll
             for (int q = 0; q < NI; ++q) {
-                const int it = tid + NT * q, r = it / TU, u = it % TU;
+                const int it = tid + NT * q, u = it % TU;
                 const int j = u0 + u;
-                if (it < NITEM && r < nrows && j < a.H) {
-                    const int e0 = max(a.rag_ptr[row0 + r], cb), e1 = min(a.rag_ptr[row0 + r + 1], cb + cn);
-                    for (int e = e0; e < e1; ++e) {
-                        float s = a.br[j];
+                if (j >= a.H) continue;
+                const int e0 = max(pe0[q], cb), e1 = min(pe1[q], cb + cn);
+                for (int e = e0; e < e1; ++e) {
+                    float s = a.br[j];
 #pragma unroll
-                        for (int w = 0; w < WK; ++w) s += Zr[(w * TM + (e - cb)) * TU + u];
-                        const float cw = a.arena_c[(size_t)seg_row(a.rag, e) * a.H + j];
-                        if constexpr (KIND == K_CS_INT) {
-                            racc[q] += sigm(s) * cw;   // f_k * c_k, rounded, then added in child order
-                        } else {
-                            const float l = sigm(zsum[q][4] + s);  // link gate of word k
-                            const float ek = __expf(l);
-                            racc[q] = fmaf(ek, cw, racc[q]);
-                            rden[q] += ek;
-                        }
+                    for (int w = 0; w < WK; ++w) s += Zr[(w * TMR + (e - cb)) * TU + u];
+                    const float cw = Crag[(e - cb) * TU + u];
+                    if constexpr (KIND == K_CS_INT) {
+                        racc[q] += sigm(s) * cw;   // f_k * c_k, rounded, then added in child order
+                    } else {
+                        const float l = sigm(zsum[q][4] + s);  // link gate of word k
+                        const float ek = __expf(l);
+                        racc[q] = fmaf(ek, cw, racc[q]);
+                        rden[q] += ek;
                     }
                 }
             }

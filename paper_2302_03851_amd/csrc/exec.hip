@@ -352,34 +352,35 @@ int flow_lds(const std::vector<int>& kinds_k) {
     return (best + 15) / 16 * 16;
 }
 
-// Estimated cycles of one batch under tile variant v: the work-groups' waves
-// are spread over the 1024 SIMDs; each wave runs its k-groups back to back
-// (matrix-core cycles plus a fixed per-k-group issue/latency cost) and then
-// the epilogue; plus a fixed launch and prologue latency.
-double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag = 0) {
+// Estimated microseconds of one batch under small tile variant v: rounds of
+// resident work-groups (LDS- and wave-limited, up to 8 per CU) times a
+// per-round time linear in the per-wave k-groups and matrix-core work and in
+// the ragged chunks, plus the L2 weight traffic of all row tiles.  The
+// coefficients are a non-negative least-squares fit to per-batch sweeps of
+// every variant on MI355X (three workloads, 890 batch/variant pairs, median
+// error 9%).
+double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int lds, int max_lds, int n_cu) {
     const int RT = VAR_RT[v], WU = VAR_WU[v], WK = VAR_WK[v];
     const int TM = 16 * RT, TU = 16 * WU;
     const double wgs = (double)((m + TM - 1) / TM) * (d.Hu / TU);
-    const double waves = wgs * WU * WK;
+    const int occ = std::max(1, std::min({max_lds / std::max(lds, 1), 32 / (WU * WK), 8}));
+    const double rounds = std::ceil(wgs / ((double)n_cu * occ));
     const int nkg = d.K / d.KG;
-    const int kg_per_wave = (nkg + WK - 1) / WK;
-    const double mfma_cyc = dtype == EDB_F32 ? 4 * 32.0 : 16.0;   // per gate and row block per k-group
-    double per_wave = kg_per_wave * (d.G * RT * mfma_cyc + 120.0) + 40.0 * WK * RT * d.G;
+    const double kpw = std::ceil((double)nkg / WK);
+    const double mf = dtype == EDB_F32 ? 8.0 : 1.0;   // matrix-core cycles per k-group relative to bf16
+    double chunks = 0, rkpw = 0, RTR = RT;
     if (d.rag && m > 0) {
-        // ragged phase: the work-group's child rows in chunks of TM rows, one
-        // gate each, with a staging and two barriers per chunk
-        const double chunks = std::ceil((double)nrag / m * TM / TM);
-        const int rkg = (d.Hk / d.KG + WK - 1) / WK;
-        per_wave += chunks * (rkg * (RT * mfma_cyc + 120.0) + 3000.0);
+        RTR = std::max(RT, 4);
+        chunks = std::ceil((double)nrag / m * TM / (16 * RTR));
+        rkpw = std::ceil((double)(d.Hk / d.KG) / WK);
     }
-    const double rounds = std::ceil(waves / 1024.0);
-    return rounds * per_wave + 2500.0;
+    const double per_round = 4.867 + 0.00063 * kpw + 0.01182 * kpw * RT * d.G * mf + 0.00564 * WK * RT * d.G +
+                             2.946 * chunks + 0.00329 * chunks * rkpw * RTR * mf + 0.3304 * chunks * rkpw;
+    // every row tile reads its units' weights: MB over the batch
+    const double weight_mb = std::ceil((double)m / TM) * d.K * d.G * d.Hu * d.esz / 1e6;
+    return rounds * per_round + 0.06408 * weight_mb;
 }
 
-// Estimated cycles of one batch under large tile variant NUM_SMALL + vb: work-
-// groups of 4 waves (one per SIMD) resident lds-limited per CU, each running
-// its 64-wide k chunks (matrix-core cycles of a wave plus a per-chunk
-// synchronisation cost) after a fixed prologue.
 // Estimated microseconds of the large tile for G gates over K (padded), m
 // rows, fitted to measurements on MI355X: a 64-wide chunk takes the L2->LDS
 // copy time of the work-groups resident on a CU (about 86 GB/s per CU at full
@@ -729,7 +730,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 if (lds > max_lds) continue;
                 if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
                 if ((flags & EDB_NO_SPLIT_K) && VAR_WK[vi] != 1) continue;
-                const double est = variant_cost(vi, m, d, dtype, nrag);
+                const double est = variant_cost(vi, m, d, dtype, nrag, lds, max_lds, n_cu);
                 if (est < best * 0.97) { best = est; var = vi; }
             }
             // large tile for batches whose main GEMM has at least 4e8 multiply-adds
@@ -737,7 +738,9 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             (void)lest;
             const bool big_gemm = (double)m * d.K * d.G * d.Hu >= 4e8;
             if (lvar >= 0 && (large_only || var < 0 || big_gemm)) var = lvar;
-            if (force_var >= 0 && force_var < NUM_SMALL && table().e[kind_id][dtype][force_var].launch) var = force_var;
+            if (force_var >= 0 && force_var < NUM_SMALL && table().e[kind_id][dtype][force_var].launch &&
+                table().e[kind_id][dtype][force_var].lds(d.K) <= max_lds)
+                var = force_var;
             if (is_large(force_var) && lvar >= 0) {
                 const int fk = cs_large ? K_CS_PARENT : kind_id;
                 if (table().e[fk][dtype][force_var].launch) var = lvar = force_var;
