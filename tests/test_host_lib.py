@@ -281,6 +281,10 @@ def test_tile_flags_select_variants():
     f = edb.Forward(w, flags=base | L.NO_LARGE | L.NO_SPLIT_K)
     for i in range(1, f.exec.launches()):
         assert f.exec.launch_info(i)["variant"] in (0, 1)
+    w2 = WL.make_config(2, instances=6)
+    f = edb.Forward(w2, flags=base | L.NO_SPLIT_K)
+    for i in range(1, f.exec.launches()):
+        assert f.exec.launch_info(i)["variant"] in (0, 1)
     big = WL.make_config(5)
     f = edb.Forward(big, flags=base)
     assert f.exec.launch_info(1)["kind"] == WL.CS_LEAF and f.exec.launch_info(1)["variant"] in L.LARGE_VARIANTS
