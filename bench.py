@@ -89,6 +89,7 @@ def launch_work(info, work, split):
 
 # small-tile variants (rows 16*RT, units 16*WU, split-K WK), in the library's order
 SMALL_VARIANTS = [(2, 4, 1), (1, 4, 1), (1, 2, 2), (1, 1, 4), (1, 1, 8), (1, 1, 16), (2, 1, 4), (2, 2, 2)]
+STREAM_SHAPES = {11: (1, 4), 12: (2, 4), 13: (1, 8), 14: (1, 16)}   # streamed tile: (rows / 16, waves)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -96,11 +97,15 @@ def kernel_symbol(kind, dtype, variant, part):
     """The kernel a launch runs, as rocprofv3 prints its name (prefix)."""
     if part == 1:
         return "edbk::child_reduce_kernel"
+    t = 'float' if dtype == 'f32' else '__bf16'
+    if variant in STREAM_SHAPES:
+        rt, wk = STREAM_SHAPES[variant]
+        return f"edbk::stream_kernel<{kind}, {t}, {rt}, {wk}>"
     if variant >= 8:
         kk = 8 if part == 2 else (9 if kind == 5 else kind)
         return f"edbk::big_kernel<{kk}, {variant - 8}>"
     rt, wu, wk = SMALL_VARIANTS[variant]
-    return f"edbk::cell_kernel<{kind}, {'float' if dtype == 'f32' else '__bf16'}, {rt}, {wu}, {wk}>"
+    return f"edbk::cell_kernel<{kind}, {t}, {rt}, {wu}, {wk}>"
 
 
 def source_digest():
@@ -356,6 +361,8 @@ def main():
     elif var_v in L.LARGE_VARIANTS:
         kk = "CS_FORGET" if part_v == 2 else ("CS_PARENT" if kind_v == WL.CS_INTERNAL else kname)
         kernel = f"big_kernel<{kk}, size class {var_v - 8}>"
+    elif var_v in STREAM_SHAPES:
+        kernel = f"stream_kernel<{kname}, {w.dtype}, variant {var_v}>"
     else:
         kernel = f"cell_kernel<{kname}, {w.dtype}, variant {var_v}>"
     symbol = kernel_symbol(kind_v, w.dtype, var_v, part_v)

@@ -230,13 +230,18 @@ typedef struct edb_exec edb_exec_t;
  * Uploads the batch descriptors and index lists to the current HIP device
  * and allocates the staged-x buffer; both are owned by the handle.
  * Each batch gets the tile variant of smallest estimated time: small tiles
- * (16-32 rows per work-group, optional split-K) for the many small batches,
- * the large bf16 tile (64-256 rows, both operands through LDS) for batches
- * of thousands of rows.  Without split-K (EDB_NO_SPLIT_K, and always in the
- * large tile) a batch's results do not depend on the variant: they are
- * bitwise equal across variants, layouts and launch modes.  For sweeps and
- * tests, the environment variable EDB_VARIANT=v (read at each call) forces
- * variant v on every batch whose cell kind has it.
+ * (16-32 rows per work-group, the operand rows staged in LDS, optional
+ * split-K over the waves), streamed tiles (the same shapes for kinds without
+ * a ragged phase, every lane loading its own operand fragments) for the many
+ * small batches, the large bf16 tile (64-256 rows, both operands through LDS)
+ * for batches of thousands of rows.  Without split-K (EDB_NO_SPLIT_K, and
+ * always in the large tile) a batch's results do not depend on the variant:
+ * they are bitwise equal across variants, layouts and launch modes; with it,
+ * variants with the same reduction split (a streamed tile and its staged
+ * counterpart) are bitwise equal.  For sweeps and tests, the environment
+ * variable EDB_VARIANT=v (read at each call) forces variant v on every batch
+ * whose cell kind has it; a forced streamed variant falls back to its staged
+ * counterpart on the other kinds.
  * Errors: EDB_ERR_INVALID, EDB_ERR_UNSUPPORTED (dimension or kind mix the
  * kernels do not handle), EDB_ERR_OOM, EDB_ERR_HIP. */
 edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
@@ -273,7 +278,8 @@ typedef struct {
     int32_t k;         /* padded reduction length of the main GEMM */
     int32_t n;         /* padded output columns (gates x padded hidden) */
     int32_t variant;   /* tile variant id: 0-7 small tiles, 8-10 the large bf16 tile (largest rows
-                          per work-group first), 100 a dataflow launch */
+                          per work-group first), 11-14 streamed tiles (counterparts of the small
+                          tiles 3, 6, 4, 5), 100 a dataflow launch */
     int32_t grid;      /* work-groups */
     int32_t block;     /* threads per work-group */
     int32_t seg_kind[4]; /* kinds of result, child 0, child 1, ragged lists */

@@ -52,14 +52,6 @@ __host__ __device__ constexpr int big_lds_bytes() {
     return 2 * big_stage_bytes<Kind<KIND>::G, big_rb(Kind<KIND>::G, VB), BIG_CU>();
 }
 
-// Raw buffer resource over `bytes` bytes at p (gfx9 resource word 3).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
-}
-// 16-byte buffer load at byte offset off; zero past the end of the buffer.
-__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
-}
 // Direct global -> LDS copy of 16 bytes per lane: lane l's bytes at byte
 // offset off land at lds + 16 l (lds is wave-uniform).  Offsets past the end
 // of the buffer read as zero.

@@ -301,6 +301,27 @@ __device__ __forceinline__ void stage_child_sum(T* A, int AS, const BatchArgs& a
     }
 }
 
+// Raw buffer resource over `bytes` bytes at p (gfx9 resource word 3).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte buffer load at byte offset off; zero past the end of the buffer.
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+// 4-byte buffer load at byte offset off; zero past the end of the buffer.
+__device__ __forceinline__ uint32_t bload32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+}
+// seg_row without a branch: an indexed list is read through a buffer of the
+// batch's m entries (zero past them), a list of another kind reads nothing.
+// Several of these issue their loads back to back and are waited for once.
+__device__ __forceinline__ int seg_row_nb(const Seg& s, int r, int m) {
+    const __amdgpu_buffer_rsrc_t ri = make_rsrc(s.idx, s.kind == S_INDEXED ? (uint32_t)m * 4u : 0u);
+    const int v = (int)bload32(ri, (uint32_t)r * 4u);
+    return s.kind == S_CONTIG ? s.base + r : v;
+}
+
 // MFMA on one (gate, row-block) accumulator for one k-group.
 template <typename T, int G, int RT>
 __device__ __forceinline__ void kgroup_mma(v4f (&acc)[G][RT], const uint4 (&av)[RT], const uint4 (&bv)[G]) {
@@ -626,12 +647,253 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
     sync.signal();
 }
 
-// One launch per batch: work-group -> (row tile, unit tile).
+// One launch per batch: work-group -> (row tile, unit tile).  Work-groups of
+// 4 waves without a ragged phase ask for at least 3 waves per SIMD (at most
+// 168 registers a lane): 3 such work-groups per CU, so batches of up to 768
+// tiles run in one round (unbounded, the compiler used up to 220 registers,
+// 2 work-groups per CU).
 template <int KIND, typename T, int RT, int WU, int WK>
-__global__ __launch_bounds__(64 * WU * WK) void cell_kernel(BatchArgs a) {
+__global__ __launch_bounds__(64 * WU * WK, WU * WK == 4 && !Kind<KIND>::RAG ? 3 : 1) void cell_kernel(BatchArgs a) {
     extern __shared__ __align__(16) char smem[];
     const int nut = a.Hu / (16 * WU);
     cell_tile<KIND, T, RT, WU, WK>(a, blockIdx.x / nut, blockIdx.x % nut, smem, NoSync{});
+}
+
+// ---------------------------------------------------------------------------
+// Streamed tile: rows [16*RT*rtile, +16*RT) x units [16*ub, +16) of a batch of
+// a kind without a ragged phase, all gates, the reduction split over WK waves.
+// No operand passes through LDS: every lane loads its own MFMA fragments, 16
+// bytes of one operand row (gathered through the segment's row list exactly
+// as the staged tile gathers) and 16 bytes of a weight block, straight into a
+// ring of PD k-groups, so the matrix cores start when the first k-group has
+// arrived instead of after the whole A tile.  With the reduction split over
+// the waves, no two waves of a work-group read the same operand byte, which is
+// all that staging through LDS would have shared.  Each accumulator adds its
+// k-groups in ascending order with the same instructions, and the partial sums
+// of the waves are added in wave order, as in cell_tile<KIND, T, RT, 1, WK>:
+// the two tiles give bitwise equal results.
+
+// Ring of PD k-groups: A fragments of the wave's RT row blocks, weight
+// fragments of its G gates.
+template <int G, int RT, int PD>
+struct SRing {
+    uint4 a[PD][RT];
+    uint4 b[PD][G];
+};
+
+// Operand loads of one k-group: this lane's 16 bytes of each row block's
+// operand row in segment s, element columns c + 4 or 8 * (lane / 16) (zero
+// past the valid width of the segment, E or H, and for rows whose offset is
+// out of range).
+template <typename T, int RT, int NSEG, bool HX>
+__device__ __forceinline__ void stream_load_a(uint4 (&av)[RT], const uint32_t (&soff)[NSEG][RT],
+                                              __amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rh, int s, int c,
+                                              int E, int H, int lane) {
+    constexpr uint32_t OOB = 0x80000000u;
+    const bool xs = HX && s == 0;
+    const int col = c + (lane >> 4) * Elem<T>::VEC;
+    const bool ok = col < (xs ? E : H);
+    const __amdgpu_buffer_rsrc_t r = xs ? rx : rh;
+#pragma unroll
+    for (int rb = 0; rb < RT; ++rb) {
+        uint32_t base = soff[0][rb];
+#pragma unroll
+        for (int q = 1; q < NSEG; ++q)
+            if (s == q) base = soff[q][rb];
+        av[rb] = bload(r, ok ? base + (uint32_t)col * (uint32_t)sizeof(T) : OOB);
+    }
+}
+
+// Advance the load cursor (k-group lk in segment ls at element lc) by one
+// k-group, holding it at the last k-group kg1 - 1 (loads past the end repeat
+// it).  Uniform values, no branches.
+template <int KG, bool HX>
+__device__ __forceinline__ void stream_next(int& lk, int& ls, int& lc, int kg1, int Ep, int Hk) {
+    const bool more = lk + 1 < kg1;
+    const int nc = lc + KG;
+    const bool wrap = nc >= ((HX && ls == 0) ? Ep : Hk);
+    lk = more ? lk + 1 : lk;
+    ls = more && wrap ? ls + 1 : ls;
+    lc = more ? (wrap ? 0 : nc) : lc;
+}
+
+template <int KIND, typename T, int RT, int WK>
+__device__ __forceinline__ void stream_tile(const BatchArgs& a, int rtile, int ub, char* smem) {
+    using KT = Kind<KIND>;
+    static_assert(!KT::RAG, "kinds with a ragged phase stage their child rows in LDS");
+    constexpr int G = KT::G, NFX = KT::NFIX;
+    constexpr bool HX = KT::X;
+    constexpr int NSEG = (HX ? 1 : 0) + NFX;
+    constexpr int NT = 64 * WK, TM = 16 * RT, TU = 16;
+    constexpr int KG = Elem<T>::KG;
+    constexpr int NITEM = TM * TU, NI = (NITEM + NT - 1) / NT;
+    constexpr int PD = WK >= 16 ? 2 : ring_depth<G>();
+    constexpr uint32_t OOB = 0x80000000u;
+    constexpr uint32_t ES = sizeof(T);
+
+    float* Z = reinterpret_cast<float*>(smem);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wk = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int row0 = rtile * TM, u0 = ub * TU;
+    const int nrows = min(TM, a.m - row0);
+    const int nkg = a.K / KG;
+    const int kg0 = (nkg * wk) / WK, kg1 = (nkg * (wk + 1)) / WK;
+
+    // ---- 1. row indices, all loads issued at once without branches: this
+    // lane's operand rows, the epilogue's result rows and child rows ----
+    int srow[NSEG][RT];
+#pragma unroll
+    for (int rb = 0; rb < RT; ++rb) {
+        const int rr = row0 + rb * 16 + (lane & 15);
+        int s = 0;
+        if constexpr (HX) srow[s++][rb] = seg_row_nb(a.x, rr, a.m);
+#pragma unroll
+        for (int p = 0; p < NFX; ++p) srow[s++][rb] = seg_row_nb(a.fix[p], rr, a.m);
+    }
+    int rres[NI], crow[NI][NFX > 0 ? NFX : 1];
+#pragma unroll
+    for (int q = 0; q < NI; ++q) {
+        const int rr = row0 + (tid + NT * q) / TU;
+        rres[q] = seg_row_nb(a.res, rr, a.m);
+#pragma unroll
+        for (int p = 0; p < NFX; ++p) crow[q][p] = seg_row_nb(a.fix[p], rr, a.m);
+    }
+
+    // ---- 2. weights of the first PD k-groups (independent of the indices), bias.
+    // The prologue loads are unconditional (a wave without k-groups loads k-group
+    // 0 and does not use it): with no branch between the index loads and their
+    // use, the wait for the indices leaves these loads in flight ----
+    const uint4* Bw = reinterpret_cast<const uint4*>(a.W) + ((size_t)ub * G * nkg) * 64 + lane;
+    SRing<G, RT, PD> ring;
+#pragma unroll
+    for (int p = 0; p < PD; ++p) load_b<G>(ring.b[p], Bw, nkg, max(min(kg0 + p, kg1 - 1), 0));
+    float bz[NI][G];   // the packed bias is zero-padded to Hu
+#pragma unroll
+    for (int q = 0; q < NI; ++q)
+#pragma unroll
+        for (int g = 0; g < G; ++g) bz[q][g] = a.bias[g * a.Hu + u0 + (tid + NT * q) % TU];
+
+    // ---- 3. operand byte offsets (out of range, i.e. zero, past the batch and
+    // for absent lists), the first PD k-groups of operands ----
+    uint32_t soff[NSEG][RT];
+#pragma unroll
+    for (int rb = 0; rb < RT; ++rb) {
+        const bool ok = rb * 16 + (lane & 15) < nrows;
+        int s = 0;
+        if constexpr (HX) {
+            soff[s][rb] = ok ? (uint32_t)srow[s][rb] * (uint32_t)a.E * ES : OOB;
+            ++s;
+        }
+#pragma unroll
+        for (int p = 0; p < NFX; ++p, ++s)
+            soff[s][rb] = ok && a.fix[p].kind != S_NONE ? (uint32_t)srow[s][rb] * (uint32_t)a.H * ES : OOB;
+    }
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.xmat, HX ? (uint32_t)a.n_xrows * (uint32_t)a.E * ES : 0u);
+    const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.arena_h, (uint32_t)a.n_slots * (uint32_t)a.H * ES);
+    const int xkg = HX ? a.Ep / KG : 0, hkg = a.Hk / KG;
+    int lk = kg0, ls, lc;   // load cursor: k-group, its segment, its first element there
+    if (kg0 < xkg) {
+        ls = 0;
+        lc = kg0 * KG;
+    } else {
+        const int t = kg0 - xkg, p = t / hkg;
+        ls = (HX ? 1 : 0) + p;
+        lc = (t - p * hkg) * KG;
+    }
+#pragma unroll
+    for (int p = 0; p < PD; ++p) {
+        stream_load_a<T, RT, NSEG, HX>(ring.a[p], soff, rx, rh, ls, lc, a.E, a.H, lane);
+        stream_next<KG, HX>(lk, ls, lc, kg1, a.Ep, a.Hk);
+    }
+
+    // ---- 4. the children's cell states for the epilogue ----
+    const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.arena_c, (uint32_t)a.n_slots * (uint32_t)a.H * 4u);
+    float cpre[NI][NFX > 0 ? NFX : 1];
+#pragma unroll
+    for (int q = 0; q < NI; ++q) {
+        const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
+        const bool ok = it < NITEM && r < nrows && j < a.H;
+#pragma unroll
+        for (int p = 0; p < (NFX > 0 ? NFX : 1); ++p)
+            cpre[q][p] = __uint_as_float(bload32(
+                rc, NFX > p && ok && a.fix[p].kind != S_NONE
+                        ? ((uint32_t)crow[q][p] * (uint32_t)a.H + (uint32_t)j) * 4u
+                        : OOB));
+    }
+
+    // ---- 4. gate GEMM over k-groups [kg0, kg1), the ring refilled PD ahead ----
+    v4f acc[G][RT];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) acc[g][rt] = v4f{0.f, 0.f, 0.f, 0.f};
+    int kg = kg0;
+    for (; kg + PD < kg1; kg += PD) {
+#pragma unroll
+        for (int p = 0; p < PD; ++p) {
+            kgroup_mma<T, G, RT>(acc, ring.a[p], ring.b[p]);
+            load_b<G>(ring.b[p], Bw, nkg, lk);
+            stream_load_a<T, RT, NSEG, HX>(ring.a[p], soff, rx, rh, ls, lc, a.E, a.H, lane);
+            stream_next<KG, HX>(lk, ls, lc, kg1, a.Ep, a.Hk);
+        }
+    }
+#pragma unroll
+    for (int p = 0; p < PD; ++p)
+        if (kg + p < kg1) kgroup_mma<T, G, RT>(acc, ring.a[p], ring.b[p]);
+    // partial sums -> Z[wk][row][g][unit] (Z has the LDS to itself)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = rt * 16 + (lane >> 4) * 4 + i;
+                Z[((wk * TM + r) * G + g) * TU + (lane & 15)] = acc[g][rt][i];
+            }
+    __syncthreads();
+
+    // ---- 5. gate pre-activations (partial sums in wave order), epilogue, scatter ----
+    T* Hout = reinterpret_cast<T*>(a.arena_h);
+#pragma unroll
+    for (int q = 0; q < NI; ++q) {
+        const int it = tid + NT * q, r = it / TU, u = it % TU;
+        const int j = u0 + u;
+        if (it >= NITEM || r >= nrows || j >= a.H) continue;
+        float z[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            float sum = 0.f;
+#pragma unroll
+            for (int w = 0; w < WK; ++w) sum += Z[((w * TM + r) * G + g) * TU + u];
+            z[g] = sum + bz[q][g];
+        }
+        float c, h;
+        cell_update<KIND>(z, cpre[q], 0.f, 0.f, 0, c, h);
+        const size_t o = (size_t)rres[q] * a.H + j;
+        a.arena_c[o] = c;
+        Hout[o] = from_f<T>(h);
+    }
+}
+
+template <int KIND, typename T, int RT, int WK>
+__host__ __device__ constexpr int stream_lds_bytes() {
+    return WK * 16 * RT * Kind<KIND>::G * 16 * 4;
+}
+
+// Work-group -> tile in XCD-aware order: work-groups are dispatched round-robin
+// over the 8 XCDs, and each XCD takes a contiguous range of tiles, row tiles
+// fastest, so the work-groups of a unit block (its weights) share one XCD's L2.
+// The grid is a multiple of 8; surplus work-groups exit at once.
+template <int KIND, typename T, int RT, int WK>
+__global__ __launch_bounds__(64 * WK, WK == 4 ? 3 : 1) void stream_kernel(BatchArgs a) {
+    extern __shared__ __align__(16) char smem[];
+    const int nut = a.Hu / 16;
+    const int nrt = (a.m + 16 * RT - 1) / (16 * RT);
+    const int ntile = nrt * nut;
+    const int per = (ntile + 7) / 8;
+    const int t = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    if (t >= ntile) return;
+    stream_tile<KIND, T, RT, WK>(a, t % nrt, t / nrt, smem);
 }
 
 // ---------------------------------------------------------------------------

@@ -25,14 +25,22 @@ namespace {
 
 constexpr int NUM_SMALL = 8;
 constexpr int NUM_LARGE = 3;
-constexpr int NUM_VARIANTS = NUM_SMALL + NUM_LARGE;
-// small tile variants: rows per work-group 16*RT, units per work-group 16*WU,
-// WK waves splitting the reduction (threads per work-group 64*WU*WK)
-constexpr int VAR_RT[NUM_SMALL] = {2, 1, 1, 1, 1, 1, 2, 2};
-constexpr int VAR_WU[NUM_SMALL] = {4, 4, 2, 1, 1, 1, 1, 2};
-constexpr int VAR_WK[NUM_SMALL] = {1, 1, 2, 4, 8, 16, 4, 2};
+constexpr int NUM_STREAM = 4;
+constexpr int FIRST_STREAM = NUM_SMALL + NUM_LARGE;
+constexpr int NUM_VARIANTS = FIRST_STREAM + NUM_STREAM;
+// small (staged) and streamed tile variants: rows per work-group 16*RT, units
+// per work-group 16*WU, WK waves splitting the reduction (threads per
+// work-group 64*WU*WK); the large variants have no entry here
+constexpr int VAR_RT[NUM_VARIANTS] = {2, 1, 1, 1, 1, 1, 2, 2, 0, 0, 0, 1, 2, 1, 1};
+constexpr int VAR_WU[NUM_VARIANTS] = {4, 4, 2, 1, 1, 1, 1, 2, 0, 0, 0, 1, 1, 1, 1};
+constexpr int VAR_WK[NUM_VARIANTS] = {1, 1, 2, 4, 8, 16, 4, 2, 0, 0, 0, 4, 4, 8, 16};
 // large tile variants NUM_SMALL + vb: 32*big_rb(G, vb) rows x 64 units, 256 threads
-bool is_large(int v) { return v >= NUM_SMALL && v < NUM_VARIANTS; }
+bool is_large(int v) { return v >= NUM_SMALL && v < FIRST_STREAM; }
+// streamed tile variants FIRST_STREAM..: 16*RT rows x 16 units, WK waves
+bool is_stream(int v) { return v >= FIRST_STREAM && v < NUM_VARIANTS; }
+bool is_small(int v) { return v >= 0 && v < NUM_SMALL; }
+// the staged variant with the same rows and reduction split as streamed variant v
+constexpr int STAGED_OF[NUM_STREAM] = {3, 6, 4, 5};
 
 struct KindInfo {
     int G, nfix;
@@ -261,6 +269,30 @@ Entry big_entry() {
     else return {nullptr, nullptr, nullptr, nullptr};
 }
 
+template <int KIND, typename T, int RT, int WK>
+void launch_stream(const BatchArgs& a, int grid, int lds, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+    if (ev0)
+        hipExtLaunchKernelGGL((stream_kernel<KIND, T, RT, WK>), dim3(grid), dim3(64 * WK), lds, st, ev0, ev1, 0, a);
+    else
+        hipLaunchKernelGGL((stream_kernel<KIND, T, RT, WK>), dim3(grid), dim3(64 * WK), lds, st, a);
+}
+template <int KIND, typename T, int RT, int WK>
+hipError_t attr_stream(int lds) {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&stream_kernel<KIND, T, RT, WK>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+}
+template <int KIND, typename T, int RT, int WK>
+int lds_stream(int) { return stream_lds_bytes<KIND, T, RT, WK>(); }
+
+// the streamed tile serves the kinds without a ragged phase
+template <int KIND, typename T, int RT, int WK>
+Entry stream_entry() {
+    if constexpr (Kind<KIND>::RAG) return {nullptr, nullptr, nullptr, nullptr};
+    else
+        return {launch_stream<KIND, T, RT, WK>, attr_stream<KIND, T, RT, WK>, lds_stream<KIND, T, RT, WK>,
+                reinterpret_cast<const void*>(&stream_kernel<KIND, T, RT, WK>)};
+}
+
 // Rows per work-group of large variant NUM_SMALL + vb for G gates.
 int large_tm(int G, int vb) { return 32 * big_rb(G, vb); }
 
@@ -277,6 +309,10 @@ void fill_kind(Entry* e) {
     e[8] = big_entry<KIND, T, 0>();
     e[9] = big_entry<KIND, T, 1>();
     e[10] = big_entry<KIND, T, 2>();
+    e[11] = stream_entry<KIND, T, 1, 4>();
+    e[12] = stream_entry<KIND, T, 2, 4>();
+    e[13] = stream_entry<KIND, T, 1, 8>();
+    e[14] = stream_entry<KIND, T, 1, 16>();
 }
 
 // The internal kinds of a child-sum batch on the large tile have large bf16 variants only.
@@ -352,33 +388,45 @@ int flow_lds(const std::vector<int>& kinds_k) {
     return (best + 15) / 16 * 16;
 }
 
-// Estimated microseconds of one batch under small tile variant v: rounds of
-// resident work-groups (LDS- and wave-limited, up to 8 per CU) times a
-// per-round time linear in the per-wave k-groups and matrix-core work and in
-// the ragged chunks, plus the L2 weight traffic of all row tiles.  The
-// coefficients are a non-negative least-squares fit to per-batch sweeps of
-// every variant on MI355X (three workloads, 890 batch/variant pairs, median
-// error 9%).
-double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int lds, int max_lds, int n_cu) {
-    const int RT = VAR_RT[v], WU = VAR_WU[v], WK = VAR_WK[v];
+// Estimated microseconds of one batch under a small (staged) or streamed tile
+// variant v, occ work-groups of it resident per CU.  The work-groups run in
+// rounds of n_cu * occ; each round costs a latency term plus, for the busiest
+// CU's c work-groups, their matrix-core time per SIMD, the bytes they load
+// (operand rows and weights) and, for the staged tile, the bytes they stage;
+// the staged tile adds its split-K reduction and the chunks of the ragged
+// phase.  The coefficients of each family are a non-negative least-squares fit
+// (relative error) to per-batch sweeps of every variant on every batch of the
+// five workloads on MI355X (1634 batch/variant pairs; median error 9% staged,
+// 6% streamed).
+double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int occ, int n_cu) {
+    static constexpr double kStaged[9] = {0.5359, 2.5249, 1.7686, 0.0014234, 0.04603, 0.0, 3.6911, 0.02489, 5.8812};
+    static constexpr double kStream[9] = {1.2620, 1.4361, 1.0504, 0.0087887, 0.0, 0.7956, 0.0, 0.0, 0.0};
+    const double* k = is_stream(v) ? kStream : kStaged;
+    const int RT = VAR_RT[v], WU = VAR_WU[v], WK = VAR_WK[v], W = WU * WK;
     const int TM = 16 * RT, TU = 16 * WU;
-    const double wgs = (double)((m + TM - 1) / TM) * (d.Hu / TU);
-    const int occ = std::max(1, std::min({max_lds / std::max(lds, 1), 32 / (WU * WK), 8}));
-    const double rounds = std::ceil(wgs / ((double)n_cu * occ));
+    const int64_t tiles = (int64_t)((m + TM - 1) / TM) * (d.Hu / TU);
+    occ = std::max(occ, 1);
+    const int64_t cap = (int64_t)n_cu * occ;
+    const int64_t full = tiles / cap, rem = tiles % cap;
     const int nkg = d.K / d.KG;
     const double kpw = std::ceil((double)nkg / WK);
-    const double mf = dtype == EDB_F32 ? 8.0 : 1.0;   // matrix-core cycles per k-group relative to bf16
+    const double cyc = dtype == EDB_F32 ? 128.0 : 16.0;   // matrix-core cycles per (k-group, gate, row block)
+    const double mf = std::max(1, W / 4) * kpw * d.G * RT * cyc / 2400.0;          // us per SIMD per work-group
+    const double ld = ((double)TM * d.K + (double)TU * d.G * d.K) * d.esz / 1024.0;  // KB loaded per work-group
+    const double st = is_stream(v) ? 0.0 : (double)TM * d.K * d.esz / 1024.0;      // KB staged per work-group
     double chunks = 0, rkpw = 0, RTR = RT;
     if (d.rag && m > 0) {
         RTR = std::max(RT, 4);
         chunks = std::ceil((double)nrag / m * TM / (16 * RTR));
         rkpw = std::ceil((double)(d.Hk / d.KG) / WK);
     }
-    const double per_round = 4.867 + 0.00063 * kpw + 0.01182 * kpw * RT * d.G * mf + 0.00564 * WK * RT * d.G +
-                             2.946 * chunks + 0.00329 * chunks * rkpw * RTR * mf + 0.3304 * chunks * rkpw;
-    // every row tile reads its units' weights: MB over the batch
-    const double weight_mb = std::ceil((double)m / TM) * d.K * d.G * d.Hu * d.esz / 1e6;
-    return rounds * per_round + 0.06408 * weight_mb;
+    const double per_round_fixed = k[1] + k[5] * WK * RT * d.G / 64.0 + k[6] * chunks +
+                                   k[7] * chunks * rkpw * RTR * (dtype == EDB_F32 ? 8.0 : 1.0) / 64.0 +
+                                   k[8] * chunks * rkpw / 16.0;
+    const double per_wg = k[2] * mf + k[3] * ld + k[4] * st;
+    double t = k[0] + (double)full * (per_round_fixed + occ * per_wg);
+    if (rem) t += per_round_fixed + (double)((rem + n_cu - 1) / n_cu) * per_wg;
+    return t;
 }
 
 // Estimated microseconds of the large tile for G gates over K (padded), m
@@ -401,9 +449,10 @@ double large_cost(int G, int vb, int m, int K, int Hu, int per_cu, int n_cu, dou
     return rounds * (nch * t_chunk + t_epi) + 3.0 + extra_us;
 }
 
-// Work-groups of 256 threads of a large-tile kernel resident on one CU: from
-// the runtime (registers and LDS) when a device is bound, else from LDS alone.
-using OccFn = std::function<int(const Entry&, int lds)>;
+// Work-groups of a kernel resident on one CU (block threads, dyn_lds bytes of
+// dynamic LDS, lds bytes of LDS in all): from the runtime (registers and LDS)
+// when a device is bound, else from LDS and waves alone.
+using OccFn = std::function<int(const Entry&, int block, int dyn_lds, int lds)>;
 
 // Best large variant (NUM_SMALL + vb) of kernel kind kk for m rows, or -1.
 int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max_lds, const OccFn& occ,
@@ -415,7 +464,7 @@ int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max
         if (!en.launch) continue;
         const int lds = en.lds(K);
         if (lds > max_lds) continue;
-        const double c = large_cost(G, vb, m, K, Hu, occ(en, lds), n_cu, extra_us);
+        const double c = large_cost(G, vb, m, K, Hu, occ(en, 256, 0, lds), n_cu, extra_us);
         if (c < est * 0.97) { est = c; var = NUM_SMALL + vb; }
     }
     return var;
@@ -432,7 +481,7 @@ struct DeviceCtx {
     hipStream_t upload = nullptr;
     hipStream_t release = nullptr;   // stream-ordered frees wait here, off the upload path
     std::map<int, int> lds_granted;
-    std::map<const void*, int> occupancy;   // resident 256-thread work-groups per CU of a kernel
+    std::map<std::pair<const void*, int>, int> occupancy;   // (kernel, dynamic LDS) -> resident work-groups per CU
     std::vector<hipEvent_t> event_pool;      // timing events of freed EDB_PROFILE executors, for reuse
 };
 std::mutex g_ctx_mu;
@@ -608,18 +657,19 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             n_cu = ctx->n_cu;
         }
         const int force_var = std::getenv("EDB_VARIANT") ? std::atoi(std::getenv("EDB_VARIANT")) : -1;
-        const OccFn occ = [&](const Entry& en, int lds) -> int {
-            const int by_lds = max_lds / std::max(lds, 1);
-            if (!ctx || !en.fn) return by_lds;
+        const OccFn occ = [&](const Entry& en, int block, int dyn_lds, int lds) -> int {
+            const int est = std::max(1, std::min({max_lds / std::max(lds, 1), 32 / std::max(block / 64, 1), 16}));
+            if (!ctx || !en.fn) return est;
             std::lock_guard<std::mutex> lk(g_ctx_mu);
-            auto it = ctx->occupancy.find(en.fn);
+            const auto key = std::make_pair(en.fn, dyn_lds);
+            auto it = ctx->occupancy.find(key);
             if (it != ctx->occupancy.end()) return it->second;
             int nb = 0;
-            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, en.fn, 256, 0) != hipSuccess) {
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, en.fn, block, (size_t)dyn_lds) != hipSuccess || nb < 1) {
                 (void)hipGetLastError();
-                nb = by_lds;
+                nb = est;
             }
-            ctx->occupancy[en.fn] = nb;
+            ctx->occupancy[key] = nb;
             return nb;
         };
 
@@ -723,14 +773,16 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 lvar = best_large(kind_id, dtype, d.G, m, d.K, d.Hu, n_cu, max_lds, occ, lest);
             }
             const bool large_only = (flags & EDB_TILE_LARGE) && lvar >= 0;
-            for (int vi = 0; vi < NUM_SMALL && !large_only; ++vi) {
+            for (int vi = 0; vi < NUM_VARIANTS && !large_only; ++vi) {
+                if (!is_small(vi) && !(is_stream(vi) && large_fits)) continue;
                 const Entry& en = table().e[kind_id][dtype][vi];
                 if (!en.launch) continue;
                 const int lds = en.lds(d.K);
                 if (lds > max_lds) continue;
                 if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
                 if ((flags & EDB_NO_SPLIT_K) && VAR_WK[vi] != 1) continue;
-                const double est = variant_cost(vi, m, d, dtype, nrag, lds, max_lds, n_cu);
+                const int block = 64 * VAR_WU[vi] * VAR_WK[vi];
+                const double est = variant_cost(vi, m, d, dtype, nrag, occ(en, block, lds, lds), n_cu);
                 if (est < best * 0.97) { best = est; var = vi; }
             }
             // large tile for batches whose main GEMM has at least 4e8 multiply-adds
@@ -738,9 +790,14 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             (void)lest;
             const bool big_gemm = (double)m * d.K * d.G * d.Hu >= 4e8;
             if (lvar >= 0 && (large_only || var < 0 || big_gemm)) var = lvar;
-            if (force_var >= 0 && force_var < NUM_SMALL && table().e[kind_id][dtype][force_var].launch &&
-                table().e[kind_id][dtype][force_var].lds(d.K) <= max_lds)
-                var = force_var;
+            // a forced streamed variant falls back to its staged counterpart
+            // for kinds it does not serve (and buffers beyond 32-bit offsets)
+            int fv = force_var;
+            if (is_stream(fv) && !(large_fits && table().e[kind_id][dtype][fv].launch))
+                fv = STAGED_OF[fv - FIRST_STREAM];
+            if ((is_small(fv) || is_stream(fv)) && table().e[kind_id][dtype][fv].launch &&
+                table().e[kind_id][dtype][fv].lds(d.K) <= max_lds)
+                var = fv;
             if (is_large(force_var) && lvar >= 0) {
                 const int fk = cs_large ? K_CS_PARENT : kind_id;
                 if (table().e[fk][dtype][force_var].launch) var = lvar = force_var;
@@ -811,6 +868,11 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 const int tiles = (m + TM - 1) / TM * (d.Hu / (32 * BIG_CU));
                 L.info.grid = (tiles + 7) / 8 * 8;   // XCD-aware order: 8 equal tile ranges
                 L.info.block = 256;
+            } else if (is_stream(var)) {
+                const int TM = 16 * VAR_RT[var];
+                const int tiles = (m + TM - 1) / TM * (d.Hu / 16);
+                L.info.grid = (tiles + 7) / 8 * 8;   // XCD-aware order: 8 equal tile ranges
+                L.info.block = 64 * VAR_WK[var];
             } else {
                 const int TM = 16 * VAR_RT[var], TU = 16 * VAR_WU[var];
                 L.info.grid = (m + TM - 1) / TM * (d.Hu / TU);

@@ -254,6 +254,49 @@ def test_large_tile_child_sum_many_children():
     _check(w, h, c, hr, cr, "child-sum up to 9 children, large tile")
 
 
+def _stream_workloads():
+    """Workloads of every kind the streamed tile serves, with ragged row tails:
+    chains (fp32), binary trees (fp32), lattices (the word cells; the
+    character cells keep the staged tile), grids with a zero-padded x segment
+    (E = 120 of 128) and padded units (H = 200 of 256), the child-sum
+    configuration (its leaves, bf16) and bf16 chains of 900 rows."""
+    out = [WL.make_config(1), WL.make_config(2, instances=SMALL[2]), WL.make_config(3, instances=SMALL[3]),
+           _grid_graph(3, 6, 7, 120, 200, seed=21, dtype="f32"), WL.make_config(5, instances=SMALL[5])]
+    n = 300
+    op = [0] * (3 * n)
+    ch = [[-1] if i % 3 == 0 else [i - 1] for i in range(3 * n)]
+    out.append(WL.make_graph([WL.LSTM_CHAIN], 64, 128, op, ch, [True] * (3 * n), seed=22, dtype="bf16",
+                             bias_scale=0.2))
+    return out
+
+
+@pytest.mark.parametrize("variant", [11, 12, 13, 14])
+def test_streamed_tile_bitwise_and_parity(variant, monkeypatch):
+    """Every batch the streamed tile serves, forced onto `variant`, is bitwise
+    equal to the staged tile with the same rows and reduction split (eager
+    against two graph replays, planned and indexed operand lists), and within
+    the bound of the oracle."""
+    _torch()
+    staged = L.STREAM_STAGED[variant]
+    for w in _stream_workloads():
+        monkeypatch.setenv("EDB_VARIANT", str(staged))
+        ref = _fwd(w, flags=0)
+        ref.run()
+        h0, c0 = ref.states()
+        monkeypatch.setenv("EDB_VARIANT", str(variant))
+        for flags in (L.USE_GRAPH, L.USE_GRAPH | L.FORCE_GATHER | L.X_DIRECT):
+            f = _fwd(w, flags=flags)
+            used = {f.exec.launch_info(i)["variant"] for i in range(1, f.exec.launches())}
+            assert variant in used, (w.name, used)
+            for _ in range(2):
+                f.run()
+                h, c = f.states()
+                np.testing.assert_array_equal(h, h0, err_msg=f"{w.name} {w.kinds} variant {variant} flags {flags}")
+                np.testing.assert_array_equal(c, c0, err_msg=f"{w.name} {w.kinds} variant {variant} flags {flags}")
+        hr, cr = _oracle(w)
+        _check(w, h, c, hr, cr, f"streamed variant {variant}")
+
+
 DATAFLOW_OFF = ("dataflow launches are switched off: their first GPU runs did not drain "
                 "(cause not yet shown); every batch runs as its own launch")
 

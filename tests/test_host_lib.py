@@ -242,7 +242,7 @@ def test_dryrun_launch_list(k, flow):
             continue
         assert info["n_batches"] == 1
         assert info["m"] == f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b]
-        assert 0 <= info["variant"] <= 10 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
+        assert 0 <= info["variant"] <= 14 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
         if info["variant"] in L.LARGE_VARIANTS:
             # large bf16 tile: every kind but the lattice character cell, 256 threads,
             # grid a multiple of 8
@@ -291,6 +291,33 @@ def test_tile_flags_select_variants():
     with pytest.raises(L.EdbError) as ei:
         edb.Forward(w, flags=base | L.TILE_LARGE | L.NO_LARGE)
     assert ei.value.status == L.EDB_ERR_INVALID
+
+
+@pytest.mark.parametrize("variant", [11, 12, 13, 14])
+def test_forced_streamed_variant(variant, monkeypatch):
+    """A forced streamed variant runs on every batch of a kind without a ragged
+    phase, 64 * WK threads, one work-group per (16 RT rows, 16 units) tile
+    rounded up to a multiple of 8 (the XCD-aware order); batches of ragged
+    kinds (lattice characters, child-sum parents) get what forcing the staged
+    variant with the same rows and reduction split gives them."""
+    rt, wk = {11: (1, 4), 12: (2, 4), 13: (1, 8), 14: (1, 16)}[variant]
+    for k in (1, 2, 3, 4, 5):
+        w = WL.make_config(k, instances={1: 8, 2: 6, 3: 6, 4: 2, 5: 4}[k])
+        monkeypatch.setenv("EDB_VARIANT", str(L.STREAM_STAGED[variant]))
+        ref = edb.Forward(w, flags=L.DRYRUN | L.NO_FLOW)
+        monkeypatch.setenv("EDB_VARIANT", str(variant))
+        f = edb.Forward(w, flags=L.DRYRUN | L.NO_FLOW)
+        assert f.exec.launches() == ref.exec.launches()
+        hu = -(-w.hidden // 64) * 64
+        for i in range(1, f.exec.launches()):
+            info = f.exec.launch_info(i)
+            if info["kind"] in (WL.LAT_CHAR, WL.CS_INTERNAL):
+                assert info["variant"] == ref.exec.launch_info(i)["variant"]
+                continue
+            assert info["variant"] == variant
+            assert info["block"] == 64 * wk
+            tiles = -(-info["m"] // (16 * rt)) * (hu // 16)
+            assert info["grid"] == -(-tiles // 8) * 8
 
 
 def test_packed_weight_bytes_layout():
