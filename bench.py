@@ -201,12 +201,14 @@ def cpu_baseline(w, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--replays", type=int, default=200)
     ap.add_argument("--streams", type=int, default=8,
                     help="mini-batches in flight: host worker threads, each with its own stream and arena")
+    ap.add_argument("--timed-events", type=int, default=8,
+                    help="steps of worker 0 in the timed region whose launches record HIP events")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 256 MiB, 5 times (to scale HBM byte counters)")
@@ -260,10 +262,10 @@ def main():
     arenas = [(ahp, acp)] + [(torch.empty_like(base.arena_h), torch.empty_like(base.arena_c)) for _ in range(S - 1)]
     arena_ptrs = [arenas[0]] + [(a.data_ptr(), c.data_ptr()) for a, c in arenas[1:]]
 
-    # the launches of worker stream 0's timed steps record start/stop HIP
-    # events in their dispatch packets (EDB_PROFILE); those executors are kept
-    # until the timed region has ended and are then read.  The other streams
-    # run without events (the events cost host time on every step).
+    # the launches of worker 0's first --timed-events steps of a region record
+    # start/stop HIP events in their dispatch packets (EDB_PROFILE); those
+    # executors are kept until the region has ended and are then read.  All
+    # other steps run without events (the events cost host time on every step).
     fwd = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
                           table=table)
     fwd_prof = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
@@ -274,20 +276,33 @@ def main():
         # a1 graph ingest, a2 schedule, a3 memory plan, descriptor upload and
         # a4..a8 device execution (asynchronous), in one C call
         ah, ac = arena_ptrs[i]
-        if i == 0:
+        if i == 0 and len(keep) < args.timed_events:
             keep.append(fwd_prof.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream, keep=True))
         else:
             fwd.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream)
 
     def run_steps(n):
-        """n steps spread over S worker threads (each its own stream and arena)."""
+        """n steps over S worker threads (each its own stream and arena), each
+        thread taking the next step when it is free: the worker whose steps
+        carry timing events does fewer of them instead of finishing last."""
         keeps = [[] for _ in range(S)]
         if S == 1:
             for _ in range(n):
                 step(0, keeps[0])
             return keeps
-        counts = [n // S + (1 if i < n % S else 0) for i in range(S)]
-        ths = [threading.Thread(target=lambda i=i: [step(i, keeps[i]) for _ in range(counts[i])]) for i in range(S)]
+        taken = [1]   # worker 0 runs the first step: the timed region has at least one with events
+        lock = threading.Lock()
+
+        def worker(i):
+            if i == 0:
+                step(0, keeps[0])
+            while True:
+                with lock:
+                    if taken[0] >= n:
+                        return
+                    taken[0] += 1
+                step(i, keeps[i])
+        ths = [threading.Thread(target=worker, args=(i,)) for i in range(S)]
         for t in ths:
             t.start()
         for t in ths:
