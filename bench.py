@@ -90,6 +90,7 @@ def launch_work(info, work, split):
 # small-tile variants (rows 16*RT, units 16*WU, split-K WK), in the library's order
 SMALL_VARIANTS = [(2, 4, 1), (1, 4, 1), (1, 2, 2), (1, 1, 4), (1, 1, 8), (1, 1, 16), (2, 1, 4), (2, 2, 2)]
 STREAM_SHAPES = {11: (1, 4), 12: (2, 4), 13: (1, 8), 14: (1, 16)}   # streamed tile: (rows / 16, waves)
+LARGE_CLASS = {8: 0, 9: 1, 10: 2, 15: 3, 16: 4}                     # large tile: size class
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -101,9 +102,9 @@ def kernel_symbol(kind, dtype, variant, part):
     if variant in STREAM_SHAPES:
         rt, wk = STREAM_SHAPES[variant]
         return f"edbk::stream_kernel<{kind}, {t}, {rt}, {wk}>"
-    if variant >= 8:
+    if variant in LARGE_CLASS:
         kk = 8 if part == 2 else (9 if kind == 5 else kind)
-        return f"edbk::big_kernel<{kk}, {variant - 8}>"
+        return f"edbk::big_kernel<{kk}, {t}, {LARGE_CLASS[variant]}>"
     rt, wu, wk = SMALL_VARIANTS[variant]
     return f"edbk::cell_kernel<{kind}, {t}, {rt}, {wu}, {wk}>"
 
@@ -375,7 +376,7 @@ def main():
         kernel = "child_reduce_kernel"
     elif var_v in L.LARGE_VARIANTS:
         kk = "CS_FORGET" if part_v == 2 else ("CS_PARENT" if kind_v == WL.CS_INTERNAL else kname)
-        kernel = f"big_kernel<{kk}, size class {var_v - 8}>"
+        kernel = f"big_kernel<{kk}, {w.dtype}, size class {LARGE_CLASS[var_v]}>"
     elif var_v in STREAM_SHAPES:
         kernel = f"stream_kernel<{kname}, {w.dtype}, variant {var_v}>"
     else:

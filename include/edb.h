@@ -277,9 +277,10 @@ typedef struct {
     int32_t m;         /* rows (all batches of a dataflow launch) */
     int32_t k;         /* padded reduction length of the main GEMM */
     int32_t n;         /* padded output columns (gates x padded hidden) */
-    int32_t variant;   /* tile variant id: 0-7 small tiles, 8-10 the large bf16 tile (largest rows
-                          per work-group first), 11-14 streamed tiles (counterparts of the small
-                          tiles 3, 6, 4, 5), 100 a dataflow launch */
+    int32_t variant;   /* tile variant id: 0-7 small tiles, 8-10 and 15-16 the large tile (size
+                          classes 0-4: 256, 128, 64 rows x 64 units, then 64 and 32 rows x 32
+                          units, fewer rows for 5-gate cells), 11-14 streamed tiles (counterparts
+                          of the small tiles 3, 6, 4, 5), 100 a dataflow launch */
     int32_t grid;      /* work-groups */
     int32_t block;     /* threads per work-group */
     int32_t seg_kind[4]; /* kinds of result, child 0, child 1, ragged lists */

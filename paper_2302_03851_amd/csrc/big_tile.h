@@ -1,16 +1,18 @@
-// Large-batch tile for bf16 cells on gfx950.
+// Large-batch tile for cells on gfx950 (bf16 and fp32).
 //
 // The first batches of a schedule can hold thousands of nodes (all leaves of
 // a mini-batch form one batch under Algorithm 1), and there the cell GEMM is a
 // dense contraction large enough to be bound by the matrix cores.  This tile
 // raises the reuse of every operand fetched from L2: a work-group of 4 waves
 // (2 along rows x 2 along units) owns TM = 32*RB rows and TU = 32*CU hidden
-// units with all G gates, and both operands pass through LDS in chunks of 64
-// k values, double buffered so that the global loads of chunk c+1 are in
-// flight while the matrix cores work on chunk c.  Each wave holds a
-// 16*RB x 16*CU x G block of accumulators (v_mfma_f32_16x16x32_bf16, fp32
-// accumulation), so the gate epilogue finds all G pre-activations of an
-// element in one lane.
+// units with all G gates, and both operands pass through LDS in chunks of 128
+// bytes of k (64 bf16 or 32 fp32 values), double buffered so that the global
+// loads of chunk c+1 are in flight while the matrix cores work on chunk c.
+// Each wave holds a 16*RB x 16*CU x G block of accumulators (fp32; bf16 on
+// v_mfma_f32_16x16x32_bf16, fp32 on four v_mfma_f32_16x16x4_f32 per 16-byte
+// fragment), so the gate epilogue finds all G pre-activations of an element
+// in one lane.  A chunk is two k-groups of either type (32 bf16 or 16 fp32
+// values: one 1 KB weight block each), so the stages have the same layout.
 //
 // The operand rows are gathered through the batch's segment descriptors
 // exactly as in the small tile (contiguous lists as base + row, indexed lists
@@ -28,16 +30,20 @@
 
 namespace edbk {
 
-constexpr int BIG_BK = 64;            // k values per LDS stage (two k-groups of 32)
+// k values per LDS stage: two k-groups, 128 bytes of each operand row
+template <typename T> constexpr int big_bk() { return 128 / (int)sizeof(T); }
 
-// Rows blocks per wave for gate count G and size class vb (0 largest): the
-// accumulators (4 * CU * G * RB registers) stay within 192.
+// Size classes vb: unit blocks per wave CU (2 for classes 0-2, 1 for 3-4: the
+// narrow classes give fp32 batches, whose matrix-core work per byte is eight
+// times bf16's, enough work-groups) and row blocks per wave RB (8, 4, 2, 2, 1,
+// capped so that the accumulators, 4 * CU * G * RB registers, stay within 192).
+constexpr int NUM_BIG_CLASSES = 5;
+__host__ __device__ constexpr int big_cu(int vb) { return vb < 3 ? 2 : 1; }
 __host__ __device__ constexpr int big_rb(int G, int vb) {
-    const int want = vb == 0 ? 8 : vb == 1 ? 4 : 2;
-    const int cap = 192 / (8 * G);
+    const int want = vb == 0 ? 8 : vb == 1 ? 4 : vb == 4 ? 1 : 2;
+    const int cap = 192 / (4 * big_cu(vb) * G);
     return want < cap ? want : cap;
 }
-constexpr int BIG_CU = 2;
 
 // One LDS stage: A [TM rows][64 k] bf16 (128 bytes a row, 16-byte pieces
 // XOR-swizzled by row: piece q of row r sits in slot q ^ (r & 7), so that the
@@ -48,8 +54,8 @@ __host__ __device__ constexpr int big_stage_bytes() {
     return 32 * RB * 128 + 2 * CU * G * 2 * 1024;
 }
 template <int KIND, int VB>
-__host__ __device__ constexpr int big_lds_bytes() {
-    return 2 * big_stage_bytes<Kind<KIND>::G, big_rb(Kind<KIND>::G, VB), BIG_CU>();
+__host__ __device__ constexpr int big_lds_bytes() {   // the same for both element types
+    return 2 * big_stage_bytes<Kind<KIND>::G, big_rb(Kind<KIND>::G, VB), big_cu(VB)>();
 }
 
 // Direct global -> LDS copy of 16 bytes per lane: lane l's bytes at byte
@@ -62,7 +68,7 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t off, ch
 // Copies of one k chunk into an LDS stage.  The chunk lies in one operand
 // segment (uniform sg: 0 = x when the kind has x, then child positions); lane
 // column col of that segment's source rows, zero where col >= lim.
-template <int RB, int NSEG, int NBW, bool HAS_X>
+template <typename T, int RB, int NSEG, int NBW, bool HAS_X>
 __device__ __forceinline__ void big_copy(const uint32_t (&soff)[NSEG][RB], const uint32_t (&woff)[NBW],
                                          __amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rh,
                                          __amdgpu_buffer_rsrc_t rw, int c, int sg, int col, int lim, char* As,
@@ -76,7 +82,7 @@ __device__ __forceinline__ void big_copy(const uint32_t (&soff)[NSEG][RB], const
 #pragma unroll
         for (int s = 1; s < NSEG; ++s)
             if (sg == s) ro = soff[s][j];
-        const uint32_t off = have ? ro + (uint32_t)col * 2u : OOB;
+        const uint32_t off = have ? ro + (uint32_t)col * (uint32_t)sizeof(T) : OOB;
         if (xs) dma16(rx, off, As + (4 * j + wave) * 1024);
         else dma16(rh, off, As + (4 * j + wave) * 1024);
     }
@@ -84,8 +90,10 @@ __device__ __forceinline__ void big_copy(const uint32_t (&soff)[NSEG][RB], const
     for (int j = 0; j < NBW; ++j) dma16(rw, woff[j] + (uint32_t)c * 2048u, Bs + (4 * j + wave) * 1024);
 }
 
-// k-group pair of one LDS stage on the matrix cores.
-template <int RB, int CU, int G>
+// k-group pair of one LDS stage on the matrix cores.  Each accumulator adds
+// its k-groups in order, and within a fp32 k-group its four k-steps in order,
+// as the small tile does.
+template <typename T, int RB, int CU, int G>
 __device__ __forceinline__ void big_compute(v4f (&acc)[CU][G][RB], const char* As, const uint4* Bs, int wr, int wc,
                                             int lane) {
 #pragma unroll
@@ -105,20 +113,31 @@ __device__ __forceinline__ void big_compute(v4f (&acc)[CU][G][RB], const char* A
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-                    acc[cu][g][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(v8bf, af[rb]), __builtin_bit_cast(v8bf, bf[cu][g]), acc[cu][g][rb], 0, 0, 0);
+                for (int rb = 0; rb < RB; ++rb) {
+                    if constexpr (sizeof(T) == 2) {
+                        acc[cu][g][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(v8bf, af[rb]), __builtin_bit_cast(v8bf, bf[cu][g]), acc[cu][g][rb], 0,
+                            0, 0);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            acc[cu][g][rb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                __uint_as_float((&af[rb].x)[j]), __uint_as_float((&bf[cu][g].x)[j]), acc[cu][g][rb], 0,
+                                0, 0);
+                    }
+                }
     }
 }
 
 // One tile: rows [TM*(tile / nut), +TM) x units [TU*(tile % nut), +TU) of the
 // batch, all gates.  st0 / st1: the kernel's two LDS stages.
-template <int KIND, int VB>
+template <int KIND, typename T, int VB>
 __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0, char* st1) {
     using KT = Kind<KIND>;
-    using T = __bf16;
+    constexpr uint32_t ES = sizeof(T);
+    constexpr int BK = big_bk<T>(), PV = 16 / (int)sizeof(T);   // k values per chunk, per 16-byte piece
     constexpr int G = KT::G, NFX = KT::NFIX;
-    constexpr int RB = big_rb(G, VB), CU = BIG_CU;
+    constexpr int RB = big_rb(G, VB), CU = big_cu(VB);
     constexpr int TM = 32 * RB, TU = 32 * CU;
     constexpr int NSEG = (KT::X ? 1 : 0) + NFX;
     constexpr int NBW = CU * G;                      // weight blocks per wave per chunk
@@ -135,16 +154,16 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wr = wave >> 1, wc = wave & 1;
     const int E = a.E, Ep = a.Ep, H = a.H, Hk = a.Hk;
-    const int nkg = a.K / 32;
-    const int nch = a.K / BIG_BK;    // segments are whole chunks (checked by the host)
+    const int nkg = a.K / Elem<T>::KG;
+    const int nch = a.K / BK;        // segments are whole chunks (checked by the host)
 
     // ---- operand copies: buffer -> LDS, 32-bit byte offsets; a masked piece
     // uses an offset past the buffer and arrives as zero, so the copies carry
     // no branches.  Buffers stay below 2^31 bytes (checked by the host); the
     // offsets are unsigned so that OOB plus a column stays out of range ----
     constexpr uint32_t OOB = 0x80000000u;
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.xmat, KT::X ? (uint32_t)a.n_xrows * (uint32_t)E * 2u : 0u);
-    const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.arena_h, (uint32_t)a.n_slots * (uint32_t)H * 2u);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.xmat, KT::X ? (uint32_t)a.n_xrows * (uint32_t)E * ES : 0u);
+    const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.arena_h, (uint32_t)a.n_slots * (uint32_t)H * ES);
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.W, (uint32_t)(a.Hu / 16) * G * nkg * 1024u);
 
     // A copies: wave w's j-th copy fills rows (4 j + w) * 8 .. + 8 of the stage;
@@ -157,12 +176,12 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
         const int r = (4 * j + wave) * 8 + (lane >> 3);
         const bool ok = r < nrows;
         int s = 0;
-        if constexpr (KT::X) soff[s++][j] = ok ? (uint32_t)seg_row(a.x, row0 + r) * (uint32_t)E * 2u : OOB;
+        if constexpr (KT::X) soff[s++][j] = ok ? (uint32_t)seg_row(a.x, row0 + r) * (uint32_t)E * ES : OOB;
 #pragma unroll
         for (int p = 0; p < NFX; ++p)
             soff[s++][j] = !ok ? OOB
                                : (a.fix[p].kind == S_NONE ? 0u
-                                                          : (uint32_t)seg_row(a.fix[p], row0 + r) * (uint32_t)H * 2u);
+                                                          : (uint32_t)seg_row(a.fix[p], row0 + r) * (uint32_t)H * ES);
     }
     // weight copies: wave w's j-th copy is block b = 4 j + w = ((ubi * G + g) * 2 + kgi)
     uint32_t woff[NBW];
@@ -187,31 +206,33 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
     // chunks live in st0, odd chunks in st1 ----
     int sg = 0, scol = 0, slim = KT::X ? E : H, send = KT::X ? Ep : Hk;
     auto next_seg = [&]() {
-        scol += BIG_BK;
+        scol += BK;
         if (scol >= send) { ++sg; scol = 0; slim = H; send = Hk; }
     };
-    big_copy<RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, 0, sg, scol + q * 8, slim, st0, st0 + A_BYTES, wave);
+    big_copy<T, RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, 0, sg, scol + q * PV, slim, st0, st0 + A_BYTES, wave);
     __syncthreads();
     int c = 0;
     for (; c + 1 < nch; c += 2) {
         next_seg();
-        big_copy<RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, c + 1, sg, scol + q * 8, slim, st1, st1 + A_BYTES,
-                                      wave);
-        big_compute<RB, CU, G>(acc, st0, reinterpret_cast<const uint4*>(st0 + A_BYTES), wr, wc, lane);
+        big_copy<T, RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, c + 1, sg, scol + q * PV, slim, st1,
+                                         st1 + A_BYTES, wave);
+        big_compute<T, RB, CU, G>(acc, st0, reinterpret_cast<const uint4*>(st0 + A_BYTES), wr, wc, lane);
         __syncthreads();
         if (c + 2 < nch) {
             next_seg();
-            big_copy<RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, c + 2, sg, scol + q * 8, slim, st0,
-                                          st0 + A_BYTES, wave);
+            big_copy<T, RB, NSEG, NBW, KT::X>(soff, woff, rx, rh, rw, c + 2, sg, scol + q * PV, slim, st0,
+                                             st0 + A_BYTES, wave);
         }
-        big_compute<RB, CU, G>(acc, st1, reinterpret_cast<const uint4*>(st1 + A_BYTES), wr, wc, lane);
+        big_compute<T, RB, CU, G>(acc, st1, reinterpret_cast<const uint4*>(st1 + A_BYTES), wr, wc, lane);
         __syncthreads();
     }
-    if (c < nch) big_compute<RB, CU, G>(acc, st0, reinterpret_cast<const uint4*>(st0 + A_BYTES), wr, wc, lane);
+    if (c < nch) big_compute<T, RB, CU, G>(acc, st0, reinterpret_cast<const uint4*>(st0 + A_BYTES), wr, wc, lane);
     __syncthreads();   // the stages are free for the epilogue's operands
 
     // ---- epilogue operands, copied into the stage buffers: rows of 64 fp32
-    // values (this tile's units), the first half of each list in st0 and the
+    // values from the tile's first unit (its TU units, and for the narrow
+    // classes 32 more that go unused; past the arena they read as zero), the
+    // first half of each list in st0 and the
     // second in st1.  Cell kinds: the positional children's cell states.  The
     // forget GEMM: the children's own cell states.  The parent GEMM: the sums
     // of the children's products sigma(f_k) c_k (one row per parent) ----
@@ -293,21 +314,21 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
 // into one stage do not alias the reads of the other and does not wait for
 // the copies before the reads.
 #define EDB_BIG_STAGES(KIND, VB)                                                                       \
-    constexpr int SB_ = big_stage_bytes<Kind<KIND>::G, big_rb(Kind<KIND>::G, VB), BIG_CU>();          \
+    constexpr int SB_ = big_stage_bytes<Kind<KIND>::G, big_rb(Kind<KIND>::G, VB), big_cu(VB)>();      \
     __shared__ __align__(16) char st0[SB_];                                                         \
     __shared__ __align__(16) char st1[SB_]
 
 // One work-group per tile, in XCD-aware order.
-template <int KIND, int VB>
+template <int KIND, typename T, int VB>
 __global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
     EDB_BIG_STAGES(KIND, VB);
-    constexpr int TM = 32 * big_rb(Kind<KIND>::G, VB), TU = 32 * BIG_CU;
+    constexpr int TM = 32 * big_rb(Kind<KIND>::G, VB), TU = 32 * big_cu(VB);
     const int nut = a.Hu / TU;
     const int ntile = ((a.m + TM - 1) / TM) * nut;
     const int per = (ntile + 7) / 8;
     const int tile = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
     if (tile >= ntile) return;
-    big_tile<KIND, VB>(a, tile, st0, st1);
+    big_tile<KIND, T, VB>(a, tile, st0, st1);
 }
 
 // Per parent of a child-sum batch, after the forget GEMM: the child sum of h,

@@ -24,20 +24,24 @@ using namespace edbk;
 namespace {
 
 constexpr int NUM_SMALL = 8;
-constexpr int NUM_LARGE = 3;
+constexpr int NUM_LARGE = 3;        // large size classes 0-2 (variants 8-10)
 constexpr int NUM_STREAM = 4;
 constexpr int FIRST_STREAM = NUM_SMALL + NUM_LARGE;
-constexpr int NUM_VARIANTS = FIRST_STREAM + NUM_STREAM;
+constexpr int FIRST_NARROW = FIRST_STREAM + NUM_STREAM;   // large size classes 3-4 (variants 15-16)
+constexpr int NUM_VARIANTS = FIRST_NARROW + NUM_BIG_CLASSES - NUM_LARGE;
 // small (staged) and streamed tile variants: rows per work-group 16*RT, units
 // per work-group 16*WU, WK waves splitting the reduction (threads per
 // work-group 64*WU*WK); the large variants have no entry here
-constexpr int VAR_RT[NUM_VARIANTS] = {2, 1, 1, 1, 1, 1, 2, 2, 0, 0, 0, 1, 2, 1, 1};
-constexpr int VAR_WU[NUM_VARIANTS] = {4, 4, 2, 1, 1, 1, 1, 2, 0, 0, 0, 1, 1, 1, 1};
-constexpr int VAR_WK[NUM_VARIANTS] = {1, 1, 2, 4, 8, 16, 4, 2, 0, 0, 0, 4, 4, 8, 16};
-// large tile variants NUM_SMALL + vb: 32*big_rb(G, vb) rows x 64 units, 256 threads
-bool is_large(int v) { return v >= NUM_SMALL && v < FIRST_STREAM; }
+constexpr int VAR_RT[NUM_VARIANTS] = {2, 1, 1, 1, 1, 1, 2, 2, 0, 0, 0, 1, 2, 1, 1, 0, 0};
+constexpr int VAR_WU[NUM_VARIANTS] = {4, 4, 2, 1, 1, 1, 1, 2, 0, 0, 0, 1, 1, 1, 1, 0, 0};
+constexpr int VAR_WK[NUM_VARIANTS] = {1, 1, 2, 4, 8, 16, 4, 2, 0, 0, 0, 4, 4, 8, 16, 0, 0};
+// large tile variants 8-10 and 15-16 = size classes 0-4: 32*big_rb(G, vb) rows x
+// 32*big_cu(vb) units, 256 threads (bf16 and fp32; chunks of 128 bytes of k)
+bool is_large(int v) { return (v >= NUM_SMALL && v < FIRST_STREAM) || (v >= FIRST_NARROW && v < NUM_VARIANTS); }
+int large_class(int v) { return v < FIRST_STREAM ? v - NUM_SMALL : v - FIRST_NARROW + NUM_LARGE; }
+int large_variant(int vb) { return vb < NUM_LARGE ? NUM_SMALL + vb : FIRST_NARROW + vb - NUM_LARGE; }
 // streamed tile variants FIRST_STREAM..: 16*RT rows x 16 units, WK waves
-bool is_stream(int v) { return v >= FIRST_STREAM && v < NUM_VARIANTS; }
+bool is_stream(int v) { return v >= FIRST_STREAM && v < FIRST_NARROW; }
 bool is_small(int v) { return v >= 0 && v < NUM_SMALL; }
 // the staged variant with the same rows and reduction split as streamed variant v
 constexpr int STAGED_OF[NUM_STREAM] = {3, 6, 4, 5};
@@ -249,12 +253,12 @@ Entry entry() {
 }
 
 // the large tile's LDS is static (its two stages are distinct objects)
-template <int KIND, int VB>
+template <int KIND, typename T, int VB>
 void launch_big(const BatchArgs& a, int grid, int, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
     if (ev0)
-        hipExtLaunchKernelGGL((big_kernel<KIND, VB>), dim3(grid), dim3(256), 0, st, ev0, ev1, 0, a);
+        hipExtLaunchKernelGGL((big_kernel<KIND, T, VB>), dim3(grid), dim3(256), 0, st, ev0, ev1, 0, a);
     else
-        hipLaunchKernelGGL((big_kernel<KIND, VB>), dim3(grid), dim3(256), 0, st, a);
+        hipLaunchKernelGGL((big_kernel<KIND, T, VB>), dim3(grid), dim3(256), 0, st, a);
 }
 template <int KIND, int VB>
 hipError_t attr_big(int) { return hipSuccess; }
@@ -263,9 +267,9 @@ int lds_big(int) { return big_lds_bytes<KIND, VB>(); }
 
 template <int KIND, typename T, int VB>
 Entry big_entry() {
-    if constexpr (sizeof(T) == 2 && !Kind<KIND>::RAG)
-        return {launch_big<KIND, VB>, attr_big<KIND, VB>, lds_big<KIND, VB>,
-                reinterpret_cast<const void*>(&big_kernel<KIND, VB>)};
+    if constexpr (!Kind<KIND>::RAG)
+        return {launch_big<KIND, T, VB>, attr_big<KIND, VB>, lds_big<KIND, VB>,
+                reinterpret_cast<const void*>(&big_kernel<KIND, T, VB>)};
     else return {nullptr, nullptr, nullptr, nullptr};
 }
 
@@ -293,8 +297,9 @@ Entry stream_entry() {
                 reinterpret_cast<const void*>(&stream_kernel<KIND, T, RT, WK>)};
 }
 
-// Rows per work-group of large variant NUM_SMALL + vb for G gates.
+// Rows and units per work-group of large size class vb for G gates.
 int large_tm(int G, int vb) { return 32 * big_rb(G, vb); }
+int large_tu(int vb) { return 32 * big_cu(vb); }
 
 template <int KIND, typename T>
 void fill_kind(Entry* e) {
@@ -313,6 +318,8 @@ void fill_kind(Entry* e) {
     e[12] = stream_entry<KIND, T, 2, 4>();
     e[13] = stream_entry<KIND, T, 1, 8>();
     e[14] = stream_entry<KIND, T, 1, 16>();
+    e[15] = big_entry<KIND, T, 3>();
+    e[16] = big_entry<KIND, T, 4>();
 }
 
 // The internal kinds of a child-sum batch on the large tile have large bf16 variants only.
@@ -323,6 +330,8 @@ void fill_internal(Entry (&e)[2][NUM_VARIANTS]) {
     e[1][8] = big_entry<KIND, __bf16, 0>();
     e[1][9] = big_entry<KIND, __bf16, 1>();
     e[1][10] = big_entry<KIND, __bf16, 2>();
+    e[1][15] = big_entry<KIND, __bf16, 3>();
+    e[1][16] = big_entry<KIND, __bf16, 4>();
 }
 
 constexpr int NUM_KERNEL_KINDS = 10;   // the 8 cell kinds, then K_CS_FORGET, K_CS_PARENT
@@ -395,12 +404,12 @@ int flow_lds(const std::vector<int>& kinds_k) {
 // (operand rows and weights) and, for the staged tile, the bytes they stage;
 // the staged tile adds its split-K reduction and the chunks of the ragged
 // phase.  The coefficients of each family are a non-negative least-squares fit
-// (relative error) to per-batch sweeps of every variant on every batch of the
-// five workloads on MI355X (1634 batch/variant pairs; median error 9% staged,
-// 6% streamed).
+// (relative error) to per-launch times of every variant on every batch of the
+// five workloads on MI355X (1786 launches; median error 10% staged, 7%
+// streamed).
 double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int occ, int n_cu) {
-    static constexpr double kStaged[9] = {0.5359, 2.5249, 1.7686, 0.0014234, 0.04603, 0.0, 3.6911, 0.02489, 5.8812};
-    static constexpr double kStream[9] = {1.2620, 1.4361, 1.0504, 0.0087887, 0.0, 0.7956, 0.0, 0.0, 0.0};
+    static constexpr double kStaged[9] = {0.0339, 3.0711, 1.7942, 0.0010485, 0.043137, 0, 3.6341, 0, 6.3721};
+    static constexpr double kStream[9] = {1.1928, 1.4973, 1.1388, 0.0085032, 0, 0.6738, 0, 0, 0};
     const double* k = is_stream(v) ? kStream : kStaged;
     const int RT = VAR_RT[v], WU = VAR_WU[v], WK = VAR_WK[v], W = WU * WK;
     const int TM = 16 * RT, TU = 16 * WU;
@@ -429,43 +438,55 @@ double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int oc
     return t;
 }
 
-// Estimated microseconds of the large tile for G gates over K (padded), m
-// rows, fitted to measurements on MI355X: a 64-wide chunk takes the L2->LDS
-// copy time of the work-groups resident on a CU (about 86 GB/s per CU at full
-// load) or their matrix-core time, whichever is longer (their sum with one
-// work-group per CU, which cannot overlap them), plus 0.3 us; the epilogue
-// about 7 us per 16k elements per CU.  extra_us: work outside the model.
-double large_cost(int G, int vb, int m, int K, int Hu, int per_cu, int n_cu, double extra_us = 0.0) {
-    const int TM = large_tm(G, vb), RB = TM / 32;
-    const double tiles = (double)((m + TM - 1) / TM) * (Hu / (32 * BIG_CU));
-    per_cu = std::max(1, std::min(2, per_cu));
-    const double rounds = std::max(1.0, tiles / (double)(n_cu * per_cu));
-    const int nch = K / BIG_BK;
-    const double bytes = (double)TM * 128 + 2.0 * BIG_CU * G * 2 * 1024;
-    const double t_bw = per_cu * bytes / 86e3;
-    const double t_mma = per_cu * 2.0 * BIG_CU * G * RB * 16 / 2400.0;
-    const double t_chunk = (per_cu >= 2 ? std::max(t_bw, t_mma) : t_bw + t_mma) + 0.3;
-    const double t_epi = 7.0 * (per_cu * TM * 32.0 * BIG_CU) / 16384.0 * std::max(G, 1) / 3.0;
-    return rounds * (nch * t_chunk + t_epi) + 3.0 + extra_us;
+// Estimated microseconds of the large tile, size class vb, for G gates over K
+// (padded) and m rows, occ work-groups resident per CU.  The work-groups run
+// in rounds of n_cu * occ; a round of c work-groups per CU costs, per 128-byte
+// chunk of k, the bytes the c work-groups copy to LDS, their matrix-core time,
+// the longer of the two (copy at about 86 GB/s per CU), and with one resident
+// work-group their sum (nothing to overlap them with); plus an epilogue term
+// per element and gate.  Coefficients: a non-negative least-squares fit to
+// per-launch times of every size class on the batches of the binary TreeLSTM,
+// grid and child-sum workloads on MI355X (500 launches, median error 7%).
+double large_cost(int G, int vb, int m, int K, int Hu, int dtype, int occ, int n_cu) {
+    static constexpr double k[8] = {2.2914, 0, 0.44298, 0.27272, 0.8926, 0.003464, 3.0456, 0.12342};
+    const int RB = big_rb(G, vb), CU = big_cu(vb), TM = 32 * RB, TU = 32 * CU;
+    const bool f32 = dtype == EDB_F32;
+    const int64_t tiles = (int64_t)((m + TM - 1) / TM) * (Hu / TU);
+    occ = std::max(1, std::min(occ, 8));
+    const int64_t cap = (int64_t)n_cu * occ, full = tiles / cap, rem = tiles % cap;
+    const double nch = K / (f32 ? 32 : 64);
+    const double cpy = (TM * 128.0 + 2.0 * CU * G * 2 * 1024) / 1024.0;    // KB per chunk per work-group
+    const double mma = 2.0 * CU * G * RB * (f32 ? 128 : 16) / 2400.0;      // us per chunk per SIMD per work-group
+    auto round_us = [&](double c) {
+        return k[1] + k[2] * nch + k[3] * c * nch * cpy / 64.0 + k[4] * c * nch * mma +
+               k[5] * nch * std::max(c * cpy / 86.0, c * mma) + k[6] * c * TM * TU * G / 16384.0 +
+               (c == 1.0 ? k[7] * nch * (cpy / 86.0 + mma) : 0.0);
+    };
+    double t = k[0] + (double)full * round_us(occ);
+    if (rem) t += round_us((double)((rem + n_cu - 1) / n_cu));
+    return t;
 }
+
+// Estimated microseconds of child_reduce_kernel over m parents (fit as above).
+double child_reduce_cost(int m) { return 3.782 + 1.0572e-3 * m; }
 
 // Work-groups of a kernel resident on one CU (block threads, dyn_lds bytes of
 // dynamic LDS, lds bytes of LDS in all): from the runtime (registers and LDS)
 // when a device is bound, else from LDS and waves alone.
 using OccFn = std::function<int(const Entry&, int block, int dyn_lds, int lds)>;
 
-// Best large variant (NUM_SMALL + vb) of kernel kind kk for m rows, or -1.
+// Best large variant of kernel kind kk for m rows, or -1.
 int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max_lds, const OccFn& occ,
-               double& est, double extra_us = 0.0) {
+               double& est, double extra_us = 0.0) {   // dtype: EDB_F32 or EDB_BF16
     int var = -1;
     est = 1e300;
-    for (int vb = 0; vb < NUM_LARGE; ++vb) {
-        const Entry& en = table().e[kk][dtype][NUM_SMALL + vb];
+    for (int vb = 0; vb < NUM_BIG_CLASSES; ++vb) {
+        const Entry& en = table().e[kk][dtype][large_variant(vb)];
         if (!en.launch) continue;
         const int lds = en.lds(K);
         if (lds > max_lds) continue;
-        const double c = large_cost(G, vb, m, K, Hu, occ(en, 256, 0, lds), n_cu, extra_us);
-        if (c < est * 0.97) { est = c; var = NUM_SMALL + vb; }
+        const double c = large_cost(G, vb, m, K, Hu, dtype, occ(en, 256, 0, lds), n_cu) + extra_us;
+        if (c < est * 0.97) { est = c; var = large_variant(vb); }
     }
     return var;
 }
@@ -754,7 +775,8 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             int var = -1;
             double best = 1e300;
             // the large tile reads whole 64-wide k chunks of one operand segment
-            const bool large_ok = large_fits && d.Ep % 64 == 0 && d.Hk % 64 == 0 && !(flags & EDB_NO_LARGE);
+            const int big_chunk = dtype == EDB_F32 ? 32 : 64;   // k values per 128-byte chunk
+            const bool large_ok = large_fits && d.Ep % big_chunk == 0 && d.Hk % big_chunk == 0 && !(flags & EDB_NO_LARGE);
             const bool cs_large = kind_id == EDB_CELL_CS_INTERNAL && dtype == EDB_BF16;
             const int64_t nrag = d.rag ? p->ragged_pool[p->ragged_off[b] + m] : 0;   // children of the batch
             // large tile: the cell's own kernel, or for child-sum cells the
@@ -767,7 +789,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                     fvar = best_large(K_CS_FORGET, dtype, 1, (int)nrag, d.K, d.Hu, n_cu, max_lds, occ, ef);
                     lvar = best_large(K_CS_PARENT, dtype, 3, m, d.K, d.Hu, n_cu, max_lds, occ, ep);
                     if (fvar < 0 || lvar < 0) lvar = fvar = -1;
-                    else lest = ef + ep + 4.0;   // + the child-reduce kernel
+                    else lest = ef + ep + child_reduce_cost(m);
                 }
             } else if (large_ok) {
                 lvar = best_large(kind_id, dtype, d.G, m, d.K, d.Hu, n_cu, max_lds, occ, lest);
@@ -785,11 +807,8 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 const double est = variant_cost(vi, m, d, dtype, nrag, occ(en, block, lds, lds), n_cu);
                 if (est < best * 0.97) { best = est; var = vi; }
             }
-            // large tile for batches whose main GEMM has at least 4e8 multiply-adds
-            // (measured: from there on it beats the small tiles at bf16, K = 512)
-            (void)lest;
-            const bool big_gemm = (double)m * d.K * d.G * d.Hu >= 4e8;
-            if (lvar >= 0 && (large_only || var < 0 || big_gemm)) var = lvar;
+            // the large tile where its estimate beats the small and streamed tiles'
+            if (lvar >= 0 && (large_only || var < 0 || lest < best)) var = lvar;
             // a forced streamed variant falls back to its staged counterpart
             // for kinds it does not serve (and buffers beyond 32-bit offsets)
             int fv = force_var;
@@ -829,8 +848,8 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 F.off_res = -1;
                 F.lds = table().e[K_CS_FORGET][dtype][fvar].lds(d.K);
                 F.info.block = 256;
-                F.info.grid = ((int)((nrag + large_tm(1, fvar - NUM_SMALL) - 1) / large_tm(1, fvar - NUM_SMALL)) *
-                                   (d.Hu / (32 * BIG_CU)) + 7) / 8 * 8;
+                F.info.grid = ((int)((nrag + large_tm(1, large_class(fvar)) - 1) / large_tm(1, large_class(fvar))) *
+                                   (d.Hu / large_tu(large_class(fvar))) + 7) / 8 * 8;
                 parts.push_back(F);
                 // 1: per parent, the child sum of h (h~) and the sum of the children's products
                 Launch C = L;
@@ -864,8 +883,8 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             L.info.n_batches = 1;
             L.info.part = 0;
             if (is_large(var)) {
-                const int TM = large_tm(d.G, var - NUM_SMALL);
-                const int tiles = (m + TM - 1) / TM * (d.Hu / (32 * BIG_CU));
+                const int TM = large_tm(d.G, large_class(var));
+                const int tiles = (m + TM - 1) / TM * (d.Hu / large_tu(large_class(var)));
                 L.info.grid = (tiles + 7) / 8 * 8;   // XCD-aware order: 8 equal tile ranges
                 L.info.block = 256;
             } else if (is_stream(var)) {

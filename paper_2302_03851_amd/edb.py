@@ -37,7 +37,7 @@ class Graph:
         self.handle = h
 
     def __del__(self):
-        if getattr(self, "handle", None) and L._lib is not None:
+        if getattr(self, "handle", None) and L is not None and L._lib is not None:
             L._lib.edb_graph_free(self.handle)
             self.handle = None
 
@@ -95,7 +95,7 @@ class Schedule:
                 for b in range(self.n_batches)]
 
     def __del__(self):
-        if getattr(self, "handle", None) and L._lib is not None:
+        if getattr(self, "handle", None) and L is not None and L._lib is not None:
             L._lib.edb_schedule_free(self.handle)
             self.handle = None
 
@@ -145,7 +145,7 @@ class Plan:
         return out
 
     def __del__(self):
-        if getattr(self, "handle", None) and L._lib is not None:
+        if getattr(self, "handle", None) and L is not None and L._lib is not None:
             L._lib.edb_plan_free(self.handle)
             self.handle = None
 
@@ -205,7 +205,7 @@ class Exec:
                                      C.c_void_p(arena_c_ptr), C.c_void_p(stream)), "edb_execute")
 
     def __del__(self):
-        if getattr(self, "handle", None) and L._lib is not None:
+        if getattr(self, "handle", None) and L is not None and L._lib is not None:
             L._lib.edb_exec_free(self.handle)
             self.handle = None
 

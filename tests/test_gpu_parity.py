@@ -157,10 +157,11 @@ def _grid_graph(n_grids, R, C, E, H, seed, dtype):
 
 
 def _large_tile_workloads():
-    """bf16 workloads whose batches span several large tiles with a ragged row
-    tail: the child-sum configuration (its leaf batch), grids with a
+    """Workloads whose batches span several large tiles with a ragged row
+    tail.  bf16: the child-sum configuration (its leaf batch), grids with a
     zero-padded x segment (E = 120 in a 128-wide segment) and padded units
-    (H = 192 of 256), chains, binary trees."""
+    (H = 192 of 256), chains, binary trees.  fp32: the binary TreeLSTM
+    configuration, the same grids, chains."""
     out = [WL.make_config(5, instances=12), _grid_graph(24, 12, 12, 120, 192, seed=11, dtype="bf16")]
     n = 300   # chains of length 3
     op = [0] * (3 * n)
@@ -175,14 +176,19 @@ def _large_tile_workloads():
         hx += [True, True, False]
     out.append(WL.make_graph([WL.NARY_LEAF, WL.NARY_INTERNAL], 128, 256, op, ch, hx, seed=13, dtype="bf16",
                              bias_scale=0.2))
+    out += [WL.make_config(2, instances=16), _grid_graph(24, 12, 12, 120, 192, seed=14, dtype="f32")]
+    op = [0] * (3 * n)
+    ch = [[-1] if i % 3 == 0 else [i - 1] for i in range(3 * n)]
+    out.append(WL.make_graph([WL.LSTM_CHAIN], 64, 128, op, ch, [True] * (3 * n), seed=15, dtype="f32",
+                             bias_scale=0.2))
     return out
 
 
-@pytest.mark.parametrize("variant", [None, 8, 9, 10])
+@pytest.mark.parametrize("variant", [None, 8, 9, 10, 15, 16])
 def test_large_tile_bitwise_and_parity(variant, monkeypatch):
-    """The large bf16 tile (every supported batch forced onto it, or one size
-    class for all) is bitwise equal to the small tile without split-K, and
-    within the bf16 bound of the oracle."""
+    """The large tile, bf16 and fp32 (every supported batch forced onto it, or
+    one size class for all), is bitwise equal to the small tile without
+    split-K, and within the bound of the oracle."""
     _torch()
     for w in _large_tile_workloads():
         monkeypatch.delenv("EDB_VARIANT", raising=False)

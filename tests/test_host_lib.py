@@ -242,11 +242,11 @@ def test_dryrun_launch_list(k, flow):
             continue
         assert info["n_batches"] == 1
         assert info["m"] == f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b]
-        assert 0 <= info["variant"] <= 14 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
+        assert 0 <= info["variant"] <= 16 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
         if info["variant"] in L.LARGE_VARIANTS:
-            # large bf16 tile: every kind but the lattice character cell, 256 threads,
-            # grid a multiple of 8
-            assert w.dtype == "bf16" and w.kinds[t] != WL.LAT_CHAR
+            # large tile: every kind but the lattice character cell (child-sum parents run
+            # as a forget GEMM, child sums and a parent GEMM), 256 threads, grid a multiple of 8
+            assert w.kinds[t] != WL.LAT_CHAR
             assert info["block"] == 256 and info["grid"] % 8 == 0
         segs = f.plan.batch_segments(b)
         assert info["seg_kind"][0] == segs[0][0]
@@ -259,8 +259,9 @@ def test_dryrun_launch_list(k, flow):
         f.exec.launch_info(n)
 
 
-LARGE_TILE_ROWS = {8: 256, 9: 128, 10: 64}      # rows per work-group of the large variants at G = 3
-LARGE_TILE_ROWS_G1 = {8: 256, 9: 128, 10: 64}   # the one-gate forget GEMM of child-sum cells
+LARGE_TILE_ROWS = {8: 256, 9: 128, 10: 64, 15: 64, 16: 32}      # rows per work-group of the large variants at G = 3
+LARGE_TILE_ROWS_G1 = {8: 256, 9: 128, 10: 64, 15: 64, 16: 32}   # the one-gate forget GEMM of child-sum cells
+LARGE_TILE_UNITS = {8: 64, 9: 64, 10: 64, 15: 32, 16: 32}       # units per work-group
 
 
 def test_tile_flags_select_variants():
@@ -277,7 +278,7 @@ def test_tile_flags_select_variants():
         assert info["variant"] in L.LARGE_VARIANTS
         rows = LARGE_TILE_ROWS_G1 if info["part"] == L.PART_FORGET else LARGE_TILE_ROWS
         tm = rows[info["variant"]]
-        assert info["grid"] == -(-(-(-info["m"] // tm) * (512 // 64)) // 8) * 8
+        assert info["grid"] == -(-(-(-info["m"] // tm) * (512 // LARGE_TILE_UNITS[info["variant"]])) // 8) * 8
     f = edb.Forward(w, flags=base | L.NO_LARGE | L.NO_SPLIT_K)
     for i in range(1, f.exec.launches()):
         assert f.exec.launch_info(i)["variant"] in (0, 1)
