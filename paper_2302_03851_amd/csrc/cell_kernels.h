@@ -759,22 +759,29 @@ __device__ __forceinline__ void stream_tile(const BatchArgs& a, int rtile, int u
         for (int p = 0; p < NFX; ++p) crow[q][p] = seg_row_nb(a.fix[p], rr, a.m);
     }
 
-    // ---- 2. weights of the first PD k-groups (independent of the indices), bias.
-    // The prologue loads are unconditional (a wave without k-groups loads k-group
-    // 0 and does not use it): with no branch between the index loads and their
-    // use, the wait for the indices leaves these loads in flight ----
+    // ---- 2. the first PD k-groups: per slot its weights, then its operands
+    // (the order of the steady state, so that the loop's waits count the same
+    // loads behind each slot on entry as on the back edge).  The loads are
+    // unconditional (a wave without k-groups loads k-group 0 and does not use
+    // it): with no branch between the index loads and their use, the wait for
+    // the indices before the first operand load leaves the weights in flight.
+    // Operand byte offsets are out of range, i.e. zero, past the batch and for
+    // absent lists ----
     const uint4* Bw = reinterpret_cast<const uint4*>(a.W) + ((size_t)ub * G * nkg) * 64 + lane;
     SRing<G, RT, PD> ring;
-#pragma unroll
-    for (int p = 0; p < PD; ++p) load_b<G>(ring.b[p], Bw, nkg, max(min(kg0 + p, kg1 - 1), 0));
-    float bz[NI][G];   // the packed bias is zero-padded to Hu
-#pragma unroll
-    for (int q = 0; q < NI; ++q)
-#pragma unroll
-        for (int g = 0; g < G; ++g) bz[q][g] = a.bias[g * a.Hu + u0 + (tid + NT * q) % TU];
-
-    // ---- 3. operand byte offsets (out of range, i.e. zero, past the batch and
-    // for absent lists), the first PD k-groups of operands ----
+    const int xkg = HX ? a.Ep / KG : 0, hkg = a.Hk / KG;
+    int lk = kg0, ls, lc;   // load cursor: k-group, its segment, its first element there
+    if (kg0 < xkg) {
+        ls = 0;
+        lc = kg0 * KG;
+    } else {
+        const int t = kg0 - xkg, p = t / hkg;
+        ls = (HX ? 1 : 0) + p;
+        lc = (t - p * hkg) * KG;
+    }
+    // slot 0's weights go out before the operand offsets wait for the indices
+    load_b<G>(ring.b[0], Bw, nkg, min(max(lk, 0), nkg - 1));
+    __builtin_amdgcn_sched_barrier(0);
     uint32_t soff[NSEG][RT];
 #pragma unroll
     for (int rb = 0; rb < RT; ++rb) {
@@ -790,23 +797,20 @@ __device__ __forceinline__ void stream_tile(const BatchArgs& a, int rtile, int u
     }
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.xmat, HX ? (uint32_t)a.n_xrows * (uint32_t)a.E * ES : 0u);
     const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.arena_h, (uint32_t)a.n_slots * (uint32_t)a.H * ES);
-    const int xkg = HX ? a.Ep / KG : 0, hkg = a.Hk / KG;
-    int lk = kg0, ls, lc;   // load cursor: k-group, its segment, its first element there
-    if (kg0 < xkg) {
-        ls = 0;
-        lc = kg0 * KG;
-    } else {
-        const int t = kg0 - xkg, p = t / hkg;
-        ls = (HX ? 1 : 0) + p;
-        lc = (t - p * hkg) * KG;
-    }
 #pragma unroll
     for (int p = 0; p < PD; ++p) {
+        if (p > 0) load_b<G>(ring.b[p], Bw, nkg, min(max(lk, 0), nkg - 1));
         stream_load_a<T, RT, NSEG, HX>(ring.a[p], soff, rx, rh, ls, lc, a.E, a.H, lane);
         stream_next<KG, HX>(lk, ls, lc, kg1, a.Ep, a.Hk);
+        __builtin_amdgcn_sched_barrier(0);
     }
 
-    // ---- 4. the children's cell states for the epilogue ----
+    // ---- 3. bias and the children's cell states for the epilogue ----
+    float bz[NI][G];   // the packed bias is zero-padded to Hu
+#pragma unroll
+    for (int q = 0; q < NI; ++q)
+#pragma unroll
+        for (int g = 0; g < G; ++g) bz[q][g] = a.bias[g * a.Hu + u0 + (tid + NT * q) % TU];
     const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.arena_c, (uint32_t)a.n_slots * (uint32_t)a.H * 4u);
     float cpre[NI][NFX > 0 ? NFX : 1];
 #pragma unroll
@@ -827,6 +831,10 @@ __device__ __forceinline__ void stream_tile(const BatchArgs& a, int rtile, int u
     for (int g = 0; g < G; ++g)
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) acc[g][rt] = v4f{0.f, 0.f, 0.f, 0.f};
+    // Each slot's refill is issued right after its matrix-core work and pinned
+    // there (scheduling barrier): left alone, the compiler sinks all refills
+    // to the end of the unrolled body, and the next iteration then waits for
+    // loads it has only just issued.
     int kg = kg0;
     for (; kg + PD < kg1; kg += PD) {
 #pragma unroll
@@ -835,6 +843,7 @@ __device__ __forceinline__ void stream_tile(const BatchArgs& a, int rtile, int u
             load_b<G>(ring.b[p], Bw, nkg, lk);
             stream_load_a<T, RT, NSEG, HX>(ring.a[p], soff, rx, rh, ls, lc, a.E, a.H, lane);
             stream_next<KG, HX>(lk, ls, lc, kg1, a.Ep, a.Hk);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 #pragma unroll
