@@ -100,6 +100,7 @@ template <> struct Elem<__bf16> { static constexpr int KG = 32; static constexpr
 // A-tile row padding in elements: 16 bytes, so that the 16 rows read by one
 // MFMA operand load start in different LDS banks.
 template <typename T> constexpr int a_pad() { return 16 / (int)sizeof(T); }
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ int seg_row(const Seg& s, int r) {
     return s.kind == S_CONTIG ? s.base + r : s.idx[r];
@@ -202,61 +203,80 @@ __host__ __device__ constexpr int lds_bytes(int K) {
     return lds_rowc_off<KIND, T, RT, WU, WK>(K);
 }
 
+// Raw buffer resource over `bytes` bytes at p (gfx9 resource word 3).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte buffer load at byte offset off; zero past the end of the buffer.
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+// 4-byte buffer load at byte offset off; zero past the end of the buffer.
+__device__ __forceinline__ uint32_t bload32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+}
+// seg_row without a branch: an indexed list is read through a buffer of the
+// batch's m entries (zero past them), a list of another kind reads nothing.
+// Several of these issue their loads back to back and are waited for once.
+__device__ __forceinline__ int seg_row_nb(const Seg& s, int r, int m) {
+    const __amdgpu_buffer_rsrc_t ri = make_rsrc(s.idx, s.kind == S_INDEXED ? (uint32_t)m * 4u : 0u);
+    const int v = (int)bload32(ri, (uint32_t)r * 4u);
+    return s.kind == S_CONTIG ? s.base + r : v;
+}
+
 // One K segment of the A tile: tile row r reads source row
-// seg_row(seg, row0 + r) (the zero row 0 when the list is absent), `nreal`
-// 16-byte chunks of data (row stride `width` elements), zero up to `nv`
-// chunks.  Contiguous lists need no index load at all.
+// seg_row(seg, row0 + r) (zeros when the list is absent), `nreal` 16-byte
+// chunks of data (row stride `width` elements), zero up to `nv` chunks.
+// Contiguous lists need no index load at all.
 template <typename T>
 struct ASeg {
     const T* src;
     Seg seg;
     int row0;
-    int col;      // first chunk of the segment in the tile row
-    int nv;       // chunks of the (padded) segment
-    int nreal;    // chunks holding data
-    int width;    // source row stride (elements)
+    int col;        // first chunk of the segment in the tile row
+    int nv;         // chunks of the (padded) segment
+    int nreal;      // chunks holding data
+    int width;      // source row stride (elements)
+    int len;        // entries of the row list
 };
 
-template <typename T>
-__device__ __forceinline__ int aseg_row(const ASeg<T>& s, int r) {
-    return s.seg.kind == S_NONE ? 0 : seg_row(s.seg, s.row0 + r);
-}
-
-// Stage the A tile [TM rows][nseg segments] with up to 8 outstanding 16-byte
-// loads per thread.
-template <typename T, int TM, int NT, int NSEG>
-__device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSEG], int nrows, int tid) {
+// Stage the A tile [TM rows][nseg segments], one segment at a time, in rounds
+// of up to SR items per thread (4: the staged values share the registers with
+// the weight ring already in flight): the round's row indices are loaded back to
+// back without branches (seg_row_nb), then its 16-byte pieces, then stored to
+// LDS.  A piece past the batch, the data or an absent list reads 16 bytes of
+// `zero` (the arena's zero row) instead of branching around its load, so the
+// round's loads issue back to back and are waited for once.
+template <typename T, int TM, int NT, int NSEG, int SR = 4>
+__device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSEG], int nrows, const T* zero,
+                                           int tid) {
     constexpr int V = Elem<T>::VEC;
-    int nvt = 0;
 #pragma unroll
-    for (int s = 0; s < NSEG; ++s) nvt += sg[s].nv;
-    const int total = TM * nvt;
-    for (int base = 0; base < total; base += NT * 8) {
-        uint4 val[8];
-        int dst[8];
+    for (int s = 0; s < NSEG; ++s) {
+        const ASeg<T>& q = sg[s];
+        const int total = TM * q.nv;
+        for (int base = 0; base < total; base += NT * SR) {
+            int row[SR];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int it = base + i * NT + tid;
-            val[i] = make_uint4(0, 0, 0, 0);
-            dst[i] = -1;
-            if (it < total) {
-                const int r = it / nvt;
-                int c = it - r * nvt;
+            for (int i = 0; i < SR; ++i) {
+                const int it = min(base + i * NT + tid, total - 1);
+                row[i] = seg_row_nb(q.seg, q.row0 + it / q.nv, q.len);
+            }
+            u32x4 val[SR];   // a vector type: struct copies of uint4 kept the array in scratch
 #pragma unroll
-                for (int s = 0; s < NSEG; ++s) {
-                    if (c >= 0 && c < sg[s].nv) {
-                        if (r < nrows && c < sg[s].nreal)
-                            val[i] = *reinterpret_cast<const uint4*>(sg[s].src + (size_t)aseg_row(sg[s], r) * sg[s].width +
-                                                                     c * V);
-                        dst[i] = r * AS + (sg[s].col + c) * V;
-                    }
-                    c -= sg[s].nv;
-                }
+            for (int i = 0; i < SR; ++i) {
+                const int it = base + i * NT + tid, r = it / q.nv, c = it - r * q.nv;
+                const bool ok = it < total && r < nrows && c < q.nreal && q.seg.kind != S_NONE;
+                val[i] = *reinterpret_cast<const u32x4*>(ok ? q.src + (size_t)row[i] * q.width + c * V : zero);
+            }
+            // keeps the loads together (the compiler would sink each into its store's branch)
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < SR; ++i) {
+                const int it = base + i * NT + tid, r = it / q.nv, c = it - r * q.nv;
+                if (it < total) *reinterpret_cast<u32x4*>(A + r * AS + (q.col + c) * V) = val[i];
             }
         }
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            if (dst[i] >= 0) *reinterpret_cast<uint4*>(A + dst[i]) = val[i];
     }
 }
 
@@ -299,27 +319,6 @@ __device__ __forceinline__ void stage_child_sum(T* A, int AS, const BatchArgs& a
         for (int i = 0; i < V; ++i) po[i] = from_f<T>(acc[i]);
         *reinterpret_cast<uint4*>(A + r * AS + c * V) = out;
     }
-}
-
-// Raw buffer resource over `bytes` bytes at p (gfx9 resource word 3).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
-}
-// 16-byte buffer load at byte offset off; zero past the end of the buffer.
-__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
-}
-// 4-byte buffer load at byte offset off; zero past the end of the buffer.
-__device__ __forceinline__ uint32_t bload32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
-}
-// seg_row without a branch: an indexed list is read through a buffer of the
-// batch's m entries (zero past them), a list of another kind reads nothing.
-// Several of these issue their loads back to back and are waited for once.
-__device__ __forceinline__ int seg_row_nb(const Seg& s, int r, int m) {
-    const __amdgpu_buffer_rsrc_t ri = make_rsrc(s.idx, s.kind == S_INDEXED ? (uint32_t)m * 4u : 0u);
-    const int v = (int)bload32(ri, (uint32_t)r * 4u);
-    return s.kind == S_CONTIG ? s.base + r : v;
 }
 
 // MFMA on one (gate, row-block) accumulator for one k-group.
@@ -454,12 +453,15 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
     // ---- 1. early loads: the epilogue's result rows and child cell states ----
     // (row indices of contiguous lists are arithmetic; indexed lists cost one
     // load, issued here in parallel with the operand and weight loads)
-    int rres[NI];
+    // (branch-free: the lookups of a thread issue back to back; a masked
+    // cell state reads the zero row instead of branching around its load)
+    int rres[NI], crow[NI][NFX > 0 ? NFX : 1];
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
-        const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
-        const bool ok = it < NITEM && r < nrows && j < a.H;
-        rres[q] = ok ? seg_row(a.res, row0 + r) : 0;
+        const int rr = row0 + min(tid + NT * q, NITEM - 1) / TU;
+        rres[q] = seg_row_nb(a.res, rr, a.m);
+#pragma unroll
+        for (int p = 0; p < NFX; ++p) crow[q][p] = seg_row_nb(a.fix[p], rr, a.m);
     }
     sync.wait();   // producers of this tile's operand rows have finished
     float cpre[NI][NFX > 0 ? NFX : 1];
@@ -469,9 +471,8 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
         const bool ok = it < NITEM && r < nrows && j < a.H;
 #pragma unroll
         for (int p = 0; p < (NFX > 0 ? NFX : 1); ++p) {
-            cpre[q][p] = 0.f;
-            if (NFX > p && ok && a.fix[p].kind != S_NONE)
-                cpre[q][p] = a.arena_c[(size_t)seg_row(a.fix[p], row0 + r) * a.H + j];
+            const bool use = NFX > p && ok && a.fix[p].kind != S_NONE;
+            cpre[q][p] = *(use ? a.arena_c + (size_t)crow[q][p] * a.H + j : a.arena_c);
         }
     }
 
@@ -484,16 +485,16 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
         ASeg<T> sg[NSEG];
         int s = 0, col = 0;
         if constexpr (KT::X) {
-            sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.xmat), a.x, row0, 0, a.Ep / V, a.E / V, a.E};
+            sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.xmat), a.x, row0, 0, a.Ep / V, a.E / V, a.E, a.m};
             col += a.Ep / V;
         }
 #pragma unroll
         for (int p = 0; p < NFX; ++p) {
             // an absent operand list reads the zero row 0
-            sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.fix[p], row0, col, a.Hk / V, a.H / V, a.H};
+            sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.fix[p], row0, col, a.Hk / V, a.H / V, a.H, a.m};
             col += a.Hk / V;
         }
-        stage_tile<T, TM, NT, NSEG>(A, AS, sg, nrows, tid);
+        stage_tile<T, TM, NT, NSEG>(A, AS, sg, nrows, reinterpret_cast<const T*>(a.arena_h), tid);
     }
     __syncthreads();
 
@@ -571,8 +572,9 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
             }
             if constexpr (KIND == K_CS_INT) {
                 constexpr int V = Elem<T>::VEC;
-                ASeg<T> sg[1] = {ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.rag, cb, 0, a.Hk / V, a.H / V, a.H}};
-                stage_tile<T, TMR, NT, 1>(A, RS, sg, cn, tid);
+                ASeg<T> sg[1] = {ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.rag, cb, 0, a.Hk / V, a.H / V, a.H,
+                                         cb + cn}};
+                stage_tile<T, TMR, NT, 1>(A, RS, sg, cn, reinterpret_cast<const T*>(a.arena_h), tid);
             } else {
                 // lattice: the word cell states c_w (fp32) converted to T
                 constexpr int V = Elem<T>::VEC;
@@ -648,12 +650,12 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
 }
 
 // One launch per batch: work-group -> (row tile, unit tile).  Work-groups of
-// 4 waves without a ragged phase ask for at least 3 waves per SIMD (at most
-// 168 registers a lane): 3 such work-groups per CU, so batches of up to 768
-// tiles run in one round (unbounded, the compiler used up to 220 registers,
-// 2 work-groups per CU).
+// 4 waves without a ragged phase (and not 32 rows x 64 units, which would
+// spill) ask for at least 3 waves per SIMD (at most 168 registers a lane): 3
+// such work-groups per CU, so batches of up to 768 tiles run in one round
+// (unbounded, the compiler used up to 220 registers, 2 work-groups per CU).
 template <int KIND, typename T, int RT, int WU, int WK>
-__global__ __launch_bounds__(64 * WU * WK, WU * WK == 4 && !Kind<KIND>::RAG ? 3 : 1) void cell_kernel(BatchArgs a) {
+__global__ __launch_bounds__(64 * WU * WK, WU * WK == 4 && RT * WU <= 4 && !Kind<KIND>::RAG ? 3 : 1) void cell_kernel(BatchArgs a) {
     extern __shared__ __align__(16) char smem[];
     const int nut = a.Hu / (16 * WU);
     cell_tile<KIND, T, RT, WU, WK>(a, blockIdx.x / nut, blockIdx.x % nut, smem, NoSync{});
