@@ -401,15 +401,16 @@ int flow_lds(const std::vector<int>& kinds_k) {
 // variant v, occ work-groups of it resident per CU.  The work-groups run in
 // rounds of n_cu * occ; each round costs a latency term plus, for the busiest
 // CU's c work-groups, their matrix-core time per SIMD, the bytes they load
-// (operand rows and weights) and, for the staged tile, the bytes they stage;
-// the staged tile adds its split-K reduction and the chunks of the ragged
-// phase.  The coefficients of each family are a non-negative least-squares fit
-// (relative error) to per-launch times of every variant on every batch of the
-// five workloads on MI355X (1786 launches; median error 10% staged, 7%
-// streamed).
+// (operand rows and weights) and, for the staged tile, the bytes they stage,
+// and the bytes beyond 100 KB per CU (L2 bandwidth saturating); the staged
+// tile adds its split-K reduction and the chunks of the ragged phase; the
+// whole batch adds a term in its total loaded bytes.  The coefficients of
+// each family are a non-negative least-squares fit (relative error) to
+// per-launch times of every variant on every batch of the five workloads on
+// MI355X (2636 launches; median error 4.4% staged, 3.5% streamed).
 double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int occ, int n_cu) {
-    static constexpr double kStaged[9] = {0.0339, 3.0711, 1.7942, 0.0010485, 0.043137, 0, 3.6341, 0, 6.3721};
-    static constexpr double kStream[9] = {1.1928, 1.4973, 1.1388, 0.0085032, 0, 0.6738, 0, 0, 0};
+    static constexpr double kStaged[11] = {0, 3.7873, 1.5822, 0, 0.0015529, 1.1881, 2.8009, 0, 7.3157, 0, 0.023189};
+    static constexpr double kStream[11] = {1.4473, 1.8894, 0.88904, 0, 0, 0.50528, 0, 0, 0, 0.0068505, 0.021677};
     const double* k = is_stream(v) ? kStream : kStaged;
     const int RT = VAR_RT[v], WU = VAR_WU[v], WK = VAR_WK[v], W = WU * WK;
     const int TM = 16 * RT, TU = 16 * WU;
@@ -432,9 +433,11 @@ double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int oc
     const double per_round_fixed = k[1] + k[5] * WK * RT * d.G / 64.0 + k[6] * chunks +
                                    k[7] * chunks * rkpw * RTR * (dtype == EDB_F32 ? 8.0 : 1.0) / 64.0 +
                                    k[8] * chunks * rkpw / 16.0;
-    const double per_wg = k[2] * mf + k[3] * ld + k[4] * st;
-    double t = k[0] + (double)full * (per_round_fixed + occ * per_wg);
-    if (rem) t += per_round_fixed + (double)((rem + n_cu - 1) / n_cu) * per_wg;
+    auto round_us = [&](double c) {
+        return per_round_fixed + c * (k[2] * mf + k[3] * ld + k[4] * st) + k[9] * std::max(0.0, c * ld - 100.0);
+    };
+    double t = k[0] + (double)full * round_us(occ) + k[10] * (double)tiles * ld / 1024.0;
+    if (rem) t += round_us((double)((rem + n_cu - 1) / n_cu));
     return t;
 }
 
@@ -444,11 +447,17 @@ double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int oc
 // chunk of k, the bytes the c work-groups copy to LDS, their matrix-core time,
 // the longer of the two (copy at about 86 GB/s per CU), and with one resident
 // work-group their sum (nothing to overlap them with); plus an epilogue term
-// per element and gate.  Coefficients: a non-negative least-squares fit to
-// per-launch times of every size class on the batches of the binary TreeLSTM,
-// grid and child-sum workloads on MI355X (500 launches, median error 7%).
+// per element and gate.  Coefficients per size class: non-negative
+// least-squares fits to per-launch times of the class on the batches of all
+// five workloads on MI355X (594 launches, median error 3-5% per class).
 double large_cost(int G, int vb, int m, int K, int Hu, int dtype, int occ, int n_cu) {
-    static constexpr double k[8] = {2.2914, 0, 0.44298, 0.27272, 0.8926, 0.003464, 3.0456, 0.12342};
+    static constexpr double kc[NUM_BIG_CLASSES][8] = {
+        {0, 3.3767, 0.016996, 1.6769, 0, 0.92299, 0.38126, 0},
+        {0, 2.3427, 0.59572, 0.5983, 0, 1.0321, 0, 0},
+        {1.3643, 1.2412, 0.46072, 0.099006, 0, 1.1841, 0, 0},
+        {1.3794, 0.13501, 0.61735, 0.35123, 0.98106, 0, 1.161, 0},
+        {1.4102, 0.6417, 0.46044, 0.24468, 1.1586, 0, 0.76119, 0}};
+    const double* k = kc[vb];
     const int RB = big_rb(G, vb), CU = big_cu(vb), TM = 32 * RB, TU = 32 * CU;
     const bool f32 = dtype == EDB_F32;
     const int64_t tiles = (int64_t)((m + TM - 1) / TM) * (Hu / TU);
@@ -468,7 +477,7 @@ double large_cost(int G, int vb, int m, int K, int Hu, int dtype, int occ, int n
 }
 
 // Estimated microseconds of child_reduce_kernel over m parents (fit as above).
-double child_reduce_cost(int m) { return 3.782 + 1.0572e-3 * m; }
+double child_reduce_cost(int m) { return 3.794 + 1.0509e-3 * m; }
 
 // Work-groups of a kernel resident on one CU (block threads, dyn_lds bytes of
 // dynamic LDS, lds bytes of LDS in all): from the runtime (registers and LDS)
