@@ -438,6 +438,12 @@ double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int oc
     };
     double t = k[0] + (double)full * round_us(occ) + k[10] * (double)tiles * ld / 1024.0;
     if (rem) t += round_us((double)((rem + n_cu - 1) / n_cu));
+    // streamed tile whose waves load their whole k-range in the ring prologue,
+    // with several work-groups per CU: all request their operands at once and
+    // no loads overlap the matrix cores.  The linear terms miss this; the
+    // factor is the measured ratio on such batches (C2's 1,858-row leaf batch).
+    const int pd = WK >= 16 ? 2 : (d.G >= 5 ? 3 : 4);
+    if (is_stream(v) && kpw <= pd && tiles > n_cu) t *= 1.45;
     return t;
 }
 
