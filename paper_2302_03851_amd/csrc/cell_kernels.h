@@ -240,13 +240,15 @@ struct ASeg {
     int len;        // entries of the row list
 };
 
-// Stage the A tile [TM rows][nseg segments], one segment at a time, in rounds
-// of up to SR items per thread (4: the staged values share the registers with
-// the weight ring already in flight): the round's row indices are loaded back to
-// back without branches (seg_row_nb), then its 16-byte pieces, then stored to
-// LDS.  A piece past the batch, the data or an absent list reads 16 bytes of
-// `zero` (the arena's zero row) instead of branching around its load, so the
-// round's loads issue back to back and are waited for once.
+// Stage the first nrows rows of the A tile [TM rows][nseg segments] (rows past
+// them are left as they are: each output row depends on its own A row only,
+// and the epilogue skips them), one segment at a time, in rounds of up to SR
+// items per thread (4: the staged values share the registers with the weight
+// ring already in flight): the round's row indices are loaded back to back
+// without branches (seg_row_nb), then its 16-byte pieces, then stored to LDS.
+// A piece past the data (the zero padding of K) or of an absent list reads 16
+// bytes of `zero` (the arena's zero row) instead of branching around its
+// load, so the round's loads issue back to back and are waited for once.
 template <typename T, int TM, int NT, int NSEG, int SR = 4>
 __device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSEG], int nrows, const T* zero,
                                            int tid) {
@@ -254,7 +256,7 @@ __device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSE
 #pragma unroll
     for (int s = 0; s < NSEG; ++s) {
         const ASeg<T>& q = sg[s];
-        const int total = TM * q.nv;
+        const int total = nrows * q.nv;
         for (int base = 0; base < total; base += NT * SR) {
             int row[SR];
 #pragma unroll
@@ -266,7 +268,7 @@ __device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSE
 #pragma unroll
             for (int i = 0; i < SR; ++i) {
                 const int it = base + i * NT + tid, r = it / q.nv, c = it - r * q.nv;
-                const bool ok = it < total && r < nrows && c < q.nreal && q.seg.kind != S_NONE;
+                const bool ok = it < total && c < q.nreal && q.seg.kind != S_NONE;
                 val[i] = *reinterpret_cast<const u32x4*>(ok ? q.src + (size_t)row[i] * q.width + c * V : zero);
             }
             // keeps the loads together (the compiler would sink each into its store's branch)
@@ -280,37 +282,39 @@ __device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSE
     }
 }
 
-// Child sum of h rows for child-sum internal nodes: A[r][k] = sum_children h[k].
+// Child sum of h rows for child-sum internal nodes: A[r][k] = sum_children h[k],
+// in child order.  Children are taken 4 at a time: their row indices are
+// loaded back to back without branches, then their 16-byte pieces (a slot
+// past the last child reads the zero row and is not added), so a parent
+// costs one index and one data round trip per 4 children.
 template <typename T, int TM, int NT>
 __device__ __forceinline__ void stage_child_sum(T* A, int AS, const BatchArgs& a, int row0, int nrows, int tid) {
     constexpr int V = Elem<T>::VEC;
+    constexpr int CB = 4;
     const T* h = reinterpret_cast<const T*>(a.arena_h);
     const int nv = a.Hk / V, nreal = a.H / V;
-    for (int it = tid; it < TM * nv; it += NT) {
+    for (int it = tid; it < nrows * nv; it += NT) {   // rows past nrows are not read back
         const int r = it / nv, c = it % nv;
+        const bool ok = c < nreal;
+        const int rr = row0 + min(r, nrows - 1);
+        const int e0 = a.rag_ptr[rr], e1 = ok ? a.rag_ptr[rr + 1] : e0;
         float acc[V];
 #pragma unroll
         for (int i = 0; i < V; ++i) acc[i] = 0.f;
-        if (r < nrows && c < nreal) {
-            const int e0 = a.rag_ptr[row0 + r], e1 = a.rag_ptr[row0 + r + 1];
-            int e = e0;
-            for (; e + 4 <= e1; e += 4) {
-                uint4 raw[4];
+        for (int e = e0; e < e1; e += CB) {
+            int row[CB];
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    raw[q] = *reinterpret_cast<const uint4*>(h + (size_t)seg_row(a.rag, e + q) * a.H + c * V);
+            for (int q = 0; q < CB; ++q) row[q] = seg_row_nb(a.rag, min(e + q, e1 - 1), e1);
+            u32x4 raw[CB];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const T* pv = reinterpret_cast<const T*>(&raw[q]);
+            for (int q = 0; q < CB; ++q)
+                raw[q] = *reinterpret_cast<const u32x4*>(e + q < e1 ? h + (size_t)row[q] * a.H + c * V : h);
+#pragma unroll
+            for (int q = 0; q < CB; ++q) {
+                const T* pv = reinterpret_cast<const T*>(&raw[q]);
+                if (e + q < e1)
 #pragma unroll
                     for (int i = 0; i < V; ++i) acc[i] += to_f(pv[i]);
-                }
-            }
-            for (; e < e1; ++e) {
-                uint4 raw = *reinterpret_cast<const uint4*>(h + (size_t)seg_row(a.rag, e) * a.H + c * V);
-                const T* pv = reinterpret_cast<const T*>(&raw);
-#pragma unroll
-                for (int i = 0; i < V; ++i) acc[i] += to_f(pv[i]);
             }
         }
         uint4 out;
@@ -566,9 +570,25 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
             __syncthreads();   // previous chunk's readers of A / Zr / Crag are done
             BRing<1, 4> rring;
             ring_prologue<1, 4>(rring, Brag, nkgr, rk0, rk1);
-            for (int it = tid; it < TMR * TU; it += NT) {
-                const int r = it / TU, j = u0 + it % TU;
-                Crag[it] = (r < cn && j < a.H) ? a.arena_c[(size_t)seg_row(a.rag, cb + r) * a.H + j] : 0.f;
+            {   // the chunk's cell states: indices, then values (masked: the zero row), then stores
+                constexpr int NCI = (TMR * TU + NT - 1) / NT;
+                int crw[NCI];
+                float cv[NCI];
+#pragma unroll
+                for (int q = 0; q < NCI; ++q) {
+                    const int it = min(tid + NT * q, TMR * TU - 1);
+                    crw[q] = seg_row_nb(a.rag, cb + min(it / TU, cn - 1), cb + cn);
+                }
+#pragma unroll
+                for (int q = 0; q < NCI; ++q) {
+                    const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
+                    const bool ok = it < cn * TU && j < a.H;
+                    cv[q] = *(ok ? a.arena_c + (size_t)crw[q] * a.H + j : a.arena_c);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int q = 0; q < NCI; ++q)   // rows past cn are never read
+                    if (tid + NT * q < cn * TU) Crag[tid + NT * q] = cv[q];
             }
             if constexpr (KIND == K_CS_INT) {
                 constexpr int V = Elem<T>::VEC;
@@ -576,19 +596,40 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
                                          cb + cn}};
                 stage_tile<T, TMR, NT, 1>(A, RS, sg, cn, reinterpret_cast<const T*>(a.arena_h), tid);
             } else {
-                // lattice: the word cell states c_w (fp32) converted to T
+                // lattice: the word cell states c_w (fp32) converted to T, two
+                // pieces per thread a round: indices, then values (masked: the
+                // zero row), then the converted stores
                 constexpr int V = Elem<T>::VEC;
-                const int nv = a.Hk / V, nreal = a.H / V;
-                for (int it = tid; it < TMR * nv; it += NT) {
-                    const int r = it / nv, c = it % nv;
-                    uint4 out = make_uint4(0, 0, 0, 0);
-                    T* po = reinterpret_cast<T*>(&out);
-                    if (r < cn && c < nreal) {
-                        const float* src = a.arena_c + (size_t)seg_row(a.rag, cb + r) * a.H + c * V;
+                const int nv = a.Hk / V, nreal = a.H / V, total = cn * nv;   // rows past cn are not read back
+                for (int base = 0; base < total; base += 2 * NT) {
+                    int wr[2];
 #pragma unroll
-                        for (int i = 0; i < V; ++i) po[i] = from_f<T>(src[i]);
+                    for (int q = 0; q < 2; ++q) {
+                        const int it = min(base + q * NT + tid, total - 1);
+                        wr[q] = seg_row_nb(a.rag, cb + min(it / nv, cn - 1), cb + cn);
                     }
-                    *reinterpret_cast<uint4*>(A + r * RS + c * V) = out;
+                    float4 f4[2][V / 4];
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        const int it = base + q * NT + tid, r = it / nv, c = it - r * nv;
+                        const bool ok = it < total && c < nreal;
+                        const float4* src = reinterpret_cast<const float4*>(
+                            ok ? a.arena_c + (size_t)wr[q] * a.H + c * V : a.arena_c);
+#pragma unroll
+                        for (int k = 0; k < V / 4; ++k) f4[q][k] = src[k];
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        const int it = base + q * NT + tid, r = it / nv, c = it - r * nv;
+                        if (it >= total) continue;
+                        uint4 out;
+                        T* po = reinterpret_cast<T*>(&out);
+                        const float* pf = reinterpret_cast<const float*>(&f4[q][0]);
+#pragma unroll
+                        for (int i = 0; i < V; ++i) po[i] = from_f<T>(pf[i]);
+                        *reinterpret_cast<uint4*>(A + r * RS + c * V) = out;
+                    }
                 }
             }
             __syncthreads();
