@@ -25,6 +25,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "node-cells/sec on 1 MI355X + % of MFMA/HBM roofline, TreeLSTM h=256"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # dense MFMA peaks (fp32, bf16)
+# --policy names -> edb policy kinds (a learned table runs as a table policy)
+POLICIES = {"table": 0, "learned": 0, "agenda": 1, "depth": 2, "sufficient": 3}
 PEAK_HBM_GBS = 8000.0
 
 WORKLOAD_TEXT = {
@@ -210,6 +212,9 @@ def main():
                     help="mini-batches in flight: host worker threads, each with its own stream and arena")
     ap.add_argument("--timed-events", type=int, default=8,
                     help="steps of worker 0 in the timed region whose launches record HIP events")
+    ap.add_argument("--policy", default="table", choices=sorted(POLICIES),
+                    help="batching policy: the configured FSM table (default), a table learned on the "
+                         "workload's graph before timing (N-step Q-learning, E_sort), or a heuristic")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 256 MiB, 5 times (to scale HBM byte counters)")
@@ -247,13 +252,26 @@ def main():
     w = WL.make_config(args.config)
     V = w.n_nodes
 
+    # batching policy (a learned table is learned here, before any timing:
+    # the paper learns one table per model offline)
+    kind = POLICIES[args.policy]
+    table = edb.LATTICE_TABLE if args.config == 3 else None
+    policy_info = {"kind": args.policy}
+    if args.policy == "learned":
+        g0 = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+        tl = time.perf_counter()
+        table, lstats, _ = edb.learn_policy(g0, L.ENC_SORT)
+        policy_info.update(lstats, learn_ms=round((time.perf_counter() - tl) * 1e3, 2), encoding="E_sort")
+        del g0
+    elif kind != L.POLICY_TABLE:
+        table = None
+
     # resident inputs: packed weights, x, arena
-    base = edb.Forward(w, flags=L.USE_GRAPH)
+    base = edb.Forward(w, policy=kind, table=table, flags=L.USE_GRAPH)
     stream = base.stream.cuda_stream
     wptrs = [b.data_ptr() for b in base.weights]
     xp, ahp, acp = base.x.data_ptr(), base.arena_h.data_ptr(), base.arena_c.data_ptr()
     shapes = edb.operand_shapes(w)
-    table = edb.LATTICE_TABLE if args.config == 3 else None
     dt = base.dtype
 
     import threading
@@ -268,9 +286,9 @@ def main():
     # executors are kept until the region has ended and are then read.  All
     # other steps run without events (the events cost host time on every step).
     fwd = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
-                          table=table)
+                          policy=kind, table=table)
     fwd_prof = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
-                               table=table, flags=L.PROFILE)
+                               policy=kind, table=table, flags=L.PROFILE)
     n_rows = base.plan.n_slots
 
     def step(i, keep):
@@ -346,7 +364,7 @@ def main():
     nh = 20
     for _ in range(nh):
         g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
-        s = edb.Schedule(g, L.POLICY_TABLE, L.ENC_SORT, table)
+        s = edb.Schedule(g, kind, L.ENC_SORT, table)
         p = edb.Plan(g, s, shapes, L.PLAN_RC)
         ex = edb.Exec(g, s, p, base.cells, 0)
     ms_host = (time.perf_counter() - th) * 1e3 / nh
@@ -401,6 +419,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.config], "nodes": V, "batches": base.sched.n_batches,
                    "launches_per_step": base.exec.launches(), "mini_batches_in_flight": S,
+                   "policy": policy_info,
                    "step": "graph ingest + schedule + memory plan + launch prep + device execution"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(tflops / peak, 4), "traffic": traffic,

@@ -80,6 +80,7 @@ edb_status edb_graph_info(const edb_graph_t* g, int32_t* n_nodes, int32_t* n_typ
 #define EDB_POLICY_TABLE  0  /* FSM policy table keyed by the state encoding */
 #define EDB_POLICY_AGENDA 1  /* type of minimal mean topological depth (DyNet agenda) */
 #define EDB_POLICY_DEPTH  2  /* groups of equal (depth, type) (TensorFlow Fold) */
+#define EDB_POLICY_SUFFICIENT 3  /* type maximizing Eq. 1's frontier ratio (Lemma 1) */
 
 #define EDB_ENC_SORT 0  /* frontier types sorted by frontier count desc, ties by id */
 #define EDB_ENC_BASE 1  /* set of frontier types, ascending id */
@@ -111,6 +112,70 @@ edb_status edb_schedule_view(const edb_schedule_t* s, int32_t* n_batches,
                              const int32_t** batch_ptr, const int32_t** batch_nodes,
                              const int32_t** batch_type);
 void edb_schedule_free(edb_schedule_t* s);
+
+/* Lower bound on the number of batches of any schedule (Appendix A.3): the
+ * sum over types of the longest path, counted in nodes, of the subgraph
+ * induced on that type's nodes (direct edges between them only).
+ * Errors: EDB_ERR_INVALID (NULL). */
+edb_status edb_lower_bound(const edb_graph_t* g, int64_t* lower_bound);
+
+/* ---- learning the FSM policy (Section 2.3) ------------------------------ */
+/* Tabular Q-learning with N-step bootstrapping over Algorithm 1's batching
+ * loop.  State S_t = E(G_t) in the given encoding; actions = the frontier
+ * types; reward (Eq. 1, its ratio taken as the worked example of Section 2.3
+ * evaluates it, in (0, 1]):
+ *     r = -1 + alpha * |Frontier_a(G_t)| / |Frontier(G^a_t)|
+ * where G^a is the subgraph induced on type-a nodes.  The target of
+ * Q(S_tau, a_tau) is the N-step return (gamma-discounted rewards of steps
+ * tau .. tau+N-1, plus gamma^N max_a Q(S_{tau+N}, a) unless the episode ended
+ * first), applied as Q += lr * (target - Q) as soon as S_{tau+N} is known,
+ * and for the remaining steps, in order, when the episode ends.  Q starts at
+ * 0.  Actions are epsilon-greedy; argmax ties go to the first action in the
+ * state key.  Every check_every trials and after the last one the greedy
+ * table (one entry per state with a Q entry) is scheduled; training stops
+ * when that schedule reaches edb_lower_bound (Section 5.4 trains up to 1000
+ * trials and checks every 50).  The learned table is that of the check with
+ * the fewest batches, the earliest on ties.
+ * Random draws: SplitMix64 (Steele, Lea and Flood 2014), draw k of the seed
+ * being the finalizer of seed + (k+1) * 0x9E3779B97F4A7C15; training step c
+ * (counted over all trials) explores when (draw 2c >> 11) * 2^-53 < epsilon and
+ * then takes action number (draw 2c+1) mod (number of frontier types). */
+typedef struct {
+    int32_t encoding;     /* EDB_ENC_* */
+    int32_t trials;       /* >= 1 (default 1000) */
+    int32_t check_every;  /* >= 1 (default 50) */
+    int32_t n_step;       /* N >= 1 (default 4) */
+    double alpha;         /* > 0 (default 0.5) */
+    double epsilon;       /* exploration probability in [0, 1] (default 0.1) */
+    double lr;            /* learning rate in (0, 1] (default 0.2) */
+    double gamma;         /* discount in [0, 1] (default 1) */
+    uint64_t seed;        /* default 0 */
+} edb_learn_params;
+
+typedef struct {
+    int32_t trials;       /* trials run */
+    int32_t batches;      /* batches of the learned table's schedule */
+    int64_t lower_bound;  /* edb_lower_bound of the graph */
+    int32_t n_states;     /* entries of the learned table */
+} edb_learn_stats;
+
+typedef struct edb_learned edb_learned_t;
+
+/* Fills *p with the defaults above. */
+void edb_learn_defaults(edb_learn_params* p);
+/* Learns a policy table for the graph (host only, single-threaded).
+ * Errors: EDB_ERR_INVALID (NULL, parameters out of range), EDB_ERR_OOM. */
+edb_status edb_learn_policy(const edb_graph_t* g, const edb_learn_params* p, edb_learned_t** out);
+/* Borrowed view, valid until edb_learned_free: the table in edb_policy's flat
+ * format (entries in ascending lexicographic key order) and the statistics. */
+edb_status edb_learned_view(const edb_learned_t* l, const int32_t** table, int64_t* table_len,
+                            edb_learn_stats* stats);
+/* Borrowed view of the final Q function: n_states states in ascending key
+ * order, keys flat as {key_len, key...} per state (keys_len int32 in all), and
+ * q double[n_states * n_types] (0 for actions never updated). */
+edb_status edb_learned_q(const edb_learned_t* l, int32_t* n_states, const int32_t** keys,
+                         int64_t* keys_len, const double** q);
+void edb_learned_free(edb_learned_t* l);
 
 /* ---- memory plan (Section 3.1) ------------------------------------------ */
 /* Operand shape of a type: exactly n_fixed positional children (-1 allowed),

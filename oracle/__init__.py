@@ -11,9 +11,12 @@ Contents
   evaluate  node-at-a-time evaluation in topological order (the unbatched
             semantics that batching must not change, Section 2.1)
   schedule  Algorithm 1 (FSM-based dynamic batching) with table / agenda /
-            depth policies, the state encodings of Section 2.3, the lower
+            depth policies and the sufficient-condition policy, the state
+            encodings of Section 2.3, the lower
             bound of Appendix A.3, the Eq. 1 frontier ratio and a brute-force
             optimum (Appendix A.1)
+  learn     the FSM policy learner (Section 2.3: Eq. 1 reward, tabular
+            Q-learning with N-step bootstrapping) and its random source
   plan      the batching-aware memory plan (Section 3.1 constraints; slot
             assignment by a reverse consumer-first pass) and its hazard check
   compare   the normwise relative error used by the parity tests

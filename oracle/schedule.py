@@ -12,6 +12,9 @@ Policies
           Section 2.1), the average taken over all unexecuted nodes of the type
   depth   batches are the groups of equal (topological depth, type)
           (TensorFlow Fold's heuristic, Section 2.1)
+  sufficient  the type maximizing the second term of Eq. 1, the frontier
+          ratio of Lemma 1 (the sufficient-condition-guided heuristic of the
+          batch-count study, Section 5); ties to the lowest type id
 
 State encodings (Section 2.3): E_base = the set of frontier types, E_max =
 E_base plus the most common frontier type, E_sort = the frontier types sorted
@@ -28,6 +31,7 @@ import numpy as np
 POLICY_TABLE = 0
 POLICY_AGENDA = 1
 POLICY_DEPTH = 2
+POLICY_SUFFICIENT = 3
 
 ENC_SORT = 0
 ENC_BASE = 1
@@ -152,6 +156,19 @@ def schedule(op_type, child_ptr, child_idx, n_types, policy=POLICY_TABLE,
             t = table.get(key, -1)
             if t < 0 or t >= n_types or counts[t] == 0:
                 t = majority_type(counts)
+        elif policy == POLICY_SUFFICIENT:
+            executed = [False] * n
+            for b in batches:
+                for v in b:
+                    executed[v] = True
+            t, best = -1, None
+            for a in range(n_types):
+                if counts[a] == 0:
+                    continue
+                num, den = frontier_ratio(op_type, child_ptr, child_idx, executed, a)
+                # ratios compared exactly: num_a / den_a > num_t / den_t
+                if t < 0 or num * best[1] > best[0] * den:
+                    t, best = a, (num, den)
         elif policy == POLICY_AGENDA:
             t = -1
             for a in range(n_types):

@@ -17,7 +17,7 @@ EDB_ERR_UNSUPPORTED = -4
 EDB_ERR_TABLE = -5
 EDB_ERR_HIP = -6
 
-POLICY_TABLE, POLICY_AGENDA, POLICY_DEPTH = 0, 1, 2
+POLICY_TABLE, POLICY_AGENDA, POLICY_DEPTH, POLICY_SUFFICIENT = 0, 1, 2, 3
 ENC_SORT, ENC_BASE, ENC_MAX = 0, 1, 2
 PLAN_RC, PLAN_IDENTITY = 0, 1
 SEG_NONE, SEG_CONTIG, SEG_GATHER, SEG_SCATTER = 0, 1, 2, 3
@@ -35,7 +35,8 @@ FLOW_VARIANT = 100
 EXPORTS = [
     "edb_last_error", "edb_version",
     "edb_build_graph", "edb_graph_free", "edb_graph_info",
-    "edb_schedule", "edb_schedule_view", "edb_schedule_free",
+    "edb_schedule", "edb_schedule_view", "edb_schedule_free", "edb_lower_bound",
+    "edb_learn_defaults", "edb_learn_policy", "edb_learned_view", "edb_learned_q", "edb_learned_free",
     "edb_plan_memory", "edb_plan_view", "edb_plan_free",
     "edb_packed_weight_bytes", "edb_pack_weights",
     "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
@@ -52,6 +53,17 @@ class EdbError(RuntimeError):
 class Policy(C.Structure):
     _fields_ = [("kind", C.c_int32), ("encoding", C.c_int32),
                 ("table", C.POINTER(C.c_int32)), ("table_len", C.c_int64)]
+
+
+class LearnParams(C.Structure):
+    _fields_ = [("encoding", C.c_int32), ("trials", C.c_int32), ("check_every", C.c_int32),
+                ("n_step", C.c_int32), ("alpha", C.c_double), ("epsilon", C.c_double), ("lr", C.c_double),
+                ("gamma", C.c_double), ("seed", C.c_uint64)]
+
+
+class LearnStats(C.Structure):
+    _fields_ = [("trials", C.c_int32), ("batches", C.c_int32), ("lower_bound", C.c_int64),
+                ("n_states", C.c_int32)]
 
 
 class OperandShape(C.Structure):
@@ -109,6 +121,12 @@ def load():
         "edb_schedule_view": (C.c_int32, [vp, P(C.c_int32), P(P(C.c_int32)), P(P(C.c_int32)),
                                           P(P(C.c_int32))]),
         "edb_schedule_free": (None, [vp]),
+        "edb_lower_bound": (C.c_int32, [vp, P(C.c_int64)]),
+        "edb_learn_defaults": (None, [P(LearnParams)]),
+        "edb_learn_policy": (C.c_int32, [vp, P(LearnParams), P(vp)]),
+        "edb_learned_view": (C.c_int32, [vp, P(P(C.c_int32)), P(C.c_int64), P(LearnStats)]),
+        "edb_learned_q": (C.c_int32, [vp, P(C.c_int32), P(P(C.c_int32)), P(C.c_int64), P(P(C.c_double))]),
+        "edb_learned_free": (None, [vp]),
         "edb_plan_memory": (C.c_int32, [vp, vp, P(OperandShape), C.c_int32, P(vp)]),
         "edb_plan_view": (C.c_int32, [vp, P(PlanView)]),
         "edb_plan_free": (None, [vp]),

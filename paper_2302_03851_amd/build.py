@@ -20,10 +20,11 @@ LIB = os.path.join(HERE, "libedb.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
-HOST_SRC = ["graph.cpp", "schedule.cpp", "plan.cpp", "forward.cpp"]
+HOST_SRC = ["graph.cpp", "schedule.cpp", "learn.cpp", "plan.cpp", "forward.cpp"]
 HIP_SRC = ["exec.hip"]
 
-CXXFLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include")]
+# -ffp-contract=off: the policy learner's floating-point updates round as written
+CXXFLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-ffp-contract=off", "-I", os.path.join(ROOT, "include")]
 # Packed fp32 instructions are disabled for all device code.
 # -ffp-contract=off: every kernel rounds the same expression the same way
 # (fused multiply-adds are written out where they are wanted), which keeps

@@ -40,4 +40,15 @@ namespace edb {
 edb_status fail(edb_status st, const std::string& msg);
 void clear_error();
 
+// Sub-frontier bookkeeping for Eq. 1's ratio: same_pending[v] counts v's
+// unexecuted present children of v's own type (per edge occurrence); subf[a]
+// counts unexecuted type-a nodes with none, i.e. |Frontier(G^a)|.
+void same_type_frontier(const edb_graph& g, std::vector<int32_t>& same_pending, std::vector<int64_t>& subf);
+// Updates both after the ready node v executed.
+void same_type_executed(const edb_graph& g, int32_t v, std::vector<int32_t>& same_pending,
+                        std::vector<int64_t>& subf);
+// Appendix A.3: sum over types of the longest path (in nodes) of the subgraph
+// induced on that type.
+int64_t lower_bound(const edb_graph& g);
+
 }  // namespace edb

@@ -1,6 +1,8 @@
 // Batching schedule: Algorithm 1 of ED-Batch (FSM-based dynamic batching) with
-// a policy table keyed by the state encodings of Section 2.3, plus the agenda
-// and depth heuristics of Section 2.1 as built-in policies.
+// a policy table keyed by the state encodings of Section 2.3, the agenda and
+// depth heuristics of Section 2.1 as built-in policies, and the
+// sufficient-condition heuristic (the type maximizing Eq. 1's frontier ratio,
+// Lemma 1; Section 5's batch-count study).
 //
 // Frontier = unexecuted nodes whose present children have all executed.  Each
 // step picks one type and batches every frontier node of that type, in
@@ -56,11 +58,68 @@ void encode(const std::vector<int64_t>& counts, int32_t enc, std::vector<int32_t
 
 }  // namespace
 
+namespace edb {
+
+void same_type_frontier(const edb_graph& g, std::vector<int32_t>& same_pending, std::vector<int64_t>& subf) {
+    same_pending.assign(g.V, 0);
+    subf.assign(g.T, 0);
+    for (int32_t v = 0; v < g.V; ++v) {
+        for (int64_t e = g.child_ptr[v]; e < g.child_ptr[v + 1]; ++e) {
+            const int32_t c = g.child_idx[e];
+            if (c >= 0 && g.op_type[c] == g.op_type[v]) ++same_pending[v];
+        }
+        if (same_pending[v] == 0) ++subf[g.op_type[v]];
+    }
+}
+
+void same_type_executed(const edb_graph& g, int32_t v, std::vector<int32_t>& same_pending,
+                        std::vector<int64_t>& subf) {
+    const int32_t a = g.op_type[v];
+    --subf[a];   // v was ready, so none of its children was pending
+    for (int32_t i = g.cons_ptr[v]; i < g.cons_ptr[v + 1]; ++i) {
+        const int32_t p = g.cons[i];
+        if (g.op_type[p] == a && --same_pending[p] == 0) ++subf[a];
+    }
+}
+
+int64_t lower_bound(const edb_graph& g) {
+    // longest path, in nodes, of each type's induced subgraph, over a Kahn order
+    std::vector<int32_t> pending(g.pending), queue, len(g.V, 1);
+    std::vector<int64_t> best(g.T, 0);
+    queue.reserve(g.V);
+    for (int32_t v = 0; v < g.V; ++v) if (pending[v] == 0) queue.push_back(v);
+    for (size_t q = 0; q < queue.size(); ++q) {
+        const int32_t v = queue[q];
+        best[g.op_type[v]] = std::max<int64_t>(best[g.op_type[v]], len[v]);
+        for (int32_t i = g.cons_ptr[v]; i < g.cons_ptr[v + 1]; ++i) {
+            const int32_t p = g.cons[i];
+            if (g.op_type[p] == g.op_type[v]) len[p] = std::max(len[p], len[v] + 1);
+            if (--pending[p] == 0) queue.push_back(p);
+        }
+    }
+    int64_t total = 0;
+    for (int64_t b : best) total += b;
+    return total;
+}
+
+}  // namespace edb
+
+extern "C" edb_status edb_lower_bound(const edb_graph_t* g, int64_t* lb) {
+    if (!g || !lb) return fail(EDB_ERR_INVALID, "edb_lower_bound: NULL argument");
+    try {
+        *lb = edb::lower_bound(*g);
+    } catch (const std::bad_alloc&) {
+        return fail(EDB_ERR_OOM, "edb_lower_bound: out of host memory");
+    }
+    edb::clear_error();
+    return EDB_OK;
+}
+
 extern "C" edb_status edb_schedule(const edb_graph_t* g, const edb_policy* pol, edb_schedule_t** out) {
     if (!out) return fail(EDB_ERR_INVALID, "edb_schedule: out is NULL");
     *out = nullptr;
     if (!g || !pol) return fail(EDB_ERR_INVALID, "edb_schedule: NULL graph or policy");
-    if (pol->kind < EDB_POLICY_TABLE || pol->kind > EDB_POLICY_DEPTH)
+    if (pol->kind < EDB_POLICY_TABLE || pol->kind > EDB_POLICY_SUFFICIENT)
         return fail(EDB_ERR_INVALID, "edb_schedule: unknown policy kind");
     if (pol->kind == EDB_POLICY_TABLE && (pol->encoding < EDB_ENC_SORT || pol->encoding > EDB_ENC_MAX))
         return fail(EDB_ERR_INVALID, "edb_schedule: unknown state encoding");
@@ -125,6 +184,11 @@ extern "C" edb_status edb_schedule(const edb_graph_t* g, const edb_policy* pol, 
                 topo_depth(*g, depth);
                 for (int32_t v = 0; v < V; ++v) { dsum[g->op_type[v]] += depth[v]; dcnt[g->op_type[v]] += 1; }
             }
+            // sufficient condition: sub-frontier of G^a = unexecuted type-a nodes
+            // without an unexecuted type-a child (per edge occurrence)
+            std::vector<int32_t> same_pending;
+            std::vector<int64_t> subf;
+            if (pol->kind == EDB_POLICY_SUFFICIENT) edb::same_type_frontier(*g, same_pending, subf);
             std::vector<int64_t> counts(T);
             std::vector<int32_t> key;
             int64_t remaining = V;
@@ -136,6 +200,12 @@ extern "C" edb_status edb_schedule(const edb_graph_t* g, const edb_policy* pol, 
                     auto it = table.find(key);
                     if (it != table.end()) t = it->second;
                     if (t < 0 || t >= T || counts[t] == 0) t = majority(counts);
+                } else if (pol->kind == EDB_POLICY_SUFFICIENT) {
+                    for (int32_t a = 0; a < T; ++a) {
+                        if (counts[a] == 0) continue;
+                        // |F_a(G)| / |F(G^a)| compared exactly, ties to the lowest id
+                        if (t < 0 || counts[a] * subf[t] > counts[t] * subf[a]) t = a;
+                    }
                 } else {
                     for (int32_t a = 0; a < T; ++a) {
                         if (counts[a] == 0) continue;
@@ -148,6 +218,7 @@ extern "C" edb_status edb_schedule(const edb_graph_t* g, const edb_policy* pol, 
                 std::sort(batch.begin(), batch.end());
                 for (int32_t v : batch) {
                     if (pol->kind == EDB_POLICY_AGENDA) { dsum[t] -= depth[v]; dcnt[t] -= 1; }
+                    if (pol->kind == EDB_POLICY_SUFFICIENT) edb::same_type_executed(*g, v, same_pending, subf);
                     for (int32_t i = cons_ptr[v]; i < cons_ptr[v + 1]; ++i) {
                         int32_t p = cons[i];
                         if (--pending[p] == 0) ready[g->op_type[p]].push_back(p);

@@ -100,6 +100,50 @@ class Schedule:
             self.handle = None
 
 
+def lower_bound(graph: Graph) -> int:
+    """edb_lower_bound: the Appendix A.3 bound on the number of batches."""
+    out = C.c_int64()
+    L.check(L.load().edb_lower_bound(graph.handle, C.byref(out)), "edb_lower_bound")
+    return int(out.value)
+
+
+def learn_policy(graph: Graph, encoding=L.ENC_SORT, **params):
+    """edb_learn_policy: learns an FSM policy table by N-step Q-learning.
+    Keyword arguments override the library defaults (trials, check_every,
+    n_step, alpha, epsilon, lr, gamma, seed).  Returns (flat table, stats dict,
+    Q) with Q = {key tuple: float64[n_types]}."""
+    lib = L.load()
+    p = L.LearnParams()
+    lib.edb_learn_defaults(C.byref(p))
+    p.encoding = encoding
+    for k, v in params.items():
+        if not hasattr(p, k):
+            raise TypeError(f"unknown learning parameter {k}")
+        setattr(p, k, v)
+    h = C.c_void_p()
+    L.check(lib.edb_learn_policy(graph.handle, C.byref(p), C.byref(h)), "edb_learn_policy")
+    try:
+        tab, tlen, st = C.POINTER(C.c_int32)(), C.c_int64(), L.LearnStats()
+        L.check(lib.edb_learned_view(h, C.byref(tab), C.byref(tlen), C.byref(st)))
+        table = np.ctypeslib.as_array(tab, shape=(tlen.value,)).tolist() if tlen.value else []
+        stats = {"trials": st.trials, "batches": st.batches, "lower_bound": st.lower_bound,
+                 "states": st.n_states}
+        ns, keys, klen, q = C.c_int32(), C.POINTER(C.c_int32)(), C.c_int64(), C.POINTER(C.c_double)()
+        L.check(lib.edb_learned_q(h, C.byref(ns), C.byref(keys), C.byref(klen), C.byref(q)))
+        Q = {}
+        if ns.value:
+            flat = np.ctypeslib.as_array(keys, shape=(klen.value,)).tolist()
+            vals = np.ctypeslib.as_array(q, shape=(ns.value * graph.n_types,)).copy()
+            pos = 0
+            for i in range(ns.value):
+                kl = flat[pos]
+                Q[tuple(flat[pos + 1:pos + 1 + kl])] = vals[i * graph.n_types:(i + 1) * graph.n_types]
+                pos += 1 + kl
+    finally:
+        lib.edb_learned_free(h)
+    return table, stats, Q
+
+
 class Plan:
     def __init__(self, graph: Graph, sched: Schedule, shapes: Sequence[Tuple[int, int, int]], mode=L.PLAN_RC):
         lib = L.load()
@@ -222,9 +266,12 @@ class ForwardCall:
         self._xr = _i32(x_row)
         flat = None
         if table:
-            flat = [len(table)]
-            for key, action in table.items():
-                flat += [len(key)] + list(key) + [action]
+            if isinstance(table, dict):
+                flat = [len(table)]
+                for key, action in table.items():
+                    flat += [len(key)] + list(key) + [action]
+            else:
+                flat = list(table)
         self._tab = _i32(flat) if flat else None
         self._pol = L.Policy(policy, encoding, _ptr(self._tab, C.c_int32) if flat else None, len(flat) if flat else 0)
         self._shapes = (L.OperandShape * len(shapes))(*[L.OperandShape(*s) for s in shapes])

@@ -355,3 +355,35 @@ def make_graph(kinds: List[int], E: int, H: int, op_type, children: List[List[in
     return Workload(name="custom", dtype=dtype, kinds=list(kinds), in_dim=E, hidden=H,
                     op_type=op, child_ptr=ptr, child_idx=idx, x_row=x_row, x=x,
                     weights=weights, n_children=list(n_children), instances=1)
+
+
+def make_typed_trees(shape: str, n_trees: int, leaves=(10, 50), seed: int = 0):
+    """Typed dataflow graphs for batch-count studies (schedules only; no cells).
+
+    shape "outputs": the tree of Figure 1 at scale.  Binary trees (the C2 shape
+      draw, leaves U{lo..hi}) whose leaves (type 0) and internal nodes (type 1)
+      each feed an output operation (type 2), and one reduction (type 3) per
+      tree over all of its outputs.
+    shape "two_type": binary trees whose internal nodes take one of two types
+      (1 or 2, probability 1/2 each), as in a TreeLSTM with two internal cell
+      types; leaves are type 0.
+    Returns (op_type, child_ptr, child_idx, n_types); node ids are
+    children-before-parents, instance by instance."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    g = _GraphBuilder()
+    for _ in range(n_trees):
+        n = int(rng.integers(leaves[0], leaves[1] + 1))
+        first = len(g.op_type)
+        _build_binary(rng, n, g)
+        tree = range(first, len(g.op_type))
+        if shape == "outputs":
+            outs = [g.add(2, [v], False) for v in tree]
+            g.add(3, outs, False)
+        elif shape == "two_type":
+            for v in tree:
+                if g.op_type[v] == 1:
+                    g.op_type[v] = 1 + int(rng.integers(0, 2))
+        else:
+            raise ValueError(f"unknown shape {shape}")
+    op, ptr, idx, _x_row, _n = g.finish()
+    return op, ptr, idx, 4 if shape == "outputs" else 3

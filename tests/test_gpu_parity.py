@@ -412,15 +412,24 @@ def test_forward_call_matches_handles(k):
 
 
 def test_policies_give_same_states():
-    """Agenda and depth schedules change the batches, not the results."""
+    """Agenda, depth, sufficient-condition and learned schedules change the
+    batches, not the results."""
     _torch()
+    from paper_2302_03851_amd import edb
     w = WL.make_config(3, instances=4)
     hr, cr = _oracle(w)
-    for pol in (L.POLICY_AGENDA, L.POLICY_DEPTH):
-        f = _fwd(w, policy=pol)
+    g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+    learned = {}
+    for enc in (L.ENC_SORT, L.ENC_BASE):
+        learned[enc], _, _ = edb.learn_policy(g, enc, trials=200)
+    cases = [dict(policy=L.POLICY_AGENDA), dict(policy=L.POLICY_DEPTH), dict(policy=L.POLICY_SUFFICIENT),
+             dict(policy=L.POLICY_TABLE, table=learned[L.ENC_SORT]),
+             dict(policy=L.POLICY_TABLE, table=learned[L.ENC_BASE], encoding=L.ENC_BASE)]
+    for kw in cases:
+        f = _fwd(w, **kw)
         f.run()
         h, c = f.states()
-        _check(w, h, c, hr, cr, f"policy {pol}")
+        _check(w, h, c, hr, cr, f"policy {kw}")
 
 
 def test_edge_cases():

@@ -42,7 +42,7 @@ CFG_INSTANCES = {1: None, 2: None, 3: None, 4: None, 5: 48}
 
 
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
-@pytest.mark.parametrize("policy", [OS.POLICY_TABLE, OS.POLICY_AGENDA, OS.POLICY_DEPTH])
+@pytest.mark.parametrize("policy", [OS.POLICY_TABLE, OS.POLICY_AGENDA, OS.POLICY_DEPTH, OS.POLICY_SUFFICIENT])
 def test_schedule_bit_exact_configs(k, policy):
     w = WL.make_config(k, instances=CFG_INSTANCES[k])
     table = edb.LATTICE_TABLE if k == 3 else None
@@ -51,6 +51,7 @@ def test_schedule_bit_exact_configs(k, policy):
     batches, bt = _oracle_schedule(w, policy, table)
     assert s.batches() == batches
     assert s.batch_type.tolist() == bt
+    assert edb.lower_bound(g) == OS.lower_bound(w.op_type, w.child_ptr, w.child_idx, w.n_types)
 
 
 def _compare_plan(pl, ref, batches):
@@ -106,7 +107,7 @@ def random_graphs(draw):
 
 @settings(max_examples=80, deadline=None)
 @given(random_graphs(), st.sampled_from([OS.ENC_SORT, OS.ENC_BASE, OS.ENC_MAX]),
-       st.sampled_from([OS.POLICY_TABLE, OS.POLICY_AGENDA, OS.POLICY_DEPTH]),
+       st.sampled_from([OS.POLICY_TABLE, OS.POLICY_AGENDA, OS.POLICY_DEPTH, OS.POLICY_SUFFICIENT]),
        st.sampled_from([OP.PLAN_RC, OP.PLAN_IDENTITY]))
 def test_random_graphs_bit_exact(g, enc, policy, mode):
     op, children, T, shapes = g
@@ -121,6 +122,7 @@ def test_random_graphs_bit_exact(g, enc, policy, mode):
     batches, bt = OS.schedule(op, ptr, idx, T, policy, table, enc)
     assert s.batches() == batches
     assert s.batch_type.tolist() == bt
+    assert edb.lower_bound(gr) == OS.lower_bound(op, ptr, idx, T)
     pl = edb.Plan(gr, s, shapes, mode)
     ref = OP.plan_memory(op, ptr, idx, batches, shapes, mode)
     _compare_plan(pl, ref, batches)
