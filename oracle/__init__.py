@@ -17,6 +17,9 @@ Contents
             optimum (Appendix A.1)
   learn     the FSM policy learner (Section 2.3: Eq. 1 reward, tabular
             Q-learning with N-step bootstrapping) and its random source
+  pqtree    a PQ tree (Booth and Lueker) with template reduction
+  pqplan    the PQ-tree memory layout of Section 3.2 (construction,
+            constraint broadcast, order decision by union-find, leaf order)
   plan      the batching-aware memory plan (Section 3.1 constraints; slot
             assignment by a reverse consumer-first pass) and its hazard check
   compare   the normwise relative error used by the parity tests

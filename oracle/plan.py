@@ -26,7 +26,9 @@ are CONTIG when slot[order_b] is consecutive, else SCATTER.  x rows are
 numbered in (batch, order_b) order so every x operand is contiguous.
 
 The IDENTITY layout (slot[v] = v + 1, every operand indexed) is the
-unplanned baseline of the ablation.
+unplanned baseline of the ablation.  The PQ layout (Section 3.2) takes its
+slots from the PQ-tree algorithm in `pqplan`; each batch's rows then follow
+their slots, and an absent positional child reads its own zero pad.
 """
 from __future__ import annotations
 
@@ -39,6 +41,7 @@ SEG_SCATTER = 3
 
 PLAN_RC = 0
 PLAN_IDENTITY = 1
+PLAN_PQ = 2
 
 UNSET = -1
 
@@ -130,6 +133,31 @@ def plan_memory(op_type, child_ptr, child_idx, batches, shapes, mode=PLAN_RC):
                         if c >= 0 and slot[c] == UNSET:
                             slot[c] = nxt
                             nxt += 1
+    elif mode == PLAN_PQ:
+        from .pqplan import pq_layout
+        slot_of, pad_var, lead, pl.pq_stats = pq_layout(op_type, child_ptr, child_idx, batches, shapes)
+        for v in range(V):
+            slot[v] = slot_of[v]
+        nxt = len(slot_of) + 1
+        pl.pads = sorted(slot_of[x] for x in pad_var.values())
+        for b in range(B):
+            if lead[b] == 0:
+                order_b = sorted(batches[b], key=lambda v: slot[v])
+            else:
+                p = lead[b] - 1
+
+                def key(v, b=b, p=p):
+                    c = int(child_idx[child_ptr[v] + p])
+                    return slot_of[c] if c >= 0 else slot_of[pad_var[(b, p, v)]]
+                order_b = sorted(batches[b], key=key)
+            orders[b] = order_b
+            t = int(op_type[order_b[0]])
+            nf, rg = shapes[t][0], shapes[t][1]
+            seg_lists[b], rptrs[b] = _lists(order_b, child_ptr, child_idx, nf, rg)
+            for p in range(nf):
+                for ei, v in enumerate(order_b):
+                    if (b, p, v) in pad_var:
+                        pad_of[(b, p, ei)] = slot_of[pad_var[(b, p, v)]]
     else:
         raise ValueError("unknown plan mode")
 
