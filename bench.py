@@ -215,6 +215,9 @@ def main():
     ap.add_argument("--policy", default="table", choices=sorted(POLICIES),
                     help="batching policy: the configured FSM table (default), a table learned on the "
                          "workload's graph before timing (N-step Q-learning, E_sort), or a heuristic")
+    ap.add_argument("--plan", default="rc", choices=["rc", "pq", "identity"],
+                    help="arena layout: the reverse consumer-first pass (default), the PQ-tree layout, "
+                         "or node ids (every operand indexed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 256 MiB, 5 times (to scale HBM byte counters)")
@@ -267,7 +270,8 @@ def main():
         table = None
 
     # resident inputs: packed weights, x, arena
-    base = edb.Forward(w, policy=kind, table=table, flags=L.USE_GRAPH)
+    plan_mode = {"rc": L.PLAN_RC, "pq": L.PLAN_PQ, "identity": L.PLAN_IDENTITY}[args.plan]
+    base = edb.Forward(w, policy=kind, table=table, plan_mode=plan_mode, flags=L.USE_GRAPH)
     stream = base.stream.cuda_stream
     wptrs = [b.data_ptr() for b in base.weights]
     xp, ahp, acp = base.x.data_ptr(), base.arena_h.data_ptr(), base.arena_c.data_ptr()
@@ -286,9 +290,9 @@ def main():
     # executors are kept until the region has ended and are then read.  All
     # other steps run without events (the events cost host time on every step).
     fwd = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
-                          policy=kind, table=table)
+                          policy=kind, table=table, plan_mode=plan_mode)
     fwd_prof = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
-                               policy=kind, table=table, flags=L.PROFILE)
+                               policy=kind, table=table, plan_mode=plan_mode, flags=L.PROFILE)
     n_rows = base.plan.n_slots
 
     def step(i, keep):
@@ -365,7 +369,7 @@ def main():
     for _ in range(nh):
         g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
         s = edb.Schedule(g, kind, L.ENC_SORT, table)
-        p = edb.Plan(g, s, shapes, L.PLAN_RC)
+        p = edb.Plan(g, s, shapes, plan_mode)
         ex = edb.Exec(g, s, p, base.cells, 0)
     ms_host = (time.perf_counter() - th) * 1e3 / nh
 
@@ -419,7 +423,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.config], "nodes": V, "batches": base.sched.n_batches,
                    "launches_per_step": base.exec.launches(), "mini_batches_in_flight": S,
-                   "policy": policy_info,
+                   "policy": policy_info, "plan": args.plan,
                    "step": "graph ingest + schedule + memory plan + launch prep + device execution"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(tflops / peak, 4), "traffic": traffic,

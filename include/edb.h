@@ -189,6 +189,15 @@ typedef struct {
 
 #define EDB_PLAN_RC       0  /* reverse consumer-first contiguous slot plan */
 #define EDB_PLAN_IDENTITY 1  /* slot[v] = v + 1, every operand indexed (ablation) */
+/* PQ-tree layout (Section 3.2, Algorithm 2): node states and one zero pad per
+ * absent entry of a positional list with a present entry are ordered so that
+ * as many batches as possible read and write contiguous, row-aligned
+ * operands (PQ-tree reduction of every operand set, constraint broadcast
+ * between a batch's operands, Q-node directions and P-node orders decided by
+ * union-find).  A batch's rows follow the memory order of its first operand
+ * that could be made consecutive.  Host cost grows with the batch sizes
+ * (Lemma 2); ragged child lists only get adjacency, not alignment. */
+#define EDB_PLAN_PQ       2
 
 #define EDB_SEG_NONE    0  /* operand absent in every row: nothing to load */
 #define EDB_SEG_CONTIG  1  /* rows base, base+1, ... */

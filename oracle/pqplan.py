@@ -41,17 +41,19 @@ from .pqtree import LEAF, PNODE, QNODE, PQTree
 
 
 def variables(op_type, child_ptr, child_idx, batches, shapes):
-    """Returns (n_vars, pad_of, operands, ragged_sets): pad_of[(b, p, v)] is
+    """Returns (n_vars, pad_of, operands, slot_ids, ragged_sets): pad_of[(b, p, v)] is
     the pad variable of row v's absent child p in batch b; operands[b] the
-    aligned operand lists; ragged_sets[b] the ragged list's variables or None."""
+    aligned operand lists and slot_ids[b] their ids (0 the rows, 1 + p child
+    p); ragged_sets[b] the ragged list's variables or None."""
     V = len(op_type)
     nxt = V
     pad_of = {}
-    operands, ragged_sets = [], []
+    operands, ids, ragged_sets = [], [], []
     for b, rows in enumerate(batches):
         t = int(op_type[rows[0]])
         nf, rg = shapes[t][0], shapes[t][1]
         ops = [list(rows)]
+        oid = [0]
         for p in range(nf):
             L = [int(child_idx[child_ptr[v] + p]) for v in rows]
             if all(c < 0 for c in L):
@@ -65,14 +67,16 @@ def variables(op_type, child_ptr, child_idx, batches, shapes):
                 vars_.append(c)
             if len(set(vars_)) == len(vars_):
                 ops.append(vars_)
+                oid.append(1 + p)
         operands.append(ops)
+        ids.append(oid)
         rs = None
         if rg:
             rl = [int(c) for v in rows for c in child_idx[child_ptr[v] + nf:child_ptr[v + 1]] if c >= 0]
             if len(rl) >= 2 and len(set(rl)) == len(rl):
                 rs = rl
         ragged_sets.append(rs)
-    return nxt, pad_of, operands, ragged_sets
+    return nxt, pad_of, operands, ids, ragged_sets
 
 
 def order_kind(tree, x):
@@ -239,7 +243,7 @@ def pq_layout(op_type, child_ptr, child_idx, batches, shapes):
     ConstructPQTree, the batches still aligned after BroadcastConstraint, the
     batches whose every operand stayed aligned and whose relations all merged
     (`fully_decided`), and the sweeps of BroadcastConstraint."""
-    n, pad_of, operands, ragged_sets = variables(op_type, child_ptr, child_idx, batches, shapes)
+    n, pad_of, operands, ids, ragged_sets = variables(op_type, child_ptr, child_idx, batches, shapes)
     tree = PQTree(n)
     B = len(batches)
     # group[b]: the operands of b taking part in alignment, as (operand index, variables)
@@ -258,7 +262,7 @@ def pq_layout(op_type, child_ptr, child_idx, batches, shapes):
             g.insert(0, (0, operands[b][0]))
         group[b] = g
     built = sum(len(g) for g in group)
-    lead = [g[0][0] if g else 0 for g in group]
+    lead = [ids[b][group[b][0][0]] if group[b] else 0 for b in range(B)]
 
     def active(b):
         return len(group[b]) >= 2 and len(group[b][0][1]) >= 2

@@ -19,7 +19,7 @@ EDB_ERR_HIP = -6
 
 POLICY_TABLE, POLICY_AGENDA, POLICY_DEPTH, POLICY_SUFFICIENT = 0, 1, 2, 3
 ENC_SORT, ENC_BASE, ENC_MAX = 0, 1, 2
-PLAN_RC, PLAN_IDENTITY = 0, 1
+PLAN_RC, PLAN_IDENTITY, PLAN_PQ = 0, 1, 2
 SEG_NONE, SEG_CONTIG, SEG_GATHER, SEG_SCATTER = 0, 1, 2, 3
 F32, BF16 = 0, 1
 USE_GRAPH, DRYRUN, FORCE_GATHER, X_DIRECT, PROFILE, NO_FLOW = 1, 2, 4, 8, 16, 32

@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libedb.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
-HOST_SRC = ["graph.cpp", "schedule.cpp", "learn.cpp", "plan.cpp", "forward.cpp"]
+HOST_SRC = ["graph.cpp", "schedule.cpp", "learn.cpp", "plan.cpp", "pqplan.cpp", "forward.cpp"]
 HIP_SRC = ["exec.hip"]
 
 # -ffp-contract=off: the policy learner's floating-point updates round as written

@@ -2,7 +2,9 @@
 #pragma once
 
 #include <cstdint>
+#include <map>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "edb.h"
@@ -50,5 +52,13 @@ void same_type_executed(const edb_graph& g, int32_t v, std::vector<int32_t>& sam
 // Appendix A.3: sum over types of the longest path (in nodes) of the subgraph
 // induced on that type.
 int64_t lower_bound(const edb_graph& g);
+
+// PQ-tree memory layout (Section 3.2): slot_of[x] for every variable (nodes,
+// then one zero pad per absent entry of a positional list with a present
+// entry), pad_of[(batch, child position, row node)] the pad variable, lead[b]
+// the operand whose order batch b's rows follow (0 rows, 1 + p child p).
+void pq_layout(const edb_graph& g, const struct edb_schedule& s, const edb_operand_shape* shapes,
+               std::vector<int32_t>& slot_of, std::map<std::tuple<int, int, int>, int32_t>& pad_of,
+               std::vector<int32_t>& lead);
 
 }  // namespace edb

@@ -242,6 +242,9 @@ extern "C" edb_status edb_learn_policy(const edb_graph_t* g, const edb_learn_par
     } catch (const std::bad_alloc&) {
         delete L;
         return fail(EDB_ERR_OOM, "edb_learn_policy: out of host memory");
+    } catch (const std::exception& e) {
+        delete L;
+        return fail(EDB_ERR_INVALID, std::string("edb_learn_policy: internal error: ") + e.what());
     }
     edb::clear_error();
     *out = L;

@@ -19,8 +19,10 @@
 // so its descriptors are emitted in the same pass.  Slot 0 is the zero row.
 // x rows are numbered in (batch, row) order.
 #include <algorithm>
+#include <map>
 #include <new>
 #include <string>
+#include <tuple>
 
 #include "edb_internal.h"
 
@@ -59,6 +61,93 @@ void sort_by_key(std::vector<std::pair<int32_t, int32_t>>& a, std::vector<std::p
         a.swap(tmp);
     }
 }
+// PQ-tree layout (Section 3.2): slots from edb::pq_layout; each batch's rows
+// follow the memory order of the first operand of its aligned group; an
+// absent positional child reads its own zero pad.
+void pq_descriptors(const edb_graph& g, const struct edb_schedule& s, const edb_operand_shape* shapes, edb_plan& pl,
+                    const std::vector<int64_t>& idx_off, const std::vector<int64_t>& rag_off) {
+    std::vector<int32_t> slot_of, lead;
+    std::map<std::tuple<int, int, int>, int32_t> pad_of;
+    edb::pq_layout(g, s, shapes, slot_of, pad_of, lead);
+    const int32_t V = g.V, B = (int32_t)s.batch_type.size();
+    const int32_t* bptr = s.batch_ptr.data();
+    for (int32_t v = 0; v < V; ++v) pl.slot[v] = slot_of[v];
+    for (const auto& kv : pad_of) pl.pads.push_back(slot_of[kv.second]);
+    pl.n_slots = (int32_t)slot_of.size() + 1;
+    std::vector<int32_t> list;
+    std::vector<std::pair<int32_t, int32_t>> keyed;
+    for (int32_t b = 0; b < B; ++b) {
+        const edb_operand_shape& sh = shapes[s.batch_type[b]];
+        const int32_t m = bptr[b + 1] - bptr[b];
+        int32_t* ord = pl.order.data() + bptr[b];
+        keyed.clear();
+        for (int32_t r = 0; r < m; ++r) {
+            const int32_t v = ord[r];
+            int32_t key = slot_of[v];
+            if (lead[b] > 0) {
+                const int p = lead[b] - 1;
+                const int32_t c = g.child_idx[g.child_ptr[v] + p];
+                key = c >= 0 ? slot_of[c] : slot_of[pad_of.at({b, p, v})];
+            }
+            keyed.emplace_back(key, v);
+        }
+        std::sort(keyed.begin(), keyed.end());
+        for (int32_t r = 0; r < m; ++r) ord[r] = keyed[r].second;
+        int64_t off = idx_off[b] + m;
+        edb_seg* sg = pl.segs.data() + pl.seg_ptr[b];
+        const int nlists = sh.n_fixed + (sh.ragged ? 1 : 0);
+        for (int li = 0; li < nlists; ++li) {
+            list.clear();
+            if (li < sh.n_fixed) {
+                for (int32_t r = 0; r < m; ++r) {
+                    const int32_t v = ord[r], c = g.child_idx[g.child_ptr[v] + li];
+                    if (c >= 0) list.push_back(slot_of[c]);
+                    else {
+                        auto it = pad_of.find({b, li, v});
+                        list.push_back(it == pad_of.end() ? -1 : slot_of[it->second]);
+                    }
+                }
+            } else {
+                int32_t* rp = pl.ragged_pool.data() + rag_off[b];
+                rp[0] = 0;
+                for (int32_t r = 0; r < m; ++r) {
+                    const int32_t v = ord[r];
+                    for (int64_t e = g.child_ptr[v] + sh.n_fixed; e < g.child_ptr[v + 1]; ++e)
+                        if (g.child_idx[e] >= 0) list.push_back(slot_of[g.child_idx[e]]);
+                    rp[r + 1] = (int32_t)list.size();
+                }
+            }
+            edb_seg& q = sg[1 + li];
+            const int64_t n = (int64_t)list.size();
+            q.len = (int32_t)n;
+            bool any = false;
+            for (int32_t x : list) any |= x >= 0;
+            if (li < sh.n_fixed) {
+                // an all-absent positional list has no pads: no operand
+                any = false;
+                for (int32_t r = 0; r < m; ++r) any |= g.child_idx[g.child_ptr[ord[r]] + li] >= 0;
+            }
+            if (!any) {
+                q.kind = EDB_SEG_NONE;
+                q.idx_off = -1;
+                continue;
+            }
+            int32_t* dst = pl.idx_pool.data() + off;
+            for (int64_t e = 0; e < n; ++e) dst[e] = list[e] < 0 ? 0 : list[e];
+            q.idx_off = off;
+            q.base = dst[0];
+            q.kind = consecutive(dst, n) ? EDB_SEG_CONTIG : EDB_SEG_GATHER;
+            off += n;
+        }
+        int32_t* rs = pl.idx_pool.data() + idx_off[b];
+        for (int32_t r = 0; r < m; ++r) rs[r] = slot_of[ord[r]];
+        edb_seg& res = sg[0];
+        res.idx_off = idx_off[b];
+        res.len = m;
+        res.base = m > 0 ? rs[0] : 0;
+        res.kind = consecutive(rs, m) ? EDB_SEG_CONTIG : EDB_SEG_SCATTER;
+    }
+}
 }  // namespace
 
 extern "C" edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t* s,
@@ -66,7 +155,7 @@ extern "C" edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t
     if (!out) return fail(EDB_ERR_INVALID, "edb_plan_memory: out is NULL");
     *out = nullptr;
     if (!g || !s || !shapes) return fail(EDB_ERR_INVALID, "edb_plan_memory: NULL argument");
-    if (flags != EDB_PLAN_RC && flags != EDB_PLAN_IDENTITY)
+    if (flags != EDB_PLAN_RC && flags != EDB_PLAN_IDENTITY && flags != EDB_PLAN_PQ)
         return fail(EDB_ERR_INVALID, "edb_plan_memory: unknown flags");
     if (s->V != g->V || s->T != g->T)
         return fail(EDB_ERR_INVALID, "edb_plan_memory: schedule does not belong to this graph");
@@ -126,6 +215,11 @@ extern "C" edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t
         p->ragged_off.assign(rag_off.begin(), rag_off.end());
         p->segs.assign((size_t)p->seg_ptr[B], edb_seg{});
 
+        if (flags == EDB_PLAN_PQ) {
+            pq_descriptors(*g, *s, shapes, *p, idx_off, rag_off);
+            goto x_rows;
+        }
+        {
         const bool identity = flags == EDB_PLAN_IDENTITY;
         int32_t next = 1;
         if (identity) {
@@ -220,7 +314,9 @@ extern "C" edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t
             res.kind = (!identity && consecutive(rs, m)) ? EDB_SEG_CONTIG : EDB_SEG_SCATTER;
         }
         p->n_slots = next;
+        }
 
+    x_rows:
         // x rows in (batch, row) order
         p->x_slot.assign(V, -1);
         int32_t nx = 0;
@@ -231,6 +327,9 @@ extern "C" edb_status edb_plan_memory(const edb_graph_t* g, const edb_schedule_t
     } catch (const std::bad_alloc&) {
         delete p;
         return fail(EDB_ERR_OOM, "edb_plan_memory: out of host memory");
+    } catch (const std::exception& e) {
+        delete p;
+        return fail(EDB_ERR_INVALID, std::string("edb_plan_memory: internal error: ") + e.what());
     }
     edb::clear_error();
     *out = p;

@@ -127,14 +127,14 @@ def test_parity_full_size_sampled_instances(k):
 @pytest.mark.parametrize("k", [2, 3, 4, 5])
 def test_layout_and_launch_mode_bitwise(k):
     """The planned layout, the identity layout with every operand indexed,
-    forced gathers, x read in place and eager launches all give bitwise the
+    the PQ-tree layout (zero pads, rows in another order), forced gathers, x read in place and eager launches all give bitwise the
     same node states: only the addressing differs."""
     _torch()
     w = WL.make_config(k, instances=SMALL[k])
     ref = _fwd(w)
     ref.run()
     h0, c0 = ref.states()
-    for kw in (dict(plan_mode=L.PLAN_IDENTITY), dict(flags=L.USE_GRAPH | L.FORCE_GATHER),
+    for kw in (dict(plan_mode=L.PLAN_IDENTITY), dict(plan_mode=L.PLAN_PQ), dict(flags=L.USE_GRAPH | L.FORCE_GATHER),
                dict(flags=L.USE_GRAPH | L.X_DIRECT), dict(flags=0),
                dict(flags=L.PROFILE)):
         f = _fwd(w, **kw)

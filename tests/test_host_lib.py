@@ -349,3 +349,56 @@ def test_forward_call_validates_before_any_device_work():
     with pytest.raises(L.EdbError) as ei:
         bad.call([256, 256], 256, 256, 256, 10 ** 6, 0)
     assert ei.value.status == L.EDB_ERR_INVALID
+
+
+PQ_INSTANCES = {1: 8, 2: 16, 3: 8, 4: 3, 5: 8}
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_pq_plan_bit_exact_configs(k):
+    """EDB_PLAN_PQ against the oracle's PQ-tree layout (smaller instances:
+    the oracle's tree walks are slow)."""
+    w = WL.make_config(k, instances=PQ_INSTANCES[k])
+    table = edb.LATTICE_TABLE if k == 3 else None
+    g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+    s = edb.Schedule(g, L.POLICY_TABLE, L.ENC_SORT, table)
+    shapes = edb.operand_shapes(w)
+    pl = edb.Plan(g, s, shapes, L.PLAN_PQ)
+    batches, _ = _oracle_schedule(w, OS.POLICY_TABLE, table)
+    ref = OP.plan_memory(w.op_type, w.child_ptr, w.child_idx, batches, shapes, OP.PLAN_PQ)
+    _compare_plan(pl, ref, batches)
+    OP.hazard_check(w.op_type, w.child_ptr, w.child_idx, batches, ref)
+
+
+@settings(max_examples=400, deadline=None)
+@given(random_graphs(), st.sampled_from([OS.POLICY_TABLE, OS.POLICY_DEPTH, OS.POLICY_AGENDA]))
+def test_pq_plan_random_graphs_bit_exact(g, policy):
+    op, children, T, shapes = g
+    ptr = np.zeros(len(children) + 1, dtype=np.int64)
+    for v, ch in enumerate(children):
+        ptr[v + 1] = ptr[v] + len(ch)
+    idx = np.array([c for ch in children for c in ch], dtype=np.int32)
+    gr = edb.Graph(op, ptr, idx, np.full(len(op), -1, dtype=np.int32), T)
+    s = edb.Schedule(gr, policy)
+    batches, _ = OS.schedule(op, ptr, idx, T, policy)
+    pl = edb.Plan(gr, s, shapes, L.PLAN_PQ)
+    ref = OP.plan_memory(op, ptr, idx, batches, shapes, OP.PLAN_PQ)
+    _compare_plan(pl, ref, batches)
+    OP.hazard_check(op, ptr, idx, batches, ref)
+
+
+def test_pq_plan_skipped_list_bit_exact():
+    from tests.test_oracle_pq import SKIPPED_LIST_CASE
+    op, children = SKIPPED_LIST_CASE
+    op = np.array(op, dtype=np.int32)
+    ptr = np.zeros(len(children) + 1, dtype=np.int64)
+    for v, ch in enumerate(children):
+        ptr[v + 1] = ptr[v] + len(ch)
+    idx = np.array([c for ch in children for c in ch], dtype=np.int32)
+    shapes = [(0, 0, 0), (2, 0, 0)]
+    gr = edb.Graph(op, ptr, idx, np.full(len(op), -1, dtype=np.int32), 2)
+    s = edb.Schedule(gr, L.POLICY_DEPTH)
+    batches, _ = OS.schedule(op, ptr, idx, 2, OS.POLICY_DEPTH)
+    pl = edb.Plan(gr, s, shapes, L.PLAN_PQ)
+    ref = OP.plan_memory(op, ptr, idx, batches, shapes, OP.PLAN_PQ)
+    _compare_plan(pl, ref, batches)

@@ -187,3 +187,27 @@ def test_pq_plan_hazard_free_and_consistent(k):
         assert cs == ns > cs0 and cr == cr0 == nb     # both grid neighbours contiguous
     if k == 3:
         assert cr > cr0
+
+
+# A batch whose rows cannot be made consecutive and whose first child list is
+# absent in every row (so not an operand): its rows follow its second child
+# list, and that list must come out contiguous.
+SKIPPED_LIST_CASE = ([0, 0, 0, 1, 1, 1, 1], [[], [], [], [-1, 2], [-1, 3], [-1, 0], [3, 0]])
+
+
+def test_rows_follow_the_leading_operand_after_a_skipped_list():
+    op, children = SKIPPED_LIST_CASE
+    op = np.array(op, dtype=np.int32)
+    ptr = np.zeros(len(children) + 1, dtype=np.int64)
+    for v, ch in enumerate(children):
+        ptr[v + 1] = ptr[v] + len(ch)
+    idx = np.array([c for ch in children for c in ch], dtype=np.int32)
+    batches, _ = S.schedule(op, ptr, idx, 2, S.POLICY_DEPTH)
+    shapes = [(0, 0, 0), (2, 0, 0)]
+    _slot, _pads, lead, _st = Q.pq_layout(op, ptr, idx, batches, shapes)
+    b = next(i for i, bt in enumerate(batches) if bt == [3, 5])
+    assert lead[b] == 2                       # positional child 1
+    pl = P.plan_memory(op, ptr, idx, batches, shapes, P.PLAN_PQ)
+    P.hazard_check(op, ptr, idx, batches, pl)
+    assert pl.segments[b][0][0] == P.SEG_NONE
+    assert pl.segments[b][1][0] == P.SEG_CONTIG
