@@ -35,6 +35,7 @@ WORKLOAD_TEXT = {
     3: "lattice LSTM forward fp32: 32 lattices, lengths U[20,60], word p=0.3 span 2-4, E=100, H=200",
     4: "2-D grid RNN forward fp32: 32 grids 16x16, E=128, H=256",
     5: "child-sum TreeLSTM forward bf16 (fp32 accumulate): 256 trees, leaves U[20,200], arity U{1..4}, E=H=512",
+    6: "binary TreeLSTM with two internal cell types forward fp32: 64 trees, leaves U[10,50], E=H=256",
 }
 
 

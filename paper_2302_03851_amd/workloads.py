@@ -233,11 +233,13 @@ CONFIG_NAMES = {
     3: "lattice_lstm_f32",
     4: "grid_rnn_f32",
     5: "childsum_treelstm_h512_bf16",
+    6: "treelstm_2type_h256_f32",
 }
 
 
 def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = None) -> Workload:
-    """Build synthetic config k (1..5).  `instances` overrides the number of
+    """Build synthetic config k (1..5; 6 is the two-internal-type TreeLSTM of
+    the batching study).  `instances` overrides the number of
     instance graphs (chains / trees / lattices / grids) for small test cases
     and scale sweeps; all other sizes and distributions stay as stated."""
     if seed is None:
@@ -310,8 +312,23 @@ def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = N
         for _ in range(inst):
             n = int(rng.integers(20, 201))
             _build_childsum(rng, n, g)
+    elif k == 6:
+        # TreeLSTM with two internal cell types (a batching study workload):
+        # the binary trees of config 2, each internal node of type 1 or 2
+        # (U{0,1} per internal node, node order, after the tree's shape),
+        # with separate weights per type.
+        inst = 64 if instances is None else instances
+        kinds, E, H, scale = [NARY_LEAF, NARY_INTERNAL, NARY_INTERNAL], 256, 256, 0.08
+        n_children = [0, 2, 2]
+        for _ in range(inst):
+            n = int(rng.integers(10, 51))
+            first = len(g.op_type)
+            _build_binary(rng, n, g)
+            for v in range(first, len(g.op_type)):
+                if g.op_type[v] == 1:
+                    g.op_type[v] = 1 + int(rng.integers(0, 2))
     else:
-        raise ValueError("config index must be 1..5")
+        raise ValueError("config index must be 1..6")
 
     op_type, ptr, idx, x_row, n_x = g.finish()
     weights = _draw_weights(rng, kinds, E, H, scale, n_children, bf16)

@@ -17,7 +17,7 @@ from paper_2302_03851_amd import workloads as WL
 pytestmark = pytest.mark.gpu
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
-SMALL = {1: 8, 2: 6, 3: 6, 4: 2, 5: 4}
+SMALL = {1: 8, 2: 6, 3: 6, 4: 2, 5: 4, 6: 6}
 
 
 def _torch():
@@ -50,7 +50,7 @@ def _check(w, h, c, hr, cr, label):
     return err
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6])
 def test_parity_small(k):
     _torch()
     w = WL.make_config(k, instances=SMALL[k])
@@ -97,7 +97,7 @@ def _subgraph(w, nodes):
                 child_idx=np.array(idx, dtype=np.int32), x_row=w.x_row[nodes])
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6])
 def test_parity_full_size_sampled_instances(k):
     _torch()
     w = WL.make_config(k)
@@ -430,6 +430,24 @@ def test_policies_give_same_states():
         f.run()
         h, c = f.states()
         _check(w, h, c, hr, cr, f"policy {kw}")
+
+
+def test_two_type_treelstm_policies_give_same_states():
+    """TreeLSTM with two internal cell types: the batching policy (learned
+    table, sufficient condition, agenda, depth) changes the batches, not the
+    results."""
+    _torch()
+    from paper_2302_03851_amd import edb
+    w = WL.make_config(6, instances=8)
+    hr, cr = _oracle(w)
+    g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+    table, _, _ = edb.learn_policy(g, L.ENC_SORT, trials=200)
+    for kw in (dict(policy=L.POLICY_TABLE, table=table), dict(policy=L.POLICY_SUFFICIENT),
+               dict(policy=L.POLICY_AGENDA), dict(policy=L.POLICY_DEPTH)):
+        f = _fwd(w, **kw)
+        f.run()
+        h, c = f.states()
+        _check(w, h, c, hr, cr, f"two-type policy {kw}")
 
 
 def test_edge_cases():
