@@ -209,7 +209,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--replays", type=int, default=200)
-    ap.add_argument("--streams", type=int, default=8,
+    ap.add_argument("--streams", type=int, default=16,
                     help="mini-batches in flight: host worker threads, each with its own stream and arena")
     ap.add_argument("--timed-events", type=int, default=8,
                     help="steps of worker 0 in the timed region whose launches record HIP events")
