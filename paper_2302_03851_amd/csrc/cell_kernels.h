@@ -981,6 +981,7 @@ struct FlowArgs {
     int* error;
     int* done;                    // per row-tile id: unit tiles finished
     int n_tiles, need, spin_us;   // spin_us: bound of one tile's wait, microseconds
+    int n_slots, n_xrows;         // arena rows; rows of the x matrix the descriptors address
     const void* x;
     const void* xstaged;
     void* arena_h;
@@ -993,7 +994,7 @@ __device__ __forceinline__ Seg desc_seg(const BatchDesc& d, const int* ibuf, int
 }
 
 __device__ __forceinline__ BatchArgs resolve(const BatchDesc& d, const FlowArgs& f) {
-    BatchArgs a;
+    BatchArgs a{};
     a.kind = d.kind;
     a.m = d.m;
     a.H = d.H;
@@ -1016,6 +1017,9 @@ __device__ __forceinline__ BatchArgs resolve(const BatchDesc& d, const FlowArgs&
     a.br = reinterpret_cast<const float*>(wb + d.off_br);
     a.arena_h = f.arena_h;
     a.arena_c = f.arena_c;
+    a.n_slots = f.n_slots;        // the buffer resources of the tile loads are sized by these
+    a.n_xrows = f.n_xrows;
+    a.fc = nullptr;               // only child-sum batches on the large tile use it (never in a run)
     return a;
 }
 

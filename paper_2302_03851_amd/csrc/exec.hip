@@ -1235,6 +1235,8 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
             f.n_tiles = L.f_ntiles;
             f.need = L.f_need;
             f.spin_us = L.args.m;
+            f.n_slots = e->n_slots;
+            f.n_xrows = (e->flags & EDB_X_DIRECT) ? e->x_direct_rows : e->n_x;
             f.x = x;
             f.xstaged = e->xstaged;
             f.arena_h = arena_h;
