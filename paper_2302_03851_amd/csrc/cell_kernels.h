@@ -118,6 +118,17 @@ __device__ __forceinline__ float tanh_f(float z) {
     return fabsf(z) < 0x1p-9f ? z : t;
 }
 
+// sigma(a) * tanh(b) from two exponentials and one reciprocal:
+// sgn(b) (1 - q) / ((1 + p)(1 + q)) with p = e^-a and q = e^{-2|b|}.  q stays in
+// (0, 1], and an overflowing p gives the exact limit 0; near b = 0 the error
+// of 1 - q is absolute (about 1e-7), not relative.
+__device__ __forceinline__ float sig_tanh(float a, float b) {
+    const float p = __expf(-a);
+    const float q = __expf(-2.0f * fabsf(b));
+    const float den = fmaf(p, q, p + q) + 1.0f;
+    return copysignf((1.0f - q) * __builtin_amdgcn_rcpf(den), b);
+}
+
 __device__ __forceinline__ float to_f(float v) { return v; }
 __device__ __forceinline__ float to_f(__bf16 v) { return (float)v; }
 template <typename T> __device__ __forceinline__ T from_f(float v);
@@ -135,28 +146,28 @@ template <int KIND>
 __device__ __forceinline__ void cell_update(const float* z, const float* cp, float racc, float rden, int nw,
                                             float& c, float& h) {
     if constexpr (KIND == K_CHAIN) {
-        c = fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[2]));
-        h = sigm(z[3]) * tanh_f(c);
+        c = fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[2]));
+        h = sig_tanh(z[3], c);
     } else if constexpr (KIND == K_NARY_LEAF || KIND == K_CS_LEAF) {
-        c = sigm(z[0]) * tanh_f(z[2]);
-        h = sigm(z[1]) * tanh_f(c);
+        c = sig_tanh(z[0], z[2]);
+        h = sig_tanh(z[1], c);
     } else if constexpr (KIND == K_NARY_INT || KIND == K_GRID) {
-        c = fmaf(sigm(z[2]), cp[1], fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[4])));
-        h = sigm(z[3]) * tanh_f(c);
+        c = fmaf(sigm(z[2]), cp[1], fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[4])));
+        h = sig_tanh(z[3], c);
     } else if constexpr (KIND == K_CS_INT) {
-        c = fmaf(sigm(z[0]), tanh_f(z[2]), racc);
-        h = sigm(z[1]) * tanh_f(c);
+        c = sig_tanh(z[0], z[2]) + racc;
+        h = sig_tanh(z[1], c);
     } else if constexpr (KIND == K_LAT_WORD) {
-        c = fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[2]));
+        c = fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[2]));
         h = 0.f;
     } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
         if (nw == 0) {
-            c = fmaf(sigm(z[1]), cp[0], sigm(z[0]) * tanh_f(z[3]));
+            c = fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[3]));
         } else {
             const float e0 = __expf(sigm(z[0]));
             c = fmaf(e0, tanh_f(z[3]), racc) / (e0 + rden);
         }
-        h = sigm(z[2]) * tanh_f(c);
+        h = sig_tanh(z[2], c);
     }
 }
 
