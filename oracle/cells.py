@@ -1,8 +1,8 @@
 """Cell equations of the recurrent / recursive models evaluated in the paper.
 
 The paper names its workloads (Section 5.1, Table 2: BiLSTM tagger, N-ary
-TreeLSTM, lattice LSTM; the gated grid RNN of the introduction's structured
-data examples) but prints no cell equations; each function below writes out
+TreeLSTM, TreeGRU, lattice LSTM; the gated grid RNN of the introduction's
+structured data examples) but prints no cell equations; each function below writes out
 the published definition of the cited model.  All arithmetic is float64.
 
 Conventions: weight matrices are K x N with rows ordered
@@ -23,6 +23,8 @@ CS_LEAF = 4
 CS_INTERNAL = 5
 LAT_CHAR = 6
 LAT_WORD = 7
+GRU_LEAF = 8
+GRU_INTERNAL = 9
 
 
 def sigmoid(z):
@@ -154,3 +156,41 @@ def lattice_char(x, h_prev, c_prev, word_cs, W, W_lx, W_lc, b, b_l):
             c = c + (ek / den) * _f64(cw)
     h = sigmoid(o) * np.tanh(c)
     return h, c
+
+
+def gru_leaf(x, W, b):
+    """Leaf of a binary TreeGRU (Table 2's TreeGRU): the gated recurrent unit
+    (Cho et al. 2014) with no children.
+
+    z = x W + b split into [z, n];  h = (1 - sigma(z)) * tanh(n).  A GRU node's
+    state is h alone; it is returned as the cell state too."""
+    zz = _f64(x) @ _f64(W) + _f64(b)
+    z, n = _split(zz, 2)
+    h = (1.0 - sigmoid(z)) * np.tanh(n)
+    return h, h
+
+
+def gru_internal(hs, U, b):
+    """Internal node of a binary TreeGRU: the gated recurrent unit extended to
+    two ordered children the way the N-ary TreeLSTM extends the LSTM, with
+    each child's reset gate applied after its recurrent product (the GRU form
+    whose candidate is tanh(W x + b + r * (U h + b_h))).
+
+    Columns of U [2H x 5H] and b [5H]: [z, r_0, r_1, n_0, n_1].  z, r_0 and r_1
+    read both children; n_0 reads only h_0 (rows 0..H-1), n_1 only h_1 (rows
+    H..2H-1); the other blocks of the n columns are not used.
+      h~ = tanh(sigma(r_0) * n_0 + sigma(r_1) * n_1)
+      h  = sigma(z) * (h_0 + h_1) / 2 + (1 - sigma(z)) * h~
+    """
+    h0, h1 = _f64(hs[0]), _f64(hs[1])
+    U, b = _f64(U), _f64(b)
+    H = h0.shape[0]
+    a = np.concatenate([h0, h1])
+    z = a @ U[:, 0:H] + b[0:H]
+    r0 = a @ U[:, H:2 * H] + b[H:2 * H]
+    r1 = a @ U[:, 2 * H:3 * H] + b[2 * H:3 * H]
+    n0 = h0 @ U[0:H, 3 * H:4 * H] + b[3 * H:4 * H]
+    n1 = h1 @ U[H:2 * H, 4 * H:5 * H] + b[4 * H:5 * H]
+    ht = np.tanh(sigmoid(r0) * n0 + sigmoid(r1) * n1)
+    h = sigmoid(z) * (h0 + h1) / 2.0 + (1.0 - sigmoid(z)) * ht
+    return h, h

@@ -113,6 +113,12 @@ def evaluate(kinds, op_type, child_ptr, child_idx, x_row, x, weights, hidden,
         elif k == C.LAT_WORD:
             hb, cb = state(ch[0])
             h, c = C.lattice_word(xv, hb, cb, w["W"], w["b"])
+        elif k == C.GRU_LEAF:
+            h, c = C.gru_leaf(xv, w["W"], w["b"])
+        elif k == C.GRU_INTERNAL:
+            # a GRU node's state is its cell-state row (h before any rounding)
+            st = [state(c)[1] for c in ch[:2]]
+            h, c = C.gru_internal(st, w["W"], w["b"])
         elif k == C.LAT_CHAR:
             hp, cp = state(ch[0])
             words = [state(c)[1] for c in ch[1:] if c >= 0]

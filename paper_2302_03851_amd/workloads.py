@@ -46,11 +46,13 @@ CS_LEAF = 4
 CS_INTERNAL = 5
 LAT_CHAR = 6
 LAT_WORD = 7
+GRU_LEAF = 8
+GRU_INTERNAL = 9
 
 KIND_NAMES = {
     LSTM_CHAIN: "lstm_chain", NARY_LEAF: "nary_leaf", NARY_INTERNAL: "nary_internal",
     GRID: "grid", CS_LEAF: "cs_leaf", CS_INTERNAL: "cs_internal",
-    LAT_CHAR: "lat_char", LAT_WORD: "lat_word",
+    LAT_CHAR: "lat_char", LAT_WORD: "lat_word", GRU_LEAF: "gru_leaf", GRU_INTERNAL: "gru_internal",
 }
 
 # Per kind: (n_fixed children, ragged children allowed, has x input).
@@ -63,6 +65,8 @@ KIND_SHAPE = {
     CS_INTERNAL: (0, True, False),
     LAT_CHAR: (1, True, True),
     LAT_WORD: (1, False, True),
+    GRU_LEAF: (0, False, True),
+    GRU_INTERNAL: (2, False, False),
 }
 
 
@@ -79,6 +83,8 @@ def weight_shapes(kind: int, E: int, H: int, n_children: int = 2) -> List[Tuple[
       CS_INTERNAL    U_iou[H x 3H] gates [i, o, u];  U_f[H x H]
       LAT_WORD       W_w[(E+H) x 3H] gates [i, f, u]
       LAT_CHAR       W_c[(E+H) x 4H] gates [i, f, o, u];  W_lx[E x H];  W_lc[H x H]
+      GRU_LEAF       W[E x 2H]      gates [z, n]
+      GRU_INTERNAL   U[2H x 5H]     gates [z, r_0, r_1, n_0, n_1] (n_k reads child k only)
     Biases follow the matrices (float32).
     """
     if kind == LSTM_CHAIN:
@@ -97,6 +103,10 @@ def weight_shapes(kind: int, E: int, H: int, n_children: int = 2) -> List[Tuple[
     if kind == LAT_CHAR:
         return [("W", (E + H, 4 * H)), ("W_lx", (E, H)), ("W_lc", (H, H)),
                 ("b", (4 * H,)), ("b_l", (H,))]
+    if kind == GRU_LEAF:
+        return [("W", (E, 2 * H)), ("b", (2 * H,))]
+    if kind == GRU_INTERNAL:
+        return [("W", (2 * H, 5 * H)), ("b", (5 * H,))]
     raise ValueError(f"unknown cell kind {kind}")
 
 
@@ -234,12 +244,13 @@ CONFIG_NAMES = {
     4: "grid_rnn_f32",
     5: "childsum_treelstm_h512_bf16",
     6: "treelstm_2type_h256_f32",
+    7: "binary_treegru_h256_f32",
 }
 
 
 def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = None) -> Workload:
     """Build synthetic config k (1..5; 6 is the two-internal-type TreeLSTM of
-    the batching study).  `instances` overrides the number of
+    the batching study, 7 the binary TreeGRU).  `instances` overrides the number of
     instance graphs (chains / trees / lattices / grids) for small test cases
     and scale sweeps; all other sizes and distributions stay as stated."""
     if seed is None:
@@ -327,8 +338,16 @@ def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = N
             for v in range(first, len(g.op_type)):
                 if g.op_type[v] == 1:
                     g.op_type[v] = 1 + int(rng.integers(0, 2))
+    elif k == 7:
+        # binary TreeGRU: the trees of config 2 (same draws), GRU cells
+        inst = 64 if instances is None else instances
+        kinds, E, H, scale = [GRU_LEAF, GRU_INTERNAL], 256, 256, 0.08
+        n_children = [0, 0]
+        for _ in range(inst):
+            n = int(rng.integers(10, 51))
+            _build_binary(rng, n, g)
     else:
-        raise ValueError("config index must be 1..6")
+        raise ValueError("config index must be 1..7")
 
     op_type, ptr, idx, x_row, n_x = g.finish()
     weights = _draw_weights(rng, kinds, E, H, scale, n_children, bf16)

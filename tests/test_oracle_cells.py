@@ -362,3 +362,102 @@ def test_p7_batched_equals_node_at_a_time(cfg):
 def test_topo_order_rejects_cycle():
     with pytest.raises(ValueError):
         topo_order(2, np.array([0, 1, 2]), np.array([1, 0]))
+
+
+# ---- TreeGRU ---------------------------------------------------------------
+
+def torch_gru_step(h, W_hh, b_hh):
+    """Reference: torch.nn.GRUCell (float64, CPU) with a zero input; gates in
+    torch's order [r, z, n]: n = tanh(r * (W_hn h + b_hn)), h' = (1 - z) n + z h."""
+    H = h.shape[0]
+    m = torch.nn.GRUCell(1, H).double()
+    with torch.no_grad():
+        m.weight_ih.zero_()
+        m.bias_ih.zero_()
+        m.weight_hh.copy_(torch.from_numpy(np.ascontiguousarray(W_hh, dtype=np.float64)))
+        m.bias_hh.copy_(torch.from_numpy(np.asarray(b_hh, dtype=np.float64)))
+        out = m(torch.zeros(1, 1, dtype=torch.float64), torch.from_numpy(h).reshape(1, H))
+    return out.numpy().reshape(H)
+
+
+def test_gru_internal_with_equal_children_equals_torch_gru():
+    # With h_0 = h_1 = h and the n_1 column block and bias zero, the internal
+    # node is one GRU step from h with zero input: the z and r_0 columns act
+    # through U[:H] + U[H:], the candidate through U[:H, n_0].
+    rng = np.random.default_rng(7)
+    H = 5
+    U = rng.uniform(-0.6, 0.6, size=(2 * H, 5 * H))
+    b = rng.uniform(-0.3, 0.3, size=5 * H)
+    U[:, 4 * H:] = 0.0
+    b[4 * H:] = 0.0
+    h = rng.standard_normal(H)
+    got, c = C.gru_internal([h, h], U, b)
+    Wsum = U[:H] + U[H:]
+    W_hh = np.concatenate([Wsum[:, H:2 * H].T, Wsum[:, 0:H].T, U[:H, 3 * H:4 * H].T])   # [r, z, n]
+    b_hh = np.concatenate([b[H:2 * H], b[0:H], b[3 * H:4 * H]])
+    np.testing.assert_allclose(got, torch_gru_step(h, W_hh, b_hh), rtol=1e-12, atol=1e-14)
+    np.testing.assert_array_equal(got, c)
+
+
+def test_gru_leaf_equals_torch_gru_from_zero_state():
+    # A leaf is one GRU step from h = 0: h' = (1 - z) tanh(W_in x + b_in + r * b_hn)
+    # with b_hn = 0.
+    rng = np.random.default_rng(8)
+    E, H = 6, 4
+    W = rng.uniform(-0.5, 0.5, size=(E, 2 * H))
+    b = rng.uniform(-0.2, 0.2, size=2 * H)
+    x = rng.standard_normal(E)
+    got, _ = C.gru_leaf(x, W, b)
+    m = torch.nn.GRUCell(E, H).double()
+    with torch.no_grad():
+        m.weight_hh.zero_()
+        m.bias_hh.zero_()
+        W_ih = np.concatenate([np.zeros((H, E)), W[:, 0:H].T, W[:, H:].T])   # [r, z, n]
+        m.weight_ih.copy_(torch.from_numpy(W_ih))
+        m.bias_ih.copy_(torch.from_numpy(np.concatenate([np.zeros(H), b[0:H], b[H:]])))
+        ref = m(torch.from_numpy(x).reshape(1, E), torch.zeros(1, H, dtype=torch.float64)).numpy().reshape(H)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-14)
+
+
+def test_gru_internal_closed_forms():
+    rng = np.random.default_rng(9)
+    H = 3
+    h0, h1 = rng.standard_normal(H), rng.standard_normal(H)
+    # zero weights and biases: z = 1/2, candidate tanh(0) = 0
+    h, _ = C.gru_internal([h0, h1], np.zeros((2 * H, 5 * H)), np.zeros(5 * H))
+    np.testing.assert_allclose(h, 0.25 * (h0 + h1), rtol=0, atol=1e-15)
+    # a saturated update gate keeps the children's mean; a closed one takes the candidate
+    U = rng.uniform(-0.5, 0.5, size=(2 * H, 5 * H))
+    b = np.zeros(5 * H)
+    b[0:H] = 60.0
+    h, _ = C.gru_internal([h0, h1], U, b)
+    np.testing.assert_allclose(h, (h0 + h1) / 2, rtol=0, atol=1e-12)
+    b[0:H] = -60.0
+    h, _ = C.gru_internal([h0, h1], U, b)
+    n0 = h0 @ U[0:H, 3 * H:4 * H]
+    n1 = h1 @ U[H:, 4 * H:]
+    r0 = 1 / (1 + np.exp(-(np.concatenate([h0, h1]) @ U[:, H:2 * H])))
+    r1 = 1 / (1 + np.exp(-(np.concatenate([h0, h1]) @ U[:, 2 * H:3 * H])))
+    np.testing.assert_allclose(h, np.tanh(r0 * n0 + r1 * n1), rtol=0, atol=1e-12)
+    # the unused blocks of the n columns do not matter
+    U2 = U.copy()
+    U2[H:, 3 * H:4 * H] = 9.0
+    U2[:H, 4 * H:] = -9.0
+    np.testing.assert_array_equal(C.gru_internal([h0, h1], U2, b)[0], C.gru_internal([h0, h1], U, b)[0])
+
+
+def test_gru_hand_values_one_unit():
+    # H = 1 by hand: h_0 = 0.5, h_1 = -0.25, U rows [h_0; h_1], columns [z, r_0, r_1, n_0, n_1]
+    U = np.array([[0.2, 1.0, 0.0, 2.0, 7.0],
+                  [0.4, 0.0, -1.0, 5.0, -1.0]])
+    b = np.array([0.0, 0.0, 0.0, 0.0, 0.0])
+    h, _ = C.gru_internal([np.array([0.5]), np.array([-0.25])], U, b)
+    z = 0.2 * 0.5 + 0.4 * -0.25            # 0.0   -> sigma = 1/2
+    r0 = 0.5                                # sigma(0.5)
+    r1 = 0.25                               # -1 * -0.25
+    n0 = 2.0 * 0.5                          # 1.0 (n_0 reads h_0 only)
+    n1 = -1.0 * -0.25                       # 0.25 (n_1 reads h_1 only)
+    s = lambda v: 1 / (1 + np.exp(-v))
+    ht = np.tanh(s(r0) * n0 + s(r1) * n1)
+    assert z == 0.0
+    assert abs(h[0] - (0.5 * 0.125 + 0.5 * ht)) < 1e-15
