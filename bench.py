@@ -36,6 +36,7 @@ WORKLOAD_TEXT = {
     4: "2-D grid RNN forward fp32: 32 grids 16x16, E=128, H=256",
     5: "child-sum TreeLSTM forward bf16 (fp32 accumulate): 256 trees, leaves U[20,200], arity U{1..4}, E=H=512",
     6: "binary TreeLSTM with two internal cell types forward fp32: 64 trees, leaves U[10,50], E=H=256",
+    7: "binary TreeGRU forward fp32: 64 trees, leaves U[10,50], E=H=256",
 }
 
 
@@ -50,7 +51,7 @@ def algorithmic_work(w, f):
     H, E = w.hidden, w.in_dim
     esz = 2 if w.dtype == "bf16" else 4
     G = {WL.LSTM_CHAIN: 4, WL.NARY_LEAF: 3, WL.NARY_INTERNAL: 5, WL.GRID: 5, WL.CS_LEAF: 3,
-         WL.CS_INTERNAL: 3, WL.LAT_CHAR: 4, WL.LAT_WORD: 3}
+         WL.CS_INTERNAL: 3, WL.LAT_CHAR: 4, WL.LAT_WORD: 3, WL.GRU_LEAF: 2, WL.GRU_INTERNAL: 3}
     out = []
     for b in range(f.sched.n_batches):
         t = int(f.sched.batch_type[b])
@@ -69,6 +70,8 @@ def algorithmic_work(w, f):
             if k == WL.LAT_CHAR and rag:
                 fl += 2 * E * H
                 flr += 2 * H * H * len(rag)                # x W_lx, c_w W_lc
+            if k == WL.GRU_INTERNAL:
+                fl += 2 * H * H * len(fixed)               # each candidate n_k reads its own child
             fl += 2 * Kp * G[k] * H
             by += (E * esz if hasx else 0) + len(fixed) * H * (esz + 4) + len(rag) * H * (esz + 4)
             by += H * (esz + 4)
@@ -106,7 +109,7 @@ def kernel_symbol(kind, dtype, variant, part):
         rt, wk = STREAM_SHAPES[variant]
         return f"edbk::stream_kernel<{kind}, {t}, {rt}, {wk}>"
     if variant in LARGE_CLASS:
-        kk = 8 if part == 2 else (9 if kind == 5 else kind)
+        kk = 10 if part == 2 else (11 if kind == 5 else kind)
         return f"edbk::big_kernel<{kk}, {t}, {LARGE_CLASS[variant]}>"
     rt, wu, wk = SMALL_VARIANTS[variant]
     return f"edbk::cell_kernel<{kind}, {t}, {rt}, {wu}, {wk}>"
@@ -393,7 +396,7 @@ def main():
     tflops = (fl / nl) / (avg_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     kname = {0: "LSTM_CHAIN", 1: "NARY_LEAF", 2: "NARY_INTERNAL", 3: "GRID", 4: "CS_LEAF",
-             5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD"}[dom[0]]
+             5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD", 8: "GRU_LEAF", 9: "GRU_INTERNAL"}[dom[0]]
     kind_v, var_v, part_v = dom
     if part_v == 1:
         kernel = "child_reduce_kernel"

@@ -254,6 +254,13 @@ void edb_plan_free(edb_plan_t* p);
 #define EDB_CELL_CS_INTERNAL   5  /* ragged children, no x;      [i,o,u] on sum h, f per child */
 #define EDB_CELL_LAT_CHAR      6  /* [prev char] + ragged words; gates [i,f,o,u] + link gates */
 #define EDB_CELL_LAT_WORD      7  /* [first char], x;            gates [i,f,u], no h output */
+/* TreeGRU (Table 2): the gated recurrent unit over two ordered children, the
+ * reset gates applied after the recurrent products.  A GRU node's state is
+ * written to both arenas (h and, in fp32, c); children's states are read from
+ * the c arena.  Leaf: h = (1 - sigma(z)) tanh(n).  Internal:
+ * h = sigma(z) (h_0 + h_1) / 2 + (1 - sigma(z)) tanh(sigma(r_0) n_0 + sigma(r_1) n_1). */
+#define EDB_CELL_GRU_LEAF      8  /* no children, x;             gates [z,n]              */
+#define EDB_CELL_GRU_INTERNAL  9  /* children [h_0, h_1], no x;  gates [z,r_0,r_1,n_0,n_1] */
 
 #define EDB_F32  0  /* W, x, h fp32 */
 #define EDB_BF16 1  /* W, x, h bf16 (round to nearest even); c fp32; fp32 accumulation */
@@ -280,6 +287,10 @@ edb_status edb_packed_weight_bytes(const edb_cell* cell, int64_t* bytes);
  *   CS_INTERNAL    U_iou[H x 3H], U_f[H x H], b_iou[3H], b_f[H]
  *   LAT_WORD       W[(E+H) x 3H], b[3H]
  *   LAT_CHAR       W[(E+H) x 4H], W_lx[E x H], W_lc[H x H], b[4H], b_l[H]
+ *   GRU_LEAF       W[E x 2H], b[2H]
+ *   GRU_INTERNAL   U[2H x 5H], b[5H]   (the n_0 columns use child 0's rows only,
+ *                                       the n_1 columns child 1's; the other
+ *                                       blocks of those columns are ignored)
  * bf16 cells round the matrices to bf16 (ties to even); biases stay fp32.
  * packed_dev: device buffer of edb_packed_weight_bytes bytes (caller-owned).
  * The copy is enqueued on `stream` (hipStream_t, NULL = default stream) and

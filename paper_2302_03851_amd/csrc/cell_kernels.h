@@ -42,10 +42,10 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 enum { K_CHAIN = 0, K_NARY_LEAF = 1, K_NARY_INT = 2, K_GRID = 3, K_CS_LEAF = 4, K_CS_INT = 5,
-       K_LAT_CHAR = 6, K_LAT_WORD = 7,
+       K_LAT_CHAR = 6, K_LAT_WORD = 7, K_GRU_LEAF = 8, K_GRU_INT = 9,
        // the two GEMMs of a child-sum batch run on the large tile: the forget
        // gates over the batch's child rows, then the parents on their child sums
-       K_CS_FORGET = 8, K_CS_PARENT = 9 };
+       K_CS_FORGET = 10, K_CS_PARENT = 11 };
 
 enum { S_NONE = 0, S_CONTIG = 1, S_INDEXED = 2 };
 
@@ -88,6 +88,9 @@ template <> struct Kind<K_CS_LEAF>  { static constexpr int G = 3, NFIX = 0; stat
 template <> struct Kind<K_CS_INT>   { static constexpr int G = 3, NFIX = 0; static constexpr bool X = false, RAG = true;  };
 template <> struct Kind<K_LAT_CHAR> { static constexpr int G = 5, NFIX = 1; static constexpr bool X = true,  RAG = true;  };
 template <> struct Kind<K_LAT_WORD> { static constexpr int G = 3, NFIX = 1; static constexpr bool X = true,  RAG = false; };
+// TreeGRU: the node state is kept in the cell-state arena (children's states read like c rows)
+template <> struct Kind<K_GRU_LEAF> { static constexpr int G = 2, NFIX = 0; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_GRU_INT>  { static constexpr int G = 5, NFIX = 2; static constexpr bool X = false, RAG = false; };
 // rows: the batch's children (x = their h rows); one gate
 template <> struct Kind<K_CS_FORGET>{ static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
 // rows: the parents (x = their child sums of h)
@@ -160,6 +163,13 @@ __device__ __forceinline__ void cell_update(const float* z, const float* cp, flo
     } else if constexpr (KIND == K_LAT_WORD) {
         c = fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[2]));
         h = 0.f;
+    } else if constexpr (KIND == K_GRU_LEAF) {   // gates [z, n]: (1 - sigma(z)) tanh(n)
+        c = sig_tanh(-z[0], z[1]);
+        h = c;
+    } else if constexpr (KIND == K_GRU_INT) {    // gates [z, r_0, r_1, n_0, n_1]; cp: the children's states
+        const float ht = tanh_f(fmaf(sigm(z[1]), z[3], sigm(z[2]) * z[4]));
+        c = fmaf(sigm(z[0]), fmaf(0.5f, cp[0] + cp[1], -ht), ht);
+        h = c;
     } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
         if (nw == 0) {
             c = fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[3]));
@@ -740,7 +750,7 @@ struct SRing {
 // past the valid width of the segment, E or H, and for rows whose offset is
 // out of range).
 template <typename T, int RT, int NSEG, bool HX>
-__device__ __forceinline__ void stream_load_a(uint4 (&av)[RT], const uint32_t (&soff)[NSEG][RT],
+__device__ __forceinline__ void stream_load_a(uint4 (&av)[RT], const u32x4 (&soff)[RT],
                                               __amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rh, int s, int c,
                                               int E, int H, int lane) {
     constexpr uint32_t OOB = 0x80000000u;
@@ -750,10 +760,9 @@ __device__ __forceinline__ void stream_load_a(uint4 (&av)[RT], const uint32_t (&
     const __amdgpu_buffer_rsrc_t r = xs ? rx : rh;
 #pragma unroll
     for (int rb = 0; rb < RT; ++rb) {
-        uint32_t base = soff[0][rb];
-#pragma unroll
-        for (int q = 1; q < NSEG; ++q)
-            if (s == q) base = soff[q][rb];
+        // a vector value: the compiler picks the segment with selects in
+        // registers (as an array it kept the offsets in scratch memory)
+        const uint32_t base = NSEG == 1 ? soff[rb][0] : soff[rb][s];
         av[rb] = bload(r, ok ? base + (uint32_t)col * (uint32_t)sizeof(T) : OOB);
     }
 }
@@ -836,18 +845,20 @@ __device__ __forceinline__ void stream_tile(const BatchArgs& a, int rtile, int u
     // slot 0's weights go out before the operand offsets wait for the indices
     load_b<G>(ring.b[0], Bw, nkg, min(max(lk, 0), nkg - 1));
     __builtin_amdgcn_sched_barrier(0);
-    uint32_t soff[NSEG][RT];
+    static_assert(NSEG <= 4, "segment offsets are held in a 4-wide vector");
+    u32x4 soff[RT];
 #pragma unroll
     for (int rb = 0; rb < RT; ++rb) {
         const bool ok = rb * 16 + (lane & 15) < nrows;
+        soff[rb] = u32x4{OOB, OOB, OOB, OOB};
         int s = 0;
         if constexpr (HX) {
-            soff[s][rb] = ok ? (uint32_t)srow[s][rb] * (uint32_t)a.E * ES : OOB;
+            soff[rb][s] = ok ? (uint32_t)srow[s][rb] * (uint32_t)a.E * ES : OOB;
             ++s;
         }
 #pragma unroll
         for (int p = 0; p < NFX; ++p, ++s)
-            soff[s][rb] = ok && a.fix[p].kind != S_NONE ? (uint32_t)srow[s][rb] * (uint32_t)a.H * ES : OOB;
+            soff[rb][s] = ok && a.fix[p].kind != S_NONE ? (uint32_t)srow[s][rb] * (uint32_t)a.H * ES : OOB;
     }
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.xmat, HX ? (uint32_t)a.n_xrows * (uint32_t)a.E * ES : 0u);
     const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.arena_h, (uint32_t)a.n_slots * (uint32_t)a.H * ES);
@@ -1113,6 +1124,8 @@ __global__ __launch_bounds__(256) void flow_kernel(FlowArgs f) {
             case K_CS_LEAF: cell_tile<K_CS_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
             case K_CS_INT: cell_tile<K_CS_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
             case K_LAT_CHAR: cell_tile<K_LAT_CHAR, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_GRU_LEAF: cell_tile<K_GRU_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
+            case K_GRU_INT: cell_tile<K_GRU_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
             default: cell_tile<K_LAT_WORD, T, FLOW_RT, FLOW_WU, FLOW_WK>(a, tl.y, tl.z, smem, sync); break;
         }
     }

@@ -61,6 +61,8 @@ KindInfo kind_info(int kind) {
         case EDB_CELL_CS_INTERNAL: return {3, 0, false, true};
         case EDB_CELL_LAT_CHAR: return {5, 1, true, true};
         case EDB_CELL_LAT_WORD: return {3, 1, true, false};
+        case EDB_CELL_GRU_LEAF: return {2, 0, true, false};
+        case EDB_CELL_GRU_INTERNAL: return {5, 2, false, false};
         default: return {0, 0, false, false};
     }
 }
@@ -193,6 +195,8 @@ extern "C" edb_status edb_pack_weights(const edb_cell* cell, const float* const*
         const int row = main_row(kind, d, k);
         if (row < 0) return 0.f;
         if (kind == EDB_CELL_LAT_CHAR && g == 4) return row < d.E ? Wlx[(int64_t)row * H + j] : 0.f;
+        // TreeGRU candidates: n_0 reads only child 0's rows, n_1 only child 1's
+        if (kind == EDB_CELL_GRU_INTERNAL && ((g == 3 && row >= H) || (g == 4 && row < H))) return 0.f;
         return W[(int64_t)row * ncol + g * H + j];
     });
     float* bias = reinterpret_cast<float*>(buf.data() + d.off_b);
@@ -334,7 +338,7 @@ void fill_internal(Entry (&e)[2][NUM_VARIANTS]) {
     e[1][16] = big_entry<KIND, __bf16, 4>();
 }
 
-constexpr int NUM_KERNEL_KINDS = 10;   // the 8 cell kinds, then K_CS_FORGET, K_CS_PARENT
+constexpr int NUM_KERNEL_KINDS = 12;   // the 10 cell kinds, then K_CS_FORGET, K_CS_PARENT
 
 struct Table {
     Entry e[NUM_KERNEL_KINDS][2][NUM_VARIANTS];
@@ -347,6 +351,8 @@ struct Table {
         fill_kind<K_CS_INT, float>(e[5][0]);       fill_kind<K_CS_INT, __bf16>(e[5][1]);
         fill_kind<K_LAT_CHAR, float>(e[6][0]);     fill_kind<K_LAT_CHAR, __bf16>(e[6][1]);
         fill_kind<K_LAT_WORD, float>(e[7][0]);     fill_kind<K_LAT_WORD, __bf16>(e[7][1]);
+        fill_kind<K_GRU_LEAF, float>(e[8][0]);     fill_kind<K_GRU_LEAF, __bf16>(e[8][1]);
+        fill_kind<K_GRU_INT, float>(e[9][0]);      fill_kind<K_GRU_INT, __bf16>(e[9][1]);
         fill_internal<K_CS_FORGET>(e[K_CS_FORGET]);
         fill_internal<K_CS_PARENT>(e[K_CS_PARENT]);
     }
@@ -390,6 +396,8 @@ int flow_lds(const std::vector<int>& kinds_k) {
             case K_CS_LEAF: l = lds_bytes<K_CS_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
             case K_CS_INT: l = lds_bytes<K_CS_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
             case K_LAT_CHAR: l = lds_bytes<K_LAT_CHAR, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
+            case K_GRU_LEAF: l = lds_bytes<K_GRU_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
+            case K_GRU_INT: l = lds_bytes<K_GRU_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
             default: l = lds_bytes<K_LAT_WORD, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
         }
         best = std::max(best, l);

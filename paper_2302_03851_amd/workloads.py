@@ -339,7 +339,7 @@ def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = N
                 if g.op_type[v] == 1:
                     g.op_type[v] = 1 + int(rng.integers(0, 2))
     elif k == 7:
-        # binary TreeGRU: the trees of config 2 (same draws), GRU cells
+        # binary TreeGRU: trees drawn as in config 2 (its own seed), GRU cells
         inst = 64 if instances is None else instances
         kinds, E, H, scale = [GRU_LEAF, GRU_INTERNAL], 256, 256, 0.08
         n_children = [0, 0]

@@ -17,7 +17,7 @@ from paper_2302_03851_amd import workloads as WL
 pytestmark = pytest.mark.gpu
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
-SMALL = {1: 8, 2: 6, 3: 6, 4: 2, 5: 4, 6: 6}
+SMALL = {1: 8, 2: 6, 3: 6, 4: 2, 5: 4, 6: 6, 7: 6}
 
 
 def _torch():
@@ -50,7 +50,7 @@ def _check(w, h, c, hr, cr, label):
     return err
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 7])
 def test_parity_small(k):
     _torch()
     w = WL.make_config(k, instances=SMALL[k])
@@ -97,7 +97,7 @@ def _subgraph(w, nodes):
                 child_idx=np.array(idx, dtype=np.int32), x_row=w.x_row[nodes])
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 7])
 def test_parity_full_size_sampled_instances(k):
     _torch()
     w = WL.make_config(k)
@@ -124,7 +124,7 @@ def test_parity_full_size_sampled_instances(k):
     assert err <= TOL[w.dtype]
 
 
-@pytest.mark.parametrize("k", [2, 3, 4, 5])
+@pytest.mark.parametrize("k", [2, 3, 4, 5, 7])
 def test_layout_and_launch_mode_bitwise(k):
     """The planned layout, the identity layout with every operand indexed,
     the PQ-tree layout (zero pads, rows in another order), forced gathers, x read in place and eager launches all give bitwise the

@@ -38,7 +38,7 @@ def _oracle_schedule(w, policy=OS.POLICY_TABLE, table=None, encoding=OS.ENC_SORT
     return OS.schedule(w.op_type, w.child_ptr, w.child_idx, w.n_types, policy, table, encoding)
 
 
-CFG_INSTANCES = {1: None, 2: None, 3: None, 4: None, 5: 48, 6: None}
+CFG_INSTANCES = {1: None, 2: None, 3: None, 4: None, 5: 48, 6: None, 7: None}
 
 
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
@@ -207,7 +207,7 @@ def test_abi_errors(lib):
     assert lib.edb_execute(None, None, None, None, None, None) == L.EDB_ERR_INVALID
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 7])
 @pytest.mark.parametrize("flow", [True, False])
 def test_dryrun_launch_list(k, flow):
     w = WL.make_config(k, instances=CFG_INSTANCES[k])
