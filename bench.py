@@ -147,15 +147,24 @@ def traffic_from(d, workload):
             raise SystemExit(f"expected one file for {pattern} under {d}, found {m}")
         return m[0]
 
-    scale = {}
+    # bytes per counted KiB for each calibration kernel (2 GiB per dispatch);
+    # the elementwise kernel's 16-byte lane accesses match this library's
+    # kernels, so its factor is the one applied
+    scale, scale_copy = {}, {}
     for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
         cp = per_kernel(one(f"copy_{ctr}/*counter_collection.csv"))
-        vals = [v for k, vs in cp.items() if "copyBuffer" in k for v in vs]
-        scale[ctr] = (256 << 10) / (sum(vals) / len(vals))   # 256 MiB per copy, in KiB
+        for name, pat, dst in (("copy", "copyBuffer", scale_copy), ("elementwise", "MulFunctor", scale)):
+            vals = [v for k, vs in cp.items() if pat in k for v in vs]
+            if not vals:
+                raise SystemExit(f"no {name} calibration dispatches in copy_{ctr}")
+            dst[ctr] = (2048 << 10) / (sum(vals) / len(vals))
     fetch = per_kernel(one("c2_FETCH_SIZE/*counter_collection.csv"))
     write = per_kernel(one("c2_WRITE_SIZE/*counter_collection.csv"))
     out = {"workload": workload, "source_sha256": source_digest(),
            "fetch_scale": round(scale["FETCH_SIZE"], 4), "write_scale": round(scale["WRITE_SIZE"], 4),
+           "copy_fetch_scale": round(scale_copy["FETCH_SIZE"], 4),
+           "copy_write_scale": round(scale_copy["WRITE_SIZE"], 4),
+           "calibration": "torch elementwise multiply (16-byte lane loads and stores), 2 GiB per dispatch",
            "kernels": {}}
     for k in sorted(set(fetch) & set(write)):
         f, w_ = fetch[k], write[k]
@@ -164,7 +173,7 @@ def traffic_from(d, workload):
                              "write_bytes": round(sum(w_) / len(w_) * 1024 * scale["WRITE_SIZE"])}
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(out, fh, indent=1)
-    print(f"wrote {TRAFFIC_FILE}: {len(out['kernels'])} kernels, scales {scale}")
+    print(f"wrote {TRAFFIC_FILE}: {len(out['kernels'])} kernels, scales {scale} (device copy: {scale_copy})")
 
 
 def traffic_of(symbol, workload):
@@ -224,7 +233,7 @@ def main():
                          "or node ids (every operand indexed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a plain device copy of 256 MiB, 5 times (to scale HBM byte counters)")
+                    help="only run plain copies of 2 GiB, 5 device copies and 5 elementwise (to scale HBM byte counters)")
     ap.add_argument("--traffic-from", metavar="DIR",
                     help="write profiles/traffic.json from rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR "
                          "(c2_<counter>/ of this benchmark, copy_<counter>/ of --copy-calibration)")
@@ -245,14 +254,19 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     if args.copy_calibration:
-        # a plain copy of known size: each dispatch reads and writes 256 MiB
-        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda:0")
+        # copies of known size, each dispatch reading and writing 2 GiB (8x the
+        # 256 MB last-level cache, so that few reads hit it): the runtime's
+        # device copy, and an elementwise kernel whose lanes load and store 16
+        # bytes each (the access width of this library's kernels)
+        src = torch.ones(512 << 20, dtype=torch.float32, device="cuda:0")
         dst = torch.empty_like(src)
         for _ in range(5):
             dst.copy_(src)
+        for _ in range(5):
+            torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": src.numel() * 4, "copy_bytes_written": dst.numel() * 4,
-                          "copies": 5}), flush=True)
+                          "copies": 5, "elementwise": 5}), flush=True)
         return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
