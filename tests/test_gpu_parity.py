@@ -156,6 +156,24 @@ def _grid_graph(n_grids, R, C, E, H, seed, dtype):
     return WL.make_graph([WL.GRID], E, H, op, ch, [True] * len(op), seed=seed, dtype=dtype, bias_scale=0.2)
 
 
+def _gru_trees(n_trees, E, H, seed, dtype):
+    """n_trees three-node TreeGRU trees (two leaves, one internal node) and a
+    chain of internal nodes over them, with non-zero biases."""
+    op, ch, hx = [], [], []
+    for t in range(n_trees):
+        op += [0, 0, 1]
+        ch += [[], [], [3 * t, 3 * t + 1]]
+        hx += [True, True, False]
+    prev = 2
+    for t in range(1, min(n_trees, 40)):     # a deeper spine: internal nodes over earlier roots
+        op.append(1)
+        ch.append([prev, 3 * t + 2])
+        hx.append(False)
+        prev = len(op) - 1
+    return WL.make_graph([WL.GRU_LEAF, WL.GRU_INTERNAL], E, H, op, ch, hx, seed=seed, dtype=dtype,
+                         bias_scale=0.2)
+
+
 def _large_tile_workloads():
     """Workloads whose batches span several large tiles with a ragged row
     tail.  bf16: the child-sum configuration (its leaf batch), grids with a
@@ -176,7 +194,9 @@ def _large_tile_workloads():
         hx += [True, True, False]
     out.append(WL.make_graph([WL.NARY_LEAF, WL.NARY_INTERNAL], 128, 256, op, ch, hx, seed=13, dtype="bf16",
                              bias_scale=0.2))
-    out += [WL.make_config(2, instances=16), _grid_graph(24, 12, 12, 120, 192, seed=14, dtype="f32")]
+    out.append(_gru_trees(200, 128, 256, seed=16, dtype="bf16"))
+    out += [WL.make_config(2, instances=16), _grid_graph(24, 12, 12, 120, 192, seed=14, dtype="f32"),
+            _gru_trees(200, 128, 192, seed=17, dtype="f32")]
     op = [0] * (3 * n)
     ch = [[-1] if i % 3 == 0 else [i - 1] for i in range(3 * n)]
     out.append(WL.make_graph([WL.LSTM_CHAIN], 64, 128, op, ch, [True] * (3 * n), seed=15, dtype="f32",
@@ -273,6 +293,7 @@ def _stream_workloads():
     ch = [[-1] if i % 3 == 0 else [i - 1] for i in range(3 * n)]
     out.append(WL.make_graph([WL.LSTM_CHAIN], 64, 128, op, ch, [True] * (3 * n), seed=22, dtype="bf16",
                              bias_scale=0.2))
+    out += [_gru_trees(60, 64, 128, seed=23, dtype="f32"), _gru_trees(60, 64, 128, seed=24, dtype="bf16")]
     return out
 
 
