@@ -214,6 +214,75 @@ def cpu_baseline(w, budget_s=12.0):
                       f"{t_total:.1f} s, numpy float64 with BLAS limited to 1 thread"}
 
 
+DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64}
+
+
+def study(configs, replays=100):
+    """Replay study of each workload (one JSON line per workload): warm and
+    cold replays of the captured batch sequence (median, p10, p90; cold = a
+    512 MB write before every replay, twice the last-level cache), the scale
+    sweep at 1x, 4x and 16x the instances, and the end-to-end time of a new
+    graph (ingest + schedule + plan + prepare + capture and first replay)."""
+    import torch
+    from paper_2302_03851_amd import _lib as L
+    from paper_2302_03851_amd import edb, workloads as WL
+
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
+
+    def replay_times(f, cold):
+        ts = []
+        for _ in range(replays):
+            if cold:
+                scratch.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(f.stream)
+            f.run()
+            e1.record(f.stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        ts = np.array(ts)
+        return {"median_us": round(float(np.median(ts)), 2), "p10_us": round(float(np.percentile(ts, 10)), 2),
+                "p90_us": round(float(np.percentile(ts, 90)), 2)}
+
+    for k in configs:
+        rec = {"workload": WORKLOAD_TEXT[k], "scale": {}}
+        for mult in (1, 4, 16):
+            w = WL.make_config(k, instances=DEFAULT_INSTANCES[k] * mult)
+            f = edb.Forward(w, flags=L.USE_GRAPH)
+            for _ in range(5):
+                f.run()
+            torch.cuda.synchronize()
+            warm = replay_times(f, False)
+            work = algorithmic_work(w, f)
+            flops = sum(x[0] + x[1] for x in work)
+            ent = {"instances": DEFAULT_INSTANCES[k] * mult, "nodes": w.n_nodes, "batches": f.sched.n_batches,
+                   "warm": warm, "node_cells_per_s": round(w.n_nodes / (warm["median_us"] * 1e-6), 1),
+                   "alg_tflops": round(flops / (warm["median_us"] * 1e-6) / 1e12, 3)}
+            if mult == 1:
+                ent["cold"] = replay_times(f, True)
+                # a new graph end to end: host objects, then capture + instantiate + first replay
+                t0 = time.perf_counter()
+                g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+                sc = edb.Schedule(g, L.POLICY_TABLE, L.ENC_SORT, edb.LATTICE_TABLE if w.kinds == [6, 7] else None)
+                pl = edb.Plan(g, sc, edb.operand_shapes(w), L.PLAN_RC)
+                ex = edb.Exec(g, sc, pl, f.cells, L.USE_GRAPH)
+                t1 = time.perf_counter()
+                ex.execute([b.data_ptr() for b in f.weights], f.x.data_ptr(), f.arena_h.data_ptr(),
+                           f.arena_c.data_ptr(), f.stream.cuda_stream)
+                torch.cuda.synchronize()
+                t2 = time.perf_counter()
+                ent["new_graph_ms"] = {"host": round((t1 - t0) * 1e3, 3),
+                                       "capture_instantiate_first_replay": round((t2 - t1) * 1e3, 3),
+                                       "total": round((t2 - t0) * 1e3, 3)}
+                del ex, pl, sc, g
+            rec["scale"][f"x{mult}"] = ent
+            print(f"study: workload {k} x{mult}: {w.n_nodes} nodes, warm median {warm['median_us']} us",
+                  file=sys.stderr, flush=True)
+            del f
+            torch.cuda.empty_cache()
+        print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -231,6 +300,9 @@ def main():
     ap.add_argument("--plan", default="rc", choices=["rc", "pq", "identity"],
                     help="arena layout: the reverse consumer-first pass (default), the PQ-tree layout, "
                          "or node ids (every operand indexed)")
+    ap.add_argument("--study", metavar="CONFIGS",
+                    help="instead of the benchmark: warm/cold replay, scale sweep and new-graph times of the "
+                         "listed workloads (comma separated, e.g. 1,2,3,4,5)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run plain copies of 2 GiB, 5 device copies and 5 elementwise (to scale HBM byte counters)")
@@ -253,6 +325,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.study:
+        study([int(c) for c in args.study.split(",")])
+        return
     if args.copy_calibration:
         # copies of known size, each dispatch reading and writing 2 GiB (8x the
         # 256 MB last-level cache, so that few reads hit it): the runtime's
