@@ -197,21 +197,124 @@ def weight_bytes(w):
 
 
 def cpu_baseline(w, budget_s=12.0):
-    """The oracle (numpy float64, node at a time, one BLAS thread) on the same
-    workload: repeated full forwards until the time budget is spent."""
+    """The oracle (numpy float64, node at a time) on the same workload: repeated
+    full forwards until the time budget is spent, first with one BLAS thread,
+    then with BLAS on every core this process may use (capped by
+    OMP_NUM_THREADS when it is set)."""
     from threadpoolctl import threadpool_limits
     from oracle.evaluate import evaluate
-    reps, t_total = 0, 0.0
-    with threadpool_limits(limits=1):
-        while t_total < budget_s and reps < 20:
-            t0 = time.perf_counter()
-            evaluate(w.kinds, w.op_type, w.child_ptr, w.child_idx, w.x_row, w.x, w.weights, w.hidden,
-                     n_fixed=w.n_children, dtype=w.dtype)
-            t_total += time.perf_counter() - t0
-            reps += 1
+
+    def timed(threads):
+        reps, t_total = 0, 0.0
+        with threadpool_limits(limits=threads):
+            while t_total < budget_s and reps < 20:
+                t0 = time.perf_counter()
+                evaluate(w.kinds, w.op_type, w.child_ptr, w.child_idx, w.x_row, w.x, w.weights, w.hidden,
+                         n_fixed=w.n_children, dtype=w.dtype)
+                t_total += time.perf_counter() - t0
+                reps += 1
+        return reps, t_total
+
+    reps, t_total = timed(1)
+    cores = len(os.sched_getaffinity(0))
+    if os.environ.get("OMP_NUM_THREADS", "").isdigit():
+        cores = max(1, min(cores, int(os.environ["OMP_NUM_THREADS"])))
+    reps_all, t_all = timed(cores)
     return {"value": round(w.n_nodes * reps / t_total, 1), "unit": "node-cells/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} full forward passes of the same {w.n_nodes}-node workload, "
-                      f"{t_total:.1f} s, numpy float64 with BLAS limited to 1 thread"}
+                      f"{t_total:.1f} s, numpy float64 with BLAS limited to 1 thread",
+            "all_cores": {"value": round(w.n_nodes * reps_all / t_all, 1), "cores": cores,
+                          "sample": f"{reps_all} full forward passes, {t_all:.1f} s, BLAS on {cores} threads"}}
+
+
+def probes(dtype_name, reps=3):
+    """Measured denominators on this GPU: the matrix-core rate of the path's
+    MFMA shape (edb_probe_mfma: 2048 work-groups of 4 waves, 8 independent
+    accumulators per wave) and the device-memory copy rate (edb_probe_copy of
+    1 GiB, 4x the last-level cache; read + written bytes), each the best of
+    `reps` runs (the copy also over four grid sizes)."""
+    import torch
+    from paper_2302_03851_amd import _lib as L, edb
+    st = torch.cuda.current_stream().cuda_stream
+    bf16 = dtype_name == "bf16"
+    n_wg, iters = 2048, (10000 if bf16 else 5000)
+    out = torch.empty(n_wg * 256, dtype=torch.float32, device="cuda:0")
+    flops = n_wg * 4 * iters * 8 * (16384 if bf16 else 2048)
+    ms = min(edb.probe_mfma(L.BF16 if bf16 else L.F32, n_wg, iters, out.data_ptr(), st) for _ in range(reps))
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    best = {}
+    for wg in (8192, 16384, 32768, 65536):
+        best[wg] = min(edb.probe_copy(src.data_ptr(), dst.data_ptr(), nbytes, wg, st) for _ in range(reps))
+    wg_best = min(best, key=best.get)
+    del src, dst, out
+    return {"mfma_tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+            "mfma_shape": "16x16x32 bf16" if bf16 else "16x16x4 f32",
+            "copy_gbs": round(2 * nbytes / (best[wg_best] * 1e-3) / 1e9, 1), "copy_workgroups": wg_best}
+
+
+def split_phase(configs, reps=5):
+    """Split-phase diagnostic of each workload (one JSON line per workload):
+    the gather and scatter of every batch as separate unfused copies
+    (edb_split_phase), median over `reps` calls.  Algorithmic bytes: gather =
+    the present operand rows read (x, present children's h and c), scatter =
+    own h and c written; moved bytes = every row the copies read and write."""
+    import torch
+    from paper_2302_03851_amd import _lib as L
+    from paper_2302_03851_amd import edb, workloads as WL
+
+    pr = {}
+    for k in configs:
+        w = WL.make_config(k)
+        if w.dtype not in pr:
+            pr[w.dtype] = probes(w.dtype)
+        f = edb.Forward(w, flags=L.USE_GRAPH)
+        f.run()
+        torch.cuda.synchronize()
+        B = f.sched.n_batches
+        nb = f.exec.split_phase_bytes()
+        buf = torch.empty(nb, dtype=torch.uint8, device="cuda:0")
+        ms = np.median([f.exec.split_phase(f.x.data_ptr(), f.arena_h.data_ptr(), f.arena_c.data_ptr(),
+                                           buf.data_ptr(), nb, f.stream.cuda_stream, B) for _ in range(reps)], axis=0)
+        work = algorithmic_work(w, f)
+        esz = 2 if w.dtype == "bf16" else 4
+        H, E = w.hidden, w.in_dim
+        shapes = edb.operand_shapes(w)
+        rows = []
+        for b in range(B):
+            t = int(f.sched.batch_type[b])
+            m = int(f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b])
+            nf, rg, hx = shapes[t]
+            segs = f.plan.segs[f.plan.seg_ptr[b]:f.plan.seg_ptr[b + 1]]
+            moved_g = m * E * esz if hx else 0
+            for kind_s, _base, _off, n in segs[1:]:
+                if kind_s != L.SEG_NONE:
+                    moved_g += n * H * (esz + 4)
+            own = m * H * (esz + 4)
+            rows.append((m, work[b][2] - own, own, 2 * moved_g, 2 * own, ms[b, 0], ms[b, 1]))
+        a = np.array(rows, dtype=np.float64)
+        g_ms, s_ms = a[:, 5].sum(), a[:, 6].sum()
+        alg = a[:, 1].sum() + a[:, 2].sum()
+        moved = a[:, 3].sum() + a[:, 4].sum()
+        big = int(np.argmax(a[:, 3]))
+        peak, meas = PEAK_HBM_GBS, pr[w.dtype]["copy_gbs"]
+        gbs = lambda by, t: by / (t * 1e-3) / 1e9
+        rec = {"workload": WORKLOAD_TEXT[k], "batches": B, "reps": reps,
+               "gather_ms": round(g_ms, 4), "scatter_ms": round(s_ms, 4),
+               "alg_bytes": int(alg), "moved_bytes": int(moved),
+               "alg_gbs": round(gbs(alg, g_ms + s_ms), 1), "moved_gbs": round(gbs(moved, g_ms + s_ms), 1),
+               "frac_alg": round(gbs(alg, g_ms + s_ms) / peak, 4),
+               "frac_moved": round(gbs(moved, g_ms + s_ms) / peak, 4),
+               "frac_moved_of_measured_copy": round(gbs(moved, g_ms + s_ms) / meas, 4),
+               "largest_batch": {"batch": big, "rows": int(a[big, 0]),
+                                 "gather_us": round(a[big, 5] * 1e3, 2), "scatter_us": round(a[big, 6] * 1e3, 2),
+                                 "gather_moved_gbs": round(gbs(a[big, 3], a[big, 5]), 1),
+                                 "scatter_moved_gbs": round(gbs(a[big, 4], a[big, 6]), 1)},
+               "peak_gbs": peak, "probes": pr[w.dtype]}
+        print(json.dumps(rec), flush=True)
+        del f, buf
+        torch.cuda.empty_cache()
 
 
 DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64}
@@ -303,6 +406,10 @@ def main():
     ap.add_argument("--study", metavar="CONFIGS",
                     help="instead of the benchmark: warm/cold replay, scale sweep and new-graph times of the "
                          "listed workloads (comma separated, e.g. 1,2,3,4,5)")
+    ap.add_argument("--split-phase", metavar="CONFIGS",
+                    help="instead of the benchmark: unfused gather and scatter times of the listed workloads")
+    ap.add_argument("--probes", action="store_true",
+                    help="instead of the benchmark: measured MFMA and copy rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run plain copies of 2 GiB, 5 device copies and 5 elementwise (to scale HBM byte counters)")
@@ -327,6 +434,12 @@ def main():
         sys.exit(1)
     if args.study:
         study([int(c) for c in args.study.split(",")])
+        return
+    if args.split_phase:
+        split_phase([int(c) for c in args.split_phase.split(",")])
+        return
+    if args.probes:
+        print(json.dumps({"f32": probes("f32"), "bf16": probes("bf16")}), flush=True)
         return
     if args.copy_calibration:
         # copies of known size, each dispatch reading and writing 2 GiB (8x the
@@ -531,6 +644,10 @@ def main():
         "host_ms_per_graph": round(ms_host, 4),
         "launch_us": [round(t * 1e3, 2) for t in times],
     }
+    pm = probes(w.dtype)
+    result["roofline"]["peak_measured"] = pm["mfma_tflops"]
+    result["roofline"]["frac_measured"] = round(tflops / pm["mfma_tflops"], 4)
+    result["probes"] = pm
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(result), flush=True)

@@ -406,6 +406,47 @@ edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
  * EDB_ERR_HIP if a bounded wait timed out (the results are then invalid). */
 edb_status edb_exec_check(edb_exec_t* e, void* stream);
 
+/* ---- Diagnostics: split-phase copies and roofline probes ---- */
+
+/* Split-phase diagnostic.  Section 3.1 prices a batch as a gather of its
+ * operand rows into one contiguous buffer, the batched computation, and a
+ * scatter of the results to their consumers' slots; the fused kernels of
+ * edb_execute do both copies inside the cell kernel.  edb_split_phase runs
+ * them alone, batch by batch in schedule order, on `stream`:
+ *   gather:  the rows the batch's cell kernel reads (x rows of the x the
+ *            executor reads; for each positional and each ragged child entry
+ *            its h row and its c row, absent children as the zero row) are
+ *            copied into `buf`, densely, one list after the other;
+ *   scatter: m rows of h and m rows of c are copied from the start of `buf`
+ *            into the batch's result slots.
+ * No cell is computed: afterwards the arenas hold copied rows, not states
+ * (run edb_execute again for states).  The executor must have run
+ * (edb_execute stages x).  buf: device, 16-byte aligned, at least
+ * edb_split_phase_bytes bytes (the largest batch's dense lists).
+ * ms (may be NULL): host float[n], n >= 2 * n_batches; receives per batch the
+ * gather and the scatter kernel's duration in milliseconds (HIP events in the
+ * dispatch packets); the call then waits for the stream.
+ * Errors: EDB_ERR_INVALID, EDB_ERR_UNSUPPORTED (a batch inside a dataflow
+ * launch), EDB_ERR_HIP. */
+edb_status edb_split_phase_bytes(const edb_exec_t* e, int64_t* bytes);
+edb_status edb_split_phase(edb_exec_t* e, const void* x, void* arena_h, void* arena_c, void* buf,
+                           int64_t buf_bytes, void* stream, float* ms, int32_t n);
+
+/* Roofline probes on the current device; each launches one kernel on
+ * `stream`, waits for it and returns its duration in *ms (HIP events).
+ * edb_probe_mfma: n_workgroups work-groups of 4 waves; each wave issues
+ *   iters x 8 independent MFMAs on register operands, v_mfma_f32_16x16x4_f32
+ *   (dtype EDB_F32, 2048 flops each) or v_mfma_f32_16x16x32_bf16 (EDB_BF16,
+ *   16384 flops each).  out: device float[n_workgroups * 256] (the
+ *   accumulators' sums, so the work is not dead).
+ * edb_probe_copy: copies `bytes` (a multiple of 16) from src to dst with
+ *   16-byte loads and stores, grid-stride over n_workgroups x 256 threads.
+ * Errors: EDB_ERR_INVALID, EDB_ERR_HIP. */
+edb_status edb_probe_mfma(int32_t dtype, int32_t n_workgroups, int32_t iters, float* out, void* stream,
+                          float* ms);
+edb_status edb_probe_copy(const void* src, void* dst, int64_t bytes, int32_t n_workgroups, void* stream,
+                          float* ms);
+
 void edb_exec_free(edb_exec_t* e);
 
 #ifdef __cplusplus

@@ -41,6 +41,7 @@ EXPORTS = [
     "edb_packed_weight_bytes", "edb_pack_weights",
     "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
     "edb_exec_check", "edb_exec_free", "edb_forward",
+    "edb_split_phase_bytes", "edb_split_phase", "edb_probe_mfma", "edb_probe_copy",
 ]
 
 
@@ -142,6 +143,10 @@ def load():
         "edb_forward": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32), P(C.c_int32),
                                     P(Policy), P(OperandShape), C.c_int32, P(Cell), C.c_int32, P(vp), vp, vp, vp,
                                     C.c_int64, vp, P(C.c_int32), P(vp)]),
+        "edb_split_phase_bytes": (C.c_int32, [vp, P(C.c_int64)]),
+        "edb_split_phase": (C.c_int32, [vp, vp, vp, vp, vp, C.c_int64, vp, P(C.c_float), C.c_int32]),
+        "edb_probe_mfma": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, P(C.c_float), vp, P(C.c_float)]),
+        "edb_probe_copy": (C.c_int32, [vp, vp, C.c_int64, C.c_int32, vp, P(C.c_float)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

@@ -21,7 +21,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
 HOST_SRC = ["graph.cpp", "schedule.cpp", "learn.cpp", "plan.cpp", "pqplan.cpp", "forward.cpp"]
-HIP_SRC = ["exec.hip"]
+HIP_SRC = ["exec.hip", "diag.hip"]
 
 # -ffp-contract=off: the policy learner's floating-point updates round as written
 CXXFLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-ffp-contract=off", "-I", os.path.join(ROOT, "include")]

@@ -16,6 +16,7 @@
 
 #include "big_tile.h"
 #include "cell_kernels.h"
+#include "diag_kernels.h"
 #include "edb_internal.h"
 
 using edb::fail;
@@ -1184,6 +1185,35 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
 
 namespace {
 
+// Launch L's arguments with the pointers of one execution filled in (w may be
+// NULL when no weights are read).
+BatchArgs resolve_args(const edb_exec* e, const Launch& L, const void* const* w, const void* x, void* arena_h,
+                       void* arena_c) {
+    const int* db = e->dbuf;
+    BatchArgs a = L.args;
+    const Dims& d = e->dims[L.type];
+    if (w) {
+        const uint8_t* wb = reinterpret_cast<const uint8_t*>(w[L.type]);
+        a.W = wb + d.off_W;
+        a.bias = reinterpret_cast<const float*>(wb + d.off_b);
+        a.Wr = d.rag ? wb + d.off_Wr : nullptr;
+        a.br = d.rag ? reinterpret_cast<const float*>(wb + d.off_br) : nullptr;
+    }
+    a.arena_h = arena_h;
+    a.arena_c = reinterpret_cast<float*>(arena_c);
+    a.xmat = (e->flags & EDB_X_DIRECT) ? x : e->xstaged;
+    a.n_slots = e->n_slots;
+    a.n_xrows = (e->flags & EDB_X_DIRECT) ? e->x_direct_rows : e->n_x;
+    a.fc = e->fc;
+    if (L.off_x >= 0) a.x.idx = db + L.off_x;
+    if (L.off_f0 >= 0) a.fix[0].idx = db + L.off_f0;
+    if (L.off_f1 >= 0) a.fix[1].idx = db + L.off_f1;
+    if (L.off_rag >= 0) a.rag.idx = db + L.off_rag;
+    if (L.off_rptr >= 0) a.rag_ptr = db + L.off_rptr;
+    if (L.off_res >= 0) a.res.idx = db + L.off_res;
+    return a;
+}
+
 hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* arena_h, void* arena_c,
                       hipStream_t st) {
     const int esz = e->dtype == EDB_F32 ? 4 : 2;
@@ -1260,25 +1290,7 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
             }
             continue;
         }
-        BatchArgs a = L.args;
-        const Dims& d = e->dims[L.type];
-        const uint8_t* wb = reinterpret_cast<const uint8_t*>(w[L.type]);
-        a.W = wb + d.off_W;
-        a.bias = reinterpret_cast<const float*>(wb + d.off_b);
-        a.Wr = d.rag ? wb + d.off_Wr : nullptr;
-        a.br = d.rag ? reinterpret_cast<const float*>(wb + d.off_br) : nullptr;
-        a.arena_h = arena_h;
-        a.arena_c = reinterpret_cast<float*>(arena_c);
-        a.xmat = (e->flags & EDB_X_DIRECT) ? x : e->xstaged;
-        a.n_slots = e->n_slots;
-        a.n_xrows = (e->flags & EDB_X_DIRECT) ? e->x_direct_rows : e->n_x;
-        a.fc = e->fc;
-        if (L.off_x >= 0) a.x.idx = db + L.off_x;
-        if (L.off_f0 >= 0) a.fix[0].idx = db + L.off_f0;
-        if (L.off_f1 >= 0) a.fix[1].idx = db + L.off_f1;
-        if (L.off_rag >= 0) a.rag.idx = db + L.off_rag;
-        if (L.off_rptr >= 0) a.rag_ptr = db + L.off_rptr;
-        if (L.off_res >= 0) a.res.idx = db + L.off_res;
+        BatchArgs a = resolve_args(e, L, w, x, arena_h, arena_c);
         hipEvent_t e0 = prof ? ev[2 * i] : nullptr, e1 = prof ? ev[2 * i + 1] : nullptr;
         if (L.kk < 0) {   // child-sum batch on the large tile: child sums and product sums
             __bf16* out = reinterpret_cast<__bf16*>(e->hsum);
@@ -1363,6 +1375,153 @@ extern "C" edb_status edb_execute(edb_exec_t* e, const void* const* w, const voi
     if (he == hipSuccess) he = hipEventRecord(e->done, st);
     if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_execute: ") + hipGetErrorString(he));
     e->ran = true;
+    return EDB_OK;
+}
+
+namespace {
+
+int64_t align16(int64_t v) { return (v + 15) & ~(int64_t)15; }
+
+// The launch of batch b that holds the batch's own operand lists: its cell
+// kernel, or for a child-sum batch on the large tile the child-sum part.
+const Launch* batch_launch(const edb_exec* e, int32_t b) {
+    for (size_t i = 1; i < e->launches.size(); ++i) {
+        const Launch& L = e->launches[i];
+        if (!L.flow && L.info.batch == b && L.info.part != 2) return &L;
+    }
+    return nullptr;
+}
+
+// Copy streams of batch b's gather (operand rows -> dense buffer) and scatter
+// (dense buffer -> result slots); returns the dense bytes each needs.
+void split_streams(const edb_exec* e, const Launch& L, const BatchArgs& a, char* buf, CopyArgs& g, CopyArgs& sc,
+                   int64_t& g_bytes, int64_t& s_bytes) {
+    const int esz = e->dtype == EDB_F32 ? 4 : 2;
+    const int m = a.m, H = a.H;
+    g = CopyArgs{};
+    sc = CopyArgs{};
+    int64_t off = 0;
+    auto add = [&](CopyArgs& c, const void* src, Seg srow, int64_t src_rows, void* dst, Seg drow, int64_t dst_rows,
+                   int n, int row_bytes) {
+        CopyStream& q = c.s[c.n_streams++];
+        q.src = reinterpret_cast<const char*>(src);
+        q.dst = reinterpret_cast<char*>(dst);
+        q.srow = srow;
+        q.drow = drow;
+        q.n = n;
+        q.row_bytes = row_bytes;
+        q.src_rows = src_rows;
+        q.dst_rows = dst_rows;
+    };
+    const Seg dense{S_CONTIG, 0, nullptr};
+    auto gather = [&](const void* src, Seg srow, int64_t src_rows, int n, int row_bytes) {
+        add(g, src, srow, src_rows, buf ? buf + off : nullptr, dense, n, n, row_bytes);
+        off = align16(off + (int64_t)n * row_bytes);
+    };
+    if (a.x.kind != S_NONE && m > 0) gather(a.xmat, a.x, a.n_xrows, m, a.E * esz);
+    for (int j = 0; j < 2; ++j)
+        if (a.fix[j].kind != S_NONE && m > 0) {
+            gather(a.arena_h, a.fix[j], a.n_slots, m, H * esz);
+            gather(a.arena_c, a.fix[j], a.n_slots, m, H * 4);
+        }
+    if (a.rag.kind != S_NONE && L.off_rptr >= 0) {
+        const int nrag = e->hbuf[L.off_rptr + m];
+        if (nrag > 0) {
+            gather(a.arena_h, a.rag, a.n_slots, nrag, H * esz);
+            gather(a.arena_c, a.rag, a.n_slots, nrag, H * 4);
+        }
+    }
+    g_bytes = off;
+    const int64_t hb = align16((int64_t)m * H * esz);
+    if (a.res.kind != S_NONE && m > 0) {
+        add(sc, buf, dense, m, a.arena_h, a.res, a.n_slots, m, H * esz);
+        add(sc, buf ? buf + hb : nullptr, dense, m, a.arena_c, a.res, a.n_slots, m, H * 4);
+    }
+    s_bytes = hb + align16((int64_t)m * H * 4);
+}
+
+int copy_grid(const CopyArgs& c) {
+    int n = 0;
+    for (int i = 0; i < c.n_streams; ++i) n = std::max(n, c.s[i].n);
+    return (n + 3) / 4;
+}
+
+}  // namespace
+
+extern "C" edb_status edb_split_phase_bytes(const edb_exec_t* e, int64_t* bytes) {
+    if (!e || !bytes) return fail(EDB_ERR_INVALID, "edb_split_phase_bytes: NULL argument");
+    int64_t need = 16;
+    for (int32_t b = 0; b < e->B; ++b) {
+        const Launch* L = batch_launch(e, b);
+        if (!L) return fail(EDB_ERR_UNSUPPORTED, "edb_split_phase_bytes: batch " + std::to_string(b) +
+                                                     " runs inside a dataflow launch");
+        const BatchArgs a = resolve_args(e, *L, nullptr, nullptr, nullptr, nullptr);
+        CopyArgs g, sc;
+        int64_t gb = 0, sb = 0;
+        split_streams(e, *L, a, nullptr, g, sc, gb, sb);
+        need = std::max(need, std::max(gb, sb));
+    }
+    *bytes = need;
+    return EDB_OK;
+}
+
+extern "C" edb_status edb_split_phase(edb_exec_t* e, const void* x, void* arena_h, void* arena_c, void* buf,
+                                      int64_t buf_bytes, void* stream, float* ms, int32_t n) {
+    if (!e) return fail(EDB_ERR_INVALID, "edb_split_phase: exec is NULL");
+    if (e->flags & EDB_DRYRUN) return fail(EDB_ERR_INVALID, "edb_split_phase: dry-run executor");
+    if (!arena_h || !arena_c || !buf) return fail(EDB_ERR_INVALID, "edb_split_phase: NULL argument");
+    if ((e->flags & EDB_X_DIRECT) && e->n_x > 0 && !x) return fail(EDB_ERR_INVALID, "edb_split_phase: x is NULL");
+    if (!e->ran) return fail(EDB_ERR_INVALID, "edb_split_phase: run edb_execute first (it stages x)");
+    if (ms && n < 2 * e->B) return fail(EDB_ERR_INVALID, "edb_split_phase: ms must hold 2 * n_batches values");
+    if ((reinterpret_cast<uintptr_t>(buf) | reinterpret_cast<uintptr_t>(arena_h) |
+         reinterpret_cast<uintptr_t>(arena_c)) & 15u)
+        return fail(EDB_ERR_INVALID, "edb_split_phase: device buffers must be 16-byte aligned");
+    int64_t need = 0;
+    if (edb_status st = edb_split_phase_bytes(e, &need)) return st;
+    if (buf_bytes < need)
+        return fail(EDB_ERR_INVALID, "edb_split_phase: buf holds " + std::to_string(buf_bytes) + " bytes, " +
+                                         std::to_string(need) + " needed");
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    std::vector<hipEvent_t> ev;
+    hipError_t he = hipSuccess;
+    if (ms) {
+        ev.assign(4 * (size_t)e->B, nullptr);
+        for (auto& q : ev)
+            if ((he = hipEventCreate(&q)) != hipSuccess) break;
+    }
+    for (int32_t b = 0; b < e->B && he == hipSuccess; ++b) {
+        const Launch* L = batch_launch(e, b);
+        const BatchArgs a = resolve_args(e, *L, nullptr, x, arena_h, arena_c);
+        CopyArgs g, sc;
+        int64_t gb = 0, sb = 0;
+        split_streams(e, *L, a, reinterpret_cast<char*>(buf), g, sc, gb, sb);
+        const CopyArgs* part[2] = {&g, &sc};
+        for (int k = 0; k < 2; ++k) {
+            const int gx = copy_grid(*part[k]);
+            if (gx > 0 && part[k]->n_streams > 0) {
+                const dim3 grid(gx, part[k]->n_streams);
+                if (ms)
+                    hipExtLaunchKernelGGL(copy_rows_kernel, grid, dim3(256), 0, st, ev[4 * b + 2 * k],
+                                          ev[4 * b + 2 * k + 1], 0, *part[k]);
+                else
+                    hipLaunchKernelGGL(copy_rows_kernel, grid, dim3(256), 0, st, *part[k]);
+            } else if (ms) {   // nothing to copy: an empty interval
+                he = hipEventRecord(ev[4 * b + 2 * k], st);
+                if (he == hipSuccess) he = hipEventRecord(ev[4 * b + 2 * k + 1], st);
+            }
+            if (he == hipSuccess) he = hipGetLastError();
+        }
+    }
+    if (ms && he == hipSuccess) {
+        he = hipStreamSynchronize(st);
+        for (int32_t b = 0; b < e->B && he == hipSuccess; ++b)
+            for (int k = 0; k < 2 && he == hipSuccess; ++k)
+                he = hipEventElapsedTime(&ms[2 * b + k], ev[4 * b + 2 * k], ev[4 * b + 2 * k + 1]);
+    }
+    for (auto q : ev)
+        if (q) (void)hipEventDestroy(q);
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_split_phase: ") + hipGetErrorString(he));
+    edb::clear_error();
     return EDB_OK;
 }
 

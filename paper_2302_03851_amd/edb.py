@@ -248,6 +248,21 @@ class Exec:
         L.check(L.load().edb_execute(self.handle, arr, C.c_void_p(x_ptr), C.c_void_p(arena_h_ptr),
                                      C.c_void_p(arena_c_ptr), C.c_void_p(stream)), "edb_execute")
 
+    def split_phase_bytes(self) -> int:
+        n = C.c_int64()
+        L.check(L.load().edb_split_phase_bytes(self.handle, C.byref(n)), "edb_split_phase_bytes")
+        return n.value
+
+    def split_phase(self, x_ptr: int, arena_h_ptr: int, arena_c_ptr: int, buf_ptr: int, buf_bytes: int,
+                    stream: int, n_batches: int) -> np.ndarray:
+        """Unfused gather and scatter of every batch (edb_split_phase); returns
+        [n_batches, 2] kernel durations in ms (gather, scatter)."""
+        out = (C.c_float * (2 * n_batches))()
+        L.check(L.load().edb_split_phase(self.handle, C.c_void_p(x_ptr), C.c_void_p(arena_h_ptr),
+                                         C.c_void_p(arena_c_ptr), C.c_void_p(buf_ptr), buf_bytes,
+                                         C.c_void_p(stream), out, 2 * n_batches), "edb_split_phase")
+        return np.array(out[:], dtype=np.float64).reshape(n_batches, 2)
+
     def __del__(self):
         if getattr(self, "handle", None) and L is not None and L._lib is not None:
             L._lib.edb_exec_free(self.handle)
@@ -330,6 +345,22 @@ def logical_weights(w, t) -> List[np.ndarray]:
     k = w.kinds[t]
     names = [n for n, _ in weight_shapes(k, w.in_dim, w.hidden, w.n_children[t] or 2)]
     return [w.weights[t][n] for n in names]
+
+
+def probe_mfma(dtype, n_workgroups: int, iters: int, out_ptr: int, stream: int) -> float:
+    """Matrix-core probe (edb_probe_mfma): kernel duration in ms."""
+    ms = C.c_float()
+    L.check(L.load().edb_probe_mfma(dtype, n_workgroups, iters, C.cast(C.c_void_p(out_ptr), C.POINTER(C.c_float)),
+                                    C.c_void_p(stream), C.byref(ms)), "edb_probe_mfma")
+    return ms.value
+
+
+def probe_copy(src_ptr: int, dst_ptr: int, nbytes: int, n_workgroups: int, stream: int) -> float:
+    """Device-memory copy probe (edb_probe_copy): kernel duration in ms."""
+    ms = C.c_float()
+    L.check(L.load().edb_probe_copy(C.c_void_p(src_ptr), C.c_void_p(dst_ptr), nbytes, n_workgroups,
+                                    C.c_void_p(stream), C.byref(ms)), "edb_probe_copy")
+    return ms.value
 
 
 LATTICE_TABLE = {(0,): 0, (1,): 1, (0, 1): 0, (1, 0): 1}
