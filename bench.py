@@ -265,8 +265,10 @@ def split_phase(configs, reps=5):
     from paper_2302_03851_amd import edb, workloads as WL
 
     pr = {}
-    for k in configs:
-        w = WL.make_config(k)
+    for spec in configs:
+        k, _, mult = str(spec).partition("x")
+        k, mult = int(k), int(mult or 1)
+        w = WL.make_config(k, instances=DEFAULT_INSTANCES[k] * mult)
         if w.dtype not in pr:
             pr[w.dtype] = probes(w.dtype)
         f = edb.Forward(w, flags=L.USE_GRAPH)
@@ -300,7 +302,7 @@ def split_phase(configs, reps=5):
         big = int(np.argmax(a[:, 3]))
         peak, meas = PEAK_HBM_GBS, pr[w.dtype]["copy_gbs"]
         gbs = lambda by, t: by / (t * 1e-3) / 1e9
-        rec = {"workload": WORKLOAD_TEXT[k], "batches": B, "reps": reps,
+        rec = {"workload": WORKLOAD_TEXT[k], "instances_scale": mult, "nodes": w.n_nodes, "batches": B, "reps": reps,
                "gather_ms": round(g_ms, 4), "scatter_ms": round(s_ms, 4),
                "alg_bytes": int(alg), "moved_bytes": int(moved),
                "alg_gbs": round(gbs(alg, g_ms + s_ms), 1), "moved_gbs": round(gbs(moved, g_ms + s_ms), 1),
@@ -407,7 +409,8 @@ def main():
                     help="instead of the benchmark: warm/cold replay, scale sweep and new-graph times of the "
                          "listed workloads (comma separated, e.g. 1,2,3,4,5)")
     ap.add_argument("--split-phase", metavar="CONFIGS",
-                    help="instead of the benchmark: unfused gather and scatter times of the listed workloads")
+                    help="instead of the benchmark: unfused gather and scatter times of the listed workloads "
+                         "(comma separated; 'KxN' = workload K with N times its instances, e.g. 5,5x4,5x16)")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the benchmark: measured MFMA and copy rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -436,7 +439,7 @@ def main():
         study([int(c) for c in args.study.split(",")])
         return
     if args.split_phase:
-        split_phase([int(c) for c in args.split_phase.split(",")])
+        split_phase(args.split_phase.split(","))
         return
     if args.probes:
         print(json.dumps({"f32": probes("f32"), "bf16": probes("bf16")}), flush=True)
