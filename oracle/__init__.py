@@ -23,4 +23,6 @@ Contents
   plan      the batching-aware memory plan (Section 3.1 constraints; slot
             assignment by a reverse consumer-first pass) and its hazard check
   compare   the normwise relative error used by the parity tests
+  mvrnn     the MV-RNN of Table 2 on binary trees (a vector and a matrix per
+            node), evaluated on the tree itself
 """
