@@ -37,6 +37,7 @@ WORKLOAD_TEXT = {
     5: "child-sum TreeLSTM forward bf16 (fp32 accumulate): 256 trees, leaves U[20,200], arity U{1..4}, E=H=512",
     6: "binary TreeLSTM with two internal cell types forward fp32: 64 trees, leaves U[10,50], E=H=256",
     7: "binary TreeGRU forward fp32: 64 trees, leaves U[10,50], E=H=256",
+    8: "MV-RNN forward fp32: 64 binary trees, leaves U[10,50], d=64 (a vector and a d x d matrix per node)",
 }
 
 
@@ -51,7 +52,13 @@ def algorithmic_work(w, f):
     H, E = w.hidden, w.in_dim
     esz = 2 if w.dtype == "bf16" else 4
     G = {WL.LSTM_CHAIN: 4, WL.NARY_LEAF: 3, WL.NARY_INTERNAL: 5, WL.GRID: 5, WL.CS_LEAF: 3,
-         WL.CS_INTERNAL: 3, WL.LAT_CHAR: 4, WL.LAT_WORD: 3, WL.GRU_LEAF: 2, WL.GRU_INTERNAL: 3}
+         WL.CS_INTERNAL: 3, WL.LAT_CHAR: 4, WL.LAT_WORD: 3, WL.GRU_LEAF: 2, WL.GRU_INTERNAL: 3,
+         WL.LINEAR: 1, WL.MV_MAT: 1, WL.MV_VEC: 1}
+    mv = (WL.LINEAR, WL.MV_MAT, WL.MV_VEC)
+    # an identity LINEAR map (an MV-RNN leaf) is no work
+    ident = [w.kinds[t] == WL.LINEAR and w.weights[t]["W"].shape[0] == w.weights[t]["W"].shape[1] and
+             np.array_equal(w.weights[t]["W"], np.eye(w.weights[t]["W"].shape[0], dtype=np.float32))
+             for t in range(len(w.kinds))]
     out = []
     for b in range(f.sched.n_batches):
         t = int(f.sched.batch_type[b])
@@ -72,6 +79,15 @@ def algorithmic_work(w, f):
                 flr += 2 * H * H * len(rag)                # x W_lx, c_w W_lc
             if k == WL.GRU_INTERNAL:
                 fl += 2 * H * H * len(fixed)               # each candidate n_k reads its own child
+            if k in mv:
+                # MV-RNN: h rows only (c mirrors h); the vector cell's two d x d
+                # matrix-vector products count as per-child work
+                if k == WL.MV_VEC:
+                    flr += 4 * H * H
+                if not ident[t]:
+                    fl += 2 * Kp * H
+                by += (E * esz if hasx else 0) + (len(fixed) + len(rag)) * H * esz + H * esz
+                continue
             fl += 2 * Kp * G[k] * H
             by += (E * esz if hasx else 0) + len(fixed) * H * (esz + 4) + len(rag) * H * (esz + 4)
             by += H * (esz + 4)
@@ -80,16 +96,17 @@ def algorithmic_work(w, f):
 
 
 def launch_work(info, work, split):
-    """Algorithmic flops of one launch: the whole batch, or for a child-sum
-    batch on the large tile (its batch index in `split`) its parts: part 2 the
-    per-child forget GEMM, part 1 the per-parent sums (no flops), part 0 the
-    parents' main GEMM."""
+    """Algorithmic flops of one launch: the whole batch, or for a batch run in
+    parts (its batch index in `split`): a child-sum batch on the large tile,
+    part 2 the per-child forget GEMM, part 1 the per-parent sums (no flops),
+    part 0 the parents' main GEMM; an MV-RNN vector batch, part 1 the
+    matrix-vector products, part 0 its GEMM."""
     fl, flr, _ = work[info["batch"]]
     part = info["part"]
     if part == 2:
         return flr
     if part == 1:
-        return 0
+        return flr if info["kind"] == 12 else 0
     return fl if info["batch"] in split else fl + flr
 
 
@@ -103,13 +120,13 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 def kernel_symbol(kind, dtype, variant, part):
     """The kernel a launch runs, as rocprofv3 prints its name (prefix)."""
     if part == 1:
-        return "edbk::child_reduce_kernel"
+        return "edbk::mv_matvec_kernel" if kind == 12 else "edbk::child_reduce_kernel"
     t = 'float' if dtype == 'f32' else '__bf16'
     if variant in STREAM_SHAPES:
         rt, wk = STREAM_SHAPES[variant]
         return f"edbk::stream_kernel<{kind}, {t}, {rt}, {wk}>"
     if variant in LARGE_CLASS:
-        kk = 10 if part == 2 else (11 if kind == 5 else kind)
+        kk = 13 if part == 2 else (14 if kind == 5 else kind)   # the child-sum forget / parent GEMMs
         return f"edbk::big_kernel<{kk}, {t}, {LARGE_CLASS[variant]}>"
     rt, wu, wk = SMALL_VARIANTS[variant]
     return f"edbk::cell_kernel<{kind}, {t}, {rt}, {wu}, {wk}>"
@@ -203,14 +220,23 @@ def cpu_baseline(w, budget_s=12.0):
     OMP_NUM_THREADS when it is set)."""
     from threadpoolctl import threadpool_limits
     from oracle.evaluate import evaluate
+    from oracle.mvrnn import mvrnn
+
+    def forward():
+        if w.aux is not None:   # MV-RNN: the oracle evaluates the trees themselves
+            a = w.aux
+            mvrnn(a["tree_left"], a["tree_right"], a["leaf_vec"], a["leaf_mat"], w.weights[2]["W"].T,
+                  w.weights[2]["b"], w.weights[1]["W_M"].T)
+        else:
+            evaluate(w.kinds, w.op_type, w.child_ptr, w.child_idx, w.x_row, w.x, w.weights, w.hidden,
+                     n_fixed=w.n_children, dtype=w.dtype)
 
     def timed(threads):
         reps, t_total = 0, 0.0
         with threadpool_limits(limits=threads):
             while t_total < budget_s and reps < 20:
                 t0 = time.perf_counter()
-                evaluate(w.kinds, w.op_type, w.child_ptr, w.child_idx, w.x_row, w.x, w.weights, w.hidden,
-                         n_fixed=w.n_children, dtype=w.dtype)
+                forward()
                 t_total += time.perf_counter() - t0
                 reps += 1
         return reps, t_total
@@ -319,7 +345,7 @@ def split_phase(configs, reps=5):
         torch.cuda.empty_cache()
 
 
-DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64}
+DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64, 8: 64}
 
 
 def study(configs, replays=100):
@@ -600,11 +626,21 @@ def main():
     avg_ms = tot_ms / nl
     tflops = (fl / nl) / (avg_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
+    # the MV-RNN matrix-vector launch streams its nodes' matrices: bound by
+    # memory; algorithmic bytes per node = the two vector children and the 2H
+    # matrix columns it reads
+    hbm_bound = dom == (WL.MV_VEC, -1, 1)
+    if hbm_bound:
+        esz_d = 2 if w.dtype == "bf16" else 4
+        rows = sum(inf["m"] for inf in infos[1:] if (inf["kind"], inf["variant"], inf["part"]) == dom)
+        by_launch = rows * (2 * w.hidden + 2) * w.hidden * esz_d / nl
+        gbs = by_launch / (avg_ms * 1e-3) / 1e9
     kname = {0: "LSTM_CHAIN", 1: "NARY_LEAF", 2: "NARY_INTERNAL", 3: "GRID", 4: "CS_LEAF",
-             5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD", 8: "GRU_LEAF", 9: "GRU_INTERNAL"}[dom[0]]
+             5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD", 8: "GRU_LEAF", 9: "GRU_INTERNAL",
+             10: "LINEAR", 11: "MV_MAT", 12: "MV_VEC"}[dom[0]]
     kind_v, var_v, part_v = dom
     if part_v == 1:
-        kernel = "child_reduce_kernel"
+        kernel = "mv_matvec_kernel" if kind_v == WL.MV_VEC else "child_reduce_kernel"
     elif var_v in L.LARGE_VARIANTS:
         kk = "CS_FORGET" if part_v == 2 else ("CS_PARENT" if kind_v == WL.CS_INTERNAL else kname)
         kernel = f"big_kernel<{kk}, {w.dtype}, size class {LARGE_CLASS[var_v]}>"
@@ -634,8 +670,11 @@ def main():
                    "launches_per_step": base.exec.launches(), "mini_batches_in_flight": S,
                    "policy": policy_info, "plan": args.plan,
                    "step": "graph ingest + schedule + memory plan + launch prep + device execution"},
-        "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(tflops / peak, 4), "traffic": traffic,
+        "roofline": ({"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                      "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                      "alg_bytes_per_launch": int(by_launch)} if hbm_bound else
+                     {"bound": "mfma", "achieved": round(tflops, 3), "peak": peak, "unit": "TFLOP/s",
+                      "frac": round(tflops / peak, 4), "traffic": traffic}) | {
                      "kernel": kernel, "symbol": symbol,
                      "launches": nl, "avg_launch_us": round(avg_ms * 1e3, 2),
                      "timing": f"HIP events in the dispatch packets of the {n_profiled} timed steps on worker stream 0",
@@ -648,8 +687,12 @@ def main():
         "launch_us": [round(t * 1e3, 2) for t in times],
     }
     pm = probes(w.dtype)
-    result["roofline"]["peak_measured"] = pm["mfma_tflops"]
-    result["roofline"]["frac_measured"] = round(tflops / pm["mfma_tflops"], 4)
+    if hbm_bound:
+        result["roofline"]["peak_measured"] = pm["copy_gbs"]
+        result["roofline"]["frac_measured"] = round(gbs / pm["copy_gbs"], 4)
+    else:
+        result["roofline"]["peak_measured"] = pm["mfma_tflops"]
+        result["roofline"]["frac_measured"] = round(tflops / pm["mfma_tflops"], 4)
     result["probes"] = pm
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w)

@@ -261,6 +261,23 @@ void edb_plan_free(edb_plan_t* p);
  * h = sigma(z) (h_0 + h_1) / 2 + (1 - sigma(z)) tanh(sigma(r_0) n_0 + sigma(r_1) n_1). */
 #define EDB_CELL_GRU_LEAF      8  /* no children, x;             gates [z,n]              */
 #define EDB_CELL_GRU_INTERNAL  9  /* children [h_0, h_1], no x;  gates [z,r_0,r_1,n_0,n_1] */
+/* MV-RNN (Table 2; every tree node carries a vector and a d x d matrix, d =
+ * hidden).  A node's matrix is held as d graph nodes, node j = column j of
+ * the matrix, so that every state is a row of the arena.  An internal tree
+ * node with left child (a, A) and right child (b, B) has vector
+ * tanh(W [B a ; A b] + b_W) and matrix W_M [A ; B].  All three kinds write h
+ * and (fp32) the same values to c.
+ *   LINEAR: h = x W + b (a leaf's vector and matrix columns, W the identity).
+ *   MV_MAT: children [column j of A, column j of B]; h = [h_0, h_1] W + b
+ *           (W = W_M transposed).
+ *   MV_VEC: children [a, b], then exactly 2H more: the H column nodes of A,
+ *           then the H column nodes of B; h = tanh([B a, A b] W + b) (W = the
+ *           model's W transposed).  B a = sum_j a_j (column j of B) is
+ *           computed by a launch of its own before the GEMM.
+ * The three MV-RNN kinds run in fp32 only (EDB_ERR_UNSUPPORTED for bf16). */
+#define EDB_CELL_LINEAR       10  /* no children, x;             h = x W + b              */
+#define EDB_CELL_MV_MAT       11  /* children [h_0, h_1], no x;  h = [h_0, h_1] W + b     */
+#define EDB_CELL_MV_VEC       12  /* children [a, b] + 2H matrix columns; tanh            */
 
 #define EDB_F32  0  /* W, x, h fp32 */
 #define EDB_BF16 1  /* W, x, h bf16 (round to nearest even); c fp32; fp32 accumulation */
@@ -291,6 +308,9 @@ edb_status edb_packed_weight_bytes(const edb_cell* cell, int64_t* bytes);
  *   GRU_INTERNAL   U[2H x 5H], b[5H]   (the n_0 columns use child 0's rows only,
  *                                       the n_1 columns child 1's; the other
  *                                       blocks of those columns are ignored)
+ *   LINEAR         W[E x H], b[H]
+ *   MV_MAT         W[2H x H], b[H]     (rows: child 0's column, then child 1's)
+ *   MV_VEC         W[2H x H], b[H]     (rows: B a, then A b)
  * bf16 cells round the matrices to bf16 (ties to even); biases stay fp32.
  * packed_dev: device buffer of edb_packed_weight_bytes bytes (caller-owned).
  * The copy is enqueued on `stream` (hipStream_t, NULL = default stream) and
@@ -373,7 +393,8 @@ typedef struct {
     int32_t part;      /* 0: the batch's cell kernel.  A child-sum batch on the large tile runs
                           as three launches in this order: 2 the forget GEMM over its children
                           (m = children), 1 per parent the child sum of h and the sum of the
-                          children's sigma(f_k) c_k, then 0 the parents */
+                          children's sigma(f_k) c_k, then 0 the parents.  An MV_VEC batch runs
+                          as 1 the matrix-vector products [B a, A b], then 0 its GEMM */
 } edb_launch_info;
 edb_status edb_exec_launch_info(const edb_exec_t* e, int32_t i, edb_launch_info* info);
 

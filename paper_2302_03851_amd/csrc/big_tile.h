@@ -237,7 +237,7 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
     // forget GEMM: the children's own cell states.  The parent GEMM: the sums
     // of the children's products sigma(f_k) c_k (one row per parent) ----
     constexpr int HALF = TM / 2;
-    constexpr int NCR = (KIND == K_CS_FORGET || KIND == K_CS_PARENT) ? 1 : NFX;
+    constexpr int NCR = (KIND == K_CS_FORGET || KIND == K_CS_PARENT) ? 1 : (reads_child_c<KIND>() ? NFX : 0);
     static_assert(NCR * HALF * 256 <= SB, "epilogue rows fit the stages");
     const __amdgpu_buffer_rsrc_t rc = KIND == K_CS_PARENT
                                           ? make_rsrc(a.fc, (uint32_t)a.m * (uint32_t)H * 4u)

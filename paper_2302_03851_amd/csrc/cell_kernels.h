@@ -43,9 +43,11 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 enum { K_CHAIN = 0, K_NARY_LEAF = 1, K_NARY_INT = 2, K_GRID = 3, K_CS_LEAF = 4, K_CS_INT = 5,
        K_LAT_CHAR = 6, K_LAT_WORD = 7, K_GRU_LEAF = 8, K_GRU_INT = 9,
+       // MV-RNN: a linear map (leaves), matrix columns, vectors (on rows [B a, A b])
+       K_LINEAR = 10, K_MV_MAT = 11, K_MV_VEC = 12,
        // the two GEMMs of a child-sum batch run on the large tile: the forget
        // gates over the batch's child rows, then the parents on their child sums
-       K_CS_FORGET = 10, K_CS_PARENT = 11 };
+       K_CS_FORGET = 13, K_CS_PARENT = 14 };
 
 enum { S_NONE = 0, S_CONTIG = 1, S_INDEXED = 2 };
 
@@ -91,10 +93,20 @@ template <> struct Kind<K_LAT_WORD> { static constexpr int G = 3, NFIX = 1; stat
 // TreeGRU: the node state is kept in the cell-state arena (children's states read like c rows)
 template <> struct Kind<K_GRU_LEAF> { static constexpr int G = 2, NFIX = 0; static constexpr bool X = true,  RAG = false; };
 template <> struct Kind<K_GRU_INT>  { static constexpr int G = 5, NFIX = 2; static constexpr bool X = false, RAG = false; };
+// MV-RNN.  LINEAR: h = x W + b.  MV_MAT: rows = matrix columns j, operands =
+// column j of the two children's matrices.  MV_VEC: x = the rows [B a, A b]
+// that mv_matvec_kernel computes; h = tanh(x W + b).
+template <> struct Kind<K_LINEAR>   { static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_MV_MAT>   { static constexpr int G = 1, NFIX = 2; static constexpr bool X = false, RAG = false; };
+template <> struct Kind<K_MV_VEC>   { static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
 // rows: the batch's children (x = their h rows); one gate
 template <> struct Kind<K_CS_FORGET>{ static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
 // rows: the parents (x = their child sums of h)
 template <> struct Kind<K_CS_PARENT>{ static constexpr int G = 3, NFIX = 0; static constexpr bool X = true,  RAG = false; };
+
+// Whether the cell update reads its positional children's cell states.
+template <int KIND>
+__host__ __device__ constexpr bool reads_child_c() { return KIND != K_MV_MAT; }
 
 template <typename T> struct Elem;
 template <> struct Elem<float>  { static constexpr int KG = 16; static constexpr int VEC = 4; };
@@ -170,6 +182,12 @@ __device__ __forceinline__ void cell_update(const float* z, const float* cp, flo
         const float ht = tanh_f(fmaf(sigm(z[1]), z[3], sigm(z[2]) * z[4]));
         c = fmaf(sigm(z[0]), fmaf(0.5f, cp[0] + cp[1], -ht), ht);
         h = c;
+    } else if constexpr (KIND == K_LINEAR || KIND == K_MV_MAT) {   // no nonlinearity; c mirrors h
+        h = z[0];
+        c = h;
+    } else if constexpr (KIND == K_MV_VEC) {
+        h = tanh_f(z[0]);
+        c = h;
     } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
         if (nw == 0) {
             c = fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[3]));
@@ -496,7 +514,7 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
         const bool ok = it < NITEM && r < nrows && j < a.H;
 #pragma unroll
         for (int p = 0; p < (NFX > 0 ? NFX : 1); ++p) {
-            const bool use = NFX > p && ok && a.fix[p].kind != S_NONE;
+            const bool use = NFX > p && reads_child_c<KIND>() && ok && a.fix[p].kind != S_NONE;
             cpre[q][p] = *(use ? a.arena_c + (size_t)crow[q][p] * a.H + j : a.arena_c);
         }
     }
@@ -885,7 +903,7 @@ __device__ __forceinline__ void stream_tile(const BatchArgs& a, int rtile, int u
 #pragma unroll
         for (int p = 0; p < (NFX > 0 ? NFX : 1); ++p)
             cpre[q][p] = __uint_as_float(bload32(
-                rc, NFX > p && ok && a.fix[p].kind != S_NONE
+                rc, NFX > p && reads_child_c<KIND>() && ok && a.fix[p].kind != S_NONE
                         ? ((uint32_t)crow[q][p] * (uint32_t)a.H + (uint32_t)j) * 4u
                         : OOB));
     }

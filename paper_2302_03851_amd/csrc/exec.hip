@@ -17,6 +17,7 @@
 #include "big_tile.h"
 #include "cell_kernels.h"
 #include "diag_kernels.h"
+#include "mv_kernels.h"
 #include "edb_internal.h"
 
 using edb::fail;
@@ -64,6 +65,10 @@ KindInfo kind_info(int kind) {
         case EDB_CELL_LAT_WORD: return {3, 1, true, false};
         case EDB_CELL_GRU_LEAF: return {2, 0, true, false};
         case EDB_CELL_GRU_INTERNAL: return {5, 2, false, false};
+        case EDB_CELL_LINEAR: return {1, 0, true, false};
+        case EDB_CELL_MV_MAT: return {1, 2, false, false};
+        // operand lists: the two children's vectors, then 2H matrix columns
+        case EDB_CELL_MV_VEC: return {1, 2, false, true};
         default: return {0, 0, false, false};
     }
 }
@@ -81,7 +86,13 @@ edb_status cell_dims(const edb_cell* c, Dims& d) {
     if (!c) return fail(EDB_ERR_INVALID, "cell is NULL");
     KindInfo ki = kind_info(c->kind);
     if (ki.G == 0) return fail(EDB_ERR_INVALID, "unknown cell kind " + std::to_string(c->kind));
+    // an MV-RNN vector batch's GEMM reads the rows [B a, A b] (2H wide) as its
+    // x operand; its operand lists feed mv_matvec_kernel
+    const bool mv_vec = c->kind == EDB_CELL_MV_VEC;
+    if (mv_vec) ki = KindInfo{1, 0, true, false};
     if (c->dtype != EDB_F32 && c->dtype != EDB_BF16) return fail(EDB_ERR_INVALID, "unknown cell dtype");
+    if ((c->kind == EDB_CELL_LINEAR || c->kind == EDB_CELL_MV_MAT || mv_vec) && c->dtype != EDB_F32)
+        return fail(EDB_ERR_UNSUPPORTED, "the MV-RNN cells (LINEAR, MV_MAT, MV_VEC) run in fp32 only");
     if (c->hidden <= 0) return fail(EDB_ERR_INVALID, "hidden must be positive");
     if (ki.x && c->in_dim <= 0) return fail(EDB_ERR_INVALID, "in_dim must be positive for this cell kind");
     if (c->kind == EDB_CELL_NARY_INTERNAL && c->n_children != 2)
@@ -93,7 +104,7 @@ edb_status cell_dims(const edb_cell* c, Dims& d) {
     d.esz = c->dtype == EDB_F32 ? 4 : 2;
     const int vec = 16 / d.esz;
     d.H = c->hidden;
-    d.E = ki.x ? c->in_dim : 0;
+    d.E = mv_vec ? 2 * c->hidden : ki.x ? c->in_dim : 0;
     if (d.H % vec != 0 || d.E % vec != 0)
         return fail(EDB_ERR_UNSUPPORTED, "hidden and in_dim must be multiples of " + std::to_string(vec) +
                                              " (16-byte rows)");
@@ -339,7 +350,7 @@ void fill_internal(Entry (&e)[2][NUM_VARIANTS]) {
     e[1][16] = big_entry<KIND, __bf16, 4>();
 }
 
-constexpr int NUM_KERNEL_KINDS = 12;   // the 10 cell kinds, then K_CS_FORGET, K_CS_PARENT
+constexpr int NUM_KERNEL_KINDS = 15;   // the 13 cell kinds, then K_CS_FORGET, K_CS_PARENT
 
 struct Table {
     Entry e[NUM_KERNEL_KINDS][2][NUM_VARIANTS];
@@ -354,6 +365,10 @@ struct Table {
         fill_kind<K_LAT_WORD, float>(e[7][0]);     fill_kind<K_LAT_WORD, __bf16>(e[7][1]);
         fill_kind<K_GRU_LEAF, float>(e[8][0]);     fill_kind<K_GRU_LEAF, __bf16>(e[8][1]);
         fill_kind<K_GRU_INT, float>(e[9][0]);      fill_kind<K_GRU_INT, __bf16>(e[9][1]);
+        // the MV-RNN kinds run in fp32 only (cell_dims rejects bf16 for them)
+        fill_kind<K_LINEAR, float>(e[10][0]);
+        fill_kind<K_MV_MAT, float>(e[11][0]);
+        fill_kind<K_MV_VEC, float>(e[12][0]);
         fill_internal<K_CS_FORGET>(e[K_CS_FORGET]);
         fill_internal<K_CS_PARENT>(e[K_CS_PARENT]);
     }
@@ -558,6 +573,8 @@ struct edb_exec {
     void* hsum = nullptr;             // [hsum_rows][H] bf16: child sums of h
     float* racc = nullptr;            // [hsum_rows][H] fp32: per parent, sum of the children's products
     float* fc = nullptr;              // [fc_rows][H] fp32: sigma(f_k) c_k per child
+    int64_t mvu_rows = 0;             // rows of MV-RNN vector batches
+    void* mvu = nullptr;              // [mvu_rows][2H] of the cells' dtype: [B a, A b]
     std::vector<Dims> dims;
     std::vector<edb_cell> cells;
     std::vector<Launch> launches;     // [0] = staging, then one per batch
@@ -636,7 +653,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
         if (cells[t].hidden != H) return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: all types must share hidden");
         if (dtype < 0) dtype = cells[t].dtype;
         if (cells[t].dtype != dtype) return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: all types must share dtype");
-        if (dims[t].x) {
+        if (kind_info(cells[t].kind).x) {   // types reading the caller's x
             if (E < 0) E = dims[t].E;
             if (dims[t].E != E) return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: all input types must share in_dim");
         }
@@ -852,6 +869,31 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                                                      std::to_string(b));
             }
             std::vector<Launch> parts;
+            if (kind_id == EDB_CELL_MV_VEC) {
+                // 1: the matrix-vector products [B a, A b] of every row into
+                // the mvu scratch, then 0: the GEMM with those rows as x
+                const int64_t ro = p->ragged_off[b];
+                for (int32_t r = 0; r < m; ++r)
+                    if (p->ragged_pool[ro + r + 1] - p->ragged_pool[ro + r] != 2 * d.H) {
+                        delete e;
+                        return fail(EDB_ERR_INVALID, "edb_prepare: an MV_VEC node of batch " + std::to_string(b) +
+                                                         " does not list exactly 2 * hidden matrix columns");
+                    }
+                Launch C = L;
+                C.kk = -2;
+                C.lds = 0;
+                C.info.part = 1;
+                C.info.variant = -1;
+                C.info.n_batches = 0;
+                C.info.k = 0;
+                C.info.n = 2 * d.H;
+                C.info.block = 256;
+                C.info.grid = (2 * m + 3) / 4;
+                parts.push_back(C);
+                L.args.x = Seg{S_CONTIG, 0, nullptr};
+                L.off_x = -1;
+                e->mvu_rows = std::max<int64_t>(e->mvu_rows, m);
+            }
             if (is_large(var) && cs_large) {
                 // 2: forget GEMM over the batch's children (rows: the child list): sigma(f_k) c_k
                 Launch F = L;
@@ -942,9 +984,11 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             int b = 0, nrun = 0;
             while (b < B) {
                 const int m0 = s->batch_ptr[b + 1] - s->batch_ptr[b];
-                if (!flow_on || m0 > flow_max_m || blaunch[b].size() != 1) { ++b; continue; }
+                // the dataflow kernel serves the kinds up to TreeGRU
+                auto flow_ok = [&](int q) { return blaunch[q].size() == 1 && blaunch[q][0].kk <= K_GRU_INT; };
+                if (!flow_on || m0 > flow_max_m || !flow_ok(b)) { ++b; continue; }
                 int b1 = b;
-                while (b1 < B && s->batch_ptr[b1 + 1] - s->batch_ptr[b1] <= flow_max_m && blaunch[b1].size() == 1) ++b1;
+                while (b1 < B && s->batch_ptr[b1 + 1] - s->batch_ptr[b1] <= flow_max_m && flow_ok(b1)) ++b1;
                 if (b1 - b >= 2) {
                     for (int q = b; q < b1; ++q) run_of[q] = nrun;
                     ++nrun;
@@ -1121,8 +1165,9 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             const size_t xbytes = (n_x > 0 && !(flags & EDB_X_DIRECT)) ? (size_t)n_x * E * (dtype == EDB_F32 ? 4 : 2) : 0;
             auto al256 = [](size_t v) { return (v + 255) / 256 * 256; };
             const size_t hbytes = al256((size_t)e->hsum_rows * H * 2), rbytes = al256((size_t)e->hsum_rows * H * 4);
-            const size_t fbytes = (size_t)e->fc_rows * H * 4;
-            const size_t total = ibytes + al256(xbytes) + hbytes + rbytes + fbytes;
+            const size_t fbytes = al256((size_t)e->fc_rows * H * 4);
+            const size_t mbytes = (size_t)e->mvu_rows * 2 * H * (dtype == EDB_F32 ? 4 : 2);
+            const size_t total = ibytes + al256(xbytes) + hbytes + rbytes + fbytes + mbytes;
             e->upload = ctx->upload;
             e->release = ctx->release;
             hipError_t he = hipMallocAsync(&e->dmem, total, ctx->upload);
@@ -1139,6 +1184,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 e->hsum = hbytes ? base + ibytes + al256(xbytes) : nullptr;
                 e->racc = rbytes ? reinterpret_cast<float*>(base + ibytes + al256(xbytes) + hbytes) : nullptr;
                 e->fc = fbytes ? reinterpret_cast<float*>(base + ibytes + al256(xbytes) + hbytes + rbytes) : nullptr;
+                e->mvu = mbytes ? base + ibytes + al256(xbytes) + hbytes + rbytes + fbytes : nullptr;
                 he = hipMemcpyAsync(e->dbuf, hb.data(), hb.size() * sizeof(int32_t), hipMemcpyHostToDevice, ctx->upload);
             }
             if (he == hipSuccess) he = hipEventCreateWithFlags(&e->ready, hipEventDisableTiming);
@@ -1292,6 +1338,15 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
         }
         BatchArgs a = resolve_args(e, L, w, x, arena_h, arena_c);
         hipEvent_t e0 = prof ? ev[2 * i] : nullptr, e1 = prof ? ev[2 * i + 1] : nullptr;
+        if (L.kk == -2) {   // MV-RNN vector batch: [B a, A b] into the mvu scratch
+            const dim3 grid(L.info.grid), blk(256);
+            {   // fp32 only (cell_dims)
+                float* out = reinterpret_cast<float*>(e->mvu);
+                if (prof) hipExtLaunchKernelGGL(mv_matvec_kernel<float>, grid, blk, 0, st, e0, e1, 0, a, out);
+                else hipLaunchKernelGGL(mv_matvec_kernel<float>, grid, blk, 0, st, a, out);
+            }
+            continue;
+        }
         if (L.kk < 0) {   // child-sum batch on the large tile: child sums and product sums
             __bf16* out = reinterpret_cast<__bf16*>(e->hsum);
             if (prof)
@@ -1306,6 +1361,9 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
             a.bias = a.br;
             a.xmat = arena_h;
             a.n_xrows = e->n_slots;
+        } else if (L.kk == K_MV_VEC) {   // rows: [B a, A b] from the matrix-vector launch
+            a.xmat = e->mvu;
+            a.n_xrows = a.m;
         } else if (L.kk == K_CS_PARENT) {   // rows: the child sums; epilogue: the product sums
             a.xmat = e->hsum;
             a.n_xrows = a.m;

@@ -48,11 +48,16 @@ LAT_CHAR = 6
 LAT_WORD = 7
 GRU_LEAF = 8
 GRU_INTERNAL = 9
+# MV-RNN: each tree node's d x d matrix is held as d nodes, node j = column j
+LINEAR = 10
+MV_MAT = 11
+MV_VEC = 12
 
 KIND_NAMES = {
     LSTM_CHAIN: "lstm_chain", NARY_LEAF: "nary_leaf", NARY_INTERNAL: "nary_internal",
     GRID: "grid", CS_LEAF: "cs_leaf", CS_INTERNAL: "cs_internal",
     LAT_CHAR: "lat_char", LAT_WORD: "lat_word", GRU_LEAF: "gru_leaf", GRU_INTERNAL: "gru_internal",
+    LINEAR: "linear", MV_MAT: "mv_mat", MV_VEC: "mv_vec",
 }
 
 # Per kind: (n_fixed children, ragged children allowed, has x input).
@@ -67,6 +72,9 @@ KIND_SHAPE = {
     LAT_WORD: (1, False, True),
     GRU_LEAF: (0, False, True),
     GRU_INTERNAL: (2, False, False),
+    LINEAR: (0, False, True),
+    MV_MAT: (2, False, False),
+    MV_VEC: (2, True, False),
 }
 
 
@@ -85,6 +93,9 @@ def weight_shapes(kind: int, E: int, H: int, n_children: int = 2) -> List[Tuple[
       LAT_CHAR       W_c[(E+H) x 4H] gates [i, f, o, u];  W_lx[E x H];  W_lc[H x H]
       GRU_LEAF       W[E x 2H]      gates [z, n]
       GRU_INTERNAL   U[2H x 5H]     gates [z, r_0, r_1, n_0, n_1] (n_k reads child k only)
+      LINEAR         W[E x H]       h = x W + b
+      MV_MAT         W_M[2H x H]    rows: column j of the left matrix, then of the right (W_M transposed)
+      MV_VEC         W[2H x H]      rows: [B a ; A b] (the model's W transposed), tanh
     Biases follow the matrices (float32).
     """
     if kind == LSTM_CHAIN:
@@ -107,6 +118,12 @@ def weight_shapes(kind: int, E: int, H: int, n_children: int = 2) -> List[Tuple[
         return [("W", (E, 2 * H)), ("b", (2 * H,))]
     if kind == GRU_INTERNAL:
         return [("W", (2 * H, 5 * H)), ("b", (5 * H,))]
+    if kind == LINEAR:
+        return [("W", (E, H)), ("b", (H,))]
+    if kind == MV_MAT:
+        return [("W_M", (2 * H, H)), ("b", (H,))]
+    if kind == MV_VEC:
+        return [("W", (2 * H, H)), ("b", (H,))]
     raise ValueError(f"unknown cell kind {kind}")
 
 
@@ -125,6 +142,7 @@ class Workload:
     weights: List[Dict[str, np.ndarray]]  # per type id, float32 logical matrices
     n_children: List[int]           # N for NARY_INTERNAL types (0 otherwise)
     instances: int
+    aux: Optional[Dict[str, np.ndarray]] = None   # model-level view (MV-RNN: trees and weights)
 
     @property
     def n_nodes(self) -> int:
@@ -245,12 +263,13 @@ CONFIG_NAMES = {
     5: "childsum_treelstm_h512_bf16",
     6: "treelstm_2type_h256_f32",
     7: "binary_treegru_h256_f32",
+    8: "mvrnn_d64_f32",
 }
 
 
 def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = None) -> Workload:
     """Build synthetic config k (1..5; 6 is the two-internal-type TreeLSTM of
-    the batching study, 7 the binary TreeGRU).  `instances` overrides the number of
+    the batching study, 7 the binary TreeGRU, 8 the MV-RNN).  `instances` overrides the number of
     instance graphs (chains / trees / lattices / grids) for small test cases
     and scale sweeps; all other sizes and distributions stay as stated."""
     if seed is None:
@@ -346,8 +365,10 @@ def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = N
         for _ in range(inst):
             n = int(rng.integers(10, 51))
             _build_binary(rng, n, g)
+    elif k == 8:
+        return _mvrnn_config(rng, 64 if instances is None else instances)
     else:
-        raise ValueError("config index must be 1..7")
+        raise ValueError("config index must be 1..8")
 
     op_type, ptr, idx, x_row, n_x = g.finish()
     weights = _draw_weights(rng, kinds, E, H, scale, n_children, bf16)
@@ -358,6 +379,64 @@ def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = N
         name=CONFIG_NAMES[k], dtype="bf16" if bf16 else "f32", kinds=kinds,
         in_dim=E, hidden=H, op_type=op_type, child_ptr=ptr, child_idx=idx,
         x_row=x_row, x=x, weights=weights, n_children=n_children, instances=inst)
+
+
+def _mvrnn_config(rng, inst: int, d: int = 64) -> Workload:
+    """MV-RNN over binary trees drawn as in config 2 (leaves U{10..50}), d = 64,
+    fp32.  Every tree node becomes d matrix-column nodes (type 1, MV_MAT; leaf:
+    type 0, LINEAR) followed by one vector node (type 2, MV_VEC; leaf: type 0).
+    Draws: (1) the tree shapes; (2) W_M = [I I] / 2 + U(-0.05, 0.05) (d x 2d)
+    and W ~ U(-0.1, 0.1) (d x 2d), row-major; biases 0, the leaf LINEAR
+    weights are the identity; (3) per leaf in node order its vector ~ N(0, 1),
+    then its matrix I + U(-0.1, 0.1) (row-major).  Word vectors and matrices
+    follow the initialisation the model's authors describe (matrices near the
+    identity)."""
+    tb = _GraphBuilder()
+    for _ in range(inst):
+        _build_binary(rng, int(rng.integers(10, 51)), tb)
+    n_tree = len(tb.op_type)
+    left = np.array([c[0] if c else -1 for c in tb.children], dtype=np.int64)
+    right = np.array([c[1] if c else -1 for c in tb.children], dtype=np.int64)
+    WM = np.concatenate([np.eye(d), np.eye(d)], axis=1) / 2 + rng.uniform(-0.05, 0.05, size=(d, 2 * d))
+    WM = WM.astype(np.float32)
+    W = rng.uniform(-0.1, 0.1, size=(d, 2 * d)).astype(np.float32)
+    leaf_vec = np.zeros((n_tree, d), dtype=np.float32)
+    leaf_mat = np.zeros((n_tree, d, d), dtype=np.float32)
+    for t in range(n_tree):
+        if left[t] < 0:
+            leaf_vec[t] = rng.standard_normal(size=d, dtype=np.float32)
+            leaf_mat[t] = np.eye(d, dtype=np.float32) + rng.uniform(-0.1, 0.1, size=(d, d)).astype(np.float32)
+    g = _GraphBuilder()
+    vec_node = np.zeros(n_tree, dtype=np.int64)
+    mat_node = np.zeros(n_tree, dtype=np.int64)   # first of the d column nodes
+    xs = []
+    for t in range(n_tree):
+        l, r = int(left[t]), int(right[t])
+        if l < 0:
+            mat_node[t] = g.add(0, [], True)
+            xs.append(leaf_mat[t][:, 0])
+            for j in range(1, d):
+                g.add(0, [], True)
+                xs.append(leaf_mat[t][:, j])
+            vec_node[t] = g.add(0, [], True)
+            xs.append(leaf_vec[t])
+        else:
+            ml, mr = int(mat_node[l]), int(mat_node[r])
+            mat_node[t] = g.add(1, [ml, mr], False)
+            for j in range(1, d):
+                g.add(1, [ml + j, mr + j], False)
+            cols = [ml + j for j in range(d)] + [mr + j for j in range(d)]
+            vec_node[t] = g.add(2, [int(vec_node[l]), int(vec_node[r])] + cols, False)
+    op_type, ptr, idx, x_row, n_x = g.finish()
+    weights = [{"W": np.eye(d, dtype=np.float32), "b": np.zeros(d, dtype=np.float32)},
+               {"W_M": np.ascontiguousarray(WM.T), "b": np.zeros(d, dtype=np.float32)},
+               {"W": np.ascontiguousarray(W.T), "b": np.zeros(d, dtype=np.float32)}]
+    aux = {"tree_left": left, "tree_right": right, "vec_node": vec_node, "mat_node": mat_node,
+           "leaf_vec": leaf_vec, "leaf_mat": leaf_mat, "W": W, "bW": np.zeros(d, dtype=np.float32), "WM": WM}
+    return Workload(name=CONFIG_NAMES[8], dtype="f32", kinds=[LINEAR, MV_MAT, MV_VEC], in_dim=d, hidden=d,
+                    op_type=op_type, child_ptr=ptr, child_idx=idx, x_row=x_row,
+                    x=np.stack(xs).astype(np.float32), weights=weights, n_children=[0, 0, 0], instances=inst,
+                    aux=aux)
 
 
 def make_graph(kinds: List[int], E: int, H: int, op_type, children: List[List[int]],
