@@ -25,4 +25,6 @@ Contents
   compare   the normwise relative error used by the parity tests
   mvrnn     the MV-RNN of Table 2 on binary trees (a vector and a matrix per
             node), evaluated on the tree itself
+  latticegru  the lattice GRU of Table 2 (per-edge GRU proposals averaged per
+            position), evaluated on the lattice itself
 """
