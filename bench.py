@@ -38,6 +38,7 @@ WORKLOAD_TEXT = {
     6: "binary TreeLSTM with two internal cell types forward fp32: 64 trees, leaves U[10,50], E=H=256",
     7: "binary TreeGRU forward fp32: 64 trees, leaves U[10,50], E=H=256",
     8: "MV-RNN forward fp32: 64 binary trees, leaves U[10,50], d=64 (a vector and a d x d matrix per node)",
+    9: "lattice GRU forward fp32: 32 lattices, lengths U[20,60], word p=0.3 span 2-4, E=100, H=200",
 }
 
 
@@ -53,7 +54,7 @@ def algorithmic_work(w, f):
     esz = 2 if w.dtype == "bf16" else 4
     G = {WL.LSTM_CHAIN: 4, WL.NARY_LEAF: 3, WL.NARY_INTERNAL: 5, WL.GRID: 5, WL.CS_LEAF: 3,
          WL.CS_INTERNAL: 3, WL.LAT_CHAR: 4, WL.LAT_WORD: 3, WL.GRU_LEAF: 2, WL.GRU_INTERNAL: 3,
-         WL.LINEAR: 1, WL.MV_MAT: 1, WL.MV_VEC: 1}
+         WL.LINEAR: 1, WL.MV_MAT: 1, WL.MV_VEC: 1, WL.LGRU_EDGE: 3, WL.POOL_MEAN: 1}
     mv = (WL.LINEAR, WL.MV_MAT, WL.MV_VEC)
     # an identity LINEAR map (an MV-RNN leaf) is no work
     ident = [w.kinds[t] == WL.LINEAR and w.weights[t]["W"].shape[0] == w.weights[t]["W"].shape[1] and
@@ -79,6 +80,12 @@ def algorithmic_work(w, f):
                 flr += 2 * H * H * len(rag)                # x W_lx, c_w W_lc
             if k == WL.GRU_INTERNAL:
                 fl += 2 * H * H * len(fixed)               # each candidate n_k reads its own child
+            if k == WL.POOL_MEAN:
+                # the mean of the edges' states (an identity map is no work)
+                if not np.array_equal(w.weights[t]["W"], np.eye(H, dtype=np.float32)):
+                    fl += 2 * H * H
+                by += len(rag) * H * esz + H * esz
+                continue
             if k in mv:
                 # MV-RNN: h rows only (c mirrors h); the vector cell's two d x d
                 # matrix-vector products count as per-child work
@@ -126,7 +133,7 @@ def kernel_symbol(kind, dtype, variant, part):
         rt, wk = STREAM_SHAPES[variant]
         return f"edbk::stream_kernel<{kind}, {t}, {rt}, {wk}>"
     if variant in LARGE_CLASS:
-        kk = 13 if part == 2 else (14 if kind == 5 else kind)   # the child-sum forget / parent GEMMs
+        kk = 15 if part == 2 else (16 if kind == 5 else kind)   # the child-sum forget / parent GEMMs
         return f"edbk::big_kernel<{kk}, {t}, {LARGE_CLASS[variant]}>"
     rt, wu, wk = SMALL_VARIANTS[variant]
     return f"edbk::cell_kernel<{kind}, {t}, {rt}, {wu}, {wk}>"
@@ -221,9 +228,16 @@ def cpu_baseline(w, budget_s=12.0):
     from threadpoolctl import threadpool_limits
     from oracle.evaluate import evaluate
     from oracle.mvrnn import mvrnn
+    from oracle.latticegru import lattice_gru
 
     def forward():
-        if w.aux is not None:   # MV-RNN: the oracle evaluates the trees themselves
+        if w.aux is not None and "lattices" in w.aux:   # lattice GRU: the oracle runs the lattices
+            a = w.aux
+            for lat in a["lattices"]:
+                lattice_gru(lat["length"], lat["words"], w.x[w.x_row[lat["char_edge"]]],
+                            w.x[w.x_row[lat["word_edge"]]] if len(lat["words"]) else np.zeros((0, w.in_dim)),
+                            a["Wx"], a["Wh"], a["bx"], a["bhn"])
+        elif w.aux is not None:   # MV-RNN: the oracle evaluates the trees themselves
             a = w.aux
             mvrnn(a["tree_left"], a["tree_right"], a["leaf_vec"], a["leaf_mat"], w.weights[2]["W"].T,
                   w.weights[2]["b"], w.weights[1]["W_M"].T)
@@ -345,7 +359,7 @@ def split_phase(configs, reps=5):
         torch.cuda.empty_cache()
 
 
-DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64, 8: 64}
+DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64, 8: 64, 9: 32}
 
 
 def study(configs, replays=100):
@@ -626,18 +640,22 @@ def main():
     avg_ms = tot_ms / nl
     tflops = (fl / nl) / (avg_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
-    # the MV-RNN matrix-vector launch streams its nodes' matrices: bound by
-    # memory; algorithmic bytes per node = the two vector children and the 2H
-    # matrix columns it reads
-    hbm_bound = dom == (WL.MV_VEC, -1, 1)
+    # Launches with no algorithmic flops are bound by memory: the MV-RNN
+    # matrix-vector launch (bytes per node: the two vector children and the 2H
+    # matrix columns it reads) and a mean over children through the identity
+    # map (the batch's algorithmic bytes)
+    hbm_bound = dom == (WL.MV_VEC, -1, 1) or fl == 0
     if hbm_bound:
         esz_d = 2 if w.dtype == "bf16" else 4
-        rows = sum(inf["m"] for inf in infos[1:] if (inf["kind"], inf["variant"], inf["part"]) == dom)
-        by_launch = rows * (2 * w.hidden + 2) * w.hidden * esz_d / nl
+        grp = [inf for inf in infos[1:] if (inf["kind"], inf["variant"], inf["part"]) == dom]
+        if dom == (WL.MV_VEC, -1, 1):
+            by_launch = sum(inf["m"] for inf in grp) * (2 * w.hidden + 2) * w.hidden * esz_d / nl
+        else:
+            by_launch = sum(work[inf["batch"]][2] for inf in grp) / nl
         gbs = by_launch / (avg_ms * 1e-3) / 1e9
     kname = {0: "LSTM_CHAIN", 1: "NARY_LEAF", 2: "NARY_INTERNAL", 3: "GRID", 4: "CS_LEAF",
              5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD", 8: "GRU_LEAF", 9: "GRU_INTERNAL",
-             10: "LINEAR", 11: "MV_MAT", 12: "MV_VEC"}[dom[0]]
+             10: "LINEAR", 11: "MV_MAT", 12: "MV_VEC", 13: "LGRU_EDGE", 14: "POOL_MEAN"}[dom[0]]
     kind_v, var_v, part_v = dom
     if part_v == 1:
         kernel = "mv_matvec_kernel" if kind_v == WL.MV_VEC else "child_reduce_kernel"

@@ -278,6 +278,17 @@ void edb_plan_free(edb_plan_t* p);
 #define EDB_CELL_LINEAR       10  /* no children, x;             h = x W + b              */
 #define EDB_CELL_MV_MAT       11  /* children [h_0, h_1], no x;  h = [h_0, h_1] W + b     */
 #define EDB_CELL_MV_VEC       12  /* children [a, b] + 2H matrix columns; tanh            */
+/* Lattice GRU (Table 2): every incoming edge of a lattice position proposes a
+ * GRU step (reset gate after the recurrent product) from its source position's
+ * state with its own input; the position's state is the mean of the
+ * proposals.  Both kinds write h and (fp32) the same values to c; the edge
+ * reads its source's state from the c arena.  fp32 only.
+ *   LGRU_EDGE: child [source position], x; gates [z, r, n_x, n_h];
+ *              h = (1 - sigma(z)) n + sigma(z) h_src, n = tanh(n_x + sigma(r) n_h).
+ *   POOL_MEAN: ragged children (the edges), no x; h = ((sum of their h) W + b) / count
+ *              (W the identity for the mean). */
+#define EDB_CELL_LGRU_EDGE    13  /* [source], x;                gates [z,r,n_x,n_h]      */
+#define EDB_CELL_POOL_MEAN    14  /* ragged children, no x;      mean of their h, then W  */
 
 #define EDB_F32  0  /* W, x, h fp32 */
 #define EDB_BF16 1  /* W, x, h bf16 (round to nearest even); c fp32; fp32 accumulation */
@@ -311,6 +322,9 @@ edb_status edb_packed_weight_bytes(const edb_cell* cell, int64_t* bytes);
  *   LINEAR         W[E x H], b[H]
  *   MV_MAT         W[2H x H], b[H]     (rows: child 0's column, then child 1's)
  *   MV_VEC         W[2H x H], b[H]     (rows: B a, then A b)
+ *   LGRU_EDGE      W[(E+H) x 4H], b[4H] (n_x's columns use the x rows only, n_h's
+ *                                       the source rows only; b of n_h = b_hn)
+ *   POOL_MEAN      W[H x H], b[H]
  * bf16 cells round the matrices to bf16 (ties to even); biases stay fp32.
  * packed_dev: device buffer of edb_packed_weight_bytes bytes (caller-owned).
  * The copy is enqueued on `stream` (hipStream_t, NULL = default stream) and

@@ -45,9 +45,11 @@ enum { K_CHAIN = 0, K_NARY_LEAF = 1, K_NARY_INT = 2, K_GRID = 3, K_CS_LEAF = 4, 
        K_LAT_CHAR = 6, K_LAT_WORD = 7, K_GRU_LEAF = 8, K_GRU_INT = 9,
        // MV-RNN: a linear map (leaves), matrix columns, vectors (on rows [B a, A b])
        K_LINEAR = 10, K_MV_MAT = 11, K_MV_VEC = 12,
+       // lattice GRU: an edge's GRU proposal, a position's mean over its edges
+       K_LGRU_EDGE = 13, K_POOL_MEAN = 14,
        // the two GEMMs of a child-sum batch run on the large tile: the forget
        // gates over the batch's child rows, then the parents on their child sums
-       K_CS_FORGET = 13, K_CS_PARENT = 14 };
+       K_CS_FORGET = 15, K_CS_PARENT = 16 };
 
 enum { S_NONE = 0, S_CONTIG = 1, S_INDEXED = 2 };
 
@@ -99,6 +101,11 @@ template <> struct Kind<K_GRU_INT>  { static constexpr int G = 5, NFIX = 2; stat
 template <> struct Kind<K_LINEAR>   { static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
 template <> struct Kind<K_MV_MAT>   { static constexpr int G = 1, NFIX = 2; static constexpr bool X = false, RAG = false; };
 template <> struct Kind<K_MV_VEC>   { static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
+// Lattice GRU.  LGRU_EDGE: gates [z, r, n_x, n_h] over [x ; h_src] (n_x reads
+// x only, n_h the source's h only).  POOL_MEAN: A = the sum of the ragged
+// children's h (staged like a child-sum node), h = (A W + b) / children.
+template <> struct Kind<K_LGRU_EDGE>{ static constexpr int G = 4, NFIX = 1; static constexpr bool X = true,  RAG = false; };
+template <> struct Kind<K_POOL_MEAN>{ static constexpr int G = 1, NFIX = 0; static constexpr bool X = false, RAG = false; };
 // rows: the batch's children (x = their h rows); one gate
 template <> struct Kind<K_CS_FORGET>{ static constexpr int G = 1, NFIX = 0; static constexpr bool X = true,  RAG = false; };
 // rows: the parents (x = their child sums of h)
@@ -107,6 +114,9 @@ template <> struct Kind<K_CS_PARENT>{ static constexpr int G = 3, NFIX = 0; stat
 // Whether the cell update reads its positional children's cell states.
 template <int KIND>
 __host__ __device__ constexpr bool reads_child_c() { return KIND != K_MV_MAT; }
+// Kinds whose A operand is the sum of the ragged children's h rows.
+template <int KIND>
+__host__ __device__ constexpr bool sums_children() { return KIND == K_CS_INT || KIND == K_POOL_MEAN; }
 
 template <typename T> struct Elem;
 template <> struct Elem<float>  { static constexpr int KG = 16; static constexpr int VEC = 4; };
@@ -188,6 +198,13 @@ __device__ __forceinline__ void cell_update(const float* z, const float* cp, flo
     } else if constexpr (KIND == K_MV_VEC) {
         h = tanh_f(z[0]);
         c = h;
+    } else if constexpr (KIND == K_LGRU_EDGE) {   // gates [z, r, n_x, n_h]; cp: the source position's state
+        const float ht = tanh_f(fmaf(sigm(z[1]), z[3], z[2]));
+        c = fmaf(sigm(z[0]), cp[0] - ht, ht);
+        h = c;
+    } else if constexpr (KIND == K_POOL_MEAN) {   // nw: the position's edges
+        c = nw > 0 ? z[0] / (float)nw : 0.f;
+        h = c;
     } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
         if (nw == 0) {
             c = fmaf(sigm(z[1]), cp[0], sig_tanh(z[0], z[3]));
@@ -520,7 +537,7 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
     }
 
     // ---- 3. stage the A tile: [x | child h ...] or [child sum of h] ----
-    if constexpr (KIND == K_CS_INT) {
+    if constexpr (sums_children<KIND>()) {
         stage_child_sum<T, TM, NT>(A, AS, a, row0, nrows, tid);
     } else {
         constexpr int NSEG = (KT::X ? 1 : 0) + NFX;
@@ -721,7 +738,8 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
         if (it >= NITEM || r >= nrows || j >= a.H) continue;
         float c, h;
         cell_update<KIND>(zsum[q], cpre[q], racc[q], rden[q],
-                          KIND == K_LAT_CHAR ? a.rag_ptr[row0 + r + 1] - a.rag_ptr[row0 + r] : 0, c, h);
+                          KIND == K_LAT_CHAR || KIND == K_POOL_MEAN ? a.rag_ptr[row0 + r + 1] - a.rag_ptr[row0 + r] : 0,
+                          c, h);
         const size_t o = (size_t)rres[q] * a.H + j;
         a.arena_c[o] = c;
         Hout[o] = from_f<T>(h);

@@ -69,6 +69,8 @@ KindInfo kind_info(int kind) {
         case EDB_CELL_MV_MAT: return {1, 2, false, false};
         // operand lists: the two children's vectors, then 2H matrix columns
         case EDB_CELL_MV_VEC: return {1, 2, false, true};
+        case EDB_CELL_LGRU_EDGE: return {4, 1, true, false};
+        case EDB_CELL_POOL_MEAN: return {1, 0, false, true};
         default: return {0, 0, false, false};
     }
 }
@@ -90,9 +92,14 @@ edb_status cell_dims(const edb_cell* c, Dims& d) {
     // x operand; its operand lists feed mv_matvec_kernel
     const bool mv_vec = c->kind == EDB_CELL_MV_VEC;
     if (mv_vec) ki = KindInfo{1, 0, true, false};
+    // a pooling node's GEMM reads the sum of its ragged children (no ragged weights)
+    const bool pool = c->kind == EDB_CELL_POOL_MEAN;
+    if (pool) ki = KindInfo{1, 0, false, false};
     if (c->dtype != EDB_F32 && c->dtype != EDB_BF16) return fail(EDB_ERR_INVALID, "unknown cell dtype");
     if ((c->kind == EDB_CELL_LINEAR || c->kind == EDB_CELL_MV_MAT || mv_vec) && c->dtype != EDB_F32)
         return fail(EDB_ERR_UNSUPPORTED, "the MV-RNN cells (LINEAR, MV_MAT, MV_VEC) run in fp32 only");
+    if ((c->kind == EDB_CELL_LGRU_EDGE || pool) && c->dtype != EDB_F32)
+        return fail(EDB_ERR_UNSUPPORTED, "the lattice GRU cells (LGRU_EDGE, POOL_MEAN) run in fp32 only");
     if (c->hidden <= 0) return fail(EDB_ERR_INVALID, "hidden must be positive");
     if (ki.x && c->in_dim <= 0) return fail(EDB_ERR_INVALID, "in_dim must be positive for this cell kind");
     if (c->kind == EDB_CELL_NARY_INTERNAL && c->n_children != 2)
@@ -112,7 +119,7 @@ edb_status cell_dims(const edb_cell* c, Dims& d) {
     d.Hk = round_up(d.H, d.KG);
     d.Ep = ki.x ? round_up(d.E, d.KG) : 0;
     d.Hu = round_up(d.H, 64);
-    if (c->kind == EDB_CELL_CS_INTERNAL) d.K = d.Hk;
+    if (c->kind == EDB_CELL_CS_INTERNAL || pool) d.K = d.Hk;
     else d.K = d.Ep + ki.nfix * d.Hk;
     const int64_t wmain = (int64_t)(d.Hu / 16) * d.G * (d.K / d.KG) * 64 * 16;
     const int64_t bmain = (int64_t)d.G * d.Hu * 4;
@@ -209,6 +216,8 @@ extern "C" edb_status edb_pack_weights(const edb_cell* cell, const float* const*
         if (kind == EDB_CELL_LAT_CHAR && g == 4) return row < d.E ? Wlx[(int64_t)row * H + j] : 0.f;
         // TreeGRU candidates: n_0 reads only child 0's rows, n_1 only child 1's
         if (kind == EDB_CELL_GRU_INTERNAL && ((g == 3 && row >= H) || (g == 4 && row < H))) return 0.f;
+        // lattice GRU edge: n_x reads only x's rows, n_h only the source state's
+        if (kind == EDB_CELL_LGRU_EDGE && ((g == 2 && row >= d.E) || (g == 3 && row < d.E))) return 0.f;
         return W[(int64_t)row * ncol + g * H + j];
     });
     float* bias = reinterpret_cast<float*>(buf.data() + d.off_b);
@@ -283,7 +292,7 @@ int lds_big(int) { return big_lds_bytes<KIND, VB>(); }
 
 template <int KIND, typename T, int VB>
 Entry big_entry() {
-    if constexpr (!Kind<KIND>::RAG)
+    if constexpr (!Kind<KIND>::RAG && !sums_children<KIND>())
         return {launch_big<KIND, T, VB>, attr_big<KIND, VB>, lds_big<KIND, VB>,
                 reinterpret_cast<const void*>(&big_kernel<KIND, T, VB>)};
     else return {nullptr, nullptr, nullptr, nullptr};
@@ -307,7 +316,7 @@ int lds_stream(int) { return stream_lds_bytes<KIND, T, RT, WK>(); }
 // the streamed tile serves the kinds without a ragged phase
 template <int KIND, typename T, int RT, int WK>
 Entry stream_entry() {
-    if constexpr (Kind<KIND>::RAG) return {nullptr, nullptr, nullptr, nullptr};
+    if constexpr (Kind<KIND>::RAG || sums_children<KIND>()) return {nullptr, nullptr, nullptr, nullptr};
     else
         return {launch_stream<KIND, T, RT, WK>, attr_stream<KIND, T, RT, WK>, lds_stream<KIND, T, RT, WK>,
                 reinterpret_cast<const void*>(&stream_kernel<KIND, T, RT, WK>)};
@@ -350,7 +359,7 @@ void fill_internal(Entry (&e)[2][NUM_VARIANTS]) {
     e[1][16] = big_entry<KIND, __bf16, 4>();
 }
 
-constexpr int NUM_KERNEL_KINDS = 15;   // the 13 cell kinds, then K_CS_FORGET, K_CS_PARENT
+constexpr int NUM_KERNEL_KINDS = 17;   // the 15 cell kinds, then K_CS_FORGET, K_CS_PARENT
 
 struct Table {
     Entry e[NUM_KERNEL_KINDS][2][NUM_VARIANTS];
@@ -369,6 +378,9 @@ struct Table {
         fill_kind<K_LINEAR, float>(e[10][0]);
         fill_kind<K_MV_MAT, float>(e[11][0]);
         fill_kind<K_MV_VEC, float>(e[12][0]);
+        // the lattice GRU kinds run in fp32 only; the pooling node on the staged tile only
+        fill_kind<K_LGRU_EDGE, float>(e[13][0]);
+        fill_kind<K_POOL_MEAN, float>(e[14][0]);
         fill_internal<K_CS_FORGET>(e[K_CS_FORGET]);
         fill_internal<K_CS_PARENT>(e[K_CS_PARENT]);
     }

@@ -52,12 +52,15 @@ GRU_INTERNAL = 9
 LINEAR = 10
 MV_MAT = 11
 MV_VEC = 12
+# lattice GRU: one GRU proposal per incoming edge, averaged per position
+LGRU_EDGE = 13
+POOL_MEAN = 14
 
 KIND_NAMES = {
     LSTM_CHAIN: "lstm_chain", NARY_LEAF: "nary_leaf", NARY_INTERNAL: "nary_internal",
     GRID: "grid", CS_LEAF: "cs_leaf", CS_INTERNAL: "cs_internal",
     LAT_CHAR: "lat_char", LAT_WORD: "lat_word", GRU_LEAF: "gru_leaf", GRU_INTERNAL: "gru_internal",
-    LINEAR: "linear", MV_MAT: "mv_mat", MV_VEC: "mv_vec",
+    LINEAR: "linear", MV_MAT: "mv_mat", MV_VEC: "mv_vec", LGRU_EDGE: "lgru_edge", POOL_MEAN: "pool_mean",
 }
 
 # Per kind: (n_fixed children, ragged children allowed, has x input).
@@ -75,6 +78,8 @@ KIND_SHAPE = {
     LINEAR: (0, False, True),
     MV_MAT: (2, False, False),
     MV_VEC: (2, True, False),
+    LGRU_EDGE: (1, False, True),
+    POOL_MEAN: (0, True, False),
 }
 
 
@@ -96,6 +101,8 @@ def weight_shapes(kind: int, E: int, H: int, n_children: int = 2) -> List[Tuple[
       LINEAR         W[E x H]       h = x W + b
       MV_MAT         W_M[2H x H]    rows: column j of the left matrix, then of the right (W_M transposed)
       MV_VEC         W[2H x H]      rows: [B a ; A b] (the model's W transposed), tanh
+      LGRU_EDGE      W[(E+H) x 4H]  gates [z, r, n_x, n_h] (n_x reads x only, n_h the source h only)
+      POOL_MEAN      W[H x H]       h = (mean of the ragged children's h) W + b
     Biases follow the matrices (float32).
     """
     if kind == LSTM_CHAIN:
@@ -124,6 +131,10 @@ def weight_shapes(kind: int, E: int, H: int, n_children: int = 2) -> List[Tuple[
         return [("W_M", (2 * H, H)), ("b", (H,))]
     if kind == MV_VEC:
         return [("W", (2 * H, H)), ("b", (H,))]
+    if kind == LGRU_EDGE:
+        return [("W", (E + H, 4 * H)), ("b", (4 * H,))]
+    if kind == POOL_MEAN:
+        return [("W", (H, H)), ("b", (H,))]
     raise ValueError(f"unknown cell kind {kind}")
 
 
@@ -264,12 +275,13 @@ CONFIG_NAMES = {
     6: "treelstm_2type_h256_f32",
     7: "binary_treegru_h256_f32",
     8: "mvrnn_d64_f32",
+    9: "lattice_gru_f32",
 }
 
 
 def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = None) -> Workload:
     """Build synthetic config k (1..5; 6 is the two-internal-type TreeLSTM of
-    the batching study, 7 the binary TreeGRU, 8 the MV-RNN).  `instances` overrides the number of
+    the batching study, 7 the binary TreeGRU, 8 the MV-RNN, 9 the lattice GRU).  `instances` overrides the number of
     instance graphs (chains / trees / lattices / grids) for small test cases
     and scale sweeps; all other sizes and distributions stay as stated."""
     if seed is None:
@@ -367,8 +379,10 @@ def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = N
             _build_binary(rng, n, g)
     elif k == 8:
         return _mvrnn_config(rng, 64 if instances is None else instances)
+    elif k == 9:
+        return _lattice_gru_config(rng, 32 if instances is None else instances)
     else:
-        raise ValueError("config index must be 1..8")
+        raise ValueError("config index must be 1..9")
 
     op_type, ptr, idx, x_row, n_x = g.finish()
     weights = _draw_weights(rng, kinds, E, H, scale, n_children, bf16)
@@ -437,6 +451,63 @@ def _mvrnn_config(rng, inst: int, d: int = 64) -> Workload:
                     op_type=op_type, child_ptr=ptr, child_idx=idx, x_row=x_row,
                     x=np.stack(xs).astype(np.float32), weights=weights, n_children=[0, 0, 0], instances=inst,
                     aux=aux)
+
+
+def _lattice_gru_config(rng, inst: int, E: int = 100, H: int = 200) -> Workload:
+    """Lattice GRU over lattices drawn as in config 3 (lengths U{20..60}; at
+    each start position a word with probability 0.3 spanning U{2,3,4}
+    characters, dropped past the end), E = 100, H = 200, fp32.  Per position
+    j: its character-edge node (type 0, LGRU_EDGE; x = the character's input,
+    source = position j-1), one word-edge node (type 0; x = the word's input,
+    source = the position before the word's first character) per word ending
+    at j, then the position node (type 1, POOL_MEAN over those edges).
+    Draws: (1) the structure; (2) the GRU weights Wx [E x 3H] then Wh [H x 3H]
+    ~ U(-0.1, 0.1) (gate columns z, r, n), biases 0, the pooling map the
+    identity; (3) the edges' inputs ~ N(0, 1) in node order."""
+    g = _GraphBuilder()
+    lattices = []
+    for _ in range(inst):
+        L = int(rng.integers(20, 61))
+        spans = []
+        for b in range(L):
+            if rng.random() < 0.3:
+                sp = int(rng.integers(2, 5))
+                spans.append(sp if b + sp - 1 <= L - 1 else 0)
+            else:
+                spans.append(0)
+        words = [(b, b + sp - 1) for b, sp in enumerate(spans) if sp]
+        ending: Dict[int, List[int]] = {}
+        for k, (b, e) in enumerate(words):
+            ending.setdefault(e, []).append(k)
+        pos = []
+        char_edge = []
+        word_edge = [0] * len(words)
+        for j in range(L):
+            ce = g.add(0, [pos[j - 1] if j else -1], True)
+            char_edge.append(ce)
+            edges = [ce]
+            for k in ending.get(j, []):
+                b = words[k][0]
+                word_edge[k] = g.add(0, [pos[b - 1] if b else -1], True)
+                edges.append(word_edge[k])
+            pos.append(g.add(1, edges, False))
+        lattices.append({"length": L, "words": words, "pos": np.array(pos), "char_edge": np.array(char_edge),
+                         "word_edge": np.array(word_edge, dtype=np.int64)})
+    op_type, ptr, idx, x_row, n_x = g.finish()
+    Wx = rng.uniform(-0.1, 0.1, size=(E, 3 * H)).astype(np.float32)
+    Wh = rng.uniform(-0.1, 0.1, size=(H, 3 * H)).astype(np.float32)
+    x = rng.standard_normal(size=(n_x, E), dtype=np.float32)
+    W = np.zeros((E + H, 4 * H), dtype=np.float32)
+    W[:E, :3 * H] = Wx                       # z, r, n_x over x
+    W[E:, :2 * H] = Wh[:, :2 * H]            # z, r over the source state
+    W[E:, 3 * H:] = Wh[:, 2 * H:]            # n_h over the source state
+    weights = [{"W": W, "b": np.zeros(4 * H, dtype=np.float32)},
+               {"W": np.eye(H, dtype=np.float32), "b": np.zeros(H, dtype=np.float32)}]
+    aux = {"lattices": lattices, "Wx": Wx, "Wh": Wh, "bx": np.zeros(3 * H, dtype=np.float32),
+           "bhn": np.zeros(H, dtype=np.float32)}
+    return Workload(name=CONFIG_NAMES[9], dtype="f32", kinds=[LGRU_EDGE, POOL_MEAN], in_dim=E, hidden=H,
+                    op_type=op_type, child_ptr=ptr, child_idx=idx, x_row=x_row, x=x, weights=weights,
+                    n_children=[0, 0], instances=inst, aux=aux)
 
 
 def make_graph(kinds: List[int], E: int, H: int, op_type, children: List[List[int]],

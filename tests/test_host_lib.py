@@ -38,10 +38,10 @@ def _oracle_schedule(w, policy=OS.POLICY_TABLE, table=None, encoding=OS.ENC_SORT
     return OS.schedule(w.op_type, w.child_ptr, w.child_idx, w.n_types, policy, table, encoding)
 
 
-CFG_INSTANCES = {1: None, 2: None, 3: None, 4: None, 5: 48, 6: None, 7: None, 8: 3}
+CFG_INSTANCES = {1: None, 2: None, 3: None, 4: None, 5: 48, 6: None, 7: None, 8: 3, 9: None}
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 8])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 8, 9])
 @pytest.mark.parametrize("policy", [OS.POLICY_TABLE, OS.POLICY_AGENDA, OS.POLICY_DEPTH, OS.POLICY_SUFFICIENT])
 def test_schedule_bit_exact_configs(k, policy):
     w = WL.make_config(k, instances=CFG_INSTANCES[k])
@@ -71,7 +71,7 @@ def _compare_plan(pl, ref, batches):
             assert pl.ragged_off[b] == -1
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 8])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 8, 9])
 @pytest.mark.parametrize("mode", [OP.PLAN_RC, OP.PLAN_IDENTITY])
 def test_plan_bit_exact_configs(k, mode):
     w = WL.make_config(k, instances=CFG_INSTANCES[k])
@@ -207,7 +207,7 @@ def test_abi_errors(lib):
     assert lib.edb_execute(None, None, None, None, None, None) == L.EDB_ERR_INVALID
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 7, 8, 9])
 @pytest.mark.parametrize("flow", [True, False])
 def test_dryrun_launch_list(k, flow):
     w = WL.make_config(k, instances=CFG_INSTANCES[k])
