@@ -107,3 +107,27 @@ def test_lattice_gru_biases_and_replays():
         torch.cuda.synchronize()
         h1, _ = f1.states()
         np.testing.assert_array_equal(h1, h0)
+
+
+@pytest.mark.gpu
+def test_lattice_gru_one_call_path():
+    """The full workload through the one-call path the benchmark times
+    (edb_forward, eager launches): bitwise equal to a graph replay, which is
+    within the bound of the oracle."""
+    import torch
+    w = WL.make_config(9)
+    f = edb.Forward(w, flags=L.USE_GRAPH)
+    f.run()
+    f.run()
+    h, c = f.states()
+    ep, ee = _check(w, h)
+    assert ep < 1e-4 and ee < 1e-4, (ep, ee)
+    fc = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w), f.cells)
+    ah = torch.full_like(f.arena_h, 5.0)
+    ac = torch.full_like(f.arena_c, 5.0)
+    fc.call([b.data_ptr() for b in f.weights], f.x.data_ptr(), ah.data_ptr(), ac.data_ptr(), ah.shape[0],
+            f.stream.cuda_stream)
+    torch.cuda.synchronize()
+    s = f.plan.slot
+    np.testing.assert_array_equal(ah.cpu().numpy()[s], h)
+    np.testing.assert_array_equal(ac.cpu().numpy()[s], c)

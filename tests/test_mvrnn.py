@@ -138,3 +138,30 @@ def test_mvrnn_bias_and_replays():
         torch.cuda.synchronize()
         h1, _ = f1.states()
         np.testing.assert_array_equal(h1, h0)
+
+
+@pytest.mark.gpu
+def test_mvrnn_full_size_and_one_call_path():
+    """The full workload (64 trees, 251 k graph nodes) in the benchmark's
+    configurations: graph replay against the oracle on every tree node, and
+    the one-call path (edb_forward, eager launches) bitwise equal to it."""
+    import torch
+    w = WL.make_config(8)
+    f = edb.Forward(w, flags=L.USE_GRAPH)
+    f.run()
+    f.run()
+    h, c = f.states()
+    V, M = _reference(w)
+    gv, gm = _split(w, h)
+    d = w.hidden
+    assert normwise_rel_err(gv, V) < 1e-4
+    assert normwise_rel_err(np.transpose(gm, (0, 2, 1)).reshape(-1, d), np.transpose(M, (0, 2, 1)).reshape(-1, d)) < 1e-4
+    fc = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w), f.cells)
+    ah = torch.full_like(f.arena_h, 5.0)
+    ac = torch.full_like(f.arena_c, 5.0)
+    fc.call([b.data_ptr() for b in f.weights], f.x.data_ptr(), ah.data_ptr(), ac.data_ptr(), ah.shape[0],
+            f.stream.cuda_stream)
+    torch.cuda.synchronize()
+    s = f.plan.slot
+    np.testing.assert_array_equal(ah.cpu().numpy()[s], h)
+    np.testing.assert_array_equal(ac.cpu().numpy()[s], c)
