@@ -371,8 +371,11 @@ edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_
  *   x        device [n_x_rows x in_dim] of the cells' dtype, rows addressed by x_row
  *   arena_h  device [n_slots x H] of the cells' dtype; node v's h is row slot[v]
  *   arena_c  device [n_slots x H] fp32;               node v's c is row slot[v]
- * The call zeroes the arena's zero row and pad rows, stages x (unless
- * EDB_X_DIRECT), then runs every batch in schedule order.  With
+ * The call zeroes the arena's zero row and pad rows, stages x, then runs
+ * every batch in schedule order.  x is not staged under EDB_X_DIRECT, when
+ * every node's staged row would be its own row of x (x is then read in
+ * place), or when a single batch reads x (it then reads the caller's rows
+ * through its row list, as under EDB_X_DIRECT).  With
  * EDB_USE_GRAPH the sequence is captured into a HIP graph on the first call
  * and whenever a pointer differs from the captured ones, and replayed with a
  * single graph launch otherwise.  Kernel faults surface at the caller's next

@@ -581,6 +581,7 @@ struct edb_exec {
     int32_t T = 0, B = 0, dtype = 0;
     int32_t n_slots = 0, n_x = 0, E = 0, H = 0;
     int32_t x_direct_rows = 0;        // rows of the caller's x the plan addresses (max x_row + 1)
+    bool x_in_place = false;          // every staged row would be the caller's row: read x in place
     int64_t hsum_rows = 0, fc_rows = 0;   // scratch rows of child-sum batches on the large tile
     void* hsum = nullptr;             // [hsum_rows][H] bf16: child sums of h
     float* racc = nullptr;            // [hsum_rows][H] fp32: per parent, sum of the children's products
@@ -695,6 +696,20 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             if (p->x_slot[v] >= 0) e->x_direct_rows = std::max(e->x_direct_rows, g->x_row[v] + 1);
         }
         e->n_x = n_x;
+        // Staging x is skipped where it would only move rows around.  When every
+        // node's staged row is its own row of the caller's x, the batches read x
+        // in place through the same contiguous segments.  When a single batch
+        // reads x (a forest's leaf batch), it reads the caller's rows through its
+        // row list, as under EDB_X_DIRECT.
+        if (!(flags & EDB_X_DIRECT) && n_x > 0) {
+            bool same = true;
+            for (int32_t v = 0; v < g->V && same; ++v)
+                if (p->x_slot[v] >= 0 && p->x_slot[v] != g->x_row[v]) same = false;
+            int x_batches = 0;
+            for (int32_t b = 0; b < B; ++b) x_batches += kind_info(cells[s->batch_type[b]].kind).x ? 1 : 0;
+            if (same) e->x_in_place = true;
+            else if (x_batches == 1) e->flags = flags = flags | EDB_X_DIRECT;
+        }
         // the large tile addresses x and the arena with 32-bit byte offsets
         const int64_t esz_b = dtype == EDB_F32 ? 4 : 2;   // x element size
         const int64_t off_limit = (int64_t)1 << 31;
@@ -753,7 +768,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             L.info.batch = -1;
             L.info.kind = -1;
             L.info.m = n_x;
-            L.info.grid = (((flags & EDB_X_DIRECT) ? 0 : n_x) + e->n_zero + 3) / 4;   // 4 rows per work-group
+            L.info.grid = (((flags & EDB_X_DIRECT) || e->x_in_place ? 0 : n_x) + e->n_zero + 3) / 4;   // 4 rows per work-group
             L.info.block = 256;
             L.info.variant = -1;
             L.info.n_batches = 0;
@@ -1047,7 +1062,7 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
                 bd.type = L.type;
                 bd.m = L.args.m;
                 bd.H = d.H; bd.Hk = d.Hk; bd.Hu = d.Hu; bd.E = d.E; bd.Ep = d.Ep; bd.K = d.K;
-                bd.x_staged = (flags & EDB_X_DIRECT) ? 0 : 1;
+                bd.x_staged = (flags & EDB_X_DIRECT) || e->x_in_place ? 0 : 1;
                 const Seg* sgs[5] = {&L.args.x, &L.args.fix[0], &L.args.fix[1], &L.args.rag, &L.args.res};
                 const int64_t offs[5] = {L.off_x, L.off_f0, L.off_f1, L.off_rag, L.off_res};
                 for (int i = 0; i < 5; ++i) {
@@ -1174,7 +1189,8 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             // on the upload stream, filled asynchronously; executions wait on
             // the `ready` event instead of the host waiting for the copy
             const size_t ibytes = (hb.size() * sizeof(int32_t) + 255) / 256 * 256;
-            const size_t xbytes = (n_x > 0 && !(flags & EDB_X_DIRECT)) ? (size_t)n_x * E * (dtype == EDB_F32 ? 4 : 2) : 0;
+            const size_t xbytes = (n_x > 0 && !(flags & EDB_X_DIRECT) && !e->x_in_place)
+                                      ? (size_t)n_x * E * (dtype == EDB_F32 ? 4 : 2) : 0;
             auto al256 = [](size_t v) { return (v + 255) / 256 * 256; };
             const size_t hbytes = al256((size_t)e->hsum_rows * H * 2), rbytes = al256((size_t)e->hsum_rows * H * 4);
             const size_t fbytes = al256((size_t)e->fc_rows * H * 4);
@@ -1259,9 +1275,10 @@ BatchArgs resolve_args(const edb_exec* e, const Launch& L, const void* const* w,
     }
     a.arena_h = arena_h;
     a.arena_c = reinterpret_cast<float*>(arena_c);
-    a.xmat = (e->flags & EDB_X_DIRECT) ? x : e->xstaged;
+    const bool x_caller = (e->flags & EDB_X_DIRECT) || e->x_in_place;
+    a.xmat = x_caller ? x : e->xstaged;
     a.n_slots = e->n_slots;
-    a.n_xrows = (e->flags & EDB_X_DIRECT) ? e->x_direct_rows : e->n_x;
+    a.n_xrows = x_caller ? e->x_direct_rows : e->n_x;
     a.fc = e->fc;
     if (L.off_x >= 0) a.x.idx = db + L.off_x;
     if (L.off_f0 >= 0) a.fix[0].idx = db + L.off_f0;
@@ -1283,7 +1300,7 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
     const int ncnt = (int)e->n_counters;
     {
         const Launch& L = e->launches[0];
-        const bool direct = (e->flags & EDB_X_DIRECT) != 0;
+        const bool direct = (e->flags & EDB_X_DIRECT) != 0 || e->x_in_place;
         const int nx = direct ? 0 : e->n_x;
         if (L.info.grid > 0) {
             if (e->dtype == EDB_F32) {
@@ -1332,7 +1349,7 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
             f.need = L.f_need;
             f.spin_us = L.args.m;
             f.n_slots = e->n_slots;
-            f.n_xrows = (e->flags & EDB_X_DIRECT) ? e->x_direct_rows : e->n_x;
+            f.n_xrows = (e->flags & EDB_X_DIRECT) || e->x_in_place ? e->x_direct_rows : e->n_x;
             f.x = x;
             f.xstaged = e->xstaged;
             f.arena_h = arena_h;
@@ -1540,7 +1557,8 @@ extern "C" edb_status edb_split_phase(edb_exec_t* e, const void* x, void* arena_
     if (!e) return fail(EDB_ERR_INVALID, "edb_split_phase: exec is NULL");
     if (e->flags & EDB_DRYRUN) return fail(EDB_ERR_INVALID, "edb_split_phase: dry-run executor");
     if (!arena_h || !arena_c || !buf) return fail(EDB_ERR_INVALID, "edb_split_phase: NULL argument");
-    if ((e->flags & EDB_X_DIRECT) && e->n_x > 0 && !x) return fail(EDB_ERR_INVALID, "edb_split_phase: x is NULL");
+    if (((e->flags & EDB_X_DIRECT) || e->x_in_place) && e->n_x > 0 && !x)
+        return fail(EDB_ERR_INVALID, "edb_split_phase: x is NULL");
     if (!e->ran) return fail(EDB_ERR_INVALID, "edb_split_phase: run edb_execute first (it stages x)");
     if (ms && n < 2 * e->B) return fail(EDB_ERR_INVALID, "edb_split_phase: ms must hold 2 * n_batches values");
     if ((reinterpret_cast<uintptr_t>(buf) | reinterpret_cast<uintptr_t>(arena_h) |

@@ -216,7 +216,13 @@ def test_dryrun_launch_list(k, flow):
     B = f.sched.n_batches
     info0 = f.exec.launch_info(0)
     assert info0["batch"] == -1 and info0["n_batches"] == 0
-    assert info0["grid"] == (int((w.x_row >= 0).sum()) + 1 + len(f.plan.pads) + 3) // 4
+    # x is staged unless every staged row would be the node's own row of x (then read in
+    # place) or a single batch reads x (then through its row list)
+    xs = f.plan.x_slot
+    in_place = bool((xs >= 0).any()) and bool(np.all(xs[xs >= 0] == w.x_row[xs >= 0]))
+    x_batches = sum(WL.KIND_SHAPE[w.kinds[int(t)]][2] for t in f.sched.batch_type)
+    staged = 0 if (in_place or x_batches == 1) else int((w.x_row >= 0).sum())
+    assert info0["grid"] == (staged + 1 + len(f.plan.pads) + 3) // 4
     seen = []
     for i in range(1, n):
         info = f.exec.launch_info(i)
