@@ -615,12 +615,20 @@ def main():
     # host part of a step (a1-a3 + descriptor upload), measured alone
     th = time.perf_counter()
     nh = 20
+    parts = np.zeros(4)   # ingest, schedule, plan, prepare (ms, summed)
     for _ in range(nh):
+        t0 = time.perf_counter()
         g = edb.Graph(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types)
+        t1 = time.perf_counter()
         s = edb.Schedule(g, kind, L.ENC_SORT, table)
+        t2 = time.perf_counter()
         p = edb.Plan(g, s, shapes, plan_mode)
+        t3 = time.perf_counter()
         ex = edb.Exec(g, s, p, base.cells, 0)
+        t4 = time.perf_counter()
+        parts += np.array([t1 - t0, t2 - t1, t3 - t2, t4 - t3]) * 1e3
     ms_host = (time.perf_counter() - th) * 1e3 / nh
+    host_parts = {k: round(float(v) / nh, 4) for k, v in zip(("ingest", "schedule", "plan", "prepare"), parts)}
 
     # per-launch durations: the timed region's own events, averaged over its steps
     times = rec_times.mean(axis=0)
@@ -702,6 +710,7 @@ def main():
                           "alg_tflops": round(tot_flops / (ms_replay * 1e-3) / 1e12, 3),
                           "alg_hbm_gbs": round(tot_bytes / (ms_replay * 1e-3) / 1e9, 1)},
         "host_ms_per_graph": round(ms_host, 4),
+        "host_ms_parts": host_parts,
         "launch_us": [round(t * 1e3, 2) for t in times],
     }
     pm = probes(w.dtype)
