@@ -693,7 +693,7 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.config], "nodes": V, "batches": base.sched.n_batches,
-                   "launches_per_step": base.exec.launches(), "mini_batches_in_flight": S,
+                   "launches_per_step": sum(1 for i in range(base.exec.launches()) if base.exec.launch_info(i)["grid"] > 0), "mini_batches_in_flight": S,
                    "policy": policy_info, "plan": args.plan,
                    "step": "graph ingest + schedule + memory plan + launch prep + device execution"},
         "roofline": ({"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -327,6 +327,7 @@ __global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
     const int ntile = ((a.m + TM - 1) / TM) * nut;
     const int per = (ntile + 7) / 8;
     const int tile = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    clear_zero_rows<T>(a);
     if (tile >= ntile) return;
     big_tile<KIND, T, VB>(a, tile, st0, st1);
 }

@@ -81,7 +81,10 @@ struct BatchArgs {
     int n_slots;          // arena rows
     int n_xrows;          // rows of the x matrix xmat points to
     float* fc;            // child-sum batches on the large tile: sigma(f_k) * c_k per child, [children][H]
+    const int* zrows;     // rows this launch clears in both arenas (the zero row and pads), or none
+    int n_zero;
 };
+
 
 template <int KIND> struct Kind;
 template <> struct Kind<K_CHAIN>    { static constexpr int G = 4, NFIX = 1; static constexpr bool X = true,  RAG = false; };
@@ -159,6 +162,23 @@ __device__ __forceinline__ float to_f(__bf16 v) { return (float)v; }
 template <typename T> __device__ __forceinline__ T from_f(float v);
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ __bf16 from_f<__bf16>(float v) { return (__bf16)v; }
+
+// The first batch's launch clears the arenas' zero row and pad rows when no
+// staging launch runs before it.  That batch reads no arena row: nothing has
+// run before it, so all of its child lists are absent, and it is used only for
+// kinds without child lists, which never touch the zero row.  Every
+// work-group takes a share, before any early exit.
+template <typename T>
+__device__ __forceinline__ void clear_zero_rows(const BatchArgs& a) {
+    if (a.n_zero == 0) return;
+    const int64_t n = (int64_t)a.n_zero * a.H;
+    T* h = reinterpret_cast<T*>(a.arena_h);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t o = (int64_t)a.zrows[i / a.H] * a.H + i % a.H;
+        h[o] = from_f<T>(0.f);
+        a.arena_c[o] = 0.f;
+    }
+}
 
 // Gate nonlinearities and cell-state update of one (node, unit) element.
 // z: the G gate pre-activations (bias included), cp: child cell states of the
@@ -755,6 +775,7 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
 template <int KIND, typename T, int RT, int WU, int WK>
 __global__ __launch_bounds__(64 * WU * WK, WU * WK == 4 && RT * WU <= 4 && !Kind<KIND>::RAG ? 3 : 1) void cell_kernel(BatchArgs a) {
     extern __shared__ __align__(16) char smem[];
+    clear_zero_rows<T>(a);
     const int nut = a.Hu / (16 * WU);
     cell_tile<KIND, T, RT, WU, WK>(a, blockIdx.x / nut, blockIdx.x % nut, smem, NoSync{});
 }
@@ -1002,6 +1023,7 @@ __global__ __launch_bounds__(64 * WK, WK == 4 ? 3 : 1) void stream_kernel(BatchA
     const int ntile = nrt * nut;
     const int per = (ntile + 7) / 8;
     const int t = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    clear_zero_rows<T>(a);
     if (t >= ntile) return;
     stream_tile<KIND, T, RT, WK>(a, t % nrt, t / nrt, smem);
 }

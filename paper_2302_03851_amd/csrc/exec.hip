@@ -399,6 +399,7 @@ struct Launch {
     BatchArgs args;  // pointer fields to data buffers are filled at execute time
     // offsets into the device int buffer (-1 = none)
     int64_t off_x, off_f0, off_f1, off_rag, off_rptr, off_res;
+    int64_t off_zrows = -1;   // the first batch clears the zero and pad rows listed here
     int x_base;
     int lds;
     // dataflow launch (info.variant == FLOW_VARIANT): offsets into the int buffer
@@ -1153,6 +1154,23 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             F.f_error += e->off_counters;
             F.f_done += e->off_counters;
         }
+        // When the staging launch would only clear the zero and pad rows, the
+        // first batch's launch clears them and the staging launch is dropped
+        // (grid 0).  Only for a first batch without child lists (it then reads
+        // no arena row) whose x segment has no padding columns (the staged
+        // tile reads the zero row for those), run as a single launch.
+        if (e->launches.size() > 1 && n_counters == 0) {
+            Launch& L1 = e->launches[1];
+            const bool staged_x = !((flags & EDB_X_DIRECT) || e->x_in_place) && n_x > 0;
+            const KindInfo k1 = L1.flow ? KindInfo{} : kind_info(L1.info.kind);
+            const bool single = !L1.flow && L1.info.batch == 0 && L1.info.part == 0 && L1.kk == L1.info.kind &&
+                                (e->launches.size() == 2 || e->launches[2].info.batch != 0);
+            if (!staged_x && single && k1.G > 0 && k1.nfix == 0 && !k1.rag && dims[L1.type].Ep == dims[L1.type].E) {
+                e->launches[0].info.grid = 0;
+                L1.off_zrows = e->off_zero;
+                L1.args.n_zero = e->n_zero;
+            }
+        }
         // dataflow grids: at most the resident work-groups (more would only exit)
         for (Launch& F : e->launches) {
             if (!F.flow) continue;
@@ -1286,6 +1304,7 @@ BatchArgs resolve_args(const edb_exec* e, const Launch& L, const void* const* w,
     if (L.off_rag >= 0) a.rag.idx = db + L.off_rag;
     if (L.off_rptr >= 0) a.rag_ptr = db + L.off_rptr;
     if (L.off_res >= 0) a.res.idx = db + L.off_res;
+    if (L.off_zrows >= 0) a.zrows = db + L.off_zrows;
     return a;
 }
 
@@ -1632,8 +1651,13 @@ extern "C" edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n)
         return fail(EDB_ERR_INVALID, "edb_exec_launch_times: no profiled execution");
     if (n != (int32_t)e->launches.size()) return fail(EDB_ERR_INVALID, "edb_exec_launch_times: n != launches");
     hipError_t he = hipEventSynchronize(e->events.back());
-    for (int32_t i = 0; he == hipSuccess && i < n; ++i)
+    for (int32_t i = 0; he == hipSuccess && i < n; ++i) {
+        if (e->launches[i].info.grid == 0) {   // not launched (the staging launch when folded)
+            ms[i] = 0.f;
+            continue;
+        }
         he = hipEventElapsedTime(&ms[i], e->events[2 * i], e->events[2 * i + 1]);
+    }
     if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_exec_launch_times: ") + hipGetErrorString(he));
     return EDB_OK;
 }
