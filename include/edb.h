@@ -389,7 +389,10 @@ edb_status edb_execute(edb_exec_t* e, const void* const* packed_weights, const v
  * EDB_NO_FLOW has no effect.  edb_exec_check reports a timed-out dataflow
  * wait when they are enabled.
  *
- * Number of kernel launches one edb_execute issues (launches per graph). */
+ * Number of launch records of one edb_execute: record 0 is the staging launch
+ * (x staging and the clearing of the zero and pad rows), then the batches'
+ * launches.  Record 0 has grid 0 and is not issued when nothing is staged and
+ * the first batch (no child lists, no x padding) clears those rows itself. */
 edb_status edb_exec_launches(const edb_exec_t* e, int32_t* n_kernels);
 
 /* Description of launch i (for tests and profiling). */
@@ -417,7 +420,8 @@ edb_status edb_exec_launch_info(const edb_exec_t* e, int32_t i, edb_launch_info*
 
 /* Per-launch GPU durations of the last edb_execute of an EDB_PROFILE handle,
  * in milliseconds: each kernel's own duration, from start and stop HIP events
- * that the dispatch packet records on the execution stream.  ms: host float[n], n = edb_exec_launches.
+ * that the dispatch packet records on the execution stream (0 for a record
+ * with grid 0, which is not issued).  ms: host float[n], n = edb_exec_launches.
  * Waits for that execution to finish.  EDB_ERR_INVALID without EDB_PROFILE
  * or before the first execute. */
 edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
