@@ -200,6 +200,41 @@ def traffic_from(d, workload):
     print(f"wrote {TRAFFIC_FILE}: {len(out['kernels'])} kernels, scales {scale} (device copy: {scale_copy})")
 
 
+def trace_summary(d, symbol=None, last=0):
+    """Markdown summary of a rocprofv3 --kernel-trace run under directory d:
+    per kernel the calls, average / min / max duration and share of the
+    summed time; with `symbol` and `last`, also the average of that kernel's
+    last `last` dispatches (by start time): the roofline pass of this
+    benchmark, which runs after every other launch of the path's kernels."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one kernel_trace.csv under {d}, found {files}")
+    rows = [(r["Kernel_Name"], int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+            for r in csv.DictReader(open(files[0]))]
+    per = {}
+    for name, t0, t1 in rows:
+        per.setdefault(name, []).append((t0, (t1 - t0) * 1e-3))
+    total = sum(dt for v in per.values() for _, dt in v)
+    out = ["| kernel | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
+    for name, v in sorted(per.items(), key=lambda kv: -sum(dt for _, dt in kv[1])):
+        ds = [dt for _, dt in v]
+        nm = name if len(name) <= 90 else name[:87] + "..."
+        out.append(f"| `{nm}` | {len(ds)} | {np.mean(ds):.2f} | {min(ds):.2f} | {max(ds):.2f} | "
+                   f"{100 * sum(ds) / total:.1f}% |")
+    if symbol:
+        match = [v for name, v in per.items() if name.startswith("void " + symbol) or name.startswith(symbol)]
+        if len(match) != 1:
+            raise SystemExit(f"{symbol}: {len(match)} kernels match")
+        v = sorted(match[0])
+        tail = [dt for _, dt in v[-last:]] if last else [dt for _, dt in v]
+        out.append("")
+        out.append(f"`{symbol}`: average of its last {len(tail)} dispatches {np.mean(tail):.2f} us "
+                   f"(min {min(tail):.2f}, max {max(tail):.2f}); all {len(v)} dispatches {np.mean([dt for _, dt in v]):.2f} us.")
+    return "\n".join(out)
+
+
 def traffic_of(symbol, workload):
     """HBM bytes per launch of a kernel from the committed counter record, or
     None when there is none for this workload or the sources have changed."""
@@ -311,52 +346,63 @@ def split_phase(configs, reps=5):
         w = WL.make_config(k, instances=DEFAULT_INSTANCES[k] * mult)
         if w.dtype not in pr:
             pr[w.dtype] = probes(w.dtype)
-        f = edb.Forward(w, flags=L.USE_GRAPH)
-        f.run()
-        torch.cuda.synchronize()
-        B = f.sched.n_batches
-        nb = f.exec.split_phase_bytes()
-        buf = torch.empty(nb, dtype=torch.uint8, device="cuda:0")
-        ms = np.median([f.exec.split_phase(f.x.data_ptr(), f.arena_h.data_ptr(), f.arena_c.data_ptr(),
-                                           buf.data_ptr(), nb, f.stream.cuda_stream, B) for _ in range(reps)], axis=0)
-        work = algorithmic_work(w, f)
-        esz = 2 if w.dtype == "bf16" else 4
-        H, E = w.hidden, w.in_dim
-        shapes = edb.operand_shapes(w)
-        rows = []
-        for b in range(B):
-            t = int(f.sched.batch_type[b])
-            m = int(f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b])
-            nf, rg, hx = shapes[t]
-            segs = f.plan.segs[f.plan.seg_ptr[b]:f.plan.seg_ptr[b + 1]]
-            moved_g = m * E * esz if hx else 0
-            for kind_s, _base, _off, n in segs[1:]:
-                if kind_s != L.SEG_NONE:
-                    moved_g += n * H * (esz + 4)
-            own = m * H * (esz + 4)
-            rows.append((m, work[b][2] - own, own, 2 * moved_g, 2 * own, ms[b, 0], ms[b, 1]))
-        a = np.array(rows, dtype=np.float64)
-        g_ms, s_ms = a[:, 5].sum(), a[:, 6].sum()
-        alg = a[:, 1].sum() + a[:, 2].sum()
-        moved = a[:, 3].sum() + a[:, 4].sum()
-        big = int(np.argmax(a[:, 3]))
-        peak, meas = PEAK_HBM_GBS, pr[w.dtype]["copy_gbs"]
-        gbs = lambda by, t: by / (t * 1e-3) / 1e9
-        rec = {"workload": WORKLOAD_TEXT[k], "instances_scale": mult, "nodes": w.n_nodes, "batches": B, "reps": reps,
-               "gather_ms": round(g_ms, 4), "scatter_ms": round(s_ms, 4),
-               "alg_bytes": int(alg), "moved_bytes": int(moved),
-               "alg_gbs": round(gbs(alg, g_ms + s_ms), 1), "moved_gbs": round(gbs(moved, g_ms + s_ms), 1),
-               "frac_alg": round(gbs(alg, g_ms + s_ms) / peak, 4),
-               "frac_moved": round(gbs(moved, g_ms + s_ms) / peak, 4),
-               "frac_moved_of_measured_copy": round(gbs(moved, g_ms + s_ms) / meas, 4),
-               "largest_batch": {"batch": big, "rows": int(a[big, 0]),
-                                 "gather_us": round(a[big, 5] * 1e3, 2), "scatter_us": round(a[big, 6] * 1e3, 2),
-                                 "gather_moved_gbs": round(gbs(a[big, 3], a[big, 5]), 1),
-                                 "scatter_moved_gbs": round(gbs(a[big, 4], a[big, 6]), 1)},
-               "peak_gbs": peak, "probes": pr[w.dtype]}
+        rec = split_phase_record(w, k, mult, pr[w.dtype]["copy_gbs"], reps)
+        rec["probes"] = pr[w.dtype]
         print(json.dumps(rec), flush=True)
-        del f, buf
         torch.cuda.empty_cache()
+
+
+def split_phase_record(w, k, mult, copy_gbs, reps=5):
+    """One workload's split-phase record (see split_phase)."""
+    import torch
+    from paper_2302_03851_amd import _lib as L
+    from paper_2302_03851_amd import edb
+
+    f = edb.Forward(w, flags=L.USE_GRAPH)
+    f.run()
+    torch.cuda.synchronize()
+    B = f.sched.n_batches
+    nb = f.exec.split_phase_bytes()
+    buf = torch.empty(nb, dtype=torch.uint8, device="cuda:0")
+    ms = np.median([f.exec.split_phase(f.x.data_ptr(), f.arena_h.data_ptr(), f.arena_c.data_ptr(),
+                                       buf.data_ptr(), nb, f.stream.cuda_stream, B) for _ in range(reps)], axis=0)
+    work = algorithmic_work(w, f)
+    esz = 2 if w.dtype == "bf16" else 4
+    H, E = w.hidden, w.in_dim
+    shapes = edb.operand_shapes(w)
+    rows = []
+    for b in range(B):
+        t = int(f.sched.batch_type[b])
+        m = int(f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b])
+        nf, rg, hx = shapes[t]
+        segs = f.plan.segs[f.plan.seg_ptr[b]:f.plan.seg_ptr[b + 1]]
+        moved_g = m * E * esz if hx else 0
+        for kind_s, _base, _off, n in segs[1:]:
+            if kind_s != L.SEG_NONE:
+                moved_g += n * H * (esz + 4)
+        own = m * H * (esz + 4)
+        rows.append((m, work[b][2] - own, own, 2 * moved_g, 2 * own, ms[b, 0], ms[b, 1]))
+    a = np.array(rows, dtype=np.float64)
+    g_ms, s_ms = a[:, 5].sum(), a[:, 6].sum()
+    alg = a[:, 1].sum() + a[:, 2].sum()
+    moved = a[:, 3].sum() + a[:, 4].sum()
+    big = int(np.argmax(a[:, 3]))
+    peak, meas = PEAK_HBM_GBS, copy_gbs
+    gbs = lambda by, t: by / (t * 1e-3) / 1e9
+    rec = {"workload": WORKLOAD_TEXT[k], "instances_scale": mult, "nodes": w.n_nodes, "batches": B, "reps": reps,
+           "gather_ms": round(g_ms, 4), "scatter_ms": round(s_ms, 4),
+           "alg_bytes": int(alg), "moved_bytes": int(moved),
+           "alg_gbs": round(gbs(alg, g_ms + s_ms), 1), "moved_gbs": round(gbs(moved, g_ms + s_ms), 1),
+           "frac_alg": round(gbs(alg, g_ms + s_ms) / peak, 4),
+           "frac_moved": round(gbs(moved, g_ms + s_ms) / peak, 4),
+           "frac_moved_of_measured_copy": round(gbs(moved, g_ms + s_ms) / meas, 4) if meas else None,
+           "largest_batch": {"batch": big, "rows": int(a[big, 0]),
+                             "gather_us": round(a[big, 5] * 1e3, 2), "scatter_us": round(a[big, 6] * 1e3, 2),
+                             "gather_moved_gbs": round(gbs(a[big, 3], a[big, 5]), 1),
+                             "scatter_moved_gbs": round(gbs(a[big, 4], a[big, 6]), 1)},
+           "peak_gbs": peak}
+    del f, buf
+    return rec
 
 
 DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64, 8: 64, 9: 32}
@@ -437,8 +483,8 @@ def main():
     ap.add_argument("--replays", type=int, default=200)
     ap.add_argument("--streams", type=int, default=16,
                     help="mini-batches in flight: host worker threads, each with its own stream and arena")
-    ap.add_argument("--timed-events", type=int, default=8,
-                    help="steps of worker 0 in the timed region whose launches record HIP events")
+    ap.add_argument("--roofline-steps", type=int, default=10,
+                    help="steps of the roofline pass (one mini-batch in flight, launches timed with HIP events)")
     ap.add_argument("--policy", default="table", choices=sorted(POLICIES),
                     help="batching policy: the configured FSM table (default), a table learned on the "
                          "workload's graph before timing (N-step Q-learning, E_sort), or a heuristic")
@@ -459,7 +505,14 @@ def main():
     ap.add_argument("--traffic-from", metavar="DIR",
                     help="write profiles/traffic.json from rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR "
                          "(c2_<counter>/ of this benchmark, copy_<counter>/ of --copy-calibration)")
+    ap.add_argument("--trace-summary", metavar="DIR",
+                    help="print a markdown summary of the rocprofv3 --kernel-trace run under DIR")
+    ap.add_argument("--symbol", help="with --trace-summary: the kernel whose last --last dispatches are averaged")
+    ap.add_argument("--last", type=int, default=0)
     args = ap.parse_args()
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary, args.symbol, args.last))
+        return
     if args.traffic_from:
         traffic_from(args.traffic_from, WORKLOAD_TEXT[args.config])
         return
@@ -534,71 +587,70 @@ def main():
     arenas = [(ahp, acp)] + [(torch.empty_like(base.arena_h), torch.empty_like(base.arena_c)) for _ in range(S - 1)]
     arena_ptrs = [arenas[0]] + [(a.data_ptr(), c.data_ptr()) for a, c in arenas[1:]]
 
-    # the launches of worker 0's first --timed-events steps of a region record
-    # start/stop HIP events in their dispatch packets (EDB_PROFILE); those
-    # executors are kept until the region has ended and are then read.  All
-    # other steps run without events (the events cost host time on every step).
     fwd = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
                           policy=kind, table=table, plan_mode=plan_mode)
-    fwd_prof = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
-                               policy=kind, table=table, plan_mode=plan_mode, flags=L.PROFILE)
     n_rows = base.plan.n_slots
 
-    def step(i, keep):
+    def step(i):
         # a1 graph ingest, a2 schedule, a3 memory plan, descriptor upload and
-        # a4..a8 device execution (asynchronous), in one C call
+        # a4..a8 device execution (asynchronous, eager launches), in one C call
         ah, ac = arena_ptrs[i]
-        if i == 0 and len(keep) < args.timed_events:
-            keep.append(fwd_prof.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream, keep=True))
-        else:
-            fwd.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream)
+        fwd.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream)
 
-    def run_steps(n):
-        """n steps over S worker threads (each its own stream and arena), each
-        thread taking the next step when it is free: the worker whose steps
-        carry timing events does fewer of them instead of finishing last."""
-        keeps = [[] for _ in range(S)]
-        if S == 1:
-            for _ in range(n):
-                step(0, keeps[0])
-            return keeps
-        taken = [1]   # worker 0 runs the first step: the timed region has at least one with events
-        lock = threading.Lock()
+    class Workers:
+        """S host threads, each with its own stream and arena, started once
+        and parked at a barrier; run(n) releases them for n steps (each thread
+        takes the next step when it is free) and returns when all are done."""
 
-        def worker(i):
-            if i == 0:
-                step(0, keeps[0])
+        def __init__(self):
+            self.go = threading.Barrier(S + 1)
+            self.end = threading.Barrier(S + 1)
+            self.lock = threading.Lock()
+            self.n = self.taken = 0
+            self.quit = False
+            self.errors = []
+            self.threads = [threading.Thread(target=self.work, args=(i,), daemon=True) for i in range(S)]
+            for t in self.threads:
+                t.start()
+
+        def work(self, i):
             while True:
-                with lock:
-                    if taken[0] >= n:
-                        return
-                    taken[0] += 1
-                step(i, keeps[i])
-        ths = [threading.Thread(target=worker, args=(i,)) for i in range(S)]
-        for t in ths:
-            t.start()
-        for t in ths:
-            t.join()
-        return keeps
+                self.go.wait()
+                if self.quit:
+                    return
+                try:
+                    while True:
+                        with self.lock:
+                            if self.taken >= self.n:
+                                break
+                            self.taken += 1
+                        step(i)
+                except Exception as e:   # reported by run()
+                    self.errors.append(e)
+                self.end.wait()
 
-    run_steps(args.warmup)
+        def run(self, n):
+            self.n, self.taken = n, 0
+            self.go.wait()
+            self.end.wait()
+            if self.errors:
+                raise self.errors[0]
+
+        def close(self):
+            self.quit = True
+            self.go.wait()
+            for t in self.threads:
+                t.join()
+
+    pool = Workers()
+    pool.run(args.warmup)
     torch.cuda.synchronize()
-    # untimed priming pass of as many steps as the timed region: the timed
-    # steps' executors are kept until the region ends, and their timing events
-    # then come from the pool these return to (not created on the host path)
-    primed = run_steps(args.steps)
-    torch.cuda.synchronize()
-    del primed
     t0 = time.perf_counter()
-    timed = run_steps(args.steps)
+    pool.run(args.steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    records = [r for rs in timed for r in rs]
-    n_profiled = len(records)
-    rec_infos = [records[0].launch_info(i) for i in range(records[0].launches())]
-    rec_times = np.array([r.launch_times() for r in records])     # [steps][launches] ms
-    del records, timed
+    pool.close()
 
     # device-only rate: the captured HIP graph of the same batch sequence replayed
     for _ in range(10):
@@ -630,7 +682,30 @@ def main():
     ms_host = (time.perf_counter() - th) * 1e3 / nh
     host_parts = {k: round(float(v) / nh, 4) for k, v in zip(("ingest", "schedule", "plan", "prepare"), parts)}
 
-    # per-launch durations: the timed region's own events, averaged over its steps
+    # gather and scatter as separate copies (split-phase diagnostic) at this
+    # workload's size: the HBM side of the roofline
+    sp = split_phase_record(w, args.config, 1, None)
+    torch.cuda.empty_cache()
+
+    # roofline pass: the same step with one mini-batch in flight, each step
+    # alone on the GPU (synchronised), its launches recording start and stop
+    # events in their dispatch packets; per-launch durations averaged over the
+    # steps.  Nothing launches the path's kernels after this pass, so a
+    # profiler trace of this command finds these dispatches as the last ones
+    # of each kernel.
+    fwd_prof = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, shapes, base.cells,
+                               policy=kind, table=table, plan_mode=plan_mode, flags=L.PROFILE)
+    rec_times, rec_infos = [], None
+    for _ in range(args.roofline_steps + 2):
+        r = fwd_prof.call(wptrs, xp, ahp, acp, n_rows, stream, keep=True)
+        torch.cuda.synchronize()
+        if rec_infos is None:
+            rec_infos = [r.launch_info(i) for i in range(r.launches())]
+        rec_times.append(r.launch_times())
+        del r
+    rec_times = np.array(rec_times[2:])   # [steps][launches] ms; the first two steps warm the pass up
+    n_profiled = rec_times.shape[0]
+
     times = rec_times.mean(axis=0)
     work = algorithmic_work(w, base)
     infos = rec_infos
@@ -703,7 +778,9 @@ def main():
                       "frac": round(tflops / peak, 4), "traffic": traffic}) | {
                      "kernel": kernel, "symbol": symbol,
                      "launches": nl, "avg_launch_us": round(avg_ms * 1e3, 2),
-                     "timing": f"HIP events in the dispatch packets of the {n_profiled} timed steps on worker stream 0",
+                     "timing": f"HIP events in the dispatch packets, {n_profiled} steps with one mini-batch in "
+                               "flight (each step alone on the GPU)",
+                     "launches_timed": nl * n_profiled, "per_step_us": round(tot_ms * 1e3, 2),
                      "alg_flops_per_launch": int(fl / nl)},
         "device_replay": {"ms_per_forward": round(ms_replay, 4),
                           "node_cells_per_s": round(V / (ms_replay * 1e-3), 1),
@@ -721,6 +798,16 @@ def main():
         result["roofline"]["peak_measured"] = pm["mfma_tflops"]
         result["roofline"]["frac_measured"] = round(tflops / pm["mfma_tflops"], 4)
     result["probes"] = pm
+    result["roofline_hbm"] = {
+        "bound": "hbm", "kernel": "copy_rows_kernel (split-phase gather and scatter of every batch)",
+        "achieved": sp["alg_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": sp["frac_alg"],
+        "alg_bytes": sp["alg_bytes"], "moved_bytes": sp["moved_bytes"],
+        "moved_gbs": sp["moved_gbs"], "frac_moved": sp["frac_moved"],
+        "frac_moved_of_measured_copy": round(sp["moved_gbs"] / pm["copy_gbs"], 4),
+        "gather_ms": sp["gather_ms"], "scatter_ms": sp["scatter_ms"], "launches": 2 * sp["batches"],
+        "bytes": "algorithmic: present operand rows read (x, children's h and c) + own h and c written; "
+                 "moved: every row the copies read and write (zero rows and the dense buffer included)",
+        "largest_batch": sp["largest_batch"]}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(result), flush=True)

@@ -2,15 +2,16 @@
 
 Bounds (normwise relative error per state vector, max over nodes and h/c):
 1e-4 for the fp32 configurations, 2e-2 for the bf16 child-sum configuration.
-Small instances compare every node; the full-size configurations run in the
-benchmark's launch configuration (HIP graph, planned layout) and compare
-whole sampled instances, which the oracle evaluates on their own (instances
-are independent graphs)."""
+Every test compares every node: small instances, and the full-size
+configurations in the benchmark's launch configuration (HIP graph, planned
+layout) and in its concurrent mode (host threads and streams), against the
+oracle evaluated instance by instance (instances are independent graphs)."""
 import numpy as np
 import pytest
 
-from oracle.compare import normwise_rel_err, state_rel_err
+from oracle.compare import state_rel_err
 from oracle.evaluate import evaluate
+from oracle_instances import evaluate_by_instance
 from paper_2302_03851_amd import _lib as L
 from paper_2302_03851_amd import workloads as WL
 
@@ -65,63 +66,69 @@ def test_parity_small(k):
         assert (h[words] == 0).all()
 
 
-def _components(w):
-    """Instance id of every node (connected components over present edges)."""
-    parent = np.arange(w.n_nodes)
-
-    def find(a):
-        while parent[a] != a:
-            parent[a] = parent[parent[a]]
-            a = parent[a]
-        return a
-    for v in range(w.n_nodes):
-        for c in w.children(v):
-            if c >= 0:
-                ra, rb = find(v), find(int(c))
-                if ra != rb:
-                    parent[ra] = rb
-    return np.array([find(v) for v in range(w.n_nodes)])
-
-
-def _subgraph(w, nodes):
-    """Workload restricted to `nodes` (closed under children), ids remapped."""
-    nodes = np.sort(nodes)
-    remap = {int(v): i for i, v in enumerate(nodes)}
-    ptr = [0]
-    idx = []
-    for v in nodes:
-        for c in w.children(int(v)):
-            idx.append(remap[int(c)] if c >= 0 else -1)
-        ptr.append(len(idx))
-    return dict(op_type=w.op_type[nodes], child_ptr=np.array(ptr, dtype=np.int64),
-                child_idx=np.array(idx, dtype=np.int32), x_row=w.x_row[nodes])
-
-
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 7])
-def test_parity_full_size_sampled_instances(k):
+def test_parity_full_size_every_node(k):
+    """The full-size workload in the benchmark's launch configuration (HIP
+    graph, planned layout, a replay of the captured graph), every node
+    against the oracle (evaluated instance by instance)."""
     _torch()
     w = WL.make_config(k)
-    f = _fwd(w)           # the benchmark's configuration: HIP graph, planned layout
+    f = _fwd(w)
     f.run()
     f.run()               # a replay of the captured graph
     h, c = f.states()
-    comp = _components(w)
-    roots = np.unique(comp)
-    rng = np.random.default_rng(k)
-    pick = rng.choice(roots, size=min(len(roots), 3), replace=False)
-    # always include the largest instance
-    sizes = {r: int((comp == r).sum()) for r in roots}
-    pick = set(pick.tolist()) | {max(sizes, key=sizes.get)}
-    nodes = np.nonzero(np.isin(comp, list(pick)))[0]
-    sg = _subgraph(w, nodes)
-    hr, cr = evaluate(w.kinds, sg["op_type"], sg["child_ptr"], sg["child_idx"], sg["x_row"], w.x,
-                      w.weights, w.hidden, n_fixed=w.n_children, dtype=w.dtype)
-    hrows = _h_rows(w)[nodes]
-    err = max(normwise_rel_err(h[nodes], hr, rows=hrows), normwise_rel_err(c[nodes], cr))
-    print(f"full k={k}: {w.name} V={w.n_nodes}, checked {len(nodes)} nodes of {len(pick)} instances, "
-          f"err {err:.3e}", flush=True)
-    assert np.isfinite(h).all() and np.isfinite(c).all()
-    assert err <= TOL[w.dtype]
+    hr, cr = evaluate_by_instance(w)
+    _check(w, h, c, hr, cr, f"full k={k}")
+
+
+def test_bench_mode_threads_and_streams_every_node():
+    """The benchmark's own mode: 16 host threads, each with its own stream and
+    arena, call edb_forward (the whole path, eager launches) on the full binary
+    TreeLSTM workload concurrently, three times each.  Every thread's arena
+    holds the oracle's states at every node, bitwise equal across threads and
+    to a single-stream graph replay."""
+    import threading
+    torch = _torch()
+    from paper_2302_03851_amd import edb
+    w = WL.make_config(2)
+    base = _fwd(w)
+    base.run()
+    h0, c0 = base.states()
+    hr, cr = evaluate_by_instance(w)
+    _check(w, h0, c0, hr, cr, "single stream")
+    S, steps = 16, 3
+    streams = [torch.cuda.Stream() for _ in range(S)]
+    arenas = [(torch.full_like(base.arena_h, 9.0), torch.full_like(base.arena_c, -9.0)) for _ in range(S)]
+    fwd = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w),
+                          base.cells)
+    wptrs = [b.data_ptr() for b in base.weights]
+    torch.cuda.synchronize()
+    errors = []
+    start = threading.Barrier(S)
+
+    def worker(i):
+        try:
+            start.wait()
+            ah, ac = arenas[i]
+            for _ in range(steps):
+                fwd.call(wptrs, base.x.data_ptr(), ah.data_ptr(), ac.data_ptr(), ah.shape[0],
+                         streams[i].cuda_stream)
+        except Exception as e:   # reported after the join
+            errors.append((i, e))
+    ths = [threading.Thread(target=worker, args=(i,)) for i in range(S)]
+    for t in ths:
+        t.start()
+    for t in ths:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    s = base.plan.slot
+    for i, (ah, ac) in enumerate(arenas):
+        h = ah.float().cpu().numpy().astype(np.float64)[s]
+        c = ac.cpu().numpy().astype(np.float64)[s]
+        _check(w, h, c, hr, cr, f"thread {i}")
+        np.testing.assert_array_equal(h, h0, err_msg=f"thread {i}")
+        np.testing.assert_array_equal(c, c0, err_msg=f"thread {i}")
 
 
 @pytest.mark.parametrize("k", [2, 3, 4, 5, 7])
