@@ -444,6 +444,31 @@ edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
                        const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
                        int32_t* n_slots, edb_exec_t** exec_out);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): edb_forward without any
+ * device allocation.  The executor's device memory (batch descriptors and
+ * index lists, staged x, the child-sum and MV-RNN scratch rows) lives in one
+ * fixed array of EDB_NOALLOC_SCRATCH_BYTES bytes per device, which the
+ * library's code object holds on every device it runs on until the process
+ * ends; its address is looked up once per device on the first call there.
+ * The descriptors are copied to it on `stream` (from host memory that the
+ * call reads before returning) and every kernel runs eagerly on `stream`.
+ * Arguments and results are those of edb_forward (no executor is handed
+ * back); EDB_USE_GRAPH, EDB_PROFILE and EDB_DRYRUN are rejected
+ * (EDB_ERR_INVALID).  A mini-batch whose device memory exceeds the array is
+ * rejected with EDB_ERR_UNSUPPORTED before anything is enqueued.  The call
+ * makes no hipMalloc, hipFree, stream or event creation.  Every call on a
+ * device shares that device's array and the array keeps the last call's
+ * contents: calls on one device must be ordered (the same stream, or streams
+ * the caller synchronises); calls that overlap on one device race. */
+#define EDB_NOALLOC_SCRATCH_BYTES (32LL << 20)
+edb_status edb_forward_noalloc(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
+                               const int64_t* child_ptr, const int32_t* child_idx, const int32_t* x_row,
+                               const edb_policy* policy, const edb_operand_shape* shapes, int32_t plan_flags,
+                               const edb_cell* cells, int32_t exec_flags, const void* const* packed_weights,
+                               const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
+                               int32_t* n_slots);
+
 /* Wait for `stream` and check the last execution's dataflow launches:
  * EDB_ERR_HIP if a bounded wait timed out (the results are then invalid). */
 edb_status edb_exec_check(edb_exec_t* e, void* stream);

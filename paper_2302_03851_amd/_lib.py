@@ -30,6 +30,7 @@ STREAM_VARIANTS = (11, 12, 13, 14)        # streamed tile: (rows / 16, waves) = 
 STREAM_STAGED = {11: 3, 12: 6, 13: 4, 14: 5}   # the staged variant with the same rows and reduction split
 PART_CELL, PART_CHILD_SUM, PART_FORGET = 0, 1, 2
 FLOW_VARIANT = 100
+NOALLOC_SCRATCH_BYTES = 32 << 20   # EDB_NOALLOC_SCRATCH_BYTES
 
 # every symbol include/edb.h declares
 EXPORTS = [
@@ -40,7 +41,7 @@ EXPORTS = [
     "edb_plan_memory", "edb_plan_view", "edb_plan_free",
     "edb_packed_weight_bytes", "edb_pack_weights",
     "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
-    "edb_exec_check", "edb_exec_free", "edb_forward",
+    "edb_exec_check", "edb_exec_free", "edb_forward", "edb_forward_noalloc",
     "edb_split_phase_bytes", "edb_split_phase", "edb_probe_mfma", "edb_probe_copy",
 ]
 
@@ -143,6 +144,9 @@ def load():
         "edb_forward": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32), P(C.c_int32),
                                     P(Policy), P(OperandShape), C.c_int32, P(Cell), C.c_int32, P(vp), vp, vp, vp,
                                     C.c_int64, vp, P(C.c_int32), P(vp)]),
+        "edb_forward_noalloc": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32),
+                                            P(C.c_int32), P(Policy), P(OperandShape), C.c_int32, P(Cell),
+                                            C.c_int32, P(vp), vp, vp, vp, C.c_int64, vp, P(C.c_int32)]),
         "edb_split_phase_bytes": (C.c_int32, [vp, P(C.c_int64)]),
         "edb_split_phase": (C.c_int32, [vp, vp, vp, vp, vp, C.c_int64, vp, P(C.c_float), C.c_int32]),
         "edb_probe_mfma": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, P(C.c_float), vp, P(C.c_float)]),

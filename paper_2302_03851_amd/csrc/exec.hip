@@ -551,8 +551,9 @@ int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max
 struct DeviceCtx {
     int max_lds = 0;
     int n_cu = 0;
-    hipStream_t upload = nullptr;
+    hipStream_t upload = nullptr;    // created on the first allocating prepare
     hipStream_t release = nullptr;   // stream-ordered frees wait here, off the upload path
+    void* scratch = nullptr;         // this device's address of the allocation-free entry point's array
     std::map<int, int> lds_granted;
     std::map<std::pair<const void*, int>, int> occupancy;   // (kernel, dynamic LDS) -> resident work-groups per CU
     std::vector<hipEvent_t> event_pool;      // timing events of freed EDB_PROFILE executors, for reuse
@@ -560,6 +561,7 @@ struct DeviceCtx {
 std::mutex g_ctx_mu;
 std::map<int, DeviceCtx> g_ctx;
 
+// The device's context (attributes only; nothing is allocated).
 hipError_t device_ctx(int dev, DeviceCtx** out) {
     std::lock_guard<std::mutex> lk(g_ctx_mu);
     auto it = g_ctx.find(dev);
@@ -570,11 +572,18 @@ hipError_t device_ctx(int dev, DeviceCtx** out) {
     DeviceCtx c;
     hipError_t he = hipDeviceGetAttribute(&c.max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (he == hipSuccess) he = hipDeviceGetAttribute(&c.n_cu, hipDeviceAttributeMultiprocessorCount, dev);
-    if (he == hipSuccess) he = hipStreamCreateWithFlags(&c.upload, hipStreamNonBlocking);
-    if (he == hipSuccess) he = hipStreamCreateWithFlags(&c.release, hipStreamNonBlocking);
     if (he != hipSuccess) return he;
     *out = &(g_ctx[dev] = c);
     return hipSuccess;
+}
+
+// The device's upload and release streams, created once (the device is current).
+hipError_t ctx_streams(DeviceCtx* ctx) {
+    std::lock_guard<std::mutex> lk(g_ctx_mu);
+    hipError_t he = hipSuccess;
+    if (!ctx->upload) he = hipStreamCreateWithFlags(&ctx->upload, hipStreamNonBlocking);
+    if (he == hipSuccess && !ctx->release) he = hipStreamCreateWithFlags(&ctx->release, hipStreamNonBlocking);
+    return he;
 }
 
 struct edb_exec {
@@ -596,8 +605,11 @@ struct edb_exec {
     int64_t off_xsrc = 0, off_zero = 0;
     int64_t off_counters = 0, n_counters = 0;   // dataflow counters, cleared every forward
     std::vector<int32_t> hbuf;        // host copy of the device int buffer
-    void* dmem = nullptr;             // one stream-ordered allocation: dbuf | xstaged
+    void* dmem = nullptr;             // one stream-ordered allocation: dbuf | xstaged | scratch rows
     bool dmem_async = true;           // allocated with hipMallocAsync
+    bool dmem_owned = true;           // false: the allocation-free entry point's array
+    // byte sizes of the parts of dmem (each a multiple of 256 but the last)
+    size_t d_ibytes = 0, d_xbytes = 0, d_hbytes = 0, d_rbytes = 0, d_fbytes = 0, d_mbytes = 0, d_total = 0;
     int* dbuf = nullptr;
     void* xstaged = nullptr;
     hipStream_t upload = nullptr;     // the device's upload stream
@@ -628,7 +640,7 @@ struct edb_exec {
         if (gexec) (void)hipGraphExecDestroy(gexec);
         if (graph) (void)hipGraphDestroy(graph);
         if (cap_stream) (void)hipStreamDestroy(cap_stream);
-        if (dmem) {
+        if (dmem && dmem_owned) {
             // free in stream order after the upload and the last execution, on a
             // stream of its own so that later uploads do not queue behind this
             // executor's kernels
@@ -645,8 +657,56 @@ struct edb_exec {
     }
 };
 
+namespace {
+
+// Sizes of the parts of an executor's device memory (descriptor ints, staged
+// x, child-sum scratch rows, MV-RNN vector rows) and their total.
+void layout_device(edb_exec* e) {
+    auto al256 = [](size_t v) { return (v + 255) / 256 * 256; };
+    const size_t esz = e->dtype == EDB_F32 ? 4 : 2;
+    e->d_ibytes = al256(e->hbuf.size() * sizeof(int32_t));
+    e->d_xbytes = (e->n_x > 0 && !(e->flags & EDB_X_DIRECT) && !e->x_in_place)
+                      ? al256((size_t)e->n_x * e->E * esz) : 0;
+    e->d_hbytes = al256((size_t)e->hsum_rows * e->H * 2);
+    e->d_rbytes = al256((size_t)e->hsum_rows * e->H * 4);
+    e->d_fbytes = al256((size_t)e->fc_rows * e->H * 4);
+    e->d_mbytes = (size_t)e->mvu_rows * 2 * e->H * esz;
+    e->d_total = e->d_ibytes + e->d_xbytes + e->d_hbytes + e->d_rbytes + e->d_fbytes + e->d_mbytes;
+}
+
+// Point the executor's device buffers into `base` (d_total bytes, 256-aligned).
+void bind_device(edb_exec* e, void* base_ptr) {
+    uint8_t* base = reinterpret_cast<uint8_t*>(base_ptr);
+    e->dmem = base_ptr;
+    e->dbuf = reinterpret_cast<int*>(base);
+    size_t o = e->d_ibytes;
+    e->xstaged = e->d_xbytes ? base + o : nullptr;
+    o += e->d_xbytes;
+    e->hsum = e->d_hbytes ? base + o : nullptr;
+    o += e->d_hbytes;
+    e->racc = e->d_rbytes ? reinterpret_cast<float*>(base + o) : nullptr;
+    o += e->d_rbytes;
+    e->fc = e->d_fbytes ? reinterpret_cast<float*>(base + o) : nullptr;
+    o += e->d_fbytes;
+    e->mvu = e->d_mbytes ? base + o : nullptr;
+}
+
+// edb_prepare; with noalloc the executor gets no device memory, no upload and
+// no events (the caller binds it to memory of its own and uploads hbuf).
+edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
+                        const edb_cell* cells, int32_t flags, bool noalloc, edb_exec_t** out);
+
+}  // namespace
+
 extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
                                   const edb_cell* cells, int32_t flags, edb_exec_t** out) {
+    return prepare_impl(g, s, p, cells, flags, false, out);
+}
+
+namespace {
+
+edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
+                        const edb_cell* cells, int32_t flags, bool noalloc, edb_exec_t** out) {
     if (!out) return fail(EDB_ERR_INVALID, "edb_prepare: out is NULL");
     *out = nullptr;
     if (!g || !s || !p || !cells) return fail(EDB_ERR_INVALID, "edb_prepare: NULL argument");
@@ -1202,41 +1262,32 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
             F.info.grid = std::max(1, std::min(F.f_ntiles, resident));
         }
 
+        layout_device(e);
         if (!(flags & EDB_DRYRUN)) {
             // descriptors and the staged-x buffer: one stream-ordered allocation
             // on the upload stream, filled asynchronously; executions wait on
             // the `ready` event instead of the host waiting for the copy
-            const size_t ibytes = (hb.size() * sizeof(int32_t) + 255) / 256 * 256;
-            const size_t xbytes = (n_x > 0 && !(flags & EDB_X_DIRECT) && !e->x_in_place)
-                                      ? (size_t)n_x * E * (dtype == EDB_F32 ? 4 : 2) : 0;
-            auto al256 = [](size_t v) { return (v + 255) / 256 * 256; };
-            const size_t hbytes = al256((size_t)e->hsum_rows * H * 2), rbytes = al256((size_t)e->hsum_rows * H * 4);
-            const size_t fbytes = al256((size_t)e->fc_rows * H * 4);
-            const size_t mbytes = (size_t)e->mvu_rows * 2 * H * (dtype == EDB_F32 ? 4 : 2);
-            const size_t total = ibytes + al256(xbytes) + hbytes + rbytes + fbytes + mbytes;
-            e->upload = ctx->upload;
-            e->release = ctx->release;
-            hipError_t he = hipMallocAsync(&e->dmem, total, ctx->upload);
-            if (he != hipSuccess) {
-                (void)hipGetLastError();
-                e->dmem = nullptr;
-                e->dmem_async = false;
-                he = hipMalloc(&e->dmem, total);
+            hipError_t he = noalloc ? hipSuccess : ctx_streams(ctx);
+            if (!noalloc && he == hipSuccess) {
+                e->upload = ctx->upload;
+                e->release = ctx->release;
+                he = hipMallocAsync(&e->dmem, e->d_total, ctx->upload);
+                if (he != hipSuccess) {
+                    (void)hipGetLastError();
+                    e->dmem = nullptr;
+                    e->dmem_async = false;
+                    he = hipMalloc(&e->dmem, e->d_total);
+                }
+                if (he == hipSuccess) {
+                    bind_device(e, e->dmem);
+                    he = hipMemcpyAsync(e->dbuf, hb.data(), hb.size() * sizeof(int32_t), hipMemcpyHostToDevice,
+                                        ctx->upload);
+                }
+                if (he == hipSuccess) he = hipEventCreateWithFlags(&e->ready, hipEventDisableTiming);
+                if (he == hipSuccess) he = hipEventCreateWithFlags(&e->done, hipEventDisableTiming);
+                if (he == hipSuccess) he = hipEventRecord(e->ready, ctx->upload);
             }
-            if (he == hipSuccess) {
-                uint8_t* base = reinterpret_cast<uint8_t*>(e->dmem);
-                e->dbuf = reinterpret_cast<int*>(e->dmem);
-                e->xstaged = xbytes ? base + ibytes : nullptr;
-                e->hsum = hbytes ? base + ibytes + al256(xbytes) : nullptr;
-                e->racc = rbytes ? reinterpret_cast<float*>(base + ibytes + al256(xbytes) + hbytes) : nullptr;
-                e->fc = fbytes ? reinterpret_cast<float*>(base + ibytes + al256(xbytes) + hbytes + rbytes) : nullptr;
-                e->mvu = mbytes ? base + ibytes + al256(xbytes) + hbytes + rbytes + fbytes : nullptr;
-                he = hipMemcpyAsync(e->dbuf, hb.data(), hb.size() * sizeof(int32_t), hipMemcpyHostToDevice, ctx->upload);
-            }
-            if (he == hipSuccess) he = hipEventCreateWithFlags(&e->ready, hipEventDisableTiming);
-            if (he == hipSuccess) he = hipEventCreateWithFlags(&e->done, hipEventDisableTiming);
-            if (he == hipSuccess) he = hipEventRecord(e->ready, ctx->upload);
-            if (flags & EDB_PROFILE) {
+            if (!noalloc && (flags & EDB_PROFILE)) {
                 e->ctx = ctx;
                 e->events.assign(2 * e->launches.size(), nullptr);
                 {
@@ -1274,8 +1325,6 @@ extern "C" edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s,
     *out = e;
     return EDB_OK;
 }
-
-namespace {
 
 // Launch L's arguments with the pointers of one execution filled in (w may be
 // NULL when no weights are read).
@@ -1424,20 +1473,32 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
 
 }  // namespace
 
+namespace {
+
+// Argument checks of an execution (name: the entry point, for the message).
+edb_status check_exec_args(const edb_exec* e, const void* const* w, const void* x, const void* arena_h,
+                           const void* arena_c, const char* name) {
+    const std::string n(name);
+    if (!w || !arena_h || !arena_c) return fail(EDB_ERR_INVALID, n + ": NULL argument");
+    if (e->n_x > 0 && !x) return fail(EDB_ERR_INVALID, n + ": x is NULL");
+    for (int32_t t = 0; t < e->T; ++t)
+        if (!w[t]) return fail(EDB_ERR_INVALID, n + ": packed weights of type " + std::to_string(t) + " are NULL");
+    auto misaligned = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) != 0; };
+    if (misaligned(x) || misaligned(arena_h) || misaligned(arena_c))
+        return fail(EDB_ERR_INVALID, n + ": device buffers must be 16-byte aligned");
+    for (int32_t t = 0; t < e->T; ++t)
+        if (reinterpret_cast<uintptr_t>(w[t]) & 255u)
+            return fail(EDB_ERR_INVALID, n + ": packed weights must be 256-byte aligned");
+    return EDB_OK;
+}
+
+}  // namespace
+
 extern "C" edb_status edb_execute(edb_exec_t* e, const void* const* w, const void* x, void* arena_h,
                                   void* arena_c, void* stream) {
     if (!e) return fail(EDB_ERR_INVALID, "edb_execute: exec is NULL");
     if (e->flags & EDB_DRYRUN) return EDB_OK;
-    if (!w || !arena_h || !arena_c) return fail(EDB_ERR_INVALID, "edb_execute: NULL argument");
-    if (e->n_x > 0 && !x) return fail(EDB_ERR_INVALID, "edb_execute: x is NULL");
-    for (int32_t t = 0; t < e->T; ++t)
-        if (!w[t]) return fail(EDB_ERR_INVALID, "edb_execute: packed weights of type " + std::to_string(t) + " are NULL");
-    auto misaligned = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) != 0; };
-    if (misaligned(x) || misaligned(arena_h) || misaligned(arena_c))
-        return fail(EDB_ERR_INVALID, "edb_execute: device buffers must be 16-byte aligned");
-    for (int32_t t = 0; t < e->T; ++t)
-        if (reinterpret_cast<uintptr_t>(w[t]) & 255u)
-            return fail(EDB_ERR_INVALID, "edb_execute: packed weights must be 256-byte aligned");
+    if (edb_status cs = check_exec_args(e, w, x, arena_h, arena_c, "edb_execute")) return cs;
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     hipError_t he = hipStreamWaitEvent(st, e->ready, 0);   // descriptors are on the device
     if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_execute: ") + hipGetErrorString(he));
@@ -1680,3 +1741,78 @@ extern "C" edb_status edb_exec_check(edb_exec_t* e, void* stream) {
 }
 
 extern "C" void edb_exec_free(edb_exec_t* e) { delete e; }
+
+// ---------------------------------------------------------------------------
+// Allocation-free forward pass: the executor's device memory (descriptor ints,
+// staged x, child-sum and MV-RNN scratch rows) lives in one fixed array per
+// device instead of a per-call allocation.  Each device that runs this entry
+// point holds its own copy of the array for the life of the process; every
+// call on a device shares it, so calls that overlap on one device race.
+
+constexpr size_t kNoAllocScratchBytes = (size_t)EDB_NOALLOC_SCRATCH_BYTES;
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+extern "C" edb_status edb_forward_noalloc(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
+                                          const int64_t* child_ptr, const int32_t* child_idx,
+                                          const int32_t* x_row, const edb_policy* policy,
+                                          const edb_operand_shape* shapes, int32_t plan_flags,
+                                          const edb_cell* cells, int32_t exec_flags,
+                                          const void* const* packed_weights, const void* x, void* arena_h,
+                                          void* arena_c, int64_t arena_rows, void* stream, int32_t* n_slots) {
+    if (exec_flags & (EDB_DRYRUN | EDB_PROFILE | EDB_USE_GRAPH))
+        return fail(EDB_ERR_INVALID, "edb_forward_noalloc: EDB_DRYRUN, EDB_PROFILE and EDB_USE_GRAPH are not allowed");
+    int dev = 0;
+    DeviceCtx* ctx = nullptr;
+    hipError_t he = hipGetDevice(&dev);
+    if (he == hipSuccess) he = device_ctx(dev, &ctx);
+    if (he == hipSuccess) {
+        // the array's address on this device, looked up once per device (with
+        // the device current); the array's name is not a device address in host code
+        std::lock_guard<std::mutex> lk(g_ctx_mu);
+        if (!ctx->scratch) {
+            void* ptr = nullptr;
+            he = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+            if (he == hipSuccess) ctx->scratch = ptr;
+        }
+    }
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_forward_noalloc: ") + hipGetErrorString(he));
+    edb_graph_t* g = nullptr;
+    edb_schedule_t* s = nullptr;
+    edb_plan_t* p = nullptr;
+    edb_exec_t* e = nullptr;
+    edb_status st = edb_build_graph(n_nodes, n_types, op_type, child_ptr, child_idx, x_row, &g);
+    if (st == EDB_OK) st = edb_schedule(g, policy, &s);
+    if (st == EDB_OK) st = edb_plan_memory(g, s, shapes, plan_flags, &p);
+    if (st == EDB_OK) {
+        if (n_slots) *n_slots = p->n_slots;
+        if (arena_rows < p->n_slots)
+            st = fail(EDB_ERR_INVALID, "edb_forward_noalloc: the arena has " + std::to_string(arena_rows) +
+                                           " rows, the plan needs " + std::to_string(p->n_slots));
+    }
+    if (st == EDB_OK) st = prepare_impl(g, s, p, cells, exec_flags, true, &e);
+    if (st == EDB_OK) st = check_exec_args(e, packed_weights, x, arena_h, arena_c, "edb_forward_noalloc");
+    if (st == EDB_OK && e->d_total > kNoAllocScratchBytes)
+        st = fail(EDB_ERR_UNSUPPORTED, "edb_forward_noalloc: this mini-batch needs " + std::to_string(e->d_total) +
+                                           " bytes of device scratch, the fixed array holds " +
+                                           std::to_string(kNoAllocScratchBytes));
+    if (st == EDB_OK) {
+        bind_device(e, ctx->scratch);
+        e->dmem_owned = false;
+        hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+        // the descriptors in stream order before the kernels that read them
+        // (the host array is read before the call returns: a copy from pageable
+        // memory is staged synchronously)
+        he = hipMemcpyAsync(e->dbuf, e->hbuf.data(), e->hbuf.size() * sizeof(int32_t), hipMemcpyHostToDevice, hs);
+        if (he == hipSuccess) he = launch_all(e, packed_weights, x, arena_h, arena_c, hs);
+        if (he != hipSuccess) st = fail(EDB_ERR_HIP, std::string("edb_forward_noalloc: ") + hipGetErrorString(he));
+    }
+    const std::string err = st == EDB_OK ? std::string() : std::string(edb_last_error());
+    edb_exec_free(e);
+    edb_plan_free(p);
+    edb_schedule_free(s);
+    edb_graph_free(g);
+    if (st != EDB_OK) return fail(st, err);
+    edb::clear_error();
+    return EDB_OK;
+}

@@ -308,6 +308,15 @@ class ForwardCall:
                                      C.byref(self.n_slots), C.byref(h) if keep else None), "edb_forward")
         return ExecRecord(h) if keep else None
 
+    def call_noalloc(self, weight_ptrs, x_ptr, arena_h_ptr, arena_c_ptr, arena_rows, stream):
+        """The same mini-batch through edb_forward_noalloc (no device
+        allocation; the library's fixed per-device array holds the
+        executor's device memory)."""
+        arr = (C.c_void_p * len(weight_ptrs))(*weight_ptrs)
+        L.check(L.load().edb_forward_noalloc(*self._args, arr, C.c_void_p(x_ptr), C.c_void_p(arena_h_ptr),
+                                             C.c_void_p(arena_c_ptr), arena_rows, C.c_void_p(stream),
+                                             C.byref(self.n_slots)), "edb_forward_noalloc")
+
 
 class ExecRecord:
     """An executor handed back by edb_forward: launch records and times."""
