@@ -483,7 +483,7 @@ def main():
     ap.add_argument("--replays", type=int, default=200)
     ap.add_argument("--streams", type=int, default=16,
                     help="mini-batches in flight: host worker threads, each with its own stream and arena")
-    ap.add_argument("--roofline-steps", type=int, default=10,
+    ap.add_argument("--roofline-steps", type=int, default=50,
                     help="steps of the roofline pass (one mini-batch in flight, launches timed with HIP events)")
     ap.add_argument("--policy", default="table", choices=sorted(POLICIES),
                     help="batching policy: the configured FSM table (default), a table learned on the "
@@ -642,6 +642,12 @@ def main():
             for t in self.threads:
                 t.join()
 
+    # every worker stream has run a kernel before the first step (a stream's
+    # first dispatch binds it to a hardware queue, a one-time cost)
+    for st_ in streams:
+        with torch.cuda.stream(st_):
+            torch.zeros(1, device=dev).add_(1.0)
+    torch.cuda.synchronize()
     pool = Workers()
     pool.run(args.warmup)
     torch.cuda.synchronize()
