@@ -342,6 +342,8 @@ edb_status edb_pack_weights(const edb_cell* cell, const float* const* logical,
 #define EDB_NO_SPLIT_K  64  /* small tiles without split-K only (each accumulator sums its k-groups in order) */
 #define EDB_TILE_LARGE 128  /* the large bf16 tile for every batch it supports, whatever the batch size */
 #define EDB_NO_LARGE   256  /* never the large tile (ablation) */
+#define EDB_FLOW_DRYRUN 512 /* with EDB_DRYRUN only: build the dataflow launches (switched off on the
+                               GPU) so that edb_exec_validate can check their descriptors */
 
 typedef struct edb_exec edb_exec_t;
 
@@ -468,6 +470,21 @@ edb_status edb_forward_noalloc(int32_t n_nodes, int32_t n_types, const int32_t* 
                                const edb_cell* cells, int32_t exec_flags, const void* const* packed_weights,
                                const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
                                int32_t* n_slots);
+
+/* Host-side check of an executor's device descriptors (works on EDB_DRYRUN
+ * handles; no HIP call).  The int buffer that edb_prepare uploads is decoded
+ * the way the kernels read it: every launch's operand lists (positional,
+ * ragged, x and result lists, ragged offsets) and, for a dataflow launch, its
+ * batch descriptors, tile records, dependency ranges and counter offsets.
+ * Every read is bounds-checked; the forward pass is replayed at the level of
+ * arena rows (each result slot written once, never the zero row or a pad,
+ * every row read after the launch or the dataflow row tile that writes it,
+ * which must be among the reading row tile's dependencies and hold smaller
+ * tickets), and each dataflow launch's ticket and dependency protocol is
+ * emulated with min(n_workers, grid) work-groups in several interleavings.
+ * *checked (may be NULL): launches and dataflow row tiles checked.
+ * EDB_ERR_INVALID with the first problem found in edb_last_error(). */
+edb_status edb_exec_validate(const edb_exec_t* e, int32_t n_workers, int64_t* checked);
 
 /* Wait for `stream` and check the last execution's dataflow launches:
  * EDB_ERR_HIP if a bounded wait timed out (the results are then invalid). */

@@ -23,7 +23,7 @@ PLAN_RC, PLAN_IDENTITY, PLAN_PQ = 0, 1, 2
 SEG_NONE, SEG_CONTIG, SEG_GATHER, SEG_SCATTER = 0, 1, 2, 3
 F32, BF16 = 0, 1
 USE_GRAPH, DRYRUN, FORCE_GATHER, X_DIRECT, PROFILE, NO_FLOW = 1, 2, 4, 8, 16, 32
-NO_SPLIT_K, TILE_LARGE, NO_LARGE = 64, 128, 256
+NO_SPLIT_K, TILE_LARGE, NO_LARGE, FLOW_DRYRUN = 64, 128, 256, 512
 LARGE_VARIANTS = (8, 9, 10, 15, 16)      # large tile size classes 0, 1, 2, 3, 4
 LARGE_CLASS = {8: 0, 9: 1, 10: 2, 15: 3, 16: 4}
 STREAM_VARIANTS = (11, 12, 13, 14)        # streamed tile: (rows / 16, waves) = (1, 4), (2, 4), (1, 8), (1, 16)
@@ -41,7 +41,7 @@ EXPORTS = [
     "edb_plan_memory", "edb_plan_view", "edb_plan_free",
     "edb_packed_weight_bytes", "edb_pack_weights",
     "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
-    "edb_exec_check", "edb_exec_free", "edb_forward", "edb_forward_noalloc",
+    "edb_exec_check", "edb_exec_validate", "edb_exec_free", "edb_forward", "edb_forward_noalloc",
     "edb_split_phase_bytes", "edb_split_phase", "edb_probe_mfma", "edb_probe_copy",
 ]
 
@@ -140,6 +140,7 @@ def load():
         "edb_exec_launch_info": (C.c_int32, [vp, C.c_int32, P(LaunchInfo)]),
         "edb_exec_launch_times": (C.c_int32, [vp, P(C.c_float), C.c_int32]),
         "edb_exec_check": (C.c_int32, [vp, vp]),
+        "edb_exec_validate": (C.c_int32, [vp, C.c_int32, P(C.c_int64)]),
         "edb_exec_free": (None, [vp]),
         "edb_forward": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32), P(C.c_int32),
                                     P(Policy), P(OperandShape), C.c_int32, P(Cell), C.c_int32, P(vp), vp, vp, vp,

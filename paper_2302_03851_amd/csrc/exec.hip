@@ -12,6 +12,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "big_tile.h"
@@ -711,8 +712,10 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
     *out = nullptr;
     if (!g || !s || !p || !cells) return fail(EDB_ERR_INVALID, "edb_prepare: NULL argument");
     if (flags & ~(EDB_USE_GRAPH | EDB_DRYRUN | EDB_FORCE_GATHER | EDB_X_DIRECT | EDB_PROFILE | EDB_NO_FLOW |
-                  EDB_NO_SPLIT_K | EDB_TILE_LARGE | EDB_NO_LARGE))
+                  EDB_NO_SPLIT_K | EDB_TILE_LARGE | EDB_NO_LARGE | EDB_FLOW_DRYRUN))
         return fail(EDB_ERR_INVALID, "edb_prepare: unknown flags");
+    if ((flags & EDB_FLOW_DRYRUN) && !(flags & EDB_DRYRUN))
+        return fail(EDB_ERR_INVALID, "edb_prepare: EDB_FLOW_DRYRUN needs EDB_DRYRUN (dataflow launches are switched off)");
     if ((flags & EDB_TILE_LARGE) && (flags & EDB_NO_LARGE))
         return fail(EDB_ERR_INVALID, "edb_prepare: EDB_TILE_LARGE and EDB_NO_LARGE exclude each other");
     if (s->V != g->V || p->V != g->V || p->B != (int32_t)s->batch_type.size())
@@ -1066,7 +1069,8 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
         // is bounded in time); until the cause is shown, every batch runs as
         // its own launch.  The code below stays for that analysis.
         constexpr bool kFlowEnabled = false;
-        const bool flow_on = kFlowEnabled && !(flags & EDB_NO_FLOW) && T <= FLOW_MAX_TYPES && flow_max_m > 0;
+        const bool flow_on = (kFlowEnabled || (flags & EDB_FLOW_DRYRUN)) && !(flags & EDB_NO_FLOW) &&
+                             T <= FLOW_MAX_TYPES && flow_max_m > 0;
         std::vector<int> run_of(B, -1);
         {
             int b = 0, nrun = 0;
@@ -1813,6 +1817,369 @@ extern "C" edb_status edb_forward_noalloc(int32_t n_nodes, int32_t n_types, cons
     edb_schedule_free(s);
     edb_graph_free(g);
     if (st != EDB_OK) return fail(st, err);
+    edb::clear_error();
+    return EDB_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Host-side validation of an executor's device descriptors: the int buffer
+// that edb_prepare uploads is decoded here the way the kernels read it (the
+// same BatchArgs offsets, the same BatchDesc / tile / dependency records of a
+// dataflow launch) and every read is bounds-checked; the forward pass is then
+// replayed at the level of arena rows (each result slot written once, every
+// row read after its producer), and a dataflow launch's ticket and dependency
+// protocol is emulated with a bounded number of work-groups.
+
+namespace {
+
+struct VCheck {
+    std::string err;
+    bool ok() const { return err.empty(); }
+    bool fail(const std::string& m) {
+        if (err.empty()) err = m;
+        return false;
+    }
+};
+
+// One operand list resolved against the int buffer: entry r's row.
+struct VList {
+    int kind = S_NONE;
+    int base = 0;
+    int64_t off = -1;
+};
+
+bool v_list(VCheck& c, const std::vector<int32_t>& hb, const VList& l, int64_t n, int64_t rows,
+            std::vector<int32_t>& out, const std::string& what) {
+    out.clear();
+    if (l.kind == S_NONE) return true;
+    if (l.kind != S_CONTIG && l.kind != S_INDEXED) return c.fail(what + ": unknown list kind");
+    if (n < 0) return c.fail(what + ": negative length");
+    if (l.kind == S_INDEXED && (l.off < 0 || l.off + n > (int64_t)hb.size()))
+        return c.fail(what + ": index list [" + std::to_string(l.off) + ", +" + std::to_string(n) +
+                      ") outside the int buffer of " + std::to_string(hb.size()));
+    out.resize((size_t)n);
+    for (int64_t r = 0; r < n; ++r) {
+        const int64_t v = l.kind == S_CONTIG ? (int64_t)l.base + r : hb[(size_t)(l.off + r)];
+        if (v < 0 || v >= rows)
+            return c.fail(what + ": entry " + std::to_string(r) + " is row " + std::to_string(v) + " of " +
+                          std::to_string(rows));
+        out[(size_t)r] = (int32_t)v;
+    }
+    return true;
+}
+
+// The arena rows one batch's cell kernel (or one tile's rows [r0, r1) of it)
+// reads and writes, from its lists.
+struct VBatch {
+    int kind, m, H, Hk, Hu, E, Ep, K, G, nfix;
+    bool x, rag;
+    VList lx, lf[2], lrag, lres;
+    int64_t rptr = -1;
+    int64_t n_xrows = 0;
+};
+
+bool v_batch_rows(VCheck& c, const std::vector<int32_t>& hb, const VBatch& b, int64_t n_slots, int r0, int r1,
+                  std::vector<int32_t>& reads, std::vector<int32_t>& writes, const std::string& what) {
+    reads.clear();
+    writes.clear();
+    std::vector<int32_t> t;
+    if (!v_list(c, hb, b.lres, b.m, n_slots, t, what + " result list")) return false;
+    if (b.lres.kind != S_NONE)
+        for (int r = r0; r < r1; ++r) writes.push_back(t[(size_t)r]);
+    for (int p = 0; p < b.nfix; ++p) {
+        if (!v_list(c, hb, b.lf[p], b.m, n_slots, t, what + " child list " + std::to_string(p))) return false;
+        if (b.lf[p].kind != S_NONE)
+            for (int r = r0; r < r1; ++r) reads.push_back(t[(size_t)r]);
+    }
+    if (b.x && b.lx.kind != S_NONE && !v_list(c, hb, b.lx, b.m, b.n_xrows, t, what + " x list")) return false;
+    if (b.rag) {
+        if (b.rptr < 0 || b.rptr + b.m + 1 > (int64_t)hb.size())
+            return c.fail(what + ": ragged offsets outside the int buffer");
+        const int32_t* rp = hb.data() + b.rptr;
+        if (rp[0] != 0) return c.fail(what + ": ragged offsets do not start at 0");
+        for (int r = 0; r < b.m; ++r)
+            if (rp[r + 1] < rp[r]) return c.fail(what + ": ragged offsets decrease at row " + std::to_string(r));
+        if (!v_list(c, hb, b.lrag, rp[b.m], n_slots, t, what + " ragged list")) return false;
+        if (b.lrag.kind != S_NONE)
+            for (int64_t k = rp[r0]; k < rp[r1]; ++k) reads.push_back(t[(size_t)k]);
+    }
+    // trip counts of the tile loops
+    if (b.K <= 0 || b.K > 3 * 4096 + 64) return c.fail(what + ": reduction length " + std::to_string(b.K));
+    if (b.Hu % 64 || b.Hu < b.H || b.Hk < b.H) return c.fail(what + ": padded widths");
+    return true;
+}
+
+}  // namespace
+
+extern "C" edb_status edb_exec_validate(const edb_exec_t* e, int32_t n_workers, int64_t* checked) {
+    if (!e) return fail(EDB_ERR_INVALID, "edb_exec_validate: exec is NULL");
+    if (n_workers < 1) return fail(EDB_ERR_INVALID, "edb_exec_validate: n_workers must be positive");
+    const std::vector<int32_t>& hb = e->hbuf;
+    const int64_t n_slots = e->n_slots;
+    const bool x_caller = (e->flags & EDB_X_DIRECT) || e->x_in_place;
+    const int64_t n_xrows = x_caller ? e->x_direct_rows : e->n_x;
+    VCheck c;
+    int64_t n_checked = 0;
+    // rows: -2 never written, -1 zero / pad row (cleared before any batch), else the writing launch
+    std::vector<int64_t> written((size_t)n_slots, -2);
+    // the zero row and the pads
+    if (e->off_zero < 0 || e->off_zero + e->n_zero > (int64_t)hb.size())
+        return fail(EDB_ERR_INVALID, "edb_exec_validate: zero-row list outside the int buffer");
+    for (int i = 0; i < e->n_zero; ++i) {
+        const int64_t z = hb[(size_t)(e->off_zero + i)];
+        if (z < 0 || z >= n_slots) return fail(EDB_ERR_INVALID, "edb_exec_validate: zero/pad row out of range");
+        written[(size_t)z] = -1;
+    }
+    if (hb[(size_t)e->off_zero] != 0) return fail(EDB_ERR_INVALID, "edb_exec_validate: the zero row is not slot 0");
+    // staged x source rows
+    if (!x_caller && e->n_x > 0) {
+        if (e->off_xsrc < 0 || e->off_xsrc + e->n_x > (int64_t)hb.size())
+            return fail(EDB_ERR_INVALID, "edb_exec_validate: x source rows outside the int buffer");
+        for (int32_t i = 0; i < e->n_x; ++i) {
+            const int32_t r = hb[(size_t)(e->off_xsrc + i)];
+            if (r < 0 || r >= e->x_direct_rows)
+                return fail(EDB_ERR_INVALID, "edb_exec_validate: x source row " + std::to_string(r) + " out of range");
+        }
+    }
+    // the dataflow counters are zero in the upload and the staging launch clears them
+    if (e->off_counters < 0 || e->off_counters + e->n_counters > (int64_t)hb.size())
+        return fail(EDB_ERR_INVALID, "edb_exec_validate: counter region outside the int buffer");
+    for (int64_t i = 0; i < e->n_counters; ++i)
+        if (hb[(size_t)(e->off_counters + i)] != 0) return fail(EDB_ERR_INVALID, "edb_exec_validate: counter not zero");
+    if (e->n_counters > 0 && e->launches[0].info.grid == 0)
+        return fail(EDB_ERR_INVALID, "edb_exec_validate: dataflow counters but no staging launch to clear them");
+
+    auto batch_of = [&](const Launch& L) {
+        VBatch b{};
+        const Dims& d = e->dims[L.type];
+        const KindInfo ki = kind_info(e->cells[L.type].kind);
+        b.kind = L.info.kind;
+        b.m = L.args.m;
+        b.H = d.H; b.Hk = d.Hk; b.Hu = d.Hu; b.E = d.E; b.Ep = d.Ep; b.K = d.K; b.G = d.G;
+        b.nfix = ki.nfix;
+        b.x = ki.x;
+        b.rag = ki.rag;
+        b.lx = VList{L.args.x.kind, L.args.x.base, L.off_x};
+        b.lf[0] = VList{L.args.fix[0].kind, L.args.fix[0].base, L.off_f0};
+        b.lf[1] = VList{L.args.fix[1].kind, L.args.fix[1].base, L.off_f1};
+        b.lrag = VList{L.args.rag.kind, L.args.rag.base, L.off_rag};
+        b.lres = VList{L.args.res.kind, L.args.res.base, L.off_res};
+        b.rptr = L.off_rptr;
+        b.n_xrows = n_xrows;
+        return b;
+    };
+    std::vector<int32_t> rd, wr;
+    auto commit = [&](int64_t li, const std::string& what) {
+        for (int32_t v : rd)
+            if (written[(size_t)v] == -2)
+                return c.fail(what + ": reads row " + std::to_string(v) + " before any launch writes it");
+        for (int32_t v : wr) {
+            if (v == 0 || written[(size_t)v] == -1)
+                return c.fail(what + ": writes the zero row or a pad row (" + std::to_string(v) + ")");
+            if (written[(size_t)v] != -2)
+                return c.fail(what + ": writes row " + std::to_string(v) + " a second time");
+            written[(size_t)v] = li;
+        }
+        return true;
+    };
+
+    for (size_t li = 1; li < e->launches.size() && c.ok(); ++li) {
+        const Launch& L = e->launches[li];
+        const std::string what = "launch " + std::to_string(li) + " (batch " + std::to_string(L.info.batch) + ")";
+        if (!L.flow) {
+            if (L.kk < 0 || L.info.part != 0) {
+                // the parts before a batch's cell kernel read its lists; they write scratch rows only
+                VBatch b = batch_of(L);
+                b.lres.kind = S_NONE;
+                if (L.info.part == 2) {   // forget GEMM: x = the child list, m = children
+                    b.rag = false;
+                    b.nfix = 0;
+                    b.x = true;
+                    b.lx = VList{L.args.x.kind, L.args.x.base, L.off_x};
+                    b.n_xrows = n_slots;
+                    std::vector<int32_t> t;
+                    if (!v_list(c, hb, b.lx, L.args.m, n_slots, t, what + " child rows")) break;
+                    for (int32_t v : t)
+                        if (written[(size_t)v] == -2) { c.fail(what + ": reads an unwritten child row"); break; }
+                    ++n_checked;
+                    continue;
+                }
+                b.x = false;
+                if (!v_batch_rows(c, hb, b, n_slots, 0, b.m, rd, wr, what)) break;
+                wr.clear();
+                if (!commit((int64_t)li, what)) break;
+                ++n_checked;
+                continue;
+            }
+            VBatch b = batch_of(L);
+            if (b.lres.kind == S_NONE) { c.fail(what + ": no result list"); break; }
+            if (L.kk == K_CS_PARENT || L.kk == K_MV_VEC) b.x = false;   // rows from scratch written just before
+            if (L.kk == K_CS_PARENT) b.rag = false;                     // its children were read by the parts
+            if (!v_batch_rows(c, hb, b, n_slots, 0, b.m, rd, wr, what)) break;
+            if (!commit((int64_t)li, what)) break;
+            ++n_checked;
+            continue;
+        }
+        // ---- dataflow launch ----
+        const int nb = L.info.n_batches;
+        if (L.f_desc < 0 || L.f_desc % 4 || L.f_desc + (int64_t)nb * (int64_t)(sizeof(BatchDesc) / 4) > (int64_t)hb.size())
+            { c.fail(what + ": batch descriptors outside the int buffer or misaligned"); break; }
+        const BatchDesc* bd = reinterpret_cast<const BatchDesc*>(hb.data() + L.f_desc);
+        const int need = L.f_need;
+        std::vector<VBatch> vb((size_t)nb);
+        std::vector<int> rt_base((size_t)nb + 1, 0);
+        for (int q = 0; q < nb && c.ok(); ++q) {
+            const BatchDesc& d = bd[q];
+            if (d.type < 0 || d.type >= e->T) { c.fail(what + ": descriptor type"); break; }
+            const KindInfo ki = kind_info(d.kind);
+            if (ki.G == 0 || d.kind != e->cells[d.type].kind) { c.fail(what + ": descriptor kind"); break; }
+            const Dims& dm = e->dims[d.type];
+            if (d.H != dm.H || d.Hk != dm.Hk || d.Hu != dm.Hu || d.E != dm.E || d.Ep != dm.Ep || d.K != dm.K)
+                { c.fail(what + ": descriptor dimensions differ from the cell's"); break; }
+            if (d.off_b != (int)dm.off_b || d.off_Wr != (int)dm.off_Wr || d.off_br != (int)dm.off_br)
+                { c.fail(what + ": descriptor weight offsets"); break; }
+            if (d.x_staged != (x_caller ? 0 : 1)) { c.fail(what + ": descriptor x source"); break; }
+            if (d.m < 1) { c.fail(what + ": empty batch in a run"); break; }
+            VBatch& b = vb[(size_t)q];
+            b.kind = d.kind; b.m = d.m; b.H = d.H; b.Hk = d.Hk; b.Hu = d.Hu; b.E = d.E; b.Ep = d.Ep; b.K = d.K;
+            b.G = ki.G; b.nfix = ki.nfix; b.x = ki.x; b.rag = ki.rag;
+            VList* ls[5] = {&b.lx, &b.lf[0], &b.lf[1], &b.lrag, &b.lres};
+            for (int i = 0; i < 5; ++i) *ls[i] = VList{d.seg_kind[i], d.seg_base[i], d.seg_off[i]};
+            b.rptr = d.rptr_off;
+            b.n_xrows = n_xrows;
+            if (b.Hu / (16 * FLOW_WU) != need) { c.fail(what + ": unit tiles of a batch differ from `need`"); break; }
+            rt_base[(size_t)q + 1] = rt_base[(size_t)q] + (d.m + 16 * FLOW_RT - 1) / (16 * FLOW_RT);
+        }
+        if (!c.ok()) break;
+        const int nrt = rt_base[(size_t)nb];
+        if (L.f_tiles < 0 || L.f_tiles % 4 || L.f_tiles + 4LL * L.f_ntiles > (int64_t)hb.size())
+            { c.fail(what + ": tile records outside the int buffer or misaligned"); break; }
+        if (L.f_rtdeps < 0 || L.f_rtdeps % 2 || L.f_rtdeps + 2LL * nrt > (int64_t)hb.size())
+            { c.fail(what + ": dependency ranges outside the int buffer or misaligned"); break; }
+        if (L.f_ticket < e->off_counters || L.f_error != L.f_ticket + 1 || L.f_done != L.f_ticket + 2 ||
+            L.f_done + nrt > e->off_counters + e->n_counters)
+            { c.fail(what + ": counters outside the counter region"); break; }
+        if (L.args.m < 1) { c.fail(what + ": wait bound"); break; }
+        if (L.info.grid < 1 || L.info.grid > L.f_ntiles) { c.fail(what + ": grid"); break; }
+        const int4* tiles = reinterpret_cast<const int4*>(hb.data() + L.f_tiles);
+        const int2* rdep = reinterpret_cast<const int2*>(hb.data() + L.f_rtdeps);
+        // tiles in (batch, row tile, unit tile) order, `need` unit tiles per row tile
+        std::vector<int> first_ticket((size_t)nrt, -1), last_ticket((size_t)nrt, -1), count((size_t)nrt, 0);
+        std::vector<int> rt_batch((size_t)nrt, -1), rt_row((size_t)nrt, -1);
+        for (int t = 0; t < L.f_ntiles && c.ok(); ++t) {
+            const int4 tl = tiles[t];
+            if (tl.x < 0 || tl.x >= nb) { c.fail(what + ": tile " + std::to_string(t) + " batch"); break; }
+            const VBatch& b = vb[(size_t)tl.x];
+            if (tl.y < 0 || tl.y * 16 * FLOW_RT >= b.m) { c.fail(what + ": tile " + std::to_string(t) + " row tile"); break; }
+            if (tl.z < 0 || tl.z >= need) { c.fail(what + ": tile " + std::to_string(t) + " unit tile"); break; }
+            if (tl.w != rt_base[(size_t)tl.x] + tl.y) { c.fail(what + ": tile " + std::to_string(t) + " row-tile id"); break; }
+            if (t > 0) {
+                const int4 p = tiles[t - 1];
+                if (std::make_tuple(p.x, p.y, p.z) >= std::make_tuple(tl.x, tl.y, tl.z))
+                    { c.fail(what + ": tiles out of order at " + std::to_string(t)); break; }
+            }
+            if (first_ticket[(size_t)tl.w] < 0) first_ticket[(size_t)tl.w] = t;
+            last_ticket[(size_t)tl.w] = t;
+            ++count[(size_t)tl.w];
+            rt_batch[(size_t)tl.w] = tl.x;
+            rt_row[(size_t)tl.w] = tl.y;
+        }
+        if (!c.ok()) break;
+        for (int r = 0; r < nrt; ++r)
+            if (count[(size_t)r] != need) { c.fail(what + ": row tile " + std::to_string(r) + " has " +
+                                                   std::to_string(count[(size_t)r]) + " unit tiles, need " +
+                                                   std::to_string(need)); break; }
+        if (!c.ok()) break;
+        int64_t ndeps = 0;
+        for (int r = 0; r < nrt; ++r) ndeps = std::max<int64_t>(ndeps, (int64_t)rdep[r].x + rdep[r].y);
+        if (L.f_deps < 0 || L.f_deps + ndeps > (int64_t)hb.size()) { c.fail(what + ": dependency list outside"); break; }
+        const int32_t* deps = hb.data() + L.f_deps;
+        // per row tile: its reads are produced by earlier launches or by its
+        // dependencies, whose every unit tile holds a smaller ticket
+        std::vector<int64_t> run_writer((size_t)n_slots, -1);   // row tile of this run writing the slot
+        for (int q = 0; q < nb; ++q)
+            if (vb[(size_t)q].lres.kind == S_NONE) c.fail(what + ": batch " + std::to_string(q) + " has no result list");
+        for (int r = 0; r < nrt && c.ok(); ++r) {
+            const VBatch& b = vb[(size_t)rt_batch[(size_t)r]];
+            const int r0 = rt_row[(size_t)r] * 16 * FLOW_RT, r1 = std::min(b.m, r0 + 16 * FLOW_RT);
+            const std::string tw = what + " row tile " + std::to_string(r);
+            if (!v_batch_rows(c, hb, b, n_slots, r0, r1, rd, wr, tw)) break;
+            const int2 di = rdep[r];
+            if (di.x < 0 || di.y < 0) { c.fail(tw + ": dependency range"); break; }
+            std::vector<int> dl(deps + di.x, deps + di.x + di.y);
+            for (int dp : dl) {
+                if (dp < 0 || dp >= nrt) { c.fail(tw + ": dependency " + std::to_string(dp) + " out of range"); break; }
+                if (last_ticket[(size_t)dp] >= first_ticket[(size_t)r])
+                    { c.fail(tw + ": depends on row tile " + std::to_string(dp) + " with a later ticket"); break; }
+            }
+            if (!c.ok()) break;
+            for (int32_t v : rd) {
+                if (written[(size_t)v] != -2) continue;   // zero / pad row or an earlier launch
+                const int64_t pw = run_writer[(size_t)v];
+                if (pw < 0) { c.fail(tw + ": reads row " + std::to_string(v) + " that nothing before it writes"); break; }
+                if (std::find(dl.begin(), dl.end(), (int)pw) == dl.end())
+                    { c.fail(tw + ": reads row " + std::to_string(v) + " of row tile " + std::to_string(pw) +
+                             ", which is not among its dependencies"); break; }
+            }
+            for (int32_t v : wr) {
+                if (v == 0 || written[(size_t)v] != -2 || run_writer[(size_t)v] >= 0)
+                    { c.fail(tw + ": writes row " + std::to_string(v) + " that is written elsewhere"); break; }
+                run_writer[(size_t)v] = r;
+            }
+            ++n_checked;
+        }
+        if (!c.ok()) break;
+        for (int64_t v = 0; v < n_slots; ++v)
+            if (run_writer[(size_t)v] >= 0) written[(size_t)v] = (int64_t)li;
+        // the ticket protocol with W work-groups, several interleavings: each
+        // work-group claims the next ticket when idle, waits until every unit
+        // tile of each dependency has finished, finishes its tile a step later
+        const int W = std::max(1, std::min<int>(n_workers, L.info.grid));
+        for (uint64_t seed = 1; seed <= 4 && c.ok(); ++seed) {
+            std::vector<int> done_ctr((size_t)nrt, 0), hold((size_t)W, -1);
+            int ticket = 0, finished = 0;
+            uint64_t rng = seed * 0x9E3779B97F4A7C15ull;
+            int64_t idle_rounds = 0;
+            while (finished < L.f_ntiles) {
+                bool progress = false;
+                for (int k = 0; k < W; ++k) {
+                    rng ^= rng << 13; rng ^= rng >> 7; rng ^= rng << 17;
+                    const int wgi = (int)(rng % (uint64_t)W);
+                    int& h = hold[(size_t)wgi];
+                    if (h < 0) {
+                        if (ticket < L.f_ntiles) { h = ticket++; progress = true; }
+                        continue;
+                    }
+                    const int r = tiles[h].w;
+                    bool ready = true;
+                    for (int i = 0; i < rdep[r].y; ++i)
+                        if (done_ctr[(size_t)deps[rdep[r].x + i]] < need) { ready = false; break; }
+                    if (ready) {
+                        ++done_ctr[(size_t)r];
+                        ++finished;
+                        h = -1;
+                        progress = true;
+                    }
+                }
+                idle_rounds = progress ? 0 : idle_rounds + 1;
+                if (idle_rounds > 4LL * W + 16) {
+                    c.fail(what + ": the ticket protocol does not drain with " + std::to_string(W) +
+                           " work-groups (" + std::to_string(finished) + " of " + std::to_string(L.f_ntiles) +
+                           " tiles finished)");
+                    break;
+                }
+            }
+        }
+    }
+    if (c.ok())
+        for (int64_t v = 0; v < n_slots; ++v)
+            if (written[(size_t)v] == -2) {
+                // a slot that no launch writes and that is not a zero / pad row
+                c.fail("slot " + std::to_string(v) + " is never written");
+                break;
+            }
+    if (checked) *checked = n_checked;
+    if (!c.ok()) return fail(EDB_ERR_INVALID, "edb_exec_validate: " + c.err);
     edb::clear_error();
     return EDB_OK;
 }

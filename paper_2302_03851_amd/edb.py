@@ -239,6 +239,13 @@ class Exec:
         L.check(L.load().edb_exec_launch_times(self.handle, out, n), "edb_exec_launch_times")
         return np.array(out[:], dtype=np.float64)
 
+    def validate(self, n_workers: int = 512) -> int:
+        """edb_exec_validate: host-side check of the device descriptors (raises
+        on the first problem); returns the launches and row tiles checked."""
+        n = C.c_int64()
+        L.check(L.load().edb_exec_validate(self.handle, n_workers, C.byref(n)), "edb_exec_validate")
+        return int(n.value)
+
     def check(self, stream: int = 0):
         """Synchronise and raise if a dataflow wait of the last execution timed out."""
         L.check(L.load().edb_exec_check(self.handle, C.c_void_p(stream)), "edb_exec_check")

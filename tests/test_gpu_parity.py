@@ -74,6 +74,7 @@ def test_parity_full_size_every_node(k):
     _torch()
     w = WL.make_config(k)
     f = _fwd(w)
+    f.exec.validate()     # the uploaded descriptors, decoded and bounds-checked on the host
     f.run()
     f.run()               # a replay of the captured graph
     h, c = f.states()
