@@ -285,8 +285,8 @@ void edb_plan_free(edb_plan_t* p);
  * reads its source's state from the c arena.  fp32 only.
  *   LGRU_EDGE: child [source position], x; gates [z, r, n_x, n_h];
  *              h = (1 - sigma(z)) n + sigma(z) h_src, n = tanh(n_x + sigma(r) n_h).
- *   POOL_MEAN: ragged children (the edges), no x; h = ((sum of their h) W + b) / count
- *              (W the identity for the mean). */
+ *   POOL_MEAN: ragged children (the edges), no x; h = (mean of their h) W + b
+ *              (W the identity and b = 0 for the plain mean; no edge: h = b). */
 #define EDB_CELL_LGRU_EDGE    13  /* [source], x;                gates [z,r,n_x,n_h]      */
 #define EDB_CELL_POOL_MEAN    14  /* ragged children, no x;      mean of their h, then W  */
 
@@ -305,7 +305,11 @@ typedef struct {
 edb_status edb_packed_weight_bytes(const edb_cell* cell, int64_t* bytes);
 
 /* Pack the logical weights of one cell type into the gate-interleaved,
- * zero-padded device layout the kernels read.  `logical` is a host array of
+ * zero-padded device layout the kernels read.  (Section 3, static subgraphs,
+ * and the discussion of Table 3: the gates of one cell run as one batched
+ * operation over one weight operand, the cell is a static subgraph whose
+ * operators are batched together; here all gates of a hidden unit block sit
+ * in one contiguous weight block so that one GEMM computes every gate.)  `logical` is a host array of
  * float32 row-major matrices in this order (K x N, rows [x ; child h ...],
  * columns gate-major in the kind's gate order):
  *   LSTM_CHAIN     W[(E+H) x 4H], b[4H]
@@ -348,6 +352,11 @@ edb_status edb_pack_weights(const edb_cell* cell, const float* const* logical,
 typedef struct edb_exec edb_exec_t;
 
 /* Bind a graph, schedule and plan to cell kernels.  cells: host [n_types].
+ * (Section 3.1: each batch of the schedule (Algorithm 1) becomes one batched
+ * operation whose source operands are gathered and whose results are
+ * scattered according to the memory plan; this call turns the plan's operand
+ * lists into the device descriptors that the fused kernels read, so that the
+ * gather and scatter happen inside the batch's kernel.)
  * Uploads the batch descriptors and index lists to the current HIP device
  * and allocates the staged-x buffer; both are owned by the handle.
  * Each batch gets the tile variant of smallest estimated time: small tiles
@@ -368,7 +377,11 @@ typedef struct edb_exec edb_exec_t;
 edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
                        const edb_cell* cells, int32_t flags, edb_exec_t** out);
 
-/* Run one forward pass, asynchronously on `stream` (hipStream_t).
+/* Run one forward pass, asynchronously on `stream` (hipStream_t): the batches
+ * in the order Algorithm 1 produced them, each as one launch of its fused
+ * gather / cell GEMM / gate epilogue / scatter kernel (Section 3.1); with
+ * EDB_USE_GRAPH the whole sequence is one graph launch (Section 1: fewer
+ * kernel launches is the first reason batching pays).
  *   packed_weights host array [n_types] of device pointers (edb_pack_weights output)
  *   x        device [n_x_rows x in_dim] of the cells' dtype, rows addressed by x_row
  *   arena_h  device [n_slots x H] of the cells' dtype; node v's h is row slot[v]
@@ -428,9 +441,11 @@ edb_status edb_exec_launch_info(const edb_exec_t* e, int32_t i, edb_launch_info*
  * or before the first execute. */
 edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
 
-/* The whole path for one mini-batch in one call: edb_build_graph,
- * edb_schedule, edb_plan_memory, edb_prepare (eager launches) and
- * edb_execute on `stream`, then every handle is released.  The call does not
+/* The whole path for one mini-batch in one call (Section 2.1: a mini-batch
+ * is the union of per-instance dataflow graphs; Algorithm 1 batches it and
+ * Section 3 lays out its memory, all at run time for every new input):
+ * edb_build_graph, edb_schedule, edb_plan_memory, edb_prepare (eager
+ * launches) and edb_execute on `stream`, then every handle is released.  The call does not
  * wait for the GPU: the executor's device buffers are freed in stream order
  * after the work.  Arguments are those of the individual calls; arena_h and
  * arena_c must hold at least the plan's n_slots rows (arena_rows), which is

@@ -25,6 +25,8 @@ LAT_CHAR = 6
 LAT_WORD = 7
 GRU_LEAF = 8
 GRU_INTERNAL = 9
+LGRU_EDGE = 13
+POOL_MEAN = 14
 
 
 def sigmoid(z):
@@ -194,3 +196,38 @@ def gru_internal(hs, U, b):
     ht = np.tanh(sigmoid(r0) * n0 + sigmoid(r1) * n1)
     h = sigmoid(z) * (h0 + h1) / 2.0 + (1.0 - sigmoid(z)) * ht
     return h, h
+
+
+def lgru_edge(x, h_src, W, b):
+    """One edge of the lattice GRU (Table 2's lattice-based GRU): a GRU step
+    (Cho et al. 2014, reset gate applied after the recurrent product) from the
+    edge's source position state with the edge's own input.
+
+    W [(E+H) x 4H] with rows [x ; h_src] and gate columns [z, r, n_x, n_h];
+    n_x reads only the x rows, n_h only the h_src rows:
+      z = [x ; h] W_z + b_z,  r = [x ; h] W_r + b_r,
+      n = tanh(x W_nx + b_nx + sigma(r) * (h W_nh + b_nh)),
+      h' = (1 - sigma(z)) * n + sigma(z) * h.
+    The edge's state is h' (returned as the cell state too)."""
+    x, h = _f64(x), _f64(h_src)
+    W, b = _f64(W), _f64(b)
+    E, H = x.shape[0], h.shape[0]
+    a = np.concatenate([x, h])
+    z = a @ W[:, 0:H] + b[0:H]
+    r = a @ W[:, H:2 * H] + b[H:2 * H]
+    nx = x @ W[:E, 2 * H:3 * H] + b[2 * H:3 * H]
+    nh = h @ W[E:, 3 * H:4 * H] + b[3 * H:4 * H]
+    n = np.tanh(nx + sigmoid(r) * nh)
+    out = (1.0 - sigmoid(z)) * n + sigmoid(z) * h
+    return out, out
+
+
+def pool_mean(hs, W, b):
+    """A lattice position's state: the mean of its incoming edges' states,
+    mapped by W [H x H] and shifted by b: h = mean_k(h_k) W + b (with no
+    edge, the mean is taken as 0 and h = b).  The lattice GRU uses W = I,
+    b = 0.  Returned as the cell state too."""
+    W, b = _f64(W), _f64(b)
+    m = np.mean([_f64(h) for h in hs], axis=0) if len(hs) else np.zeros(W.shape[0])
+    out = m @ W + b
+    return out, out

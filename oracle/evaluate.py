@@ -119,6 +119,11 @@ def evaluate(kinds, op_type, child_ptr, child_idx, x_row, x, weights, hidden,
             # a GRU node's state is its cell-state row (h before any rounding)
             st = [state(c)[1] for c in ch[:2]]
             h, c = C.gru_internal(st, w["W"], w["b"])
+        elif k == C.LGRU_EDGE:
+            # the source position's state is read from its cell-state row
+            h, c = C.lgru_edge(xv, state(ch[0])[1], w["W"], w["b"])
+        elif k == C.POOL_MEAN:
+            h, c = C.pool_mean([state(c)[0] for c in ch if c >= 0], w["W"], w["b"])
         elif k == C.LAT_CHAR:
             hp, cp = state(ch[0])
             words = [state(c)[1] for c in ch[1:] if c >= 0]

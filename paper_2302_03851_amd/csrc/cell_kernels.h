@@ -222,8 +222,10 @@ __device__ __forceinline__ void cell_update(const float* z, const float* cp, flo
         const float ht = tanh_f(fmaf(sigm(z[1]), z[3], z[2]));
         c = fmaf(sigm(z[0]), cp[0] - ht, ht);
         h = c;
-    } else if constexpr (KIND == K_POOL_MEAN) {   // nw: the position's edges
-        c = nw > 0 ? z[0] / (float)nw : 0.f;
+    } else if constexpr (KIND == K_POOL_MEAN) {
+        // nw: the position's edges; z[0] = (sum of their h) W without the
+        // bias, which racc carries: mean(h) W + b (with no edge, b)
+        c = (nw > 0 ? z[0] / (float)nw : 0.f) + racc;
         h = c;
     } else {  // K_LAT_CHAR: gates [i, f, o, u, lx]
         if (nw == 0) {
@@ -613,7 +615,8 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
             float s = 0.f;
 #pragma unroll
             for (int w = 0; w < WK; ++w) s += Z[((w * TM + r) * G + g) * TU + u];
-            zsum[q][g] = s + a.bias[g * a.Hu + j];
+            // a pooling node adds its bias after the mean (in the epilogue)
+            zsum[q][g] = KIND == K_POOL_MEAN ? s : s + a.bias[g * a.Hu + j];
         }
     }
 
@@ -621,6 +624,10 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
     float racc[NI], rden[NI];
 #pragma unroll
     for (int q = 0; q < NI; ++q) { racc[q] = 0.f; rden[q] = 0.f; }
+    if constexpr (KIND == K_POOL_MEAN) {
+#pragma unroll
+        for (int q = 0; q < NI; ++q) racc[q] = a.bias[u0 + (tid + NT * q) % TU];   // the packed bias is padded to Hu
+    }
     if constexpr (KT::RAG) {
         // children (words) of the tile's parents in chunks of TMR rows: their
         // h rows (child-sum) or cell states (lattice) staged to A, their cell

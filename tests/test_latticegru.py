@@ -131,3 +131,28 @@ def test_lattice_gru_one_call_path():
     s = f.plan.slot
     np.testing.assert_array_equal(ah.cpu().numpy()[s], h)
     np.testing.assert_array_equal(ac.cpu().numpy()[s], c)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("variant", [None, 0, 3])
+def test_pool_mean_with_map_and_bias(variant, monkeypatch):
+    """The pooling node as its kind defines it, h = mean(edges' h) W + b, with
+    a non-identity W and non-zero biases in both kinds, against the graph
+    oracle (every node)."""
+    from oracle.compare import state_rel_err
+    from oracle.evaluate import evaluate_workload
+    if variant is not None:
+        monkeypatch.setenv("EDB_VARIANT", str(variant))
+    w = WL.make_config(9, instances=6)
+    H = w.hidden
+    rng = np.random.Generator(np.random.PCG64(31))
+    w.weights[0]["b"] = rng.uniform(-0.3, 0.3, 4 * H).astype(np.float32)
+    w.weights[1]["W"] = rng.uniform(-0.15, 0.15, (H, H)).astype(np.float32)
+    w.weights[1]["b"] = rng.uniform(-0.5, 0.5, H).astype(np.float32)
+    f = edb.Forward(w, flags=L.NO_LARGE)
+    f.run()
+    h, c = f.states()
+    hr, cr = evaluate_workload(w)
+    err = state_rel_err(h, c, hr, cr)
+    print(f"pool with map and bias, variant {variant}: err {err:.3e}", flush=True)
+    assert err < 1e-4, err

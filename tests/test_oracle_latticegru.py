@@ -84,3 +84,61 @@ def test_mean_of_gru_cells():
                 if e == j:
                     props.append(c(t(xw[k]), t(h[s - 1] if s else zero))[0].numpy())
             np.testing.assert_allclose(h[j], np.mean(props, axis=0), rtol=1e-12, atol=1e-13)
+
+
+# ---- the node-level cells of the lattice GRU in the graph oracle -----------
+
+def test_lgru_edge_is_torch_gru_cell():
+    """oracle.cells.lgru_edge: W [(E+H) x 4H] with gate columns [z, r, n_x,
+    n_h] (n_x over the x rows, n_h over the h rows, b_nh on the recurrent
+    candidate product) is one torch.nn.GRUCell step."""
+    from oracle import cells as C
+    rng = np.random.Generator(np.random.PCG64(11))
+    E, H = 5, 4
+    W = rng.uniform(-0.5, 0.5, (E + H, 4 * H))
+    b = rng.uniform(-0.3, 0.3, 4 * H)
+    x, h = rng.normal(size=E), rng.normal(size=H)
+    got, c = C.lgru_edge(x, h, W, b)
+    cell = torch.nn.GRUCell(E, H).double()
+    blk = lambda m, g: m[:, g * H:(g + 1) * H]
+    with torch.no_grad():
+        # torch rows [r, z, n]
+        cell.weight_ih.copy_(torch.from_numpy(np.concatenate([blk(W[:E], 1), blk(W[:E], 0), blk(W[:E], 2)], 1).T))
+        cell.weight_hh.copy_(torch.from_numpy(np.concatenate([blk(W[E:], 1), blk(W[E:], 0), blk(W[E:], 3)], 1).T))
+        cell.bias_ih.copy_(torch.from_numpy(np.concatenate([b[H:2 * H], b[:H], b[2 * H:3 * H]])))
+        cell.bias_hh.copy_(torch.from_numpy(np.concatenate([np.zeros(2 * H), b[3 * H:]])))
+        ref = cell(torch.from_numpy(x)[None], torch.from_numpy(h)[None]).numpy()[0]
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-13)
+    np.testing.assert_array_equal(got, c)
+
+
+def test_pool_mean_hand_values():
+    """mean([1, 2], [3, 4]) = [2, 3]; W = [[1, 2], [0, 1]] maps it to [2, 7];
+    b = [1, -1] gives [3, 6].  With no edge the state is b."""
+    from oracle import cells as C
+    W = np.array([[1.0, 2.0], [0.0, 1.0]])
+    b = np.array([1.0, -1.0])
+    h, c = C.pool_mean([np.array([1.0, 2.0]), np.array([3.0, 4.0])], W, b)
+    np.testing.assert_array_equal(h, [3.0, 6.0])
+    np.testing.assert_array_equal(c, h)
+    np.testing.assert_array_equal(C.pool_mean([], W, b)[0], b)
+
+
+def test_graph_oracle_equals_lattice_oracle():
+    """The graph oracle (oracle.evaluate over the lattice GRU's LGRU_EDGE and
+    POOL_MEAN nodes, identity pooling, zero biases) gives the lattice-level
+    oracle's position states and edge proposals."""
+    from oracle.evaluate import evaluate_workload
+    from paper_2302_03851_amd import workloads as WL
+    w = WL.make_config(9, instances=4)
+    h, c = evaluate_workload(w)
+    a = w.aux
+    for lat in a["lattices"]:
+        xw = w.x[w.x_row[lat["word_edge"]]] if len(lat["words"]) else np.zeros((0, w.in_dim))
+        hp, gc, gw = lattice_gru(lat["length"], lat["words"], w.x[w.x_row[lat["char_edge"]]], xw,
+                                 a["Wx"], a["Wh"], a["bx"], a["bhn"])
+        np.testing.assert_allclose(h[lat["pos"]], hp, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(h[lat["char_edge"]], gc, rtol=0, atol=1e-12)
+        if len(lat["words"]):
+            np.testing.assert_allclose(h[lat["word_edge"]], gw, rtol=0, atol=1e-12)
+    np.testing.assert_array_equal(c, h)
