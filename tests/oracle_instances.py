@@ -4,9 +4,9 @@ Instances (trees, chains, lattices, grids) are independent graphs, so the
 oracle evaluates each connected component on its own (`oracle.evaluate`
 unchanged, node at a time) and the results are put back in node order; a
 selection of instances costs only their own nodes.  Optional worker threads
-spread independent oracle calls; nothing of the oracle's arithmetic changes.  Test infrastructure: the GPU tests call it
-for full-size workloads (the largest, 52k child-sum nodes, takes about half a
-minute on one core).
+spread independent oracle calls; nothing of the oracle's arithmetic changes.
+Test infrastructure: the GPU tests call it for full-size workloads (the
+largest, 52k child-sum nodes, takes about half a minute on one core).
 """
 from __future__ import annotations
 
