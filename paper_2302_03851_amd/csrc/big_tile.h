@@ -129,6 +129,49 @@ __device__ __forceinline__ void big_compute(v4f (&acc)[CU][G][RB], const char* A
     }
 }
 
+// Rows of cell states the epilogue reads per tile row (copied into the
+// stages after the chunk loop): the positional children's, the forget GEMM's
+// own children's, the parent GEMM's product sums.  Kinds with none leave the
+// stages free during the epilogue.
+template <int KIND>
+__host__ __device__ constexpr int big_ncr() {
+    return (KIND == K_CS_FORGET || KIND == K_CS_PARENT) ? 1 : (reads_child_c<KIND>() ? Kind<KIND>::NFIX : 0);
+}
+
+// Byte offsets of one tile's chunk copies (see big_tile): per A copy j the
+// source row of each operand segment (OOB: zero), per weight copy j its block.
+template <int KIND, typename T, int VB, int NSEG, int RB, int NBW>
+__device__ __forceinline__ void big_offsets(const BatchArgs& a, int tile, int wave, int lane,
+                                            uint32_t (&soff)[NSEG][RB], uint32_t (&woff)[NBW]) {
+    using KT = Kind<KIND>;
+    constexpr uint32_t ES = sizeof(T), OOB = 0x80000000u;
+    constexpr int G = KT::G, NFX = KT::NFIX, TM = 32 * RB, TU = 32 * big_cu(VB);
+    const int nut = a.Hu / TU;
+    const int row0 = (tile / nut) * TM, u0 = (tile % nut) * TU;
+    const int nrows = min(TM, a.m - row0);
+    const int nkg = a.K / Elem<T>::KG;
+    // A copies: wave w's j-th copy fills rows (4 j + w) * 8 .. + 8 of the stage
+#pragma unroll
+    for (int j = 0; j < RB; ++j) {
+        const int r = (4 * j + wave) * 8 + (lane >> 3);
+        const bool ok = r < nrows;
+        int s = 0;
+        if constexpr (KT::X) soff[s++][j] = ok ? (uint32_t)seg_row(a.x, row0 + r) * (uint32_t)a.E * ES : OOB;
+#pragma unroll
+        for (int p = 0; p < NFX; ++p)
+            soff[s++][j] = !ok ? OOB
+                               : (a.fix[p].kind == S_NONE ? 0u
+                                                          : (uint32_t)seg_row(a.fix[p], row0 + r) * (uint32_t)a.H * ES);
+    }
+    // weight copies: wave w's j-th copy is block b = 4 j + w = ((ubi * G + g) * 2 + kgi)
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+        const int b = 4 * j + wave;
+        const int kgi = b & 1, g = (b >> 1) % G, ubi = (b >> 1) / G;
+        woff[j] = (uint32_t)((((u0 / 16 + ubi) * G + g) * nkg + kgi) * 1024 + lane * 16);
+    }
+}
+
 // One tile: rows [TM*(tile / nut), +TM) x units [TU*(tile % nut), +TU) of the
 // batch, all gates.  st0 / st1: the kernel's two LDS stages.
 template <int KIND, typename T, int VB>
@@ -171,26 +214,8 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
     // q = (l & 7) ^ (l / 8) of that row.
     const int q = (lane & 7) ^ (lane >> 3);
     uint32_t soff[NSEG][RB];   // byte offset of each segment's source row (OOB: zero)
-#pragma unroll
-    for (int j = 0; j < RB; ++j) {
-        const int r = (4 * j + wave) * 8 + (lane >> 3);
-        const bool ok = r < nrows;
-        int s = 0;
-        if constexpr (KT::X) soff[s++][j] = ok ? (uint32_t)seg_row(a.x, row0 + r) * (uint32_t)E * ES : OOB;
-#pragma unroll
-        for (int p = 0; p < NFX; ++p)
-            soff[s++][j] = !ok ? OOB
-                               : (a.fix[p].kind == S_NONE ? 0u
-                                                          : (uint32_t)seg_row(a.fix[p], row0 + r) * (uint32_t)H * ES);
-    }
-    // weight copies: wave w's j-th copy is block b = 4 j + w = ((ubi * G + g) * 2 + kgi)
     uint32_t woff[NBW];
-#pragma unroll
-    for (int j = 0; j < NBW; ++j) {
-        const int b = 4 * j + wave;
-        const int kgi = b & 1, g = (b >> 1) % G, ubi = (b >> 1) / G;
-        woff[j] = (uint32_t)((((u0 / 16 + ubi) * G + g) * nkg + kgi) * 1024 + lane * 16);
-    }
+    big_offsets<KIND, T, VB, NSEG, RB, NBW>(a, tile, wave, lane, soff, woff);
 
     v4f acc[CU][G][RB];
 #pragma unroll
@@ -237,7 +262,22 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
     // forget GEMM: the children's own cell states.  The parent GEMM: the sums
     // of the children's products sigma(f_k) c_k (one row per parent) ----
     constexpr int HALF = TM / 2;
-    constexpr int NCR = (KIND == K_CS_FORGET || KIND == K_CS_PARENT) ? 1 : (reads_child_c<KIND>() ? NFX : 0);
+    constexpr int NCR = big_ncr<KIND>();
+    // the epilogue's own loads (bias, result rows), issued with the copies of
+    // the children's rows below
+    float bz[CU][G];   // bias of this lane's units (the packed bias is zero-padded to Hu)
+#pragma unroll
+    for (int cu = 0; cu < CU; ++cu)
+#pragma unroll
+        for (int g = 0; g < G; ++g) bz[cu][g] = a.bias[g * a.Hu + u0 + (wc * CU + cu) * 16 + (lane & 15)];
+    int rres[RB][4];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = min(wr * 16 * RB + rb * 16 + (lane >> 4) * 4 + i, nrows - 1);
+            rres[rb][i] = KIND == K_CS_FORGET ? row0 + r : seg_row(a.res, row0 + r);
+        }
     static_assert(NCR * HALF * 256 <= SB, "epilogue rows fit the stages");
     const __amdgpu_buffer_rsrc_t rc = KIND == K_CS_PARENT
                                           ? make_rsrc(a.fc, (uint32_t)a.m * (uint32_t)H * 4u)
@@ -268,12 +308,6 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
         __syncthreads();
     }
 
-    float bz[CU][G];   // bias of this lane's units (the packed bias is zero-padded to Hu)
-#pragma unroll
-    for (int cu = 0; cu < CU; ++cu)
-#pragma unroll
-        for (int g = 0; g < G; ++g) bz[cu][g] = a.bias[g * a.Hu + u0 + (wc * CU + cu) * 16 + (lane & 15)];
-
     // ---- gate epilogue and scatter ----
     T* Hout = reinterpret_cast<T*>(a.arena_h);
 #pragma unroll
@@ -282,7 +316,6 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
         for (int i = 0; i < 4; ++i) {
             const int r = wr * 16 * RB + rb * 16 + (lane >> 4) * 4 + i;
             if (r >= nrows) continue;
-            const int rres = KIND == K_CS_FORGET ? row0 + r : seg_row(a.res, row0 + r);
 #pragma unroll
             for (int cu = 0; cu < CU; ++cu) {
                 const int u = (wc * CU + cu) * 16 + (lane & 15), j = u0 + u;
@@ -293,7 +326,7 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
                 cp[0] = 0.f;
 #pragma unroll
                 for (int p = 0; p < NCR; ++p) cp[p] = crow_ptr(p, r)[u];
-                const size_t o = (size_t)rres * a.H + j;
+                const size_t o = (size_t)rres[rb][i] * a.H + j;
                 if constexpr (KIND == K_CS_FORGET) {
                     a.fc[o] = sigm(z[0]) * cp[0];   // sigma(f_k) c_k, row = position in the child list
                 } else {
@@ -318,9 +351,18 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
     __shared__ __align__(16) char st0[SB_];                                                         \
     __shared__ __align__(16) char st1[SB_]
 
-// One work-group per tile, in XCD-aware order.
+// Waves per SIMD the compiler is held to: two work-groups per CU where the
+// accumulators (4 CU G RB registers) leave room for them, else one.
+template <int KIND, int VB>
+__host__ __device__ constexpr int big_waves_per_simd() {
+    return 4 * big_cu(VB) * Kind<KIND>::G * big_rb(Kind<KIND>::G, VB) <= 96 ? 2 : 1;
+}
+
+// One work-group per tile, in XCD-aware order: work-groups are dispatched
+// round-robin over the 8 XCDs and XCD x owns the contiguous tile range
+// [x per, (x + 1) per), unit tiles fastest.  The grid is a multiple of 8.
 template <int KIND, typename T, int VB>
-__global__ __launch_bounds__(256) void big_kernel(BatchArgs a) {
+__global__ __launch_bounds__(256, (big_waves_per_simd<KIND, VB>())) void big_kernel(BatchArgs a) {
     EDB_BIG_STAGES(KIND, VB);
     constexpr int TM = 32 * big_rb(Kind<KIND>::G, VB), TU = 32 * big_cu(VB);
     const int nut = a.Hu / TU;
