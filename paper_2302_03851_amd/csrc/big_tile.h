@@ -308,39 +308,88 @@ __device__ __forceinline__ void big_tile(const BatchArgs& a, int tile, char* st0
         __syncthreads();
     }
 
-    // ---- gate epilogue and scatter ----
-    T* Hout = reinterpret_cast<T*>(a.arena_h);
+    // ---- gate epilogue: every element's new c and h in registers (the
+    // children's cell states are still in the stages) ----
+    constexpr bool FORGET = KIND == K_CS_FORGET;
+    float cv[RB][4][CU], hv[RB][4][CU];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int r = wr * 16 * RB + rb * 16 + (lane >> 4) * 4 + i;
-            if (r >= nrows) continue;
+            const int r = min(wr * 16 * RB + rb * 16 + (lane >> 4) * 4 + i, TM - 1);
 #pragma unroll
             for (int cu = 0; cu < CU; ++cu) {
-                const int u = (wc * CU + cu) * 16 + (lane & 15), j = u0 + u;
-                if (j >= a.H) continue;
+                const int u = (wc * CU + cu) * 16 + (lane & 15);
                 float z[G], cp[NFX > 0 ? NFX : 1];
 #pragma unroll
                 for (int g = 0; g < G; ++g) z[g] = acc[cu][g][rb][i] + bz[cu][g];
                 cp[0] = 0.f;
 #pragma unroll
                 for (int p = 0; p < NCR; ++p) cp[p] = crow_ptr(p, r)[u];
-                const size_t o = (size_t)rres[rb][i] * a.H + j;
-                if constexpr (KIND == K_CS_FORGET) {
-                    a.fc[o] = sigm(z[0]) * cp[0];   // sigma(f_k) c_k, row = position in the child list
+                if constexpr (FORGET) {
+                    cv[rb][i][cu] = sigm(z[0]) * cp[0];   // sigma(f_k) c_k, row = position in the child list
+                    hv[rb][i][cu] = 0.f;
+                } else if constexpr (KIND == K_CS_PARENT) {
+                    cell_update<K_CS_INT>(z, cp, cp[0], 0.f, 0, cv[rb][i][cu], hv[rb][i][cu]);
                 } else {
-                    float c, h;
-                    if constexpr (KIND == K_CS_PARENT) cell_update<K_CS_INT>(z, cp, cp[0], 0.f, 0, c, h);
-                    else cell_update<KIND>(z, cp, 0.f, 0.f, 0, c, h);
-                    a.arena_c[o] = c;
-                    Hout[o] = from_f<T>(h);
+                    cell_update<KIND>(z, cp, 0.f, 0.f, 0, cv[rb][i][cu], hv[rb][i][cu]);
                 }
             }
-            // one row at a time: keeps the unrolled epilogue's live registers
-            // (and the pressure on the chunk loop's allocation) small
+            // one row at a time: keeps the unrolled epilogue's live registers small
             __builtin_amdgcn_sched_barrier(0);
         }
+    if constexpr (NCR > 0) __syncthreads();   // every read of the children's cell states is done
+    (void)rres;
+
+    // ---- scatter through LDS: per row block rb, the 32 rows it covers (16 of
+    // each row half) go to the stages as [32][TU] tiles (c fp32 in st0, h in
+    // st1, rows padded by 16 bytes so that the 4 rows one store instruction
+    // covers fall in distinct banks), then every thread writes whole 16-byte
+    // pieces of those rows to their slots: each row's TU units are contiguous
+    // in its slot ----
+    constexpr int CS = TU + 4;                       // c tile row stride (floats)
+    constexpr int HS = TU + 16 / (int)sizeof(T);     // h tile row stride (elements)
+    static_assert(32 * CS * 4 <= SB && 32 * HS * (int)sizeof(T) <= SB, "an output pass fits a stage");
+    float* Cs = reinterpret_cast<float*>(st0);
+    T* Hs = reinterpret_cast<T*>(st1);
+    T* Hout = reinterpret_cast<T*>(a.arena_h);
+    constexpr int CP = TU / 4, HP = TU * (int)sizeof(T) / 16;   // 16-byte pieces of a row of c, of h
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int lr = wr * 16 + (lane >> 4) * 4 + i;   // row in the pass
+#pragma unroll
+            for (int cu = 0; cu < CU; ++cu) {
+                const int u = (wc * CU + cu) * 16 + (lane & 15);
+                Cs[lr * CS + u] = cv[rb][i][cu];
+                if constexpr (!FORGET) Hs[lr * HS + u] = from_f<T>(hv[rb][i][cu]);
+            }
+        }
+        __syncthreads();
+        // pass row lr is tile row (lr / 16) * 16 * RB + rb * 16 + lr % 16
+        for (int pc = tid; pc < 32 * CP; pc += 256) {
+            const int lr = pc / CP, qq = pc - lr * CP;
+            const int r = (lr >> 4) * 16 * RB + rb * 16 + (lr & 15);
+            const int j = u0 + qq * 4;
+            if (r >= nrows || j >= a.H) continue;
+            const int rr = FORGET ? row0 + r : seg_row(a.res, row0 + r);
+            float* dst = (FORGET ? a.fc : a.arena_c) + (size_t)rr * a.H + j;
+            *reinterpret_cast<float4*>(dst) = *reinterpret_cast<const float4*>(Cs + lr * CS + qq * 4);
+        }
+        if constexpr (!FORGET) {
+            for (int ph = tid; ph < 32 * HP; ph += 256) {
+                const int lr = ph / HP, qq = ph - lr * HP;
+                const int r = (lr >> 4) * 16 * RB + rb * 16 + (lr & 15);
+                const int j = u0 + qq * PV;
+                if (r >= nrows || j >= a.H) continue;
+                const int rr = seg_row(a.res, row0 + r);
+                *reinterpret_cast<uint4*>(Hout + (size_t)rr * a.H + j) =
+                    *reinterpret_cast<const uint4*>(Hs + lr * HS + qq * PV);
+            }
+        }
+        __syncthreads();   // the next pass overwrites the tiles
+    }
 }
 
 // Two stages as distinct objects: the compiler can then tell that the copies
