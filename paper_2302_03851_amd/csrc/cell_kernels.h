@@ -246,10 +246,19 @@ __host__ __device__ constexpr int rag_rt() {
     return Kind<KIND>::RAG ? (RT < 4 ? 4 : RT) : RT;
 }
 
-// ---- LDS budget of one work-group (bytes) ----
+// Kinds whose first chunk of ragged rows (the lattice words ending at the
+// tile's characters) is gathered together with the main A tile, into an LDS
+// tile of its own, so that its loads overlap the main tile's and its GEMM
+// follows the main GEMM without another round trip to memory.
+template <int KIND>
+__host__ __device__ constexpr bool early_rag() { return KIND == K_LAT_CHAR; }
+
+// ---- LDS budget of one work-group (bytes); Hk: the ragged rows' width ----
 template <int KIND, typename T, int RT, int WU, int WK>
-__host__ __device__ constexpr int lds_a_bytes(int K) {
-    // ragged kinds reuse A for the chunk's child rows (Hk <= K columns)
+__host__ __device__ constexpr int lds_a_bytes(int K, int Hk) {
+    if (early_rag<KIND>())   // main tile, then the ragged tile [16*rag_rt rows][Hk + pad]
+        return (16 * RT * (K + a_pad<T>()) + 16 * rag_rt<KIND, RT>() * (Hk + a_pad<T>())) * (int)sizeof(T);
+    // other ragged kinds reuse A for the chunk's child rows (Hk <= K columns)
     return 16 * rag_rt<KIND, RT>() * (K + a_pad<T>()) * (int)sizeof(T);
 }
 template <int KIND, typename T, int RT, int WU, int WK>
@@ -264,21 +273,21 @@ __host__ __device__ constexpr int lds_zr_bytes() {
 // Offset of Z: after A for kinds with a ragged phase (A is reused for child
 // rows while Z must persist), else Z aliases A (written after the GEMM).
 template <int KIND, typename T, int RT, int WU, int WK>
-__host__ __device__ constexpr int lds_z_off(int K) {
-    return Kind<KIND>::RAG ? lds_a_bytes<KIND, T, RT, WU, WK>(K) : 0;
+__host__ __device__ constexpr int lds_z_off(int K, int Hk) {
+    return Kind<KIND>::RAG ? lds_a_bytes<KIND, T, RT, WU, WK>(K, Hk) : 0;
 }
 template <int KIND, typename T, int RT, int WU, int WK>
-__host__ __device__ constexpr int lds_rowc_off(int K) {
+__host__ __device__ constexpr int lds_rowc_off(int K, int Hk) {
     return Kind<KIND>::RAG
-               ? lds_a_bytes<KIND, T, RT, WU, WK>(K) + lds_z_bytes<KIND, T, RT, WU, WK>() +
+               ? lds_a_bytes<KIND, T, RT, WU, WK>(K, Hk) + lds_z_bytes<KIND, T, RT, WU, WK>() +
                      lds_zr_bytes<KIND, T, RT, WU, WK>()
-               : (lds_a_bytes<KIND, T, RT, WU, WK>(K) > lds_z_bytes<KIND, T, RT, WU, WK>()
-                      ? lds_a_bytes<KIND, T, RT, WU, WK>(K)
+               : (lds_a_bytes<KIND, T, RT, WU, WK>(K, Hk) > lds_z_bytes<KIND, T, RT, WU, WK>()
+                      ? lds_a_bytes<KIND, T, RT, WU, WK>(K, Hk)
                       : lds_z_bytes<KIND, T, RT, WU, WK>());
 }
 template <int KIND, typename T, int RT, int WU, int WK>
-__host__ __device__ constexpr int lds_bytes(int K) {
-    return lds_rowc_off<KIND, T, RT, WU, WK>(K);
+__host__ __device__ constexpr int lds_bytes(int K, int Hk) {
+    return lds_rowc_off<KIND, T, RT, WU, WK>(K, Hk);
 }
 
 // Raw buffer resource over `bytes` bytes at p (gfx9 resource word 3).
@@ -360,46 +369,170 @@ __device__ __forceinline__ void stage_tile(T* A, int AS, const ASeg<T> (&sg)[NSE
     }
 }
 
-// Child sum of h rows for child-sum internal nodes: A[r][k] = sum_children h[k],
-// in child order.  Children are taken 4 at a time: their row indices are
-// loaded back to back without branches, then their 16-byte pieces (a slot
-// past the last child reads the zero row and is not added), so a parent
-// costs one index and one data round trip per 4 children.
-template <typename T, int TM, int NT>
-__device__ __forceinline__ void stage_child_sum(T* A, int AS, const BatchArgs& a, int row0, int nrows, int tid) {
-    constexpr int V = Elem<T>::VEC;
-    constexpr int CB = 4;
-    const T* h = reinterpret_cast<const T*>(a.arena_h);
-    const int nv = a.Hk / V, nreal = a.H / V;
-    for (int it = tid; it < nrows * nv; it += NT) {   // rows past nrows are not read back
-        const int r = it / nv, c = it % nv;
-        const bool ok = c < nreal;
-        const int rr = row0 + min(r, nrows - 1);
-        const int e0 = a.rag_ptr[rr], e1 = ok ? a.rag_ptr[rr + 1] : e0;
-        float acc[V];
+// Segment-parallel staging of the A tile for kinds with early loads: round
+// `base` takes up to SR items of every segment per thread, all their row
+// indices first (idx, descriptor data only), then all their 16-byte pieces
+// (vals), then the LDS stores (store), so that a tile whose segments fit one
+// round costs one index and one data round trip however many segments it
+// has, and the indices can be issued before the wait for the producers.
+template <typename T, int NSEG, int SR>
+struct StageRound {
+    int row[NSEG][SR];
+    u32x4 val[NSEG][SR];
+
+    template <int NT>
+    __device__ __forceinline__ void idx(const ASeg<T> (&sg)[NSEG], int nrows, int base, int tid) {
 #pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] = 0.f;
-        for (int e = e0; e < e1; e += CB) {
-            int row[CB];
+        for (int s = 0; s < NSEG; ++s) {
+            const int total = nrows * sg[s].nv;
 #pragma unroll
-            for (int q = 0; q < CB; ++q) row[q] = seg_row_nb(a.rag, min(e + q, e1 - 1), e1);
-            u32x4 raw[CB];
-#pragma unroll
-            for (int q = 0; q < CB; ++q)
-                raw[q] = *reinterpret_cast<const u32x4*>(e + q < e1 ? h + (size_t)row[q] * a.H + c * V : h);
-#pragma unroll
-            for (int q = 0; q < CB; ++q) {
-                const T* pv = reinterpret_cast<const T*>(&raw[q]);
-                if (e + q < e1)
-#pragma unroll
-                    for (int i = 0; i < V; ++i) acc[i] += to_f(pv[i]);
+            for (int i = 0; i < SR; ++i) {
+                const int it = min(base + i * NT + tid, total - 1);
+                row[s][i] = seg_row_nb(sg[s].seg, sg[s].row0 + it / sg[s].nv, sg[s].len);
             }
         }
-        uint4 out;
-        T* po = reinterpret_cast<T*>(&out);
+    }
+    template <int NT>
+    __device__ __forceinline__ void vals(const ASeg<T> (&sg)[NSEG], int nrows, int base, const T* zero, int tid) {
+        constexpr int V = Elem<T>::VEC;
 #pragma unroll
-        for (int i = 0; i < V; ++i) po[i] = from_f<T>(acc[i]);
-        *reinterpret_cast<uint4*>(A + r * AS + c * V) = out;
+        for (int s = 0; s < NSEG; ++s) {
+            const ASeg<T>& q = sg[s];
+            const int total = nrows * q.nv;
+#pragma unroll
+            for (int i = 0; i < SR; ++i) {
+                const int it = base + i * NT + tid, r = it / q.nv, c = it - r * q.nv;
+                const bool ok = it < total && c < q.nreal && q.seg.kind != S_NONE;
+                val[s][i] = *reinterpret_cast<const u32x4*>(ok ? q.src + (size_t)row[s][i] * q.width + c * V : zero);
+            }
+        }
+    }
+    template <int NT>
+    __device__ __forceinline__ void store(T* A, int AS, const ASeg<T> (&sg)[NSEG], int nrows, int base, int tid) const {
+        constexpr int V = Elem<T>::VEC;
+#pragma unroll
+        for (int s = 0; s < NSEG; ++s) {
+            const ASeg<T>& q = sg[s];
+            const int total = nrows * q.nv;
+#pragma unroll
+            for (int i = 0; i < SR; ++i) {
+                const int it = base + i * NT + tid, r = it / q.nv, c = it - r * q.nv;
+                if (it < total) *reinterpret_cast<u32x4*>(A + r * AS + (q.col + c) * V) = val[s][i];
+            }
+        }
+    }
+};
+
+// Child sum of h rows for child-sum internal nodes and pooling nodes:
+// A[r][k] = the sum of the row's ragged children's h[k], added in child order
+// in fp32 and rounded to T once.  Items (row, 16-byte piece) are taken SR per
+// thread at a time: bounds() loads their rows' child ranges (descriptor data,
+// issued with the tile's other indices, before the wait for the producers);
+// gather() takes the children CB at a time for all SR items, their row
+// indices back to back, then their pieces (a slot past an item's last child
+// reads the zero row and is not added), then stores the sums.  A round costs
+// one index and one data round trip per CB children of its largest parent.
+template <typename T, int NT, int SR, int CB>
+struct ChildSum {
+    int e0[SR], e1[SR];
+
+    __device__ __forceinline__ void bounds(const BatchArgs& a, int row0, int nrows, int base, int tid) {
+        const int nv = a.Hk / Elem<T>::VEC, nreal = a.H / Elem<T>::VEC, total = nrows * nv;
+#pragma unroll
+        for (int i = 0; i < SR; ++i) {
+            const int it = base + i * NT + tid, itc = min(it, total - 1);
+            const int r = itc / nv, c = itc - r * nv;
+            const int p0 = a.rag_ptr[row0 + r], p1 = a.rag_ptr[row0 + r + 1];
+            e0[i] = p0;
+            e1[i] = it < total && c < nreal ? p1 : p0;   // zero padding and past the tile: no children
+        }
+    }
+    __device__ __forceinline__ void gather(T* A, int AS, const BatchArgs& a, int nrows, int base, int tid) const {
+        constexpr int V = Elem<T>::VEC;
+        const T* h = reinterpret_cast<const T*>(a.arena_h);
+        const int nv = a.Hk / V, total = nrows * nv;
+        float acc[SR][V];
+        int n = 0;
+#pragma unroll
+        for (int i = 0; i < SR; ++i) {
+            n = max(n, e1[i] - e0[i]);
+#pragma unroll
+            for (int k = 0; k < V; ++k) acc[i][k] = 0.f;
+        }
+        for (int j = 0; j < n; j += CB) {
+            int row[SR][CB];
+#pragma unroll
+            for (int i = 0; i < SR; ++i)
+#pragma unroll
+                for (int q = 0; q < CB; ++q) row[i][q] = seg_row_nb(a.rag, min(e0[i] + j + q, e1[i] - 1), e1[i]);
+            u32x4 raw[SR][CB];
+#pragma unroll
+            for (int i = 0; i < SR; ++i) {
+                const int it = min(base + i * NT + tid, total - 1), c = it - (it / nv) * nv;
+#pragma unroll
+                for (int q = 0; q < CB; ++q)
+                    raw[i][q] = *reinterpret_cast<const u32x4*>(
+                        e0[i] + j + q < e1[i] ? h + (size_t)row[i][q] * a.H + c * V : h);
+            }
+#pragma unroll
+            for (int i = 0; i < SR; ++i)
+#pragma unroll
+                for (int q = 0; q < CB; ++q) {
+                    const T* pv = reinterpret_cast<const T*>(&raw[i][q]);
+                    if (e0[i] + j + q < e1[i])
+#pragma unroll
+                        for (int k = 0; k < V; ++k) acc[i][k] += to_f(pv[k]);
+                }
+        }
+#pragma unroll
+        for (int i = 0; i < SR; ++i) {
+            const int it = base + i * NT + tid, r = it / nv, c = it - r * nv;
+            if (it >= total) continue;
+            uint4 out;
+            T* po = reinterpret_cast<T*>(&out);
+#pragma unroll
+            for (int k = 0; k < V; ++k) po[k] = from_f<T>(acc[i][k]);
+            *reinterpret_cast<uint4*>(A + r * AS + c * V) = out;
+        }
+    }
+};
+
+// Lattice words' cell states c_w (fp32 arena rows of the ragged list entries
+// [cb, cb + cn)) converted to T into the ragged tile R (stride RS), pieces
+// [base0, cn * Hk / VEC) of V elements, two per thread a round: indices,
+// then values (past H: the zero row), then the converted stores.
+template <typename T, int NT>
+__device__ __forceinline__ void stage_word_rows(T* R, int RS, const BatchArgs& a, int cb, int cn, int base0, int tid) {
+    constexpr int V = Elem<T>::VEC;
+    const int nv = a.Hk / V, nreal = a.H / V, total = cn * nv;   // rows past cn are not read back
+    for (int base = base0; base < total; base += 2 * NT) {
+        int wr[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int it = min(base + q * NT + tid, total - 1);
+            wr[q] = seg_row_nb(a.rag, cb + min(it / nv, cn - 1), cb + cn);
+        }
+        float4 f4[2][V / 4];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int it = base + q * NT + tid, r = it / nv, c = it - r * nv;
+            const bool ok = it < total && c < nreal;
+            const float4* src = reinterpret_cast<const float4*>(ok ? a.arena_c + (size_t)wr[q] * a.H + c * V : a.arena_c);
+#pragma unroll
+            for (int k = 0; k < V / 4; ++k) f4[q][k] = src[k];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int it = base + q * NT + tid, r = it / nv, c = it - r * nv;
+            if (it >= total) continue;
+            uint4 out;
+            T* po = reinterpret_cast<T*>(&out);
+            const float* pf = reinterpret_cast<const float*>(&f4[q][0]);
+#pragma unroll
+            for (int i = 0; i < V; ++i) po[i] = from_f<T>(pf[i]);
+            *reinterpret_cast<uint4*>(R + r * RS + c * V) = out;
+        }
     }
 }
 
@@ -514,10 +647,20 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
     constexpr int NFX = KT::NFIX;
 
     const int AS = a.K + AS_PAD;                           // A row stride (elements)
+    constexpr int TMR = 16 * rag_rt<KIND, RT>();           // rows per chunk of the ragged phase
+    constexpr bool ER = early_rag<KIND>();
+    constexpr bool CSUM = sums_children<KIND>();
+    // kinds that load their biases and child ranges with the row indices
+    // (their work-groups hold one per CU, with registers to spare)
+    constexpr bool EARLY = KT::RAG || CSUM;
     T* A = reinterpret_cast<T*>(smem);
-    float* Z = reinterpret_cast<float*>(smem + lds_z_off<KIND, T, RT, WU, WK>(a.K));
+    T* Ar = ER ? A + TM * AS : A;                          // the ragged chunk's rows
+    const int RS = a.Hk + AS_PAD;                          // their row stride
+    float* Z = reinterpret_cast<float*>(smem + lds_z_off<KIND, T, RT, WU, WK>(a.K, a.Hk));
     float* Zr = Z + WK * TM * G * TU;
+    float* Crag = Zr + WK * TMR * TU;
     constexpr int PD = WK >= 16 ? 2 : ring_depth<G>();   // 1024-thread groups have 128 VGPRs
+    constexpr int V = Elem<T>::VEC;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row0 = rtile * TM, u0 = ut * TU;
@@ -532,6 +675,20 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
     BRing<G, PD> ring;
     ring_prologue<G, PD>(ring, Bmain, nkg, kg0, kg1);
 
+    // the ragged phase's weights (W_lc for the early chunk: issued now) and
+    // the tile's child range [cbeg, cend) (uniform)
+    const int nkgr = KT::RAG ? a.Hk / KG : 0;
+    const uint4* Brag = nullptr;
+    if constexpr (KT::RAG) Brag = reinterpret_cast<const uint4*>(a.Wr) + ((size_t)ub * nkgr) * 64 + lane;
+    const int rk0 = (nkgr * wk) / WK, rk1 = (nkgr * (wk + 1)) / WK;
+    BRing<1, 4> rring;
+    int cbeg = 0, cend = 0;
+    if constexpr (KT::RAG) {
+        cbeg = a.rag_ptr[row0];
+        cend = a.rag_ptr[row0 + nrows];
+    }
+    if constexpr (ER) ring_prologue<1, 4>(rring, Brag, nkgr, rk0, rk1);
+
     // ---- 1. early loads: the epilogue's result rows and child cell states ----
     // (row indices of contiguous lists are arithmetic; indexed lists cost one
     // load, issued here in parallel with the operand and weight loads)
@@ -545,26 +702,29 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
 #pragma unroll
         for (int p = 0; p < NFX; ++p) crow[q][p] = seg_row_nb(a.fix[p], rr, a.m);
     }
-    sync.wait();   // producers of this tile's operand rows have finished
-    float cpre[NI][NFX > 0 ? NFX : 1];
+    // biases (the packed ones are padded to Hu) and each item's child range
+    float bz[NI][G], brj[NI];
+    int pe0[NI], pe1[NI];
+    if constexpr (EARLY) {
 #pragma unroll
-    for (int q = 0; q < NI; ++q) {
-        const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
-        const bool ok = it < NITEM && r < nrows && j < a.H;
+        for (int q = 0; q < NI; ++q) {
+            const int it = tid + NT * q, itc = it < NITEM ? it : 0;
+            const int r = itc / TU, u = itc % TU;
 #pragma unroll
-        for (int p = 0; p < (NFX > 0 ? NFX : 1); ++p) {
-            const bool use = NFX > p && reads_child_c<KIND>() && ok && a.fix[p].kind != S_NONE;
-            cpre[q][p] = *(use ? a.arena_c + (size_t)crow[q][p] * a.H + j : a.arena_c);
+            for (int g = 0; g < G; ++g) bz[q][g] = a.bias[g * a.Hu + u0 + u];
+            if constexpr (KT::RAG) brj[q] = a.br[u0 + u];
+            const int rr = row0 + min(r, nrows - 1);
+            const int p0 = a.rag_ptr[rr], p1 = a.rag_ptr[rr + 1];
+            const bool ok = it < NITEM && r < nrows;
+            pe0[q] = ok ? p0 : 0;
+            pe1[q] = ok ? p1 : 0;
         }
     }
-
-    // ---- 3. stage the A tile: [x | child h ...] or [child sum of h] ----
-    if constexpr (sums_children<KIND>()) {
-        stage_child_sum<T, TM, NT>(A, AS, a, row0, nrows, tid);
-    } else {
-        constexpr int NSEG = (KT::X ? 1 : 0) + NFX;
-        constexpr int V = Elem<T>::VEC;
-        ASeg<T> sg[NSEG];
+    // the main A tile's sources: [x | child h ...] (kinds that do not sum children)
+    constexpr int NSEG = (KT::X ? 1 : 0) + NFX;
+    constexpr int NS1 = NSEG > 0 ? NSEG : 1;   // the kinds that sum children have no segments
+    ASeg<T> sg[NS1];
+    if constexpr (!CSUM) {
         int s = 0, col = 0;
         if constexpr (KT::X) {
             sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.xmat), a.x, row0, 0, a.Ep / V, a.E / V, a.E, a.m};
@@ -576,11 +736,90 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
             sg[s++] = ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.fix[p], row0, col, a.Hk / V, a.H / V, a.H, a.m};
             col += a.Hk / V;
         }
-        stage_tile<T, TM, NT, NSEG>(A, AS, sg, nrows, reinterpret_cast<const T*>(a.arena_h), tid);
+    }
+    constexpr int SR = 4;
+    ChildSum<T, NT, SR, KT::RAG ? 4 : 2> csum;   // pooling nodes: 168 registers a lane
+    if constexpr (CSUM) csum.bounds(a, row0, nrows, 0, tid);
+    StageRound<T, NS1, SR> st;
+    if constexpr (ER) st.template idx<NT>(sg, nrows, 0, tid);
+    // the early ragged chunk's row indices: its cell states for this tile's
+    // units (Crag) and the first NWQ pieces per thread of its rows (Ar)
+    constexpr int NCI = (TMR * TU + NT - 1) / NT;
+    constexpr int NWQ = 4;
+    const int cn0 = min(TMR, cend - cbeg);
+    const int nvr = a.Hk / V, total0 = cn0 * nvr;
+    int crw[NCI], wr[NWQ];
+    if constexpr (ER) {
+#pragma unroll
+        for (int q = 0; q < NCI; ++q) {
+            const int it = min(tid + NT * q, TMR * TU - 1);
+            crw[q] = seg_row_nb(a.rag, cbeg + min(it / TU, max(cn0 - 1, 0)), cbeg + cn0);
+        }
+#pragma unroll
+        for (int q = 0; q < NWQ; ++q) {
+            const int it = min(q * NT + tid, max(total0 - 1, 0));
+            wr[q] = seg_row_nb(a.rag, cbeg + min(it / nvr, max(cn0 - 1, 0)), cbeg + cn0);
+        }
+    }
+    sync.wait();   // producers of this tile's operand rows have finished
+
+    // ---- 2. stage the A tile: [x | child h ...] or [child sum of h] ----
+    float cv[NCI];
+    float4 f4[NWQ][V / 4];
+    const T* zero = reinterpret_cast<const T*>(a.arena_h);
+    if constexpr (CSUM) {
+        csum.gather(A, AS, a, nrows, 0, tid);
+        for (int base = NT * SR; base < nrows * nvr; base += NT * SR) {
+            csum.bounds(a, row0, nrows, base, tid);
+            csum.gather(A, AS, a, nrows, base, tid);
+        }
+    } else if constexpr (ER) {
+        st.template vals<NT>(sg, nrows, 0, zero, tid);
+        // the early chunk's values (masked: the zero row), behind the tile's
+#pragma unroll
+        for (int q = 0; q < NCI; ++q) {
+            const int it = tid + NT * q, j = u0 + it % TU;
+            const bool ok = it < cn0 * TU && j < a.H;
+            cv[q] = *(ok ? a.arena_c + (size_t)crw[q] * a.H + j : a.arena_c);
+        }
+#pragma unroll
+        for (int q = 0; q < NWQ; ++q) {
+            const int it = q * NT + tid, r = it / nvr, c = it - r * nvr;
+            const bool ok = it < total0 && c < a.H / V;
+            const float4* src = reinterpret_cast<const float4*>(ok ? a.arena_c + (size_t)wr[q] * a.H + c * V : a.arena_c);
+#pragma unroll
+            for (int k = 0; k < V / 4; ++k) f4[q][k] = src[k];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        st.template store<NT>(A, AS, sg, nrows, 0, tid);
+        int nmax = 0;
+#pragma unroll
+        for (int s = 0; s < NSEG; ++s) nmax = max(nmax, nrows * sg[s].nv);
+        for (int base = NT * SR; base < nmax; base += NT * SR) {
+            st.template idx<NT>(sg, nrows, base, tid);
+            st.template vals<NT>(sg, nrows, base, zero, tid);
+            __builtin_amdgcn_sched_barrier(0);
+            st.template store<NT>(A, AS, sg, nrows, base, tid);
+        }
+    } else {
+        stage_tile<T, TM, NT, NSEG>(A, AS, sg, nrows, zero, tid);
+    }
+    // the children's cell states: only the epilogue reads them, so they are
+    // loaded behind the operand rows
+    float cpre[NI][NFX > 0 ? NFX : 1];
+#pragma unroll
+    for (int q = 0; q < NI; ++q) {
+        const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
+        const bool ok = it < NITEM && r < nrows && j < a.H;
+#pragma unroll
+        for (int p = 0; p < (NFX > 0 ? NFX : 1); ++p) {
+            const bool use = NFX > p && reads_child_c<KIND>() && ok && a.fix[p].kind != S_NONE;
+            cpre[q][p] = *(use ? a.arena_c + (size_t)crow[q][p] * a.H + j : a.arena_c);
+        }
     }
     __syncthreads();
 
-    // ---- 4. gate GEMM: wave (wu, wk) -> unit block ub, k-groups [kg0, kg1) ----
+    // ---- 3. gate GEMM: wave (wu, wk) -> unit block ub, k-groups [kg0, kg1) ----
     {
         v4f acc[G][RT];
 #pragma unroll
@@ -601,9 +840,62 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
                     Z[((wk * TM + r) * G + g) * TU + u] = acc[g][rt][i];
                 }
     }
+
+    // the ragged phase's per-child GEMM of rows [cb, cb + cn) staged in Ar:
+    // partials -> Zr[wk][row][unit]
+    // (only the row blocks holding rows: a chunk of a few words takes one)
+    auto rag_gemm = [&](int cn) {
+        constexpr int RTR = TMR / 16;
+        v4f acc[1][RTR];
+#pragma unroll
+        for (int rt = 0; rt < RTR; ++rt) acc[0][rt] = v4f{0.f, 0.f, 0.f, 0.f};
+        if (rk0 < rk1 && cn > 0) {
+            if (RTR > 1 && cn <= 16) {
+                v4f a1[1][1] = {{v4f{0.f, 0.f, 0.f, 0.f}}};
+                wave_gemm<T, 1, 1, 4>(a1, Ar, RS, Brag, nkgr, rk0, rk1, lane, rring);
+                acc[0][0] = a1[0][0];
+            } else if (RTR > 2 && cn <= 32) {
+                v4f a2[1][2] = {{v4f{0.f, 0.f, 0.f, 0.f}, v4f{0.f, 0.f, 0.f, 0.f}}};
+                wave_gemm<T, 1, 2, 4>(a2, Ar, RS, Brag, nkgr, rk0, rk1, lane, rring);
+                acc[0][0] = a2[0][0];
+                acc[0][1] = a2[0][1];
+            } else {
+                wave_gemm<T, 1, RTR, 4>(acc, Ar, RS, Brag, nkgr, rk0, rk1, lane, rring);
+            }
+        }
+#pragma unroll
+        for (int rt = 0; rt < RTR; ++rt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = rt * 16 + (lane >> 4) * 4 + i;
+                const int u = wu * 16 + (lane & 15);
+                Zr[(wk * TMR + r) * TU + u] = acc[0][rt][i];
+            }
+    };
+    if constexpr (ER) {
+        // the early chunk: cell states to Crag, rows converted to T into Ar
+        // (pieces beyond the early ones loaded now), then its GEMM
+#pragma unroll
+        for (int q = 0; q < NCI; ++q)   // rows past cn0 are never read
+            if (tid + NT * q < cn0 * TU) Crag[tid + NT * q] = cv[q];
+#pragma unroll
+        for (int q = 0; q < NWQ; ++q) {
+            const int it = q * NT + tid, r = it / nvr, c = it - r * nvr;
+            if (it >= total0) continue;
+            uint4 out;
+            T* po = reinterpret_cast<T*>(&out);
+            const float* pf = reinterpret_cast<const float*>(&f4[q][0]);
+#pragma unroll
+            for (int i = 0; i < V; ++i) po[i] = from_f<T>(pf[i]);
+            *reinterpret_cast<uint4*>(Ar + r * RS + c * V) = out;
+        }
+        stage_word_rows<T, NT>(Ar, RS, a, cbeg, cn0, NWQ * NT, tid);
+        __syncthreads();
+        rag_gemm(cn0);
+    }
     __syncthreads();
 
-    // ---- 5. per-item gate pre-activations (fixed-order sum over the K split) ----
+    // ---- 4. per-item gate pre-activations (fixed-order sum over the K split) ----
     float zsum[NI][G];
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
@@ -616,122 +908,23 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
 #pragma unroll
             for (int w = 0; w < WK; ++w) s += Z[((w * TM + r) * G + g) * TU + u];
             // a pooling node adds its bias after the mean (in the epilogue)
-            zsum[q][g] = KIND == K_POOL_MEAN ? s : s + a.bias[g * a.Hu + j];
+            const float b = EARLY ? bz[q][g] : a.bias[g * a.Hu + j];
+            zsum[q][g] = KIND == K_POOL_MEAN ? s : s + b;
         }
     }
 
-    // ---- 6. ragged phase: per-child GEMM (child-sum U_f, lattice W_lc) ----
+    // ---- 5. ragged phase: per-child GEMM (child-sum U_f, lattice W_lc) ----
     float racc[NI], rden[NI];
 #pragma unroll
     for (int q = 0; q < NI; ++q) { racc[q] = 0.f; rden[q] = 0.f; }
     if constexpr (KIND == K_POOL_MEAN) {
 #pragma unroll
-        for (int q = 0; q < NI; ++q) racc[q] = a.bias[u0 + (tid + NT * q) % TU];   // the packed bias is padded to Hu
+        for (int q = 0; q < NI; ++q) racc[q] = bz[q][0];
     }
     if constexpr (KT::RAG) {
-        // children (words) of the tile's parents in chunks of TMR rows: their
-        // h rows (child-sum) or cell states (lattice) staged to A, their cell
-        // states for this tile's units to Crag, the per-child GEMM to Zr
-        constexpr int TMR = 16 * rag_rt<KIND, RT>();
-        float* Crag = Zr + WK * TMR * TU;
-        const int cbeg = a.rag_ptr[row0];
-        const int cend = a.rag_ptr[row0 + nrows];
-        const int nkgr = a.Hk / KG;
-        const uint4* Brag = reinterpret_cast<const uint4*>(a.Wr) + ((size_t)ub * nkgr) * 64 + lane;
-        const int rk0 = (nkgr * wk) / WK, rk1 = (nkgr * (wk + 1)) / WK;
-        const int RS = a.Hk + AS_PAD;
-        int pe0[NI], pe1[NI];   // child range of each item's parent
-#pragma unroll
-        for (int q = 0; q < NI; ++q) {
-            const int it = tid + NT * q, r = it / TU;
-            const bool ok = it < NITEM && r < nrows;
-            pe0[q] = ok ? a.rag_ptr[row0 + r] : 0;
-            pe1[q] = ok ? a.rag_ptr[row0 + r + 1] : 0;
-        }
-        for (int cb = cbeg; cb < cend; cb += TMR) {
-            const int cn = min(TMR, cend - cb);
-            __syncthreads();   // previous chunk's readers of A / Zr / Crag are done
-            BRing<1, 4> rring;
-            ring_prologue<1, 4>(rring, Brag, nkgr, rk0, rk1);
-            {   // the chunk's cell states: indices, then values (masked: the zero row), then stores
-                constexpr int NCI = (TMR * TU + NT - 1) / NT;
-                int crw[NCI];
-                float cv[NCI];
-#pragma unroll
-                for (int q = 0; q < NCI; ++q) {
-                    const int it = min(tid + NT * q, TMR * TU - 1);
-                    crw[q] = seg_row_nb(a.rag, cb + min(it / TU, cn - 1), cb + cn);
-                }
-#pragma unroll
-                for (int q = 0; q < NCI; ++q) {
-                    const int it = tid + NT * q, r = it / TU, j = u0 + it % TU;
-                    const bool ok = it < cn * TU && j < a.H;
-                    cv[q] = *(ok ? a.arena_c + (size_t)crw[q] * a.H + j : a.arena_c);
-                }
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int q = 0; q < NCI; ++q)   // rows past cn are never read
-                    if (tid + NT * q < cn * TU) Crag[tid + NT * q] = cv[q];
-            }
-            if constexpr (KIND == K_CS_INT) {
-                constexpr int V = Elem<T>::VEC;
-                ASeg<T> sg[1] = {ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.rag, cb, 0, a.Hk / V, a.H / V, a.H,
-                                         cb + cn}};
-                stage_tile<T, TMR, NT, 1>(A, RS, sg, cn, reinterpret_cast<const T*>(a.arena_h), tid);
-            } else {
-                // lattice: the word cell states c_w (fp32) converted to T, two
-                // pieces per thread a round: indices, then values (masked: the
-                // zero row), then the converted stores
-                constexpr int V = Elem<T>::VEC;
-                const int nv = a.Hk / V, nreal = a.H / V, total = cn * nv;   // rows past cn are not read back
-                for (int base = 0; base < total; base += 2 * NT) {
-                    int wr[2];
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        const int it = min(base + q * NT + tid, total - 1);
-                        wr[q] = seg_row_nb(a.rag, cb + min(it / nv, cn - 1), cb + cn);
-                    }
-                    float4 f4[2][V / 4];
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        const int it = base + q * NT + tid, r = it / nv, c = it - r * nv;
-                        const bool ok = it < total && c < nreal;
-                        const float4* src = reinterpret_cast<const float4*>(
-                            ok ? a.arena_c + (size_t)wr[q] * a.H + c * V : a.arena_c);
-#pragma unroll
-                        for (int k = 0; k < V / 4; ++k) f4[q][k] = src[k];
-                    }
-                    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        const int it = base + q * NT + tid, r = it / nv, c = it - r * nv;
-                        if (it >= total) continue;
-                        uint4 out;
-                        T* po = reinterpret_cast<T*>(&out);
-                        const float* pf = reinterpret_cast<const float*>(&f4[q][0]);
-#pragma unroll
-                        for (int i = 0; i < V; ++i) po[i] = from_f<T>(pf[i]);
-                        *reinterpret_cast<uint4*>(A + r * RS + c * V) = out;
-                    }
-                }
-            }
-            __syncthreads();
-            {
-                constexpr int RTR = TMR / 16;
-                v4f acc[1][RTR];
-#pragma unroll
-                for (int rt = 0; rt < RTR; ++rt) acc[0][rt] = v4f{0.f, 0.f, 0.f, 0.f};
-                if (rk0 < rk1) wave_gemm<T, 1, RTR, 4>(acc, A, RS, Brag, nkgr, rk0, rk1, lane, rring);
-#pragma unroll
-                for (int rt = 0; rt < RTR; ++rt)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int r = rt * 16 + (lane >> 4) * 4 + i;
-                        const int u = wu * 16 + (lane & 15);
-                        Zr[(wk * TMR + r) * TU + u] = acc[0][rt][i];
-                    }
-            }
-            __syncthreads();
+        // each item's children (words) among rows [cb, cb + cn): the per-child
+        // sums from Zr, their cell states from Crag
+        auto accumulate = [&](int cb, int cn) {
 #pragma unroll
             for (int q = 0; q < NI; ++q) {
                 const int it = tid + NT * q, u = it % TU;
@@ -739,7 +932,7 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
                 if (j >= a.H) continue;
                 const int e0 = max(pe0[q], cb), e1 = min(pe1[q], cb + cn);
                 for (int e = e0; e < e1; ++e) {
-                    float s = a.br[j];
+                    float s = brj[q];
 #pragma unroll
                     for (int w = 0; w < WK; ++w) s += Zr[(w * TMR + (e - cb)) * TU + u];
                     const float cw = Crag[(e - cb) * TU + u];
@@ -753,10 +946,49 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
                     }
                 }
             }
+        };
+        if constexpr (ER) accumulate(cbeg, cn0);
+        // the remaining chunks of TMR rows: their h rows (child-sum) or cell
+        // states (lattice) staged to Ar, their cell states for this tile's
+        // units to Crag, the per-child GEMM to Zr
+        for (int cb = ER ? cbeg + TMR : cbeg; cb < cend; cb += TMR) {
+            const int cn = min(TMR, cend - cb);
+            __syncthreads();   // previous chunk's readers of Ar / Zr / Crag are done
+            ring_prologue<1, 4>(rring, Brag, nkgr, rk0, rk1);
+            {   // the chunk's cell states: indices, then values (masked: the zero row), then stores
+                int crx[NCI];
+                float cvx[NCI];
+#pragma unroll
+                for (int q = 0; q < NCI; ++q) {
+                    const int it = min(tid + NT * q, TMR * TU - 1);
+                    crx[q] = seg_row_nb(a.rag, cb + min(it / TU, cn - 1), cb + cn);
+                }
+#pragma unroll
+                for (int q = 0; q < NCI; ++q) {
+                    const int it = tid + NT * q, j = u0 + it % TU;
+                    const bool ok = it < cn * TU && j < a.H;
+                    cvx[q] = *(ok ? a.arena_c + (size_t)crx[q] * a.H + j : a.arena_c);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int q = 0; q < NCI; ++q)   // rows past cn are never read
+                    if (tid + NT * q < cn * TU) Crag[tid + NT * q] = cvx[q];
+            }
+            if constexpr (KIND == K_CS_INT) {
+                ASeg<T> sr[1] = {ASeg<T>{reinterpret_cast<const T*>(a.arena_h), a.rag, cb, 0, a.Hk / V, a.H / V, a.H,
+                                         cb + cn}};
+                stage_tile<T, TMR, NT, 1>(Ar, RS, sr, cn, zero, tid);
+            } else {
+                stage_word_rows<T, NT>(Ar, RS, a, cb, cn, 0, tid);
+            }
+            __syncthreads();
+            rag_gemm(cn);
+            __syncthreads();
+            accumulate(cb, cn);
         }
     }
 
-    // ---- 7. gate epilogue and scatter of h, c ----
+    // ---- 6. gate epilogue and scatter of h, c ----
     T* Hout = reinterpret_cast<T*>(a.arena_h);
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
@@ -764,9 +996,9 @@ __device__ __forceinline__ void cell_tile(const BatchArgs& a, int rtile, int ut,
         const int j = u0 + u;
         if (it >= NITEM || r >= nrows || j >= a.H) continue;
         float c, h;
+        // words ending at a lattice character, edges of a pooled position
         cell_update<KIND>(zsum[q], cpre[q], racc[q], rden[q],
-                          KIND == K_LAT_CHAR || KIND == K_POOL_MEAN ? a.rag_ptr[row0 + r + 1] - a.rag_ptr[row0 + r] : 0,
-                          c, h);
+                          KIND == K_LAT_CHAR || KIND == K_POOL_MEAN ? pe1[q] - pe0[q] : 0, c, h);
         const size_t o = (size_t)rres[q] * a.H + j;
         a.arena_c[o] = c;
         Hout[o] = from_f<T>(h);

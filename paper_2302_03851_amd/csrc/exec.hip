@@ -263,12 +263,12 @@ hipError_t attr_cell(int lds) {
                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
 }
 template <int KIND, typename T, int RT, int WU, int WK>
-int lds_cell(int K) { return lds_bytes<KIND, T, RT, WU, WK>(K); }
+int lds_cell(int K, int Hk) { return lds_bytes<KIND, T, RT, WU, WK>(K, Hk); }
 
 struct Entry {
     LaunchFn launch;
     AttrFn attr;
-    int (*lds)(int);
+    int (*lds)(int K, int Hk);   // LDS bytes for reduction length K and ragged row width Hk
     const void* fn;   // the kernel (occupancy queries)
 };
 
@@ -289,7 +289,7 @@ void launch_big(const BatchArgs& a, int grid, int, hipStream_t st, hipEvent_t ev
 template <int KIND, int VB>
 hipError_t attr_big(int) { return hipSuccess; }
 template <int KIND, int VB>
-int lds_big(int) { return big_lds_bytes<KIND, VB>(); }
+int lds_big(int, int) { return big_lds_bytes<KIND, VB>(); }
 
 template <int KIND, typename T, int VB>
 Entry big_entry() {
@@ -312,7 +312,7 @@ hipError_t attr_stream(int lds) {
                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
 }
 template <int KIND, typename T, int RT, int WK>
-int lds_stream(int) { return stream_lds_bytes<KIND, T, RT, WK>(); }
+int lds_stream(int, int) { return stream_lds_bytes<KIND, T, RT, WK>(); }
 
 // the streamed tile serves the kinds without a ragged phase
 template <int KIND, typename T, int RT, int WK>
@@ -413,22 +413,23 @@ constexpr int FLOW_VARIANT = 100;
 
 template <typename T>
 int flow_lds(const std::vector<int>& kinds_k) {
-    // LDS of the largest tile body among (kind, K) pairs of the run
+    // LDS of the largest tile body among (kind, K) pairs of the run (a ragged
+    // row is at most K wide: K bounds Hk)
     int best = 0;
     for (size_t i = 0; i + 1 < kinds_k.size(); i += 2) {
         const int kind = kinds_k[i], K = kinds_k[i + 1];
         int l = 0;
         switch (kind) {
-            case K_CHAIN: l = lds_bytes<K_CHAIN, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_NARY_LEAF: l = lds_bytes<K_NARY_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_NARY_INT: l = lds_bytes<K_NARY_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_GRID: l = lds_bytes<K_GRID, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_CS_LEAF: l = lds_bytes<K_CS_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_CS_INT: l = lds_bytes<K_CS_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_LAT_CHAR: l = lds_bytes<K_LAT_CHAR, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_GRU_LEAF: l = lds_bytes<K_GRU_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            case K_GRU_INT: l = lds_bytes<K_GRU_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
-            default: l = lds_bytes<K_LAT_WORD, T, FLOW_RT, FLOW_WU, FLOW_WK>(K); break;
+            case K_CHAIN: l = lds_bytes<K_CHAIN, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_NARY_LEAF: l = lds_bytes<K_NARY_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_NARY_INT: l = lds_bytes<K_NARY_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_GRID: l = lds_bytes<K_GRID, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_CS_LEAF: l = lds_bytes<K_CS_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_CS_INT: l = lds_bytes<K_CS_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_LAT_CHAR: l = lds_bytes<K_LAT_CHAR, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_GRU_LEAF: l = lds_bytes<K_GRU_LEAF, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            case K_GRU_INT: l = lds_bytes<K_GRU_INT, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
+            default: l = lds_bytes<K_LAT_WORD, T, FLOW_RT, FLOW_WU, FLOW_WK>(K, K); break;
         }
         best = std::max(best, l);
     }
@@ -536,7 +537,7 @@ int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max
     for (int vb = 0; vb < NUM_BIG_CLASSES; ++vb) {
         const Entry& en = table().e[kk][dtype][large_variant(vb)];
         if (!en.launch) continue;
-        const int lds = en.lds(K);
+        const int lds = en.lds(K, 0);   // the large tile's LDS is static
         if (lds > max_lds) continue;
         const double c = large_cost(G, vb, m, K, Hu, dtype, occ(en, 256, 0, lds), n_cu) + extra_us;
         if (c < est * 0.97) { est = c; var = large_variant(vb); }
@@ -931,7 +932,7 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
                 if (!is_small(vi) && !(is_stream(vi) && large_fits)) continue;
                 const Entry& en = table().e[kind_id][dtype][vi];
                 if (!en.launch) continue;
-                const int lds = en.lds(d.K);
+                const int lds = en.lds(d.K, d.Hk);
                 if (lds > max_lds) continue;
                 if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
                 if ((flags & EDB_NO_SPLIT_K) && VAR_WK[vi] != 1) continue;
@@ -947,7 +948,7 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
             if (is_stream(fv) && !(large_fits && table().e[kind_id][dtype][fv].launch))
                 fv = STAGED_OF[fv - FIRST_STREAM];
             if ((is_small(fv) || is_stream(fv)) && table().e[kind_id][dtype][fv].launch &&
-                table().e[kind_id][dtype][fv].lds(d.K) <= max_lds)
+                table().e[kind_id][dtype][fv].lds(d.K, d.Hk) <= max_lds)
                 var = fv;
             if (is_large(force_var) && lvar >= 0) {
                 const int fk = cs_large ? K_CS_PARENT : kind_id;
@@ -1003,7 +1004,7 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
                 F.args.Ep = d.Hk;
                 F.args.res = Seg{S_NONE, 0, nullptr};
                 F.off_res = -1;
-                F.lds = table().e[K_CS_FORGET][dtype][fvar].lds(d.K);
+                F.lds = table().e[K_CS_FORGET][dtype][fvar].lds(d.K, d.Hk);
                 F.info.block = 256;
                 F.info.grid = ((int)((nrag + large_tm(1, large_class(fvar)) - 1) / large_tm(1, large_class(fvar))) *
                                    (d.Hu / large_tu(large_class(fvar))) + 7) / 8 * 8;
@@ -1030,7 +1031,7 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
                 e->hsum_rows = std::max<int64_t>(e->hsum_rows, m);
                 e->fc_rows = std::max<int64_t>(e->fc_rows, nrag);
             }
-            L.lds = table().e[L.kk][dtype][var].lds(d.K);
+            L.lds = table().e[L.kk][dtype][var].lds(d.K, d.Hk);
             if (L.lds > max_lds) {
                 delete e;
                 return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: LDS need of batch " + std::to_string(b) +
