@@ -408,6 +408,76 @@ def split_phase_record(w, k, mult, copy_gbs, reps=5):
 DEFAULT_INSTANCES = {1: 8, 2: 64, 3: 32, 4: 32, 5: 256, 6: 64, 7: 64, 8: 64, 9: 32}
 
 
+def vendor_gemm(configs, reps=50):
+    """Context for the large tile (one JSON line per workload): the longest
+    launch of a leaf batch (x operand only, so the GEMM is m x E times E x
+    gates*H) beside the vendor GEMM of the same shape and element type
+    (torch.matmul, served by hipBLASLt), plain and after a row gather (torch
+    indexing).  Our launch also gathers its rows, applies the gate epilogue
+    and writes h (element type) and c (fp32); the vendor GEMM writes its
+    product in the element type only.  Medians over `reps` runs; ours from the
+    per-launch events of a profiled forward."""
+    import torch
+    from paper_2302_03851_amd import _lib as L
+    from paper_2302_03851_amd import edb, workloads as WL
+
+    gates = {WL.NARY_LEAF: 3, WL.CS_LEAF: 3, WL.GRU_LEAF: 2}
+    for k in configs:
+        w = WL.make_config(k)
+        f = edb.Forward(w, flags=L.PROFILE)
+        for _ in range(3):
+            f.run()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            f.run()
+            torch.cuda.synchronize()
+            ts.append(f.exec.launch_times())
+        t_us = np.median(np.array(ts), axis=0) * 1e3
+        infos = [f.exec.launch_info(i) for i in range(f.exec.launches())]
+        cand = [i for i in range(1, len(infos)) if infos[i]["kind"] in gates and infos[i]["part"] == 0]
+        if not cand:
+            print(json.dumps({"workload": WORKLOAD_TEXT[k], "leaf_launch": None}), flush=True)
+            continue
+        i = max(cand, key=lambda j: t_us[j])
+        m, E, N = int(infos[i]["m"]), w.in_dim, gates[infos[i]["kind"]] * w.hidden
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        gen = torch.Generator(device="cuda:0").manual_seed(0)
+        x = torch.randn(m, E, device="cuda:0", dtype=dt, generator=gen)
+        W = torch.randn(E, N, device="cuda:0", dtype=dt, generator=gen)
+        rows = torch.randperm(m, device="cuda:0", generator=gen)
+
+        def timed(fn):
+            for _ in range(5):
+                fn()
+            torch.cuda.synchronize()
+            out = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                e1.synchronize()
+                out.append(e0.elapsed_time(e1) * 1e3)
+            return float(np.median(out))
+
+        flops = 2.0 * m * E * N
+        peak = PEAK_TFLOPS[w.dtype]
+        rec = {"workload": WORKLOAD_TEXT[k], "shape": {"m": m, "K": E, "N": N, "dtype": w.dtype},
+               "ours": {"us": round(float(t_us[i]), 2), "variant": int(infos[i]["variant"]),
+                        "work": "row gather + GEMM + gate epilogue, h and c written"}}
+        for name, fn in (("vendor_mm", lambda: x @ W), ("vendor_gather_mm", lambda: x[rows] @ W)):
+            us = timed(fn)
+            rec[name] = {"us": round(us, 2)}
+        for key in ("ours", "vendor_mm", "vendor_gather_mm"):
+            rec[key]["tflops"] = round(flops / (rec[key]["us"] * 1e-6) / 1e12, 1)
+            rec[key]["frac_of_peak"] = round(rec[key]["tflops"] / peak, 4)
+        rec["peak_tflops"] = peak
+        print(json.dumps(rec), flush=True)
+        del f, x, W, rows
+        torch.cuda.empty_cache()
+
+
 def study(configs, replays=100):
     """Replay study of each workload (one JSON line per workload): warm and
     cold replays of the captured batch sequence (median, p10, p90; cold = a
@@ -497,6 +567,8 @@ def main():
     ap.add_argument("--split-phase", metavar="CONFIGS",
                     help="instead of the benchmark: unfused gather and scatter times of the listed workloads "
                          "(comma separated; 'KxN' = workload K with N times its instances, e.g. 5,5x4,5x16)")
+    ap.add_argument("--vendor-gemm", metavar="CONFIGS",
+                    help="comma-separated workloads: the longest leaf-batch launch beside the vendor GEMM of its shape")
     ap.add_argument("--probes", action="store_true",
                     help="instead of the benchmark: measured MFMA and copy rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -536,6 +608,9 @@ def main():
         return
     if args.probes:
         print(json.dumps({"f32": probes("f32"), "bf16": probes("bf16")}), flush=True)
+        return
+    if args.vendor_gemm:
+        vendor_gemm([int(c) for c in args.vendor_gemm.split(",")])
         return
     if args.copy_calibration:
         # copies of known size, each dispatch reading and writing 2 GiB (8x the
