@@ -446,8 +446,16 @@ edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
  * Section 3 lays out its memory, all at run time for every new input):
  * edb_build_graph, edb_schedule, edb_plan_memory, edb_prepare (eager
  * launches) and edb_execute on `stream`, then every handle is released.  The call does not
- * wait for the GPU: the executor's device buffers are freed in stream order
- * after the work.  Arguments are those of the individual calls; arena_h and
+ * wait for the GPU.  Device memory: without exec_out and EDB_PROFILE the call
+ * uses a device block that the library keeps for the current device and
+ * `stream` and reuses on the next call there (the descriptors are copied on
+ * `stream` from pinned host buffers that the library also keeps for the
+ * stream, so the next call overwrites them after this call's kernels); the
+ * block grows in stream order when a call needs more (EDB_ERR_OOM if it
+ * cannot) and is held until edb_stream_release.  Calls on one stream from
+ * several threads enqueue one at a time.  With exec_out or EDB_PROFILE the
+ * executor has device buffers of its own, freed in stream order after the
+ * work.  Arguments are those of the individual calls; arena_h and
  * arena_c must hold at least the plan's n_slots rows (arena_rows), which is
  * returned in *n_slots (may be NULL) also when the arena is too small
  * (EDB_ERR_INVALID).  EDB_DRYRUN is rejected.
@@ -460,6 +468,15 @@ edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
                        const edb_cell* cells, int32_t exec_flags, const void* const* packed_weights,
                        const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
                        int32_t* n_slots, edb_exec_t** exec_out);
+
+/* Returns the device block and pinned host buffers that edb_forward keeps
+ * for the current device and `stream` (the device block by a stream-ordered
+ * free on `stream`, after the work already enqueued there; the host buffers
+ * once the copies from them have run, which this call waits for); a later
+ * edb_forward on the stream allocates new ones.
+ * Call it before destroying a stream that edb_forward used.  No block: a
+ * no-op.  Errors: EDB_ERR_HIP. */
+edb_status edb_stream_release(void* stream);
 
 /* For callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc): edb_forward without any

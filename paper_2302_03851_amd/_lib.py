@@ -41,7 +41,8 @@ EXPORTS = [
     "edb_plan_memory", "edb_plan_view", "edb_plan_free",
     "edb_packed_weight_bytes", "edb_pack_weights",
     "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
-    "edb_exec_check", "edb_exec_validate", "edb_exec_free", "edb_forward", "edb_forward_noalloc",
+    "edb_exec_check", "edb_exec_validate", "edb_exec_free", "edb_forward", "edb_stream_release",
+    "edb_forward_noalloc",
     "edb_split_phase_bytes", "edb_split_phase", "edb_probe_mfma", "edb_probe_copy",
 ]
 
@@ -145,6 +146,7 @@ def load():
         "edb_forward": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32), P(C.c_int32),
                                     P(Policy), P(OperandShape), C.c_int32, P(Cell), C.c_int32, P(vp), vp, vp, vp,
                                     C.c_int64, vp, P(C.c_int32), P(vp)]),
+        "edb_stream_release": (C.c_int32, [vp]),
         "edb_forward_noalloc": (C.c_int32, [C.c_int32, C.c_int32, P(C.c_int32), P(C.c_int64), P(C.c_int32),
                                             P(C.c_int32), P(Policy), P(OperandShape), C.c_int32, P(Cell),
                                             C.c_int32, P(vp), vp, vp, vp, C.c_int64, vp, P(C.c_int32)]),

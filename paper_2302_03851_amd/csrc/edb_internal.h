@@ -61,4 +61,12 @@ void pq_layout(const edb_graph& g, const struct edb_schedule& s, const edb_opera
                std::vector<int32_t>& slot_of, std::map<std::tuple<int, int, int>, int32_t>& pad_of,
                std::vector<int32_t>& lead);
 
+// edb_forward's plain path (no executor handed back, no profiling): prepares
+// the launches without device memory of their own, binds them to the device
+// block cached for (current device, stream), copies the descriptors on the
+// stream and launches; the block grows in stream order when a call needs more.
+edb_status forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
+                             const edb_cell* cells, int32_t flags, const void* const* packed_weights,
+                             const void* x, void* arena_h, void* arena_c, void* stream);
+
 }  // namespace edb

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <functional>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <new>
 #include <string>
@@ -1746,6 +1747,187 @@ extern "C" edb_status edb_exec_check(edb_exec_t* e, void* stream) {
 }
 
 extern "C" void edb_exec_free(edb_exec_t* e) { delete e; }
+
+// ---------------------------------------------------------------------------
+// edb_forward's plain path.  A call's device memory comes from a block kept
+// per device and stream instead of a per-call allocation:
+// * its descriptor ints go to one of NH slots, each a device buffer and a
+//   pinned host buffer, used in turn (a copy from pageable memory would be
+//   done synchronously, after the copying stream's earlier work): the host
+//   fills the pinned buffer; while the stream still runs earlier calls, the
+//   device's upload stream copies it, ahead of the stream's kernels, which
+//   wait for it (event); on an idle stream the stream itself copies it;
+//   a slot is refilled only after the kernels of its last use, NH calls
+//   earlier, have finished (event, usually long done);
+// * its staged x and scratch rows go to one region, which only kernels on
+//   the stream touch, so the next call reuses it in stream order.
+// Buffers grow, with a quarter to spare, when a call needs more.  Calls on one
+// stream from several threads enqueue one at a time (the block's lock).
+
+namespace {
+
+struct StreamBlock {
+    static constexpr int NH = 4;
+    struct Slot {
+        void* dev = nullptr;        // descriptor ints on the device
+        size_t cap = 0;
+        void* host = nullptr;       // pinned staging copy
+        size_t hcap = 0;
+        hipEvent_t ready = nullptr; // the upload has run
+        hipEvent_t done = nullptr;  // the kernels that read it have run
+        bool used = false;
+    };
+    std::mutex mu;
+    void* rest = nullptr;           // staged x and scratch rows
+    size_t rest_cap = 0;
+    Slot slot[NH];
+    int next = 0;
+};
+std::mutex g_blocks_mu;
+std::map<std::pair<int, hipStream_t>, std::unique_ptr<StreamBlock>> g_blocks;
+
+size_t with_spare(size_t v, size_t align) { return (v + v / 4 + align - 1) / align * align; }
+
+}  // namespace
+
+edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
+                                  const edb_cell* cells, int32_t flags, const void* const* packed_weights,
+                                  const void* x, void* arena_h, void* arena_c, void* stream) {
+    int dev = 0;
+    DeviceCtx* ctx = nullptr;
+    hipError_t he = hipGetDevice(&dev);
+    if (he == hipSuccess) he = device_ctx(dev, &ctx);
+    if (he == hipSuccess) he = ctx_streams(ctx);
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_forward: ") + hipGetErrorString(he));
+    edb_exec_t* e = nullptr;
+    edb_status st = prepare_impl(g, s, p, cells, flags, true, &e);
+    if (st == EDB_OK) st = check_exec_args(e, packed_weights, x, arena_h, arena_c, "edb_forward");
+    StreamBlock* blk = nullptr;
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    if (st == EDB_OK) {
+        std::lock_guard<std::mutex> lk(g_blocks_mu);
+        std::unique_ptr<StreamBlock>& up = g_blocks[{dev, hs}];
+        if (!up) up.reset(new (std::nothrow) StreamBlock);
+        blk = up.get();
+        if (!blk) st = fail(EDB_ERR_OOM, "edb_forward: out of host memory");
+    }
+    if (st == EDB_OK) {
+        std::lock_guard<std::mutex> lk(blk->mu);
+        StreamBlock::Slot& sl = blk->slot[blk->next];
+        const size_t ibytes = e->d_ibytes, rbytes = e->d_total - e->d_ibytes;
+        const size_t hbytes = e->hbuf.size() * sizeof(int32_t);
+        // the slot's last kernels have finished: its buffers are free
+        if (sl.used) he = hipEventSynchronize(sl.done);
+        if (he == hipSuccess && !sl.ready) he = hipEventCreateWithFlags(&sl.ready, hipEventDisableTiming);
+        if (he == hipSuccess && !sl.done) he = hipEventCreateWithFlags(&sl.done, hipEventDisableTiming);
+        if (he == hipSuccess && sl.cap < ibytes) {
+            if (sl.dev) (void)hipFreeAsync(sl.dev, ctx->upload);
+            sl.dev = nullptr;
+            sl.cap = 0;
+            const size_t want = with_spare(ibytes, 256);
+            he = hipMallocAsync(&sl.dev, want, ctx->upload);
+            if (he == hipSuccess) sl.cap = want;
+            else sl.dev = nullptr;
+        }
+        if (he == hipSuccess && sl.hcap < hbytes) {
+            if (sl.host) (void)hipHostFree(sl.host);
+            sl.host = nullptr;
+            sl.hcap = 0;
+            const size_t want = with_spare(hbytes, 4096);
+            he = hipHostMalloc(&sl.host, want, hipHostMallocDefault);
+            if (he == hipSuccess) sl.hcap = want;
+            else sl.host = nullptr;
+        }
+        if (he == hipSuccess && rbytes > 0 && blk->rest_cap < rbytes) {
+            // the old region after the stream's earlier kernels
+            if (blk->rest) (void)hipFreeAsync(blk->rest, hs);
+            blk->rest = nullptr;
+            blk->rest_cap = 0;
+            const size_t want = with_spare(rbytes, 256);
+            he = hipMallocAsync(&blk->rest, want, hs);
+            if (he == hipSuccess) blk->rest_cap = want;
+            else blk->rest = nullptr;
+        }
+        // an idle stream (the previous call's kernels have run) copies the
+        // descriptors itself: nothing to overlap, and no wait across streams;
+        // a busy one has the upload stream copy them ahead of its kernels
+        bool idle = true;
+        if (he == hipSuccess) {
+            const StreamBlock::Slot& prev = blk->slot[(blk->next + StreamBlock::NH - 1) % StreamBlock::NH];
+            if (prev.used) {
+                const hipError_t q = hipEventQuery(prev.done);
+                if (q == hipErrorNotReady) {
+                    idle = false;
+                    (void)hipGetLastError();
+                } else if (q != hipSuccess) {
+                    he = q;
+                }
+            }
+        }
+        if (he == hipSuccess) {
+            std::memcpy(sl.host, e->hbuf.data(), hbytes);
+            he = hipMemcpyAsync(sl.dev, sl.host, hbytes, hipMemcpyHostToDevice, idle ? hs : ctx->upload);
+        }
+        if (he == hipSuccess && !idle) he = hipEventRecord(sl.ready, ctx->upload);
+        if (he == hipSuccess && !idle) he = hipStreamWaitEvent(hs, sl.ready, 0);
+        if (he == hipSuccess) {
+            // descriptors in the slot; staged x and scratch rows in the region
+            // (bound as one block at rest - d_ibytes, whose first d_ibytes are
+            // never touched: dbuf is re-pointed to the slot)
+            uint8_t* base = blk->rest ? reinterpret_cast<uint8_t*>(blk->rest) - e->d_ibytes
+                                      : reinterpret_cast<uint8_t*>(sl.dev);   // no region: no parts past dbuf
+            bind_device(e, base);
+            e->dbuf = reinterpret_cast<int*>(sl.dev);
+            e->dmem = nullptr;
+            e->dmem_owned = false;
+            he = launch_all(e, packed_weights, x, arena_h, arena_c, hs);
+        }
+        if (he == hipSuccess) he = hipEventRecord(sl.done, hs);
+        if (he == hipSuccess) {
+            sl.used = true;
+            blk->next = (blk->next + 1) % StreamBlock::NH;
+        }
+        if (he != hipSuccess) {
+            (void)hipGetLastError();
+            st = fail(he == hipErrorOutOfMemory ? EDB_ERR_OOM : EDB_ERR_HIP,
+                      std::string("edb_forward: ") + hipGetErrorString(he));
+        }
+    }
+    edb_exec_free(e);
+    return st;
+}
+
+extern "C" edb_status edb_stream_release(void* stream) {
+    int dev = 0;
+    DeviceCtx* ctx = nullptr;
+    hipError_t he = hipGetDevice(&dev);
+    if (he == hipSuccess) he = device_ctx(dev, &ctx);
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_stream_release: ") + hipGetErrorString(he));
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    std::unique_ptr<StreamBlock> blk;
+    {
+        std::lock_guard<std::mutex> lk(g_blocks_mu);
+        auto it = g_blocks.find({dev, hs});
+        if (it == g_blocks.end()) return EDB_OK;
+        blk = std::move(it->second);
+        g_blocks.erase(it);
+    }
+    std::lock_guard<std::mutex> lk(blk->mu);
+    if (blk->rest) he = hipFreeAsync(blk->rest, hs);
+    for (StreamBlock::Slot& sl : blk->slot) {
+        // each slot once the kernels of its last use have run
+        if (sl.used) {
+            const hipError_t we = hipEventSynchronize(sl.done);
+            if (he == hipSuccess) he = we;
+        }
+        if (sl.dev) (void)hipFreeAsync(sl.dev, ctx->upload);
+        if (sl.host) (void)hipHostFree(sl.host);
+        if (sl.ready) (void)hipEventDestroy(sl.ready);
+        if (sl.done) (void)hipEventDestroy(sl.done);
+    }
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_stream_release: ") + hipGetErrorString(he));
+    return EDB_OK;
+}
 
 // ---------------------------------------------------------------------------
 // Allocation-free forward pass: the executor's device memory (descriptor ints,

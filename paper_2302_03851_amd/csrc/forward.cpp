@@ -1,10 +1,12 @@
 // One call for one mini-batch: graph ingest, schedule, memory plan, launch
 // preparation and asynchronous execution (the whole hot path, Algorithm 1 and
 // Section 3.1 of ED-Batch), with every host object released before return.
-// Device buffers owned by the executor are freed in stream order after the
-// work completes, so the call never waits for the GPU.  The executor can be
-// handed back instead (exec_out) to read its launch records and, under
-// EDB_PROFILE, the per-launch times.
+// The call never waits for the GPU.  Without exec_out and EDB_PROFILE the
+// launches use the device block the library keeps per device and stream
+// (edb::forward_on_stream); otherwise an executor of their own, whose device
+// buffers are freed in stream order after the work, and which can be handed
+// back (exec_out) to read its launch records and, under EDB_PROFILE, the
+// per-launch times.
 #include <string>
 
 #include "edb_internal.h"
@@ -30,8 +32,15 @@ extern "C" edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_
             st = edb::fail(EDB_ERR_INVALID, "edb_forward: the arena has " + std::to_string(arena_rows) +
                                                 " rows, the plan needs " + std::to_string(p->n_slots));
     }
-    if (st == EDB_OK) st = edb_prepare(g, s, p, cells, exec_flags & ~EDB_USE_GRAPH, &e);
-    if (st == EDB_OK) st = edb_execute(e, packed_weights, x, arena_h, arena_c, stream);
+    const int32_t flags = exec_flags & ~EDB_USE_GRAPH;
+    if (st == EDB_OK && !exec_out && !(flags & EDB_PROFILE)) {
+        // the plain path: the stream's cached device block, no per-call
+        // allocation, upload stream, events or stream-ordered free
+        st = edb::forward_on_stream(g, s, p, cells, flags, packed_weights, x, arena_h, arena_c, stream);
+    } else {
+        if (st == EDB_OK) st = edb_prepare(g, s, p, cells, flags, &e);
+        if (st == EDB_OK) st = edb_execute(e, packed_weights, x, arena_h, arena_c, stream);
+    }
     // keep the error text of the failing step across the frees below
     const std::string err = st == EDB_OK ? std::string() : std::string(edb_last_error());
     if (st == EDB_OK && exec_out) *exec_out = e;

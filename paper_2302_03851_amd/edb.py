@@ -315,6 +315,12 @@ class ForwardCall:
                                      C.byref(self.n_slots), C.byref(h) if keep else None), "edb_forward")
         return ExecRecord(h) if keep else None
 
+    @staticmethod
+    def release_stream(stream):
+        """edb_stream_release: return the device block that call() keeps for
+        `stream` on the current device."""
+        L.check(L.load().edb_stream_release(C.c_void_p(stream)), "edb_stream_release")
+
     def call_noalloc(self, weight_ptrs, x_ptr, arena_h_ptr, arena_c_ptr, arena_rows, stream):
         """The same mini-batch through edb_forward_noalloc (no device
         allocation; the library's fixed per-device array holds the

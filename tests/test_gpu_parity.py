@@ -440,6 +440,76 @@ def test_forward_call_matches_handles(k):
     np.testing.assert_array_equal(ac.cpu().numpy()[s], c0)
 
 
+@pytest.mark.gpu
+def test_forward_stream_block_growth_release_and_shared_stream():
+    """edb_forward's device block per stream: a small mini-batch, then a
+    larger one on the same stream (the block grows in stream order), the
+    release, another call, and two threads enqueueing on one stream; every
+    arena is bitwise the one of the separate calls with eager launches."""
+    torch = _torch()
+    import threading
+    from paper_2302_03851_amd import edb
+
+    def case(k, inst):
+        w = WL.make_config(k, instances=inst)
+        ref = _fwd(w, flags=0)
+        ref.run()
+        torch.cuda.synchronize()
+        h0, c0 = ref.states()
+        fc = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w),
+                             ref.cells)
+        return w, ref, fc, h0, c0
+
+    def run(cs, stream, fill):
+        w, ref, fc, h0, c0 = cs
+        ah = torch.full_like(ref.arena_h, fill)
+        ac = torch.full_like(ref.arena_c, fill)
+        torch.cuda.synchronize()
+        fc.call([b.data_ptr() for b in ref.weights], ref.x.data_ptr(), ah.data_ptr(), ac.data_ptr(),
+                ah.shape[0], stream.cuda_stream)
+        return ah, ac
+
+    def check(cs, ah, ac, what):
+        _, ref, _, h0, c0 = cs
+        s = ref.plan.slot
+        np.testing.assert_array_equal(ah.float().cpu().numpy()[s], h0, err_msg=what)
+        np.testing.assert_array_equal(ac.cpu().numpy()[s], c0, err_msg=what)
+
+    small, large = case(2, 4), case(5, 24)
+    st = torch.cuda.Stream()
+    outs = [(small, run(small, st, 5.0), "small"), (large, run(large, st, 7.0), "larger after smaller"),
+            (small, run(small, st, 9.0), "small after larger")]
+    torch.cuda.synchronize()
+    for cs, (ah, ac), what in outs:
+        check(cs, ah, ac, what)
+    edb.ForwardCall.release_stream(st.cuda_stream)
+    ah, ac = run(large, st, 3.0)
+    torch.cuda.synchronize()
+    check(large, ah, ac, "after release")
+    edb.ForwardCall.release_stream(st.cuda_stream)
+    edb.ForwardCall.release_stream(st.cuda_stream)   # no block: a no-op
+
+    # two threads, one stream, eight calls each, every call with its own arena
+    res, errs = {}, []
+
+    def worker(t):
+        try:
+            for j in range(8):
+                res[(t, j)] = run(small if (t + j) % 2 else large, st, float(t * 8 + j))
+        except Exception as e:   # reported below
+            errs.append(e)
+    th = [threading.Thread(target=worker, args=(t,)) for t in range(2)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errs, errs
+    for (t, j), (ah, ac) in res.items():
+        check(small if (t + j) % 2 else large, ah, ac, f"thread {t} call {j}")
+    edb.ForwardCall.release_stream(st.cuda_stream)
+
+
 def test_policies_give_same_states():
     """Agenda, depth, sufficient-condition and learned schedules change the
     batches, not the results."""
