@@ -871,6 +871,12 @@ def main():
                                "flight (each step alone on the GPU)",
                      "launches_timed": nl * n_profiled, "per_step_us": round(tot_ms * 1e3, 2),
                      "alg_flops_per_launch": int(fl / nl)},
+        # the whole timed region's algorithmic work rate: every step's
+        # flops over the region's wall time (mini-batches in flight share
+        # the GPU, so this is the chip's rate, not one kernel's)
+        "timed_region": {"alg_tflops": round(tot_flops / (ms_step * 1e-3) / 1e12, 3),
+                         "frac_of_peak": round(tot_flops / (ms_step * 1e-3) / 1e12 / peak, 4),
+                         "alg_hbm_gbs": round(tot_bytes / (ms_step * 1e-3) / 1e9, 1)},
         "device_replay": {"ms_per_forward": round(ms_replay, 4),
                           "node_cells_per_s": round(V / (ms_replay * 1e-3), 1),
                           "alg_tflops": round(tot_flops / (ms_replay * 1e-3) / 1e12, 3),

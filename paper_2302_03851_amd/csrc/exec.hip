@@ -1786,7 +1786,8 @@ struct StreamBlock {
 std::mutex g_blocks_mu;
 std::map<std::pair<int, hipStream_t>, std::unique_ptr<StreamBlock>> g_blocks;
 
-size_t with_spare(size_t v, size_t align) { return (v + v / 4 + align - 1) / align * align; }
+// at least one alignment unit, so that no buffer is of zero size
+size_t with_spare(size_t v, size_t align) { return std::max(align, (v + v / 4 + align - 1) / align * align); }
 
 }  // namespace
 
@@ -1864,7 +1865,7 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
                 }
             }
         }
-        if (he == hipSuccess) {
+        if (he == hipSuccess && hbytes > 0) {
             std::memcpy(sl.host, e->hbuf.data(), hbytes);
             he = hipMemcpyAsync(sl.dev, sl.host, hbytes, hipMemcpyHostToDevice, idle ? hs : ctx->upload);
         }

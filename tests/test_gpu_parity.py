@@ -595,10 +595,19 @@ def test_edge_cases():
 
 
 def test_empty_graph():
-    _torch()
+    torch = _torch()
+    from paper_2302_03851_amd import edb
     w = WL.make_graph([WL.NARY_LEAF, WL.NARY_INTERNAL], 64, 64, [], [], [], seed=1)
     f = _fwd(w)
     assert f.sched.n_batches == 0 and f.exec.launches() == 1
     f.run()
     h, c = f.states()
     assert h.shape == (0, 64)
+    # the one-call path on a stream of its own: nothing to copy or launch
+    fc = edb.ForwardCall(w.op_type, w.child_ptr, w.child_idx, w.x_row, w.n_types, edb.operand_shapes(w), f.cells)
+    st = torch.cuda.Stream()
+    for _ in range(2):
+        fc.call([b.data_ptr() for b in f.weights], f.x.data_ptr(), f.arena_h.data_ptr(), f.arena_c.data_ptr(),
+                f.arena_h.shape[0], st.cuda_stream)
+    torch.cuda.synchronize()
+    edb.ForwardCall.release_stream(st.cuda_stream)
