@@ -674,11 +674,14 @@ def main():
                           policy=kind, table=table, plan_mode=plan_mode)
     n_rows = base.plan.n_slots
 
+    # a1 graph ingest, a2 schedule, a3 memory plan, descriptor upload and
+    # a4..a8 device execution (asynchronous, eager launches), in one C call;
+    # each worker's arguments (its stream and arena) marshalled once
+    calls = [fwd.bind(wptrs, xp, arena_ptrs[i][0], arena_ptrs[i][1], n_rows, streams[i].cuda_stream)
+             for i in range(S)]
+
     def step(i):
-        # a1 graph ingest, a2 schedule, a3 memory plan, descriptor upload and
-        # a4..a8 device execution (asynchronous, eager launches), in one C call
-        ah, ac = arena_ptrs[i]
-        fwd.call(wptrs, xp, ah, ac, n_rows, streams[i].cuda_stream)
+        calls[i]()
 
     class Workers:
         """S host threads, each with its own stream and arena, started once

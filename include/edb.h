@@ -449,8 +449,8 @@ edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
  * wait for the GPU.  Device memory: without exec_out and EDB_PROFILE the call
  * uses a device block that the library keeps for the current device and
  * `stream` and reuses on the next call there (the descriptors are copied on
- * `stream` from pinned host buffers that the library also keeps for the
- * stream, so the next call overwrites them after this call's kernels); the
+ * `stream` from pinned host buffers of a pool that the library keeps for the
+ * process, so the next call overwrites them after this call's kernels); the
  * block grows in stream order when a call needs more (EDB_ERR_OOM if it
  * cannot) and is held until edb_stream_release.  Calls on one stream from
  * several threads enqueue one at a time.  With exec_out or EDB_PROFILE the
@@ -469,11 +469,12 @@ edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
                        const void* x, void* arena_h, void* arena_c, int64_t arena_rows, void* stream,
                        int32_t* n_slots, edb_exec_t** exec_out);
 
-/* Returns the device block and pinned host buffers that edb_forward keeps
- * for the current device and `stream` (the device block by a stream-ordered
- * free on `stream`, after the work already enqueued there; the host buffers
- * once the copies from them have run, which this call waits for); a later
- * edb_forward on the stream allocates new ones.
+/* Returns the device block that edb_forward keeps for the current device
+ * and `stream` (a stream-ordered free on `stream`, after the work already
+ * enqueued there; the call waits for the copies of the stream's descriptors
+ * to have run); a later edb_forward on the stream allocates a new one.  The
+ * pinned host memory of the copies comes from a pool that the library keeps
+ * for the life of the process.
  * Call it before destroying a stream that edb_forward used.  No block: a
  * no-op.  Errors: EDB_ERR_HIP. */
 edb_status edb_stream_release(void* stream);

@@ -1752,11 +1752,12 @@ extern "C" void edb_exec_free(edb_exec_t* e) { delete e; }
 // edb_forward's plain path.  A call's device memory comes from a block kept
 // per device and stream instead of a per-call allocation:
 // * its descriptor ints go to one of NH slots, each a device buffer and a
-//   pinned host buffer, used in turn (a copy from pageable memory would be
+//   pinned host buffer (from a pool kept for the process), used in turn (a
+//   copy from pageable memory would be
 //   done synchronously, after the copying stream's earlier work): the host
 //   fills the pinned buffer; while the stream still runs earlier calls, the
 //   device's upload stream copies it, ahead of the stream's kernels, which
-//   wait for it (event); on an idle stream the stream itself copies it;
+//   wait for it (event); on an idle stream a kernel on the stream copies it;
 //   a slot is refilled only after the kernels of its last use, NH calls
 //   earlier, have finished (event, usually long done);
 // * its staged x and scratch rows go to one region, which only kernels on
@@ -1785,6 +1786,49 @@ struct StreamBlock {
 };
 std::mutex g_blocks_mu;
 std::map<std::pair<int, hipStream_t>, std::unique_ptr<StreamBlock>> g_blocks;
+
+// Pinned host memory for the slots, carved from chunks of at least 4 MB that
+// are allocated rarely and kept for the process (pinning memory can make the
+// runtime wait for the device, which a call inside a busy run must not do).
+// A slot that grows takes a new range; the old one is not reused (growth is
+// rare, and ranges are a few tens of KB).
+struct PinnedPool {
+    std::mutex mu;
+    uint8_t* cur = nullptr;
+    size_t left = 0;
+    std::vector<void*> chunks;
+};
+PinnedPool g_pinned;
+
+hipError_t pinned_range(size_t bytes, void** out) {
+    std::lock_guard<std::mutex> lk(g_pinned.mu);
+    bytes = (bytes + 255) / 256 * 256;
+    if (g_pinned.left < bytes) {
+        void* c = nullptr;
+        const size_t n = std::max<size_t>(bytes, (size_t)4 << 20);
+        // coherent: the upload kernel reads it directly, and a slot's buffer is
+        // rewritten every few calls, so the device must not keep old copies
+        const hipError_t he = hipHostMalloc(&c, n, hipHostMallocCoherent);
+        if (he != hipSuccess) return he;
+        g_pinned.chunks.push_back(c);
+        g_pinned.cur = reinterpret_cast<uint8_t*>(c);
+        g_pinned.left = n;
+    }
+    *out = g_pinned.cur;
+    g_pinned.cur += bytes;
+    g_pinned.left -= bytes;
+    return hipSuccess;
+}
+
+// Descriptor upload by the stream itself: a kernel reads the slot's pinned
+// host buffer (the device reads host memory directly) and writes the slot's
+// device buffer, 16 bytes a thread.  A copy through the copy engines would
+// set up that stream's copy path on its first use (milliseconds, once per
+// stream), a kernel runs where the stream's kernels already run.
+__global__ __launch_bounds__(256) void upload_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                     int n16) {
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < n16; i += gridDim.x * 256) dst[i] = src[i];
+}
 
 // at least one alignment unit, so that no buffer is of zero size
 size_t with_spare(size_t v, size_t align) { return std::max(align, (v + v / 4 + align - 1) / align * align); }
@@ -1819,25 +1863,44 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
         const size_t hbytes = e->hbuf.size() * sizeof(int32_t);
         // the slot's last kernels have finished: its buffers are free
         if (sl.used) he = hipEventSynchronize(sl.done);
-        if (he == hipSuccess && !sl.ready) he = hipEventCreateWithFlags(&sl.ready, hipEventDisableTiming);
-        if (he == hipSuccess && !sl.done) he = hipEventCreateWithFlags(&sl.done, hipEventDisableTiming);
-        if (he == hipSuccess && sl.cap < ibytes) {
-            if (sl.dev) (void)hipFreeAsync(sl.dev, ctx->upload);
-            sl.dev = nullptr;
-            sl.cap = 0;
-            const size_t want = with_spare(ibytes, 256);
-            he = hipMallocAsync(&sl.dev, want, ctx->upload);
-            if (he == hipSuccess) sl.cap = want;
-            else sl.dev = nullptr;
-        }
-        if (he == hipSuccess && sl.hcap < hbytes) {
-            if (sl.host) (void)hipHostFree(sl.host);
-            sl.host = nullptr;
-            sl.hcap = 0;
-            const size_t want = with_spare(hbytes, 4096);
-            he = hipHostMalloc(&sl.host, want, hipHostMallocDefault);
-            if (he == hipSuccess) sl.hcap = want;
-            else sl.host = nullptr;
+        // Buffers and events: a slot that is too small is resized, and every
+        // other slot that is too small and idle with it (never used, or its
+        // last kernels finished), so that the next calls on the stream find
+        // their slots ready instead of each allocating in turn
+        for (int k = 0; he == hipSuccess && k < StreamBlock::NH; ++k) {
+            StreamBlock::Slot& o = blk->slot[k];
+            const bool mine = &o == &sl;
+            if (!mine && o.cap >= ibytes && o.hcap >= hbytes && o.ready && o.done) continue;
+            if (!mine && o.used) {
+                const hipError_t q = hipEventQuery(o.done);
+                if (q == hipErrorNotReady) {
+                    (void)hipGetLastError();
+                    continue;   // still in use: resized when its turn comes
+                }
+                if (q != hipSuccess) {
+                    he = q;
+                    break;
+                }
+            }
+            if (!o.ready) he = hipEventCreateWithFlags(&o.ready, hipEventDisableTiming);
+            if (he == hipSuccess && !o.done) he = hipEventCreateWithFlags(&o.done, hipEventDisableTiming);
+            if (he == hipSuccess && o.cap < ibytes) {
+                if (o.dev) (void)hipFreeAsync(o.dev, ctx->upload);
+                o.dev = nullptr;
+                o.cap = 0;
+                const size_t want = with_spare(ibytes, 256);
+                he = hipMallocAsync(&o.dev, want, ctx->upload);
+                if (he == hipSuccess) o.cap = want;
+                else o.dev = nullptr;
+            }
+            if (he == hipSuccess && o.hcap < hbytes) {
+                o.host = nullptr;
+                o.hcap = 0;
+                const size_t want = with_spare(hbytes, 4096);
+                he = pinned_range(want, &o.host);
+                if (he == hipSuccess) o.hcap = want;
+                else o.host = nullptr;
+            }
         }
         if (he == hipSuccess && rbytes > 0 && blk->rest_cap < rbytes) {
             // the old region after the stream's earlier kernels
@@ -1867,7 +1930,16 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
         }
         if (he == hipSuccess && hbytes > 0) {
             std::memcpy(sl.host, e->hbuf.data(), hbytes);
-            he = hipMemcpyAsync(sl.dev, sl.host, hbytes, hipMemcpyHostToDevice, idle ? hs : ctx->upload);
+            if (idle) {
+                // whole 16-byte pieces: both buffers hold at least hbytes
+                // rounded up to 256 bytes
+                const int n16 = (int)((hbytes + 15) / 16);
+                hipLaunchKernelGGL(upload_kernel, dim3(std::min(64, (n16 + 255) / 256)), dim3(256), 0, hs,
+                                   reinterpret_cast<const uint4*>(sl.host), reinterpret_cast<uint4*>(sl.dev), n16);
+                he = hipGetLastError();
+            } else {
+                he = hipMemcpyAsync(sl.dev, sl.host, hbytes, hipMemcpyHostToDevice, ctx->upload);
+            }
         }
         if (he == hipSuccess && !idle) he = hipEventRecord(sl.ready, ctx->upload);
         if (he == hipSuccess && !idle) he = hipStreamWaitEvent(hs, sl.ready, 0);
@@ -1922,7 +1994,6 @@ extern "C" edb_status edb_stream_release(void* stream) {
             if (he == hipSuccess) he = we;
         }
         if (sl.dev) (void)hipFreeAsync(sl.dev, ctx->upload);
-        if (sl.host) (void)hipHostFree(sl.host);
         if (sl.ready) (void)hipEventDestroy(sl.ready);
         if (sl.done) (void)hipEventDestroy(sl.done);
     }

@@ -315,6 +315,23 @@ class ForwardCall:
                                      C.byref(self.n_slots), C.byref(h) if keep else None), "edb_forward")
         return ExecRecord(h) if keep else None
 
+    def bind(self, weight_ptrs, x_ptr, arena_h_ptr, arena_c_ptr, arena_rows, stream):
+        """The arguments of call() marshalled once, for a caller that repeats
+        them (a worker with its own stream and arena): returns a function of no
+        arguments that runs the path with them."""
+        arr = (C.c_void_p * len(weight_ptrs))(*weight_ptrs)
+        n_slots = C.c_int32()
+        args = self._args + (arr, C.c_void_p(x_ptr), C.c_void_p(arena_h_ptr), C.c_void_p(arena_c_ptr),
+                             arena_rows, C.c_void_p(stream), C.byref(n_slots), None)
+        fn = L.load().edb_forward
+
+        def run():
+            st = fn(*args)
+            if st:
+                L.check(st, "edb_forward")
+        run.keep = (arr, n_slots)   # the marshalled arrays live as long as the function
+        return run
+
     @staticmethod
     def release_stream(stream):
         """edb_stream_release: return the device block that call() keeps for
