@@ -1785,7 +1785,8 @@ struct StreamBlock {
     int next = 0;
 };
 std::mutex g_blocks_mu;
-std::map<std::pair<int, hipStream_t>, std::unique_ptr<StreamBlock>> g_blocks;
+// shared: a release can take a block out of the map while a call still holds it
+std::map<std::pair<int, hipStream_t>, std::shared_ptr<StreamBlock>> g_blocks;
 
 // Pinned host memory for the slots, carved from chunks of at least 4 MB that
 // are allocated rarely and kept for the process (pinning memory can make the
@@ -1847,13 +1848,13 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
     edb_exec_t* e = nullptr;
     edb_status st = prepare_impl(g, s, p, cells, flags, true, &e);
     if (st == EDB_OK) st = check_exec_args(e, packed_weights, x, arena_h, arena_c, "edb_forward");
-    StreamBlock* blk = nullptr;
+    std::shared_ptr<StreamBlock> blk;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     if (st == EDB_OK) {
         std::lock_guard<std::mutex> lk(g_blocks_mu);
-        std::unique_ptr<StreamBlock>& up = g_blocks[{dev, hs}];
+        std::shared_ptr<StreamBlock>& up = g_blocks[{dev, hs}];
         if (!up) up.reset(new (std::nothrow) StreamBlock);
-        blk = up.get();
+        blk = up;
         if (!blk) st = fail(EDB_ERR_OOM, "edb_forward: out of host memory");
     }
     if (st == EDB_OK) {
@@ -1866,7 +1867,11 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
         // Buffers and events: a slot that is too small is resized, and every
         // other slot that is too small and idle with it (never used, or its
         // last kernels finished), so that the next calls on the stream find
-        // their slots ready instead of each allocating in turn
+        // their slots ready instead of each allocating in turn.  Slot buffers
+        // are allocated in the upload stream's order: a call that allocates
+        // copies on the upload stream, and the stream's wait for that copy
+        // orders it, and every later call on it, after the allocations.
+        bool allocated = false;
         for (int k = 0; he == hipSuccess && k < StreamBlock::NH; ++k) {
             StreamBlock::Slot& o = blk->slot[k];
             const bool mine = &o == &sl;
@@ -1892,6 +1897,7 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
                 he = hipMallocAsync(&o.dev, want, ctx->upload);
                 if (he == hipSuccess) o.cap = want;
                 else o.dev = nullptr;
+                allocated = true;
             }
             if (he == hipSuccess && o.hcap < hbytes) {
                 o.host = nullptr;
@@ -1915,8 +1921,8 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
         // an idle stream (the previous call's kernels have run) copies the
         // descriptors itself: nothing to overlap, and no wait across streams;
         // a busy one has the upload stream copy them ahead of its kernels
-        bool idle = true;
-        if (he == hipSuccess) {
+        bool idle = !allocated;
+        if (he == hipSuccess && idle) {
             const StreamBlock::Slot& prev = blk->slot[(blk->next + StreamBlock::NH - 1) % StreamBlock::NH];
             if (prev.used) {
                 const hipError_t q = hipEventQuery(prev.done);
@@ -1977,7 +1983,7 @@ extern "C" edb_status edb_stream_release(void* stream) {
     if (he == hipSuccess) he = device_ctx(dev, &ctx);
     if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_stream_release: ") + hipGetErrorString(he));
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-    std::unique_ptr<StreamBlock> blk;
+    std::shared_ptr<StreamBlock> blk;
     {
         std::lock_guard<std::mutex> lk(g_blocks_mu);
         auto it = g_blocks.find({dev, hs});
@@ -1985,6 +1991,8 @@ extern "C" edb_status edb_stream_release(void* stream) {
         blk = std::move(it->second);
         g_blocks.erase(it);
     }
+    // a call on the stream that still holds the block finishes enqueueing
+    // first (the block's lock); later calls start a new block
     std::lock_guard<std::mutex> lk(blk->mu);
     if (blk->rest) he = hipFreeAsync(blk->rest, hs);
     for (StreamBlock::Slot& sl : blk->slot) {
