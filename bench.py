@@ -129,6 +129,9 @@ def kernel_symbol(kind, dtype, variant, part):
     if part == 1:
         return "edbk::mv_matvec_kernel" if kind == 12 else "edbk::child_reduce_kernel"
     t = 'float' if dtype == 'f32' else '__bf16'
+    from paper_2302_03851_amd import _lib as L
+    if variant == L.WS_VARIANT:
+        return f"edbk::ws_kernel<{kind}>"
     if variant in STREAM_SHAPES:
         rt, wk = STREAM_SHAPES[variant]
         return f"edbk::stream_kernel<{kind}, {t}, {rt}, {wk}>"
@@ -834,6 +837,8 @@ def main():
     kind_v, var_v, part_v = dom
     if part_v == 1:
         kernel = "mv_matvec_kernel" if kind_v == WL.MV_VEC else "child_reduce_kernel"
+    elif var_v == L.WS_VARIANT:
+        kernel = f"ws_kernel<{kname}, bf16>"
     elif var_v in L.LARGE_VARIANTS:
         kk = "CS_FORGET" if part_v == 2 else ("CS_PARENT" if kind_v == WL.CS_INTERNAL else kname)
         kernel = f"big_kernel<{kk}, {w.dtype}, size class {LARGE_CLASS[var_v]}>"

@@ -364,8 +364,12 @@ typedef struct edb_exec edb_exec_t;
  * split-K over the waves), streamed tiles (the same shapes for kinds without
  * a ragged phase, every lane loading its own operand fragments) for the many
  * small batches, the large bf16 tile (64-256 rows, both operands through LDS)
- * for batches of thousands of rows.  Without split-K (EDB_NO_SPLIT_K, and
- * always in the large tile) a batch's results do not depend on the variant:
+ * for batches of thousands of rows, and for bf16 x-only leaf batches of at
+ * least 8192 rows the weight-stationary tile (32 units' weights held in LDS for
+ * the whole launch, 256-row tiles walked in turn; off under EDB_NO_LARGE and
+ * when another variant is forced).  Without split-K (EDB_NO_SPLIT_K, and
+ * always in the large and weight-stationary tiles) a batch's results do not
+ * depend on the variant:
  * they are bitwise equal across variants, layouts and launch modes; with it,
  * variants with the same reduction split (a streamed tile and its staged
  * counterpart) are bitwise equal.  For sweeps and tests, the environment
@@ -420,7 +424,8 @@ typedef struct {
     int32_t variant;   /* tile variant id: 0-7 small tiles, 8-10 and 15-16 the large tile (size
                           classes 0-4: 256, 128, 64 rows x 64 units, then 64 and 32 rows x 32
                           units, fewer rows for 5-gate cells), 11-14 streamed tiles (counterparts
-                          of the small tiles 3, 6, 4, 5), 100 a dataflow launch */
+                          of the small tiles 3, 6, 4, 5), 17 the weight-stationary tile
+                          (256-row tiles x 32 units, 512 threads), 100 a dataflow launch */
     int32_t grid;      /* work-groups */
     int32_t block;     /* threads per work-group */
     int32_t seg_kind[4]; /* kinds of result, child 0, child 1, ragged lists */

@@ -26,6 +26,7 @@ USE_GRAPH, DRYRUN, FORCE_GATHER, X_DIRECT, PROFILE, NO_FLOW = 1, 2, 4, 8, 16, 32
 NO_SPLIT_K, TILE_LARGE, NO_LARGE, FLOW_DRYRUN = 64, 128, 256, 512
 LARGE_VARIANTS = (8, 9, 10, 15, 16)      # large tile size classes 0, 1, 2, 3, 4
 LARGE_CLASS = {8: 0, 9: 1, 10: 2, 15: 3, 16: 4}
+WS_VARIANT = 17                          # weight-stationary tile (bf16 x-only leaf batches)
 STREAM_VARIANTS = (11, 12, 13, 14)        # streamed tile: (rows / 16, waves) = (1, 4), (2, 4), (1, 8), (1, 16)
 STREAM_STAGED = {11: 3, 12: 6, 13: 4, 14: 5}   # the staged variant with the same rows and reduction split
 PART_CELL, PART_CHILD_SUM, PART_FORGET = 0, 1, 2

@@ -17,6 +17,7 @@
 #include <vector>
 
 #include "big_tile.h"
+#include "ws_tile.h"
 #include "cell_kernels.h"
 #include "diag_kernels.h"
 #include "mv_kernels.h"
@@ -32,16 +33,18 @@ constexpr int NUM_LARGE = 3;        // large size classes 0-2 (variants 8-10)
 constexpr int NUM_STREAM = 4;
 constexpr int FIRST_STREAM = NUM_SMALL + NUM_LARGE;
 constexpr int FIRST_NARROW = FIRST_STREAM + NUM_STREAM;   // large size classes 3-4 (variants 15-16)
-constexpr int NUM_VARIANTS = FIRST_NARROW + NUM_BIG_CLASSES - NUM_LARGE;
+constexpr int WS_VARIANT = FIRST_NARROW + NUM_BIG_CLASSES - NUM_LARGE;   // the weight-stationary tile
+constexpr int NUM_VARIANTS = WS_VARIANT + 1;
 // small (staged) and streamed tile variants: rows per work-group 16*RT, units
 // per work-group 16*WU, WK waves splitting the reduction (threads per
 // work-group 64*WU*WK); the large variants have no entry here
-constexpr int VAR_RT[NUM_VARIANTS] = {2, 1, 1, 1, 1, 1, 2, 2, 0, 0, 0, 1, 2, 1, 1, 0, 0};
-constexpr int VAR_WU[NUM_VARIANTS] = {4, 4, 2, 1, 1, 1, 1, 2, 0, 0, 0, 1, 1, 1, 1, 0, 0};
-constexpr int VAR_WK[NUM_VARIANTS] = {1, 1, 2, 4, 8, 16, 4, 2, 0, 0, 0, 4, 4, 8, 16, 0, 0};
+constexpr int VAR_RT[NUM_VARIANTS] = {2, 1, 1, 1, 1, 1, 2, 2, 0, 0, 0, 1, 2, 1, 1, 0, 0, 0};
+constexpr int VAR_WU[NUM_VARIANTS] = {4, 4, 2, 1, 1, 1, 1, 2, 0, 0, 0, 1, 1, 1, 1, 0, 0, 0};
+constexpr int VAR_WK[NUM_VARIANTS] = {1, 1, 2, 4, 8, 16, 4, 2, 0, 0, 0, 4, 4, 8, 16, 0, 0, 0};
 // large tile variants 8-10 and 15-16 = size classes 0-4: 32*big_rb(G, vb) rows x
 // 32*big_cu(vb) units, 256 threads (bf16 and fp32; chunks of 128 bytes of k)
-bool is_large(int v) { return (v >= NUM_SMALL && v < FIRST_STREAM) || (v >= FIRST_NARROW && v < NUM_VARIANTS); }
+bool is_large(int v) { return (v >= NUM_SMALL && v < FIRST_STREAM) || (v >= FIRST_NARROW && v < WS_VARIANT); }
+bool is_ws(int v) { return v == WS_VARIANT; }
 int large_class(int v) { return v < FIRST_STREAM ? v - NUM_SMALL : v - FIRST_NARROW + NUM_LARGE; }
 int large_variant(int vb) { return vb < NUM_LARGE ? NUM_SMALL + vb : FIRST_NARROW + vb - NUM_LARGE; }
 // streamed tile variants FIRST_STREAM..: 16*RT rows x 16 units, WK waves
@@ -279,6 +282,29 @@ Entry entry() {
             reinterpret_cast<const void*>(&cell_kernel<KIND, T, RT, WU, WK>)};
 }
 
+// the weight-stationary tile (bf16 leaf kinds): dynamic LDS for the weights
+template <int KIND>
+void launch_ws(const BatchArgs& a, int grid, int lds, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+    if (ev0)
+        hipExtLaunchKernelGGL((ws_kernel<KIND>), dim3(grid), dim3(WS_NT), lds, st, ev0, ev1, 0, a);
+    else
+        hipLaunchKernelGGL((ws_kernel<KIND>), dim3(grid), dim3(WS_NT), lds, st, a);
+}
+template <int KIND>
+hipError_t attr_ws(int lds) {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&ws_kernel<KIND>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+}
+template <int KIND>
+int lds_ws(int K, int) { return ws_lds_bytes(Kind<KIND>::G, K); }
+
+template <int KIND, typename T>
+Entry ws_entry() {
+    if constexpr (ws_kind<KIND>() && sizeof(T) == 2)
+        return {launch_ws<KIND>, attr_ws<KIND>, lds_ws<KIND>, reinterpret_cast<const void*>(&ws_kernel<KIND>)};
+    else return {nullptr, nullptr, nullptr, nullptr};
+}
+
 // the large tile's LDS is static (its two stages are distinct objects)
 template <int KIND, typename T, int VB>
 void launch_big(const BatchArgs& a, int grid, int, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
@@ -347,6 +373,7 @@ void fill_kind(Entry* e) {
     e[14] = stream_entry<KIND, T, 1, 16>();
     e[15] = big_entry<KIND, T, 3>();
     e[16] = big_entry<KIND, T, 4>();
+    e[WS_VARIANT] = ws_entry<KIND, T>();
 }
 
 // The internal kinds of a child-sum batch on the large tile have large bf16 variants only.
@@ -361,6 +388,7 @@ void fill_internal(Entry (&e)[2][NUM_VARIANTS]) {
     e[1][16] = big_entry<KIND, __bf16, 4>();
 }
 
+constexpr int kWsMinRows = 8192;   // batches the weight-stationary tile takes (at least)
 constexpr int NUM_KERNEL_KINDS = 17;   // the 15 cell kinds, then K_CS_FORGET, K_CS_PARENT
 
 struct Table {
@@ -956,6 +984,17 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
                 if (table().e[fk][dtype][force_var].launch) var = lvar = force_var;
                 if (cs_large && table().e[K_CS_FORGET][dtype][force_var].launch) fvar = force_var;
             }
+            // the weight-stationary tile for the largest x-only batches (bf16):
+            // the weights of its 32 units and its row table fit the LDS, the
+            // reduction is a whole number of the ring's groups of k-groups, and
+            // offsets stay 32-bit
+            {
+                const Entry& wen = table().e[kind_id][dtype][WS_VARIANT];
+                const bool ws_ok = wen.launch && !cs_large && large_fits && !(flags & EDB_NO_LARGE) &&
+                                   d.K % (32 * WS_D) == 0 &&
+                                   d.Hu % WS_TU == 0 && wen.lds(d.K, d.Hk) <= max_lds;
+                if (ws_ok && ((m >= kWsMinRows && force_var < 0) || force_var == WS_VARIANT)) var = WS_VARIANT;
+            }
             if (var < 0) {
                 delete e;
                 return fail(EDB_ERR_UNSUPPORTED, "edb_prepare: no tile variant fits the LDS of batch " +
@@ -1041,7 +1080,17 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
             L.info.variant = var;
             L.info.n_batches = 1;
             L.info.part = 0;
-            if (is_large(var)) {
+            if (is_ws(var)) {
+                // unit tiles x row groups, the row groups a multiple of 8 (one XCD
+                // holds whole row groups), about one work-group per CU, and at
+                // most WS_MAXT row tiles per work-group (its row table)
+                const int nut = d.Hu / WS_TU;
+                const int nrt = (m + WS_TM - 1) / WS_TM;
+                const int need = (nrt + WS_MAXT - 1) / WS_MAXT;
+                const int ngr = std::max({8, std::min((n_cu / nut) / 8 * 8, (nrt + 7) / 8 * 8), (need + 7) / 8 * 8});
+                L.info.grid = nut * ngr;
+                L.info.block = WS_NT;
+            } else if (is_large(var)) {
                 const int TM = large_tm(d.G, large_class(var));
                 const int tiles = (m + TM - 1) / TM * (d.Hu / large_tu(large_class(var)));
                 L.info.grid = (tiles + 7) / 8 * 8;   // XCD-aware order: 8 equal tile ranges

@@ -257,6 +257,53 @@ def test_large_tile_indexed_operands_bitwise():
         np.testing.assert_array_equal(c, c0, err_msg=str(kw))
 
 
+def _two_leaf_trees(kinds, n_trees, E, H, seed):
+    """n_trees trees of two x leaves under one internal node (bf16)."""
+    op, ch, hx = [], [], []
+    for t in range(n_trees):
+        op += [0, 0, 1]
+        ch += [[], [], [3 * t, 3 * t + 1]]
+        hx += [True, True, False]
+    return WL.make_graph(kinds, E, H, op, ch, hx, seed=seed, dtype="bf16", scale=0.05, bias_scale=0.2)
+
+
+WS_CASES = {
+    # the child-sum configuration's leaves: 16 k-groups, several row tiles, a ragged tail
+    "child-sum": lambda: WL.make_config(5, instances=12),
+    # N-ary leaves: a zero-padded x segment (E = 120 of 128: one group of k-groups) and padded units (H = 200 of 256)
+    "nary-padded": lambda: _two_leaf_trees([WL.NARY_LEAF, WL.NARY_INTERNAL], 400, 120, 200, seed=31),
+    # TreeGRU leaves
+    "gru": lambda: _gru_trees(300, 128, 256, seed=32, dtype="bf16"),
+    # 70,000 leaves: more row tiles than the row table holds at one work-group per CU
+    "row-table-bound": lambda: _two_leaf_trees([WL.CS_LEAF, WL.CS_INTERNAL], 35000, 128, 512, seed=33),
+}
+
+
+@pytest.mark.parametrize("case", list(WS_CASES))
+def test_weight_stationary_tile_bitwise_and_parity(case, monkeypatch):
+    """The weight-stationary tile (every leaf batch forced onto it) is bitwise
+    equal to the small tile without split-K, and within the bound of the
+    oracle."""
+    _torch()
+    w = WS_CASES[case]()
+    monkeypatch.delenv("EDB_VARIANT", raising=False)
+    small = _fwd(w, flags=L.USE_GRAPH | L.NO_SPLIT_K | L.NO_LARGE)
+    small.run()
+    h0, c0 = small.states()
+    monkeypatch.setenv("EDB_VARIANT", str(L.WS_VARIANT))
+    f = _fwd(w, flags=L.USE_GRAPH | L.NO_SPLIT_K)
+    used = {f.exec.launch_info(i)["variant"] for i in range(1, f.exec.launches())}
+    assert L.WS_VARIANT in used, used
+    f.run()
+    f.run()
+    h, c = f.states()
+    np.testing.assert_array_equal(h, h0, err_msg=case)
+    np.testing.assert_array_equal(c, c0, err_msg=case)
+    if case != "row-table-bound":
+        hr, cr = _oracle(w)
+        _check(w, h, c, hr, cr, f"weight-stationary tile {case}")
+
+
 def test_large_tile_child_sum_many_children():
     """Child-sum parents with up to 9 children on the large tile (the per-parent
     reduction's loop beyond 4 children) against the small tile and the oracle."""

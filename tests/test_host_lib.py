@@ -266,7 +266,11 @@ def test_dryrun_launch_list(k, flow):
             continue
         assert info["n_batches"] == 1
         assert info["m"] == f.sched.batch_ptr[b + 1] - f.sched.batch_ptr[b]
-        assert 0 <= info["variant"] <= 16 and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
+        assert 0 <= info["variant"] <= L.WS_VARIANT and info["grid"] >= 1 and info["block"] in (256, 512, 1024)
+        if info["variant"] == L.WS_VARIANT:
+            # weight-stationary tile: bf16 x-only leaves, 512 threads, (units / 32) x (row groups, a multiple of 8)
+            assert w.dtype == "bf16" and w.kinds[t] in (WL.NARY_LEAF, WL.CS_LEAF, WL.GRU_LEAF)
+            assert info["block"] == 512 and info["grid"] % 8 == 0
         if info["variant"] in L.LARGE_VARIANTS:
             # large tile: every kind but the lattice character cell (child-sum parents run
             # as a forget GEMM, child sums and a parent GEMM), 256 threads, grid a multiple of 8
@@ -286,6 +290,55 @@ def test_dryrun_launch_list(k, flow):
 LARGE_TILE_ROWS = {8: 256, 9: 128, 10: 64, 15: 64, 16: 32}      # rows per work-group of the large variants at G = 3
 LARGE_TILE_ROWS_G1 = {8: 256, 9: 128, 10: 64, 15: 64, 16: 32}   # the one-gate forget GEMM of child-sum cells
 LARGE_TILE_UNITS = {8: 64, 9: 64, 10: 64, 15: 32, 16: 32}       # units per work-group
+
+
+WS_ROWS, WS_UNITS, WS_MAX_TILES = 256, 32, 16   # rows per row tile, units per work-group, row tiles per work-group
+
+
+def _ws_grid(m, H, n_cu=256):
+    """The weight-stationary launch's grid: unit tiles x row groups, the row groups
+    a multiple of 8, about one work-group per CU, at most 16 row tiles each."""
+    nut = -(-H // 64) * 64 // WS_UNITS
+    nrt = -(-m // WS_ROWS)
+    need = -(-nrt // WS_MAX_TILES)
+    ngr = max(8, min(n_cu // nut // 8 * 8, -(-nrt // 8) * 8), -(-need // 8) * 8)
+    return nut * ngr
+
+
+def test_weight_stationary_selection_and_grid(monkeypatch):
+    """bf16 x-only leaf batches of at least 8192 rows take the weight-stationary
+    tile (a forced variant or EDB_NO_LARGE keeps them off it; fp32 never takes
+    it), with the grid its kernel assumes, including the row table's bound."""
+    monkeypatch.delenv("EDB_VARIANT", raising=False)
+    base = L.DRYRUN | L.NO_FLOW
+    big = WL.make_config(5)
+    f = edb.Forward(big, flags=base)
+    info = f.exec.launch_info(1)
+    assert info["kind"] == WL.CS_LEAF and info["m"] == 28629 and info["variant"] == L.WS_VARIANT
+    assert info["block"] == 512 and info["grid"] == _ws_grid(28629, 512) == 256
+    for i in range(2, f.exec.launches()):
+        assert f.exec.launch_info(i)["variant"] != L.WS_VARIANT   # internal nodes and small leaf batches
+    monkeypatch.setenv("EDB_VARIANT", "9")
+    assert edb.Forward(big, flags=base).exec.launch_info(1)["variant"] == 9
+    monkeypatch.delenv("EDB_VARIANT")
+    # 70,000 leaves of 512 units: 274 row tiles need 24 row groups (16 tiles each at most)
+    op, ch, hx = [], [], []
+    for t in range(35000):
+        op += [0, 0, 1]
+        ch += [[], [], [3 * t, 3 * t + 1]]
+        hx += [True, True, False]
+    w = WL.make_graph([WL.CS_LEAF, WL.CS_INTERNAL], 128, 512, op, ch, hx, seed=3, dtype="bf16")
+    info = edb.Forward(w, flags=base).exec.launch_info(1)
+    assert info["variant"] == L.WS_VARIANT and info["m"] == 70000
+    assert info["grid"] == _ws_grid(70000, 512) == 16 * 24
+    # a forced weight-stationary tile on a small batch; fp32 keeps the other tiles
+    monkeypatch.setenv("EDB_VARIANT", str(L.WS_VARIANT))
+    small = WL.make_config(5, instances=12)
+    info = edb.Forward(small, flags=base).exec.launch_info(1)
+    assert info["variant"] == L.WS_VARIANT and info["grid"] == _ws_grid(info["m"], 512)
+    f32 = WL.make_config(2, instances=6)
+    f = edb.Forward(f32, flags=base)
+    assert all(f.exec.launch_info(i)["variant"] != L.WS_VARIANT for i in range(1, f.exec.launches()))
 
 
 def test_tile_flags_select_variants():
@@ -312,7 +365,9 @@ def test_tile_flags_select_variants():
         assert f.exec.launch_info(i)["variant"] in (0, 1)
     big = WL.make_config(5)
     f = edb.Forward(big, flags=base)
-    assert f.exec.launch_info(1)["kind"] == WL.CS_LEAF and f.exec.launch_info(1)["variant"] in L.LARGE_VARIANTS
+    assert f.exec.launch_info(1)["kind"] == WL.CS_LEAF and f.exec.launch_info(1)["variant"] == L.WS_VARIANT
+    f = edb.Forward(big, flags=base | L.NO_LARGE)
+    assert f.exec.launch_info(1)["variant"] not in L.LARGE_VARIANTS + (L.WS_VARIANT,)
     with pytest.raises(L.EdbError) as ei:
         edb.Forward(w, flags=base | L.TILE_LARGE | L.NO_LARGE)
     assert ei.value.status == L.EDB_ERR_INVALID
