@@ -24,12 +24,15 @@
 // cell update as the large tile does, so the results are bitwise equal to the
 // large tile's.
 //
+// The epilogue passes each wave's c and h rows through a staging tile of its
+// own in LDS, so that every lane stores whole 16-byte pieces of the rows.
+//
 // On MI355X this tile is bound by the operand loads in the MFMA lane layout
 // (each load touches 16 rows, 16 bytes a lane) and by the epilogue (gate
-// nonlinearities and 4- and 2-byte stores of c and h), not by the matrix
-// cores or the LDS: with the loads' data replaced by register values the loop
-// takes 60% of its time, without the weight reads from LDS it takes the same
-// time, and the matrix cores are busy about a quarter of the launch.
+// nonlinearities and the stores, which each tile start waits for), not by the
+// matrix cores or the LDS: with the loads' data replaced by register values
+// the loop takes 60% of its time, without the weight reads from LDS it takes
+// the same time, and the matrix cores are busy about a quarter of the launch.
 //
 // Work-groups are dispatched round-robin over the 8 XCDs; they are numbered
 // so that the work-groups of one row group (all unit tiles of the same rows)
@@ -48,7 +51,11 @@ constexpr int WS_TM = WS_W * 16 * WS_RB;   // rows per row tile
 constexpr int WS_UB = 2;                // unit blocks of 16 per work-group
 constexpr int WS_TU = 16 * WS_UB;       // units per work-group
 constexpr int WS_D = 4;                 // k-groups of operands in flight per wave
-constexpr int WS_MAXT = 16;             // row tiles per work-group (the row table's capacity)
+constexpr int WS_MAXT = 8;              // row tiles per work-group (the row table's capacity)
+constexpr int WS_RW = 16 * WS_RB;       // rows per wave
+constexpr int WS_CST = WS_TU * 4 + 16;  // staging row stride (bytes) for c (fp32, 16 bytes of padding)
+constexpr int WS_HST = WS_TU * 2 + 16;  // staging row stride (bytes) for h (bf16, 16 bytes of padding)
+constexpr int WS_STAGE = WS_RW * WS_CST;   // one wave's staging tile (c, then h in the same bytes)
 
 // Kinds the tile serves: x is the only operand (no child lists, no ragged
 // phase) and the update reads no child state.
@@ -59,15 +66,19 @@ __host__ __device__ constexpr bool ws_kind() {
 }
 
 // LDS: the work-group's weight blocks [WS_UB][G][K / 32][64 lanes][16 bytes],
-// then the row table: x byte offsets [WS_MAXT][WS_TM], result rows [WS_MAXT][WS_TM].
+// then the row table: x byte offsets [WS_MAXT][WS_TM], result rows [WS_MAXT][WS_TM],
+// then each wave's staging tile for its results.
 __host__ __device__ constexpr int ws_weight_bytes(int G, int K) { return WS_UB * G * (K / 32) * 1024; }
-__host__ __device__ constexpr int ws_lds_bytes(int G, int K) { return ws_weight_bytes(G, K) + WS_MAXT * WS_TM * 8; }
+__host__ __device__ constexpr int ws_lds_bytes(int G, int K) {
+    return ws_weight_bytes(G, K) + WS_MAXT * WS_TM * 8 + WS_W * WS_STAGE;
+}
 
 // grid = (Hu / WS_TU) unit tiles x ngr row groups, ngr a multiple of 8 with
 // ceil(m / WS_TM) <= ngr * WS_MAXT; K / 32 a multiple of WS_D.
 template <int KIND>
 __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
     static_assert(WS_TM <= WS_NT, "one row of the row table per thread and tile");
+    static_assert(WS_RW * 8 % 64 == 0 && WS_RW * 4 % 64 == 0, "whole 16-byte pieces per lane");
     constexpr int G = Kind<KIND>::G;
     constexpr uint32_t OOB = 0x80000000u;
     extern __shared__ __align__(16) char smem[];
@@ -89,6 +100,7 @@ __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
     const int nw = WS_UB * G * nkg;                  // 1 KB weight blocks
     uint32_t* xo_l = reinterpret_cast<uint32_t*>(smem + nw * 1024);
     int* res_l = reinterpret_cast<int*>(xo_l + WS_MAXT * WS_TM);
+    char* stg = reinterpret_cast<char*>(res_l + WS_MAXT * WS_TM) + wave * WS_STAGE;   // this wave's staging tile
     {
         // the stationary weights: the two unit blocks' blocks are contiguous in
         // the packed matrix ((unit block * G + gate) * nkg + k-group), copied
@@ -218,28 +230,52 @@ __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
         }
 
         // ---- epilogue of row tile i: bias, gates, cell update, h and c ----
-        const int base = (rg + i * ngr) * WS_TM;
+        // The wave's results pass through its staging tile so that every lane
+        // stores whole 16-byte pieces of the rows (c: 8 a row, h: 4 a row); H
+        // is a multiple of 8, so a piece is either inside the row or past H.
+        // The wave's LDS operations run in order, so no wait separates the
+        // staging writes from the reads, nor the c reads from the h writes.
+        const int base = (rg + i * ngr) * WS_TM + wave * WS_RW;   // the wave's first row
+        const int* rres = res_l + i * WS_TM + wave * WS_RW;
+        float hv[WS_RB][4][WS_UB];
 #pragma unroll
         for (int rb = 0; rb < WS_RB; ++rb)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const int rt = wave * 16 * WS_RB + rb * 16 + (lane >> 4) * 4 + q;   // row in the tile
-                const int r = base + rt;
-                const size_t orow = (size_t)res_l[i * WS_TM + rt] * a.H;
+                const int rw = rb * 16 + (lane >> 4) * 4 + q;   // row of the wave
 #pragma unroll
                 for (int ub = 0; ub < WS_UB; ++ub) {
-                    const int j = u0 + ub * 16 + (lane & 15);
                     float z[G], cp[1] = {0.f};
 #pragma unroll
                     for (int g = 0; g < G; ++g) z[g] = acc[ub][g][rb][q] + bz[ub][g];
                     float c, h;
                     cell_update<KIND>(z, cp, 0.f, 0.f, 0, c, h);
-                    if (r < a.m && j < a.H) {
-                        a.arena_c[orow + j] = c;
-                        Hout[orow + j] = from_f<__bf16>(h);
-                    }
+                    *reinterpret_cast<float*>(stg + rw * WS_CST + (ub * 16 + (lane & 15)) * 4) = c;
+                    hv[rb][q][ub] = h;
                 }
             }
+#pragma unroll
+        for (int k = 0; k < WS_RW * 8 / 64; ++k) {
+            const int e = k * 64 + lane, rw = e >> 3, p = e & 7;
+            const float4 v = *reinterpret_cast<const float4*>(stg + rw * WS_CST + p * 16);
+            if (base + rw < a.m && u0 + p * 4 < a.H)
+                *reinterpret_cast<float4*>(a.arena_c + (size_t)rres[rw] * a.H + u0 + p * 4) = v;
+        }
+#pragma unroll
+        for (int rb = 0; rb < WS_RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int ub = 0; ub < WS_UB; ++ub)
+                    *reinterpret_cast<__bf16*>(stg + (rb * 16 + (lane >> 4) * 4 + q) * WS_HST +
+                                               (ub * 16 + (lane & 15)) * 2) = from_f<__bf16>(hv[rb][q][ub]);
+#pragma unroll
+        for (int k = 0; k < WS_RW * 4 / 64; ++k) {
+            const int e = k * 64 + lane, rw = e >> 2, p = e & 3;
+            const uint4 v = *reinterpret_cast<const uint4*>(stg + rw * WS_HST + p * 16);
+            if (base + rw < a.m && u0 + p * 8 < a.H)
+                *reinterpret_cast<uint4*>(Hout + (size_t)rres[rw] * a.H + u0 + p * 8) = v;
+        }
 #pragma unroll
         for (int rb = 0; rb < WS_RB; ++rb) offc[rb] = offn[rb];
     }

@@ -292,12 +292,12 @@ LARGE_TILE_ROWS_G1 = {8: 256, 9: 128, 10: 64, 15: 64, 16: 32}   # the one-gate f
 LARGE_TILE_UNITS = {8: 64, 9: 64, 10: 64, 15: 32, 16: 32}       # units per work-group
 
 
-WS_ROWS, WS_UNITS, WS_MAX_TILES = 256, 32, 16   # rows per row tile, units per work-group, row tiles per work-group
+WS_ROWS, WS_UNITS, WS_MAX_TILES = 256, 32, 8    # rows per row tile, units per work-group, row tiles per work-group
 
 
 def _ws_grid(m, H, n_cu=256):
     """The weight-stationary launch's grid: unit tiles x row groups, the row groups
-    a multiple of 8, about one work-group per CU, at most 16 row tiles each."""
+    a multiple of 8, about one work-group per CU, at most 8 row tiles each."""
     nut = -(-H // 64) * 64 // WS_UNITS
     nrt = -(-m // WS_ROWS)
     need = -(-nrt // WS_MAX_TILES)
@@ -321,7 +321,7 @@ def test_weight_stationary_selection_and_grid(monkeypatch):
     monkeypatch.setenv("EDB_VARIANT", "9")
     assert edb.Forward(big, flags=base).exec.launch_info(1)["variant"] == 9
     monkeypatch.delenv("EDB_VARIANT")
-    # 70,000 leaves of 512 units: 274 row tiles need 24 row groups (16 tiles each at most)
+    # 70,000 leaves of 512 units: 274 row tiles need 40 row groups (8 tiles each at most)
     op, ch, hx = [], [], []
     for t in range(35000):
         op += [0, 0, 1]
@@ -330,7 +330,7 @@ def test_weight_stationary_selection_and_grid(monkeypatch):
     w = WL.make_graph([WL.CS_LEAF, WL.CS_INTERNAL], 128, 512, op, ch, hx, seed=3, dtype="bf16")
     info = edb.Forward(w, flags=base).exec.launch_info(1)
     assert info["variant"] == L.WS_VARIANT and info["m"] == 70000
-    assert info["grid"] == _ws_grid(70000, 512) == 16 * 24
+    assert info["grid"] == _ws_grid(70000, 512) == 16 * 40
     # a forced weight-stationary tile on a small batch; fp32 keeps the other tiles
     monkeypatch.setenv("EDB_VARIANT", str(L.WS_VARIANT))
     small = WL.make_config(5, instances=12)
