@@ -304,6 +304,28 @@ def test_weight_stationary_tile_bitwise_and_parity(case, monkeypatch):
         _check(w, h, c, hr, cr, f"weight-stationary tile {case}")
 
 
+def test_weight_stationary_tile_indexed_operands_bitwise(monkeypatch):
+    """On the weight-stationary tile, indexed lists (forced gathers, x read in
+    place through its row list, the identity layout with every list indexed)
+    give bitwise the states of the planned layout's contiguous lists."""
+    _torch()
+    w = WL.make_config(5, instances=12)
+    monkeypatch.setenv("EDB_VARIANT", str(L.WS_VARIANT))
+    base = _fwd(w, flags=L.USE_GRAPH | L.NO_SPLIT_K)
+    assert base.exec.launch_info(1)["variant"] == L.WS_VARIANT
+    base.run()
+    h0, c0 = base.states()
+    for kw in (dict(flags=L.USE_GRAPH | L.NO_SPLIT_K | L.FORCE_GATHER),
+               dict(flags=L.USE_GRAPH | L.NO_SPLIT_K | L.X_DIRECT),
+               dict(flags=L.USE_GRAPH | L.NO_SPLIT_K, plan_mode=L.PLAN_IDENTITY)):
+        f = _fwd(w, **kw)
+        assert f.exec.launch_info(1)["variant"] == L.WS_VARIANT, kw
+        f.run()
+        h, c = f.states()
+        np.testing.assert_array_equal(h, h0, err_msg=str(kw))
+        np.testing.assert_array_equal(c, c0, err_msg=str(kw))
+
+
 def test_large_tile_child_sum_many_children():
     """Child-sum parents with up to 9 children on the large tile (the per-parent
     reduction's loop beyond 4 children) against the small tile and the oracle."""
