@@ -986,12 +986,13 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
             }
             // the weight-stationary tile for the largest x-only batches (bf16):
             // the weights of its 32 units and its row table fit the LDS, the
-            // reduction is a whole number of the ring's groups of k-groups, and
+            // reduction is a whole number of the ring's groups of k-groups, at
+            // least two (the ring then reaches at most one tile ahead), and
             // offsets stay 32-bit
             {
                 const Entry& wen = table().e[kind_id][dtype][WS_VARIANT];
                 const bool ws_ok = wen.launch && !cs_large && large_fits && !(flags & EDB_NO_LARGE) &&
-                                   d.K % (32 * WS_D) == 0 &&
+                                   d.K % (32 * WS_D) == 0 && d.K / 32 >= 2 * WS_D &&
                                    d.Hu % WS_TU == 0 && wen.lds(d.K, d.Hk) <= max_lds;
                 if (ws_ok && ((m >= kWsMinRows && force_var < 0) || force_var == WS_VARIANT)) var = WS_VARIANT;
             }

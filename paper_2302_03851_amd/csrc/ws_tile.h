@@ -8,11 +8,12 @@
 // reduction in LDS (G * K / 16 KB), and walks its row tiles of 256 rows in
 // turn.  Each of its 8 waves (two per SIMD, so that one wave's gate epilogue
 // overlaps the other's matrix-core work) owns 32 rows of a tile: it loads its
-// own rows' MFMA fragments straight from the gathered x rows into a ring of D
-// k-groups (16 bytes a lane), so the loop shares nothing between waves but the
-// read-only weights and needs no barrier.  The ring runs across row tiles: the
-// last D k-group loads of a tile fetch the next tile's first k-groups, which
-// are in flight while the tile's epilogue runs.
+// own rows' operand pieces straight from the gathered x rows into a ring of D
+// k-groups (16 bytes a lane, row-contiguous) and permutes each into the MFMA
+// lane layout one step before use, so the loop shares nothing between waves
+// but the read-only weights and needs no barrier.  The ring runs across row
+// tiles: the last refills of a tile fetch the next tile's first k-groups,
+// which are in flight while the tile's epilogue runs.
 //
 // The work-group's row table (each row's x offset and result row, for all of
 // its tiles) is read once into LDS next to the weights, so the loop issues no
@@ -27,12 +28,11 @@
 // The epilogue passes each wave's c and h rows through a staging tile of its
 // own in LDS, so that every lane stores whole 16-byte pieces of the rows.
 //
-// On MI355X this tile is bound by the operand loads in the MFMA lane layout
-// (each load touches 16 rows, 16 bytes a lane) and by the epilogue (gate
-// nonlinearities and the stores, which each tile start waits for), not by the
-// matrix cores or the LDS: with the loads' data replaced by register values
-// the loop takes 60% of its time, without the weight reads from LDS it takes
-// the same time, and the matrix cores are busy about a quarter of the launch.
+// On MI355X the operand loads bound this tile: loaded straight in the MFMA
+// lane layout they made the launch a quarter slower than the row-contiguous
+// loads and lane permutation below; the epilogue (gate nonlinearities and the
+// stores, which each tile start waits for) comes next.  The LDS reads of the
+// weights do not limit it.
 //
 // Work-groups are dispatched round-robin over the 8 XCDs; they are numbered
 // so that the work-groups of one row group (all unit tiles of the same rows)
@@ -74,7 +74,8 @@ __host__ __device__ constexpr int ws_lds_bytes(int G, int K) {
 }
 
 // grid = (Hu / WS_TU) unit tiles x ngr row groups, ngr a multiple of 8 with
-// ceil(m / WS_TM) <= ngr * WS_MAXT; K / 32 a multiple of WS_D.
+// ceil(m / WS_TM) <= ngr * WS_MAXT; K / 32 a multiple of WS_D and at least
+// 2 WS_D, so that a refill targets at most the next row tile.
 template <int KIND>
 __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
     static_assert(WS_TM <= WS_NT, "one row of the row table per thread and tile");
@@ -140,40 +141,72 @@ __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
         for (int g = 0; g < G; ++g) bz[ub][g] = a.bias[g * a.Hu + u0 + ub * 16 + (lane & 15)];
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.xmat, (uint32_t)a.n_xrows * (uint32_t)a.E * 2u);
-    const int wrow = wave * 16 * WS_RB + (lane & 15);   // this lane's operand row in a tile (row block 0)
+    // The operand rows are loaded row-contiguous: lanes 4j .. 4j + 3 read the
+    // 64 bytes of one k-group of row j of a row block (16 bytes each), so each
+    // group of four lanes touches one cache line.  (In the MFMA lane layout,
+    // lane l holding row l % 16, four lanes in a row touch four lines: the
+    // vector L1 then handles four times the accesses per load, and that bound
+    // the loop.)  A lane permutation (lane bits rotated by two) then moves
+    // each fragment to the MFMA layout.
+    const int wrow = wave * WS_RW + (lane >> 2);   // this lane's operand row in a tile (row block 0)
+    const int perm = ((((lane & 15) << 2) | (lane >> 4))) * 4;   // byte address of the source lane
 
     // x offsets of this lane's operand rows in tile t (out of range past the last tile)
     auto offsets = [&](int t, uint32_t (&off)[WS_RB]) {
 #pragma unroll
         for (int rb = 0; rb < WS_RB; ++rb) off[rb] = t < ntile ? xo_l[t * WS_TM + wrow + rb * 16] : OOB;
     };
-    // operand fragments of k-group kg: 16 bytes of each row at element
-    // kg * 32 + 8 * (lane / 16), zero past E
+    // row-contiguous operand pieces of k-group kg: 16 bytes of the lane's row
+    // at element kg * 32 + 8 * (lane % 4), zero past E
     auto load_a = [&](uint4 (&av)[WS_RB], const uint32_t (&off)[WS_RB], int kg) {
-        const int col = kg * 32 + (lane >> 4) * 8;
+        const int col = kg * 32 + (lane & 3) * 8;
         const bool ok = col < a.E;
 #pragma unroll
         for (int rb = 0; rb < WS_RB; ++rb) av[rb] = bload(rx, ok ? off[rb] + (uint32_t)col * 2u : OOB);
     };
+    // the MFMA fragments: lane l takes the piece of lane 4 (l % 16) + l / 16
+    auto permute = [&](const uint4 (&av)[WS_RB], uint4 (&fa)[WS_RB]) {
+#pragma unroll
+        for (int rb = 0; rb < WS_RB; ++rb) {
+            fa[rb].x = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)av[rb].x);
+            fa[rb].y = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)av[rb].y);
+            fa[rb].z = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)av[rb].z);
+            fa[rb].w = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)av[rb].w);
+        }
+    };
 
     v4f acc[WS_UB][G][WS_RB];
-    uint4 ring[WS_D][WS_RB];
-    uint4 bfa[WS_UB][G], bfb[WS_UB][G];   // weight fragments: the current step's, the next step's
+    uint4 ring[WS_D][WS_RB];   // row-contiguous pieces of the next WS_D steps
+    uint4 fa[2][WS_RB];        // MFMA fragments: this step's, the next step's
+    uint4 bfa[WS_UB][G], bfb[WS_UB][G];   // weight fragments: this step's, the next step's
     auto read_b = [&](uint4 (&bf)[WS_UB][G], int kg) {
 #pragma unroll
         for (int ub = 0; ub < WS_UB; ++ub)
 #pragma unroll
             for (int g = 0; g < G; ++g) bf[ub][g] = Ws[((ub * G + g) * nkg + kg) * 64];
     };
-    // one step: the next step's weight fragments (k-group kgb) are read from
-    // LDS, ring slot p meets the current ones, and the slot is refilled with
-    // k-group kga of the rows at offr.  The scheduling barriers keep the reads
-    // at the start of the step and its refill in place (the scheduler would
-    // sink every refill to the end of the group, where the next group would
-    // wait for all of them).
-    auto step = [&](const uint4 (&bfc)[WS_UB][G], uint4 (&bfn)[WS_UB][G], int p, int kgb,
-                    const uint32_t (&offr)[WS_RB], int kga) {
+    uint32_t offc[WS_RB], offn[WS_RB];   // the current and the next row tile
+    // the ring slot that holds step kg0 + p + 1 (p + 1 mod WS_D) is permuted into
+    // the next step's fragments and refilled with the step WS_D after it,
+    // k-group t of the current tile or t - nkg of the next
+    auto advance = [&](int q, uint4 (&fn)[WS_RB], int t) {
+        permute(ring[q], fn);
+        const bool nxt = t >= nkg;
+        uint32_t offr[WS_RB];
+#pragma unroll
+        for (int rb = 0; rb < WS_RB; ++rb) offr[rb] = nxt ? offn[rb] : offc[rb];
+        load_a(ring[q], offr, nxt ? t - nkg : t);
+    };
+    // one step of k-group kg0 + p: the next step's weight fragments (k-group
+    // kgb) are read from LDS and its operand fragments permuted, the ring slot
+    // refilled, then this step's MFMAs.  The scheduling barriers keep the
+    // reads, the permutation and the refill ahead of the MFMAs (the scheduler
+    // would sink every refill to the end of the group, where the next group
+    // would wait for all of them).
+    auto step = [&](const uint4 (&bfc)[WS_UB][G], uint4 (&bfn)[WS_UB][G], const uint4 (&fc)[WS_RB],
+                    uint4 (&fn)[WS_RB], int kg0, int p, int kgb) {
         read_b(bfn, kgb);
+        advance((p + 1) % WS_D, fn, kg0 + p + 1 + WS_D);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int ub = 0; ub < WS_UB; ++ub)
@@ -182,29 +215,29 @@ __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
 #pragma unroll
                 for (int rb = 0; rb < WS_RB; ++rb)
                     acc[ub][g][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(v8bf, ring[p][rb]), __builtin_bit_cast(v8bf, bfc[ub][g]),
+                        __builtin_bit_cast(v8bf, fc[rb]), __builtin_bit_cast(v8bf, bfc[ub][g]),
                         acc[ub][g][rb], 0, 0, 0);
-        load_a(ring[p], offr, kga);
         __builtin_amdgcn_sched_barrier(0);
     };
-    // k-groups kg0 .. kg0 + WS_D - 1 (WS_D even: the fragments alternate
-    // between bfa and bfb and bfa holds the next group's first); slot p is
-    // refilled with k-group kgr + p of the rows at offr
-    auto group = [&](int kg0, const uint32_t (&offr)[WS_RB], int kgr) {
-        static_assert(WS_D % 2 == 0, "the weight fragments alternate between two sets");
+    // k-groups kg0 .. kg0 + WS_D - 1 (WS_D even: the weight and operand
+    // fragments alternate between two sets each, and the first set holds the
+    // next group's first step)
+    auto group = [&](int kg0) {
+        static_assert(WS_D % 2 == 0, "the fragments alternate between two sets");
 #pragma unroll
         for (int p = 0; p < WS_D; p += 2) {
-            step(bfa, bfb, p, kg0 + p + 1, offr, kgr + p);
+            step(bfa, bfb, fa[0], fa[1], kg0, p, kg0 + p + 1);
             const int kn = kg0 + p + 2;
-            step(bfb, bfa, p + 1, kn < nkg ? kn : 0, offr, kgr + p + 1);
+            step(bfb, bfa, fa[1], fa[0], kg0, p + 1, kn < nkg ? kn : 0);
         }
     };
 
-    uint32_t offc[WS_RB], offn[WS_RB];   // the current and the next row tile
     offsets(0, offc);
+    offsets(1, offn);
 #pragma unroll
     for (int p = 0; p < WS_D; ++p) load_a(ring[p], offc, p);
     read_b(bfa, 0);
+    advance(0, fa[0], WS_D);   // step 0's fragments; slot 0 refilled with step WS_D
     __bf16* Hout = reinterpret_cast<__bf16*>(a.arena_h);
     for (int i = 0; i < ntile; ++i) {
 #pragma unroll
@@ -213,21 +246,13 @@ __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int rb = 0; rb < WS_RB; ++rb) acc[ub][g][rb] = v4f{0.f, 0.f, 0.f, 0.f};
-        offsets(i + 1, offn);
         // the previous tile's stores are pending with the ring's loads, and the
         // compiler waits for every vector-memory operation where loads and
         // stores are pending together: wait once here (unconditionally, so that
         // no path into the loop carries stores), and the loop waits for the
         // ring slot by slot
         __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
-        for (int kg0 = 0; kg0 < nkg; kg0 += WS_D) {
-            // the tile's last group refills the ring from the next tile
-            const bool last = kg0 + WS_D == nkg;
-            uint32_t offr[WS_RB];
-#pragma unroll
-            for (int rb = 0; rb < WS_RB; ++rb) offr[rb] = last ? offn[rb] : offc[rb];
-            group(kg0, offr, last ? 0 : kg0 + WS_D);
-        }
+        for (int kg0 = 0; kg0 < nkg; kg0 += WS_D) group(kg0);
 
         // ---- epilogue of row tile i: bias, gates, cell update, h and c ----
         // The wave's results pass through its staging tile so that every lane
@@ -278,6 +303,7 @@ __global__ __launch_bounds__(WS_NT, 1) void ws_kernel(BatchArgs a) {
         }
 #pragma unroll
         for (int rb = 0; rb < WS_RB; ++rb) offc[rb] = offn[rb];
+        offsets(i + 2, offn);
     }
 }
 

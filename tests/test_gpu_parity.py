@@ -270,12 +270,12 @@ def _two_leaf_trees(kinds, n_trees, E, H, seed):
 WS_CASES = {
     # the child-sum configuration's leaves: 16 k-groups, several row tiles, a ragged tail
     "child-sum": lambda: WL.make_config(5, instances=12),
-    # N-ary leaves: a zero-padded x segment (E = 120 of 128: one group of k-groups) and padded units (H = 200 of 256)
-    "nary-padded": lambda: _two_leaf_trees([WL.NARY_LEAF, WL.NARY_INTERNAL], 400, 120, 200, seed=31),
+    # N-ary leaves: a zero-padded x segment (E = 248 of 256: two groups of k-groups) and padded units (H = 200 of 256)
+    "nary-padded": lambda: _two_leaf_trees([WL.NARY_LEAF, WL.NARY_INTERNAL], 400, 248, 200, seed=31),
     # TreeGRU leaves
-    "gru": lambda: _gru_trees(300, 128, 256, seed=32, dtype="bf16"),
+    "gru": lambda: _gru_trees(300, 256, 256, seed=32, dtype="bf16"),
     # 70,000 leaves: more row tiles than the row table holds at one work-group per CU
-    "row-table-bound": lambda: _two_leaf_trees([WL.CS_LEAF, WL.CS_INTERNAL], 35000, 128, 512, seed=33),
+    "row-table-bound": lambda: _two_leaf_trees([WL.CS_LEAF, WL.CS_INTERNAL], 35000, 256, 512, seed=33),
 }
 
 

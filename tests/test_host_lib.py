@@ -327,10 +327,15 @@ def test_weight_stationary_selection_and_grid(monkeypatch):
         op += [0, 0, 1]
         ch += [[], [], [3 * t, 3 * t + 1]]
         hx += [True, True, False]
-    w = WL.make_graph([WL.CS_LEAF, WL.CS_INTERNAL], 128, 512, op, ch, hx, seed=3, dtype="bf16")
+    w = WL.make_graph([WL.CS_LEAF, WL.CS_INTERNAL], 256, 512, op, ch, hx, seed=3, dtype="bf16")
     info = edb.Forward(w, flags=base).exec.launch_info(1)
     assert info["variant"] == L.WS_VARIANT and info["m"] == 70000
     assert info["grid"] == _ws_grid(70000, 512) == 16 * 40
+    # a reduction of one group of four k-groups (K = 128) keeps the other tiles
+    k128 = WL.make_graph([WL.CS_LEAF, WL.CS_INTERNAL], 128, 512, op[:3000], ch[:3000], hx[:3000], seed=4,
+                         dtype="bf16")
+    monkeypatch.setenv("EDB_VARIANT", str(L.WS_VARIANT))
+    assert edb.Forward(k128, flags=base).exec.launch_info(1)["variant"] != L.WS_VARIANT
     # a forced weight-stationary tile on a small batch; fp32 keeps the other tiles
     monkeypatch.setenv("EDB_VARIANT", str(L.WS_VARIANT))
     small = WL.make_config(5, instances=12)
