@@ -124,6 +124,27 @@ LARGE_CLASS = {8: 0, 9: 1, 10: 2, 15: 3, 16: 4}                     # large tile
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
+KIND_NAMES = {0: "LSTM_CHAIN", 1: "NARY_LEAF", 2: "NARY_INTERNAL", 3: "GRID", 4: "CS_LEAF", 5: "CS_INTERNAL",
+              6: "LAT_CHAR", 7: "LAT_WORD", 8: "GRU_LEAF", 9: "GRU_INTERNAL", 10: "LINEAR", 11: "MV_MAT",
+              12: "MV_VEC", 13: "LGRU_EDGE", 14: "POOL_MEAN"}
+
+
+def kernel_name(kind, variant, part, dtype):
+    """A readable name of the kernel a launch runs (kind, tile family, variant)."""
+    from paper_2302_03851_amd import _lib as L
+    kname = KIND_NAMES[kind]
+    if part == 1:
+        return "mv_matvec_kernel" if kind == 12 else "child_reduce_kernel"
+    if variant == L.WS_VARIANT:
+        return f"ws_kernel<{kname}, bf16>"
+    if variant in L.LARGE_VARIANTS:
+        kk = "CS_FORGET" if part == 2 else ("CS_PARENT" if kind == 5 else kname)
+        return f"big_kernel<{kk}, {dtype}, size class {LARGE_CLASS[variant]}>"
+    if variant in STREAM_SHAPES:
+        return f"stream_kernel<{kname}, {dtype}, variant {variant}>"
+    return f"cell_kernel<{kname}, {dtype}, variant {variant}>"
+
+
 def kernel_symbol(kind, dtype, variant, part):
     """The kernel a launch runs, as rocprofv3 prints its name (prefix)."""
     if part == 1:
@@ -831,22 +852,18 @@ def main():
         else:
             by_launch = sum(work[inf["batch"]][2] for inf in grp) / nl
         gbs = by_launch / (avg_ms * 1e-3) / 1e9
-    kname = {0: "LSTM_CHAIN", 1: "NARY_LEAF", 2: "NARY_INTERNAL", 3: "GRID", 4: "CS_LEAF",
-             5: "CS_INTERNAL", 6: "LAT_CHAR", 7: "LAT_WORD", 8: "GRU_LEAF", 9: "GRU_INTERNAL",
-             10: "LINEAR", 11: "MV_MAT", 12: "MV_VEC", 13: "LGRU_EDGE", 14: "POOL_MEAN"}[dom[0]]
     kind_v, var_v, part_v = dom
-    if part_v == 1:
-        kernel = "mv_matvec_kernel" if kind_v == WL.MV_VEC else "child_reduce_kernel"
-    elif var_v == L.WS_VARIANT:
-        kernel = f"ws_kernel<{kname}, bf16>"
-    elif var_v in L.LARGE_VARIANTS:
-        kk = "CS_FORGET" if part_v == 2 else ("CS_PARENT" if kind_v == WL.CS_INTERNAL else kname)
-        kernel = f"big_kernel<{kk}, {w.dtype}, size class {LARGE_CLASS[var_v]}>"
-    elif var_v in STREAM_SHAPES:
-        kernel = f"stream_kernel<{kname}, {w.dtype}, variant {var_v}>"
-    else:
-        kernel = f"cell_kernel<{kname}, {w.dtype}, variant {var_v}>"
+    kernel = kernel_name(kind_v, var_v, part_v, w.dtype)
     symbol = kernel_symbol(kind_v, w.dtype, var_v, part_v)
+    # the largest contraction: the launch with the most algorithmic flops
+    big_i = max(range(1, len(infos)), key=lambda i: launch_work(infos[i], work, split))
+    big_inf, big_fl = infos[big_i], launch_work(infos[big_i], work, split)
+    big_tflops = big_fl / (times[big_i] * 1e-3) / 1e12 if times[big_i] > 0 else 0.0
+    largest = {"kernel": kernel_name(big_inf["kind"], big_inf["variant"], big_inf["part"], w.dtype),
+               "symbol": kernel_symbol(big_inf["kind"], w.dtype, big_inf["variant"], big_inf["part"]),
+               "launch": big_i, "rows": big_inf["m"], "alg_flops": int(big_fl),
+               "avg_launch_us": round(float(times[big_i]) * 1e3, 2), "achieved": round(big_tflops, 3),
+               "peak": peak, "unit": "TFLOP/s", "frac": round(big_tflops / peak, 4)}
     traffic = traffic_of(symbol, WORKLOAD_TEXT[args.config])
     tot_flops = sum(x[0] + x[1] for x in work)
     tot_bytes = sum(x[2] for x in work) + weight_bytes(w)
@@ -892,6 +909,7 @@ def main():
         "host_ms_per_graph": round(ms_host, 4),
         "host_ms_parts": host_parts,
         "launch_us": [round(t * 1e3, 2) for t in times],
+        "largest_launch": largest,
     }
     pm = probes(w.dtype)
     if hbm_bound:
