@@ -274,6 +274,8 @@ WS_CASES = {
     "nary-padded": lambda: _two_leaf_trees([WL.NARY_LEAF, WL.NARY_INTERNAL], 400, 248, 200, seed=31),
     # TreeGRU leaves
     "gru": lambda: _gru_trees(300, 256, 256, seed=32, dtype="bf16"),
+    # 10 leaves (one row block, most rows past the batch) of 64 units (two unit tiles)
+    "tiny": lambda: _two_leaf_trees([WL.CS_LEAF, WL.CS_INTERNAL], 5, 256, 64, seed=34),
     # 70,000 leaves: more row tiles than the row table holds at one work-group per CU
     "row-table-bound": lambda: _two_leaf_trees([WL.CS_LEAF, WL.CS_INTERNAL], 35000, 256, 512, seed=33),
 }
