@@ -28,11 +28,12 @@
 // The epilogue passes each wave's c and h rows through a staging tile of its
 // own in LDS, so that every lane stores whole 16-byte pieces of the rows.
 //
-// On MI355X the operand loads bound this tile: loaded straight in the MFMA
-// lane layout they made the launch a quarter slower than the row-contiguous
-// loads and lane permutation below; the epilogue (gate nonlinearities and the
-// stores, which each tile start waits for) comes next.  The LDS reads of the
-// weights do not limit it.
+// On MI355X the LDS pipe bounds the loop: the weight reads and the lane
+// permutation share it, over about as much matrix-core time again.  Loaded
+// straight in the MFMA lane layout (four rows in each group of four lanes)
+// the operands made the launch a quarter slower than the row-contiguous loads
+// and permutation below.  The epilogue (gate nonlinearities and the stores,
+// which each tile start waits for) adds the rest.
 //
 // Work-groups are dispatched round-robin over the 8 XCDs; they are numbered
 // so that the work-groups of one row group (all unit tiles of the same rows)
