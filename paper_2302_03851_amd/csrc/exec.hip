@@ -516,42 +516,42 @@ double variant_cost(int v, int m, const Dims& d, int dtype, int64_t nrag, int oc
 }
 
 // Estimated microseconds of the large tile, size class vb, for G gates over K
-// (padded) and m rows, occ work-groups resident per CU.  The work-groups run
-// in rounds of n_cu * occ; a round of c work-groups per CU costs, per 128-byte
-// chunk of k, the bytes the c work-groups copy to LDS, their matrix-core time,
-// the longer of the two (copy at about 86 GB/s per CU), and with one resident
-// work-group their sum (nothing to overlap them with); plus an epilogue term
-// per element and gate.  Coefficients per size class: non-negative
-// least-squares fits to per-launch times of the class on the batches of all
-// five workloads on MI355X (594 launches, median error 3-5% per class).
+// (padded) and m rows, occ work-groups resident per CU.  The busiest CU runs
+// T = ceil(tiles / n_cu) tiles in R = ceil(tiles / (n_cu * occ)) rounds.  The
+// estimate adds a fixed term; the bytes the whole launch copies to LDS (the
+// L2s' shared bandwidth); a latency term per round and 128-byte chunk of k;
+// the busiest CU's matrix-core time; its LDS-copy time at about 86 GB/s; its
+// epilogue elements per gate; a term per round; and, with one tile per CU,
+// that tile's copy and matrix-core time, which nothing overlaps.  A tail
+// round of a few tiles costs little here: it runs once the other CUs have
+// finished, with the memory system to itself.  Coefficients per size class:
+// non-negative least-squares fits (relative error) to the per-launch times of
+// each class forced on every batch of five workloads on MI355X (611 launches;
+// median error 2.0-3.7% per class).
 double large_cost(int G, int vb, int m, int K, int Hu, int dtype, int occ, int n_cu) {
     static constexpr double kc[NUM_BIG_CLASSES][8] = {
-        {0, 3.3767, 0.016996, 1.6769, 0, 0.92299, 0.38126, 0},
-        {0, 2.3427, 0.59572, 0.5983, 0, 1.0321, 0, 0},
-        {1.3643, 1.2412, 0.46072, 0.099006, 0, 1.1841, 0, 0},
-        {1.3794, 0.13501, 0.61735, 0.35123, 0.98106, 0, 1.161, 0},
-        {1.4102, 0.6417, 0.46044, 0.24468, 1.1586, 0, 0.76119, 0}};
+        {0.93142, 10.331, 0.68536, 0.52968, 0, 1.9054, 3.0777, 0.44844},
+        {2.9115, 6.0844, 0.57178, 0.71069, 0, 1.1642, 0.075934, 0.34943},
+        {2.2408, 4.8979, 0.43479, 0.4966, 0, 1.3676, 0, 0.5421},
+        {2.2977, 3.7322, 0.45709, 0.70584, 0, 0.078758, 0, 0.39545},
+        {1.7341, 2.5833, 0.40146, 0.77375, 0.069121, 0.939, 0, 0.39636}};
     const double* k = kc[vb];
     const int RB = big_rb(G, vb), CU = big_cu(vb), TM = 32 * RB, TU = 32 * CU;
     const bool f32 = dtype == EDB_F32;
     const int64_t tiles = (int64_t)((m + TM - 1) / TM) * (Hu / TU);
     occ = std::max(1, std::min(occ, 8));
-    const int64_t cap = (int64_t)n_cu * occ, full = tiles / cap, rem = tiles % cap;
+    const double T = (double)((tiles + n_cu - 1) / n_cu);
+    const double R = (double)((tiles + (int64_t)n_cu * occ - 1) / ((int64_t)n_cu * occ));
     const double nch = K / (f32 ? 32 : 64);
     const double cpy = (TM * 128.0 + 2.0 * CU * G * 2 * 1024) / 1024.0;    // KB per chunk per work-group
     const double mma = 2.0 * CU * G * RB * (f32 ? 128 : 16) / 2400.0;      // us per chunk per SIMD per work-group
-    auto round_us = [&](double c) {
-        return k[1] + k[2] * nch + k[3] * c * nch * cpy / 64.0 + k[4] * c * nch * mma +
-               k[5] * nch * std::max(c * cpy / 86.0, c * mma) + k[6] * c * TM * TU * G / 16384.0 +
-               (c == 1.0 ? k[7] * nch * (cpy / 86.0 + mma) : 0.0);
-    };
-    double t = k[0] + (double)full * round_us(occ);
-    if (rem) t += round_us((double)((rem + n_cu - 1) / n_cu));
-    return t;
+    return k[0] + k[1] * (double)tiles * nch * cpy / 102400.0 + k[2] * R * nch + k[3] * T * nch * mma +
+           k[4] * T * nch * cpy / 86.0 + k[5] * T * TM * TU * G / 16384.0 + k[6] * R +
+           (T == 1.0 ? k[7] * nch * (cpy / 86.0 + mma) : 0.0);
 }
 
 // Estimated microseconds of child_reduce_kernel over m parents (fit as above).
-double child_reduce_cost(int m) { return 3.794 + 1.0509e-3 * m; }
+double child_reduce_cost(int m) { return 3.739 + 1.0300e-3 * m; }
 
 // Work-groups of a kernel resident on one CU (block threads, dyn_lds bytes of
 // dynamic LDS, lds bytes of LDS in all): from the runtime (registers and LDS)
@@ -569,7 +569,7 @@ int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max
         const int lds = en.lds(K, 0);   // the large tile's LDS is static
         if (lds > max_lds) continue;
         const double c = large_cost(G, vb, m, K, Hu, dtype, occ(en, 256, 0, lds), n_cu) + extra_us;
-        if (c < est * 0.97) { est = c; var = large_variant(vb); }
+        if (c < est) { est = c; var = large_variant(vb); }
     }
     return var;
 }
