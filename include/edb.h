@@ -104,7 +104,9 @@ typedef struct edb_schedule edb_schedule_t;
 
 /* Runs the batching loop on the host.  Every batch holds all ready nodes of
  * the chosen type in ascending node id (Algorithm 1's frontier batch).
- * Errors: EDB_ERR_INVALID (NULL, unknown kind/encoding), EDB_ERR_TABLE. */
+ * Errors: EDB_ERR_INVALID (NULL, unknown kind/encoding), EDB_ERR_TABLE;
+ * EDB_ERR_CYCLE when no node is ready while nodes remain (the frontier
+ * policies; only a graph with a cycle, which edb_build_graph rejects). */
 edb_status edb_schedule(const edb_graph_t* g, const edb_policy* policy, edb_schedule_t** out);
 /* Borrowed views, valid until edb_schedule_free:
  *   batch_ptr int32[n_batches+1], batch_nodes int32[V], batch_type int32[n_batches]. */
@@ -463,7 +465,9 @@ edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
  * work.  Arguments are those of the individual calls; arena_h and
  * arena_c must hold at least the plan's n_slots rows (arena_rows), which is
  * returned in *n_slots (may be NULL) also when the arena is too small
- * (EDB_ERR_INVALID).  EDB_DRYRUN is rejected.
+ * (EDB_ERR_INVALID).  EDB_DRYRUN is rejected.  With a frontier policy the
+ * ingest leaves the acyclicity check to the schedule, which returns
+ * EDB_ERR_CYCLE for a cycle as edb_build_graph would.
  * exec_out (may be NULL): on success receives the executor instead of it
  * being freed; the caller reads edb_exec_launch_info and, with EDB_PROFILE in
  * exec_flags, edb_exec_launch_times, and releases it with edb_exec_free. */

@@ -42,6 +42,12 @@ namespace edb {
 edb_status fail(edb_status st, const std::string& msg);
 void clear_error();
 
+// edb_build_graph with the acyclicity check optional: without it the graph
+// must go to a frontier policy's schedule, which reports a cycle itself (no
+// node ready while some remain).
+edb_status build_graph(int32_t n_nodes, int32_t n_types, const int32_t* op_type, const int64_t* child_ptr,
+                       const int32_t* child_idx, const int32_t* x_row, bool check_acyclic, edb_graph_t** out);
+
 // Sub-frontier bookkeeping for Eq. 1's ratio: same_pending[v] counts v's
 // unexecuted present children of v's own type (per edge occurrence); subf[a]
 // counts unexecuted type-a nodes with none, i.e. |Frontier(G^a)|.

@@ -840,19 +840,32 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
             n_cu = ctx->n_cu;
         }
         const int force_var = std::getenv("EDB_VARIANT") ? std::atoi(std::getenv("EDB_VARIANT")) : -1;
+        // occupancy per (kernel, dynamic LDS): the device context's cache is
+        // shared by every thread behind one lock, so each prepare keeps the
+        // values it has looked up (a few dozen) in a list of its own
+        std::vector<std::tuple<const void*, int, int>> occ_seen;
         const OccFn occ = [&](const Entry& en, int block, int dyn_lds, int lds) -> int {
             const int est = std::max(1, std::min({max_lds / std::max(lds, 1), 32 / std::max(block / 64, 1), 16}));
             if (!ctx || !en.fn) return est;
-            std::lock_guard<std::mutex> lk(g_ctx_mu);
-            const auto key = std::make_pair(en.fn, dyn_lds);
-            auto it = ctx->occupancy.find(key);
-            if (it != ctx->occupancy.end()) return it->second;
+            for (const auto& o : occ_seen)
+                if (std::get<0>(o) == en.fn && std::get<1>(o) == dyn_lds) return std::get<2>(o);
             int nb = 0;
-            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, en.fn, block, (size_t)dyn_lds) != hipSuccess || nb < 1) {
-                (void)hipGetLastError();
-                nb = est;
+            {
+                std::lock_guard<std::mutex> lk(g_ctx_mu);
+                const auto key = std::make_pair(en.fn, dyn_lds);
+                auto it = ctx->occupancy.find(key);
+                if (it != ctx->occupancy.end()) {
+                    nb = it->second;
+                } else {
+                    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, en.fn, block, (size_t)dyn_lds) != hipSuccess ||
+                        nb < 1) {
+                        (void)hipGetLastError();
+                        nb = est;
+                    }
+                    ctx->occupancy[key] = nb;
+                }
             }
-            ctx->occupancy[key] = nb;
+            occ_seen.emplace_back(en.fn, dyn_lds, nb);
             return nb;
         };
 
@@ -2098,7 +2111,9 @@ extern "C" edb_status edb_forward_noalloc(int32_t n_nodes, int32_t n_types, cons
     edb_schedule_t* s = nullptr;
     edb_plan_t* p = nullptr;
     edb_exec_t* e = nullptr;
-    edb_status st = edb_build_graph(n_nodes, n_types, op_type, child_ptr, child_idx, x_row, &g);
+    // a frontier policy's schedule reports a cycle itself: the ingest skips its own check
+    const bool frontier = policy && policy->kind != EDB_POLICY_DEPTH;
+    edb_status st = edb::build_graph(n_nodes, n_types, op_type, child_ptr, child_idx, x_row, !frontier, &g);
     if (st == EDB_OK) st = edb_schedule(g, policy, &s);
     if (st == EDB_OK) st = edb_plan_memory(g, s, shapes, plan_flags, &p);
     if (st == EDB_OK) {

@@ -23,7 +23,9 @@ extern "C" edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_
     edb_schedule_t* s = nullptr;
     edb_plan_t* p = nullptr;
     edb_exec_t* e = nullptr;
-    edb_status st = edb_build_graph(n_nodes, n_types, op_type, child_ptr, child_idx, x_row, &g);
+    // a frontier policy's schedule reports a cycle itself: the ingest skips its own check
+    const bool frontier = policy && policy->kind != EDB_POLICY_DEPTH;
+    edb_status st = edb::build_graph(n_nodes, n_types, op_type, child_ptr, child_idx, x_row, !frontier, &g);
     if (st == EDB_OK) st = edb_schedule(g, policy, &s);
     if (st == EDB_OK) st = edb_plan_memory(g, s, shapes, plan_flags, &p);
     if (st == EDB_OK) {

@@ -37,7 +37,8 @@ bool consecutive(const int32_t* s, int64_t n) {
 }
 
 // Sort (key, value) pairs by their non-negative, distinct keys: LSD radix
-// sort with 11-bit digits (a comparison sort for short lists).
+// sort with 8-bit digits, as many passes as the largest key needs (a
+// comparison sort for short lists).
 void sort_by_key(std::vector<std::pair<int32_t, int32_t>>& a, std::vector<std::pair<int32_t, int32_t>>& tmp) {
     const size_t n = a.size();
     if (n < 64) {
@@ -47,17 +48,17 @@ void sort_by_key(std::vector<std::pair<int32_t, int32_t>>& a, std::vector<std::p
     uint32_t maxk = 0;
     for (const auto& x : a) maxk = std::max(maxk, (uint32_t)x.first);
     tmp.resize(n);
-    uint32_t count[2048];
-    for (int shift = 0; shift < 32 && (maxk >> shift) != 0; shift += 11) {
-        std::fill(count, count + 2048, 0u);
-        for (const auto& x : a) ++count[((uint32_t)x.first >> shift) & 2047u];
+    uint32_t count[256];
+    for (int shift = 0; shift < 32 && (maxk >> shift) != 0; shift += 8) {
+        std::fill(count, count + 256, 0u);
+        for (const auto& x : a) ++count[((uint32_t)x.first >> shift) & 255u];
         uint32_t sum = 0;
         for (uint32_t& c : count) {
             const uint32_t t = c;
             c = sum;
             sum += t;
         }
-        for (const auto& x : a) tmp[count[((uint32_t)x.first >> shift) & 2047u]++] = x;
+        for (const auto& x : a) tmp[count[((uint32_t)x.first >> shift) & 255u]++] = x;
         a.swap(tmp);
     }
 }

@@ -175,25 +175,38 @@ extern "C" edb_status edb_schedule(const edb_graph_t* g, const edb_policy* pol, 
         } else {
             // pending counters and consumer lists over present edges (from ingest)
             std::vector<int32_t> pending(g->pending);
-            const std::vector<int32_t>& cons_ptr = g->cons_ptr;
-            const std::vector<int32_t>& cons = g->cons;
-            std::vector<std::vector<int32_t>> ready(T);
-            for (int32_t v = 0; v < V; ++v) if (pending[v] == 0) ready[g->op_type[v]].push_back(v);
+            const int32_t* cons_ptr = g->cons_ptr.data();
+            const int32_t* cons = g->cons.data();
+            const int32_t* op = g->op_type.data();
+            // the ready nodes of each type as a bitmap over node ids (words
+            // [lo, hi) may be non-zero): a batch comes out in ascending id by
+            // scanning its type's words, without sorting
+            const int64_t W = ((int64_t)V + 63) / 64;
+            std::vector<uint64_t> ready((size_t)T * (size_t)W, 0);
+            std::vector<int64_t> lo(T, W), hi(T, 0);
+            std::vector<int64_t> counts(T, 0);
+            auto make_ready = [&](int32_t v) {
+                const int32_t a = op[v];
+                const int64_t w = v >> 6;
+                ready[(size_t)a * W + w] |= uint64_t(1) << (v & 63);
+                lo[a] = std::min(lo[a], w);
+                hi[a] = std::max(hi[a], w + 1);
+                ++counts[a];
+            };
+            for (int32_t v = 0; v < V; ++v) if (pending[v] == 0) make_ready(v);
             std::vector<int64_t> depth, dsum(T, 0), dcnt(T, 0);
             if (pol->kind == EDB_POLICY_AGENDA) {
                 topo_depth(*g, depth);
-                for (int32_t v = 0; v < V; ++v) { dsum[g->op_type[v]] += depth[v]; dcnt[g->op_type[v]] += 1; }
+                for (int32_t v = 0; v < V; ++v) { dsum[op[v]] += depth[v]; dcnt[op[v]] += 1; }
             }
             // sufficient condition: sub-frontier of G^a = unexecuted type-a nodes
             // without an unexecuted type-a child (per edge occurrence)
             std::vector<int32_t> same_pending;
             std::vector<int64_t> subf;
             if (pol->kind == EDB_POLICY_SUFFICIENT) edb::same_type_frontier(*g, same_pending, subf);
-            std::vector<int64_t> counts(T);
             std::vector<int32_t> key;
             int64_t remaining = V;
             while (remaining > 0) {
-                for (int32_t t = 0; t < T; ++t) counts[t] = (int64_t)ready[t].size();
                 int32_t t = -1;
                 if (pol->kind == EDB_POLICY_TABLE) {
                     encode(counts, pol->encoding, key);
@@ -213,20 +226,39 @@ extern "C" edb_status edb_schedule(const edb_graph_t* g, const edb_policy* pol, 
                         if (t < 0 || dsum[a] * dcnt[t] < dsum[t] * dcnt[a]) t = a;
                     }
                 }
-                std::vector<int32_t> batch;
-                batch.swap(ready[t]);
-                std::sort(batch.begin(), batch.end());
-                for (int32_t v : batch) {
+                if (t < 0) {
+                    // nothing ready while nodes remain: a cycle (a graph built
+                    // without the ingest's acyclicity check)
+                    delete s;
+                    return fail(EDB_ERR_CYCLE, "edb_schedule: the graph has a cycle");
+                }
+                // the batch: every node ready now, ascending; nodes that become
+                // ready below wait for a later step
+                const size_t first = s->batch_nodes.size();
+                uint64_t* rw = ready.data() + (size_t)t * W;
+                for (int64_t w = lo[t]; w < hi[t]; ++w) {
+                    uint64_t x = rw[w];
+                    rw[w] = 0;
+                    while (x) {
+                        s->batch_nodes.push_back((int32_t)(w * 64 + __builtin_ctzll(x)));
+                        x &= x - 1;
+                    }
+                }
+                lo[t] = W;
+                hi[t] = 0;
+                counts[t] = 0;
+                const size_t last = s->batch_nodes.size();
+                for (size_t i = first; i < last; ++i) {
+                    const int32_t v = s->batch_nodes[i];
                     if (pol->kind == EDB_POLICY_AGENDA) { dsum[t] -= depth[v]; dcnt[t] -= 1; }
                     if (pol->kind == EDB_POLICY_SUFFICIENT) edb::same_type_executed(*g, v, same_pending, subf);
-                    for (int32_t i = cons_ptr[v]; i < cons_ptr[v + 1]; ++i) {
-                        int32_t p = cons[i];
-                        if (--pending[p] == 0) ready[g->op_type[p]].push_back(p);
+                    for (int32_t j = cons_ptr[v]; j < cons_ptr[v + 1]; ++j) {
+                        const int32_t p = cons[j];
+                        if (--pending[p] == 0) make_ready(p);
                     }
-                    s->batch_nodes.push_back(v);
                 }
-                remaining -= (int64_t)batch.size();
-                s->batch_ptr.push_back((int32_t)s->batch_nodes.size());
+                remaining -= (int64_t)(last - first);
+                s->batch_ptr.push_back((int32_t)last);
                 s->batch_type.push_back(t);
             }
         }

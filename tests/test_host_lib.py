@@ -433,6 +433,41 @@ def test_forward_call_validates_before_any_device_work():
     assert ei.value.status == L.EDB_ERR_INVALID
 
 
+
+@pytest.mark.parametrize("policy", [L.POLICY_TABLE, L.POLICY_AGENDA, L.POLICY_SUFFICIENT, L.POLICY_DEPTH])
+def test_forward_call_rejects_cycles_before_any_device_work(policy):
+    """edb_forward skips the ingest's own acyclicity check for the frontier
+    policies (their schedule finds no ready node while nodes remain and
+    reports the cycle); the depth policy keeps the ingest's check.  Either
+    way a cycle fails with EDB_ERR_CYCLE before any HIP call.  The graph is a
+    valid tree with a two-node cycle beside it."""
+    w = WL.make_config(2, instances=2)
+    cells = [edb.cell_struct(k, w.in_dim, w.hidden, w.n_children[t] if k == WL.NARY_INTERNAL else 0, L.F32)
+             for t, k in enumerate(w.kinds)]
+    V = len(w.op_type)
+    internal = [t for t, k in enumerate(w.kinds) if k == WL.NARY_INTERNAL][0]
+    n_ch = w.n_children[internal]
+    # two extra internal nodes, each the other's first child (the rest absent)
+    op = np.concatenate([np.asarray(w.op_type, np.int32), np.array([internal, internal], np.int32)])
+    kids = [V + 1] + [-1] * (n_ch - 1) + [V] + [-1] * (n_ch - 1)
+    idx = np.concatenate([np.asarray(w.child_idx, np.int32), np.array(kids, np.int32)])
+    ptr = np.concatenate([np.asarray(w.child_ptr, np.int64),
+                          w.child_ptr[-1] + np.array([n_ch, 2 * n_ch], np.int64)])
+    xr = np.concatenate([np.asarray(w.x_row, np.int32), np.array([-1, -1], np.int32)])
+    fc = edb.ForwardCall(op, ptr, idx, xr, w.n_types, edb.operand_shapes(w), cells, policy=policy)
+    with pytest.raises(L.EdbError) as ei:
+        fc.call([256, 256], 256, 256, 256, 10 ** 6, 0)
+    assert ei.value.status == L.EDB_ERR_CYCLE and "cycle" in str(ei.value)
+    # the same graph without the cycle's back edge goes past the ingest and
+    # the schedule (it fails later, on the too-small arena)
+    idx2 = idx.copy()
+    idx2[len(w.child_idx)] = -1
+    fc2 = edb.ForwardCall(op, ptr, idx2, xr, w.n_types, edb.operand_shapes(w), cells, policy=policy)
+    with pytest.raises(L.EdbError) as ei:
+        fc2.call([256, 256], 256, 256, 256, 3, 0)
+    assert ei.value.status == L.EDB_ERR_INVALID and "arena" in str(ei.value)
+
+
 PQ_INSTANCES = {1: 8, 2: 16, 3: 8, 4: 3, 5: 8}
 
 
