@@ -339,7 +339,7 @@ edb_status edb_pack_weights(const edb_cell* cell, const float* const* logical,
                             void* packed_dev, void* stream);
 
 /* ---- execution ------------------------------------------------------------ */
-#define EDB_USE_GRAPH    1  /* capture the batch sequence once, replay it per call */
+#define EDB_USE_GRAPH    1  /* run the batch sequence as one HIP graph launch (graph kept per stream) */
 #define EDB_DRYRUN       2  /* record the launch list only; no HIP call (CPU testing) */
 #define EDB_FORCE_GATHER 4  /* treat every CONTIG operand as indexed (ablation) */
 #define EDB_X_DIRECT     8  /* read x rows in place by x_row instead of staging them */
@@ -397,12 +397,24 @@ edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_
  * every node's staged row would be its own row of x (x is then read in
  * place), or when a single batch reads x (it then reads the caller's rows
  * through its row list, as under EDB_X_DIRECT).  With
- * EDB_USE_GRAPH the sequence is captured into a HIP graph on the first call
- * and whenever a pointer differs from the captured ones, and replayed with a
- * single graph launch otherwise.  Kernel faults surface at the caller's next
- * synchronisation.  One edb_exec_t must not run on two streams at once. */
+ * EDB_USE_GRAPH the sequence runs as one launch of a HIP graph that the
+ * library keeps per device and stream and reuses for every later execution
+ * there, of any executor, whose sequence has the same kernels and block sizes
+ * (a new input graph of the same shape of schedule): the graph's kernel nodes
+ * get the new arguments, grids and LDS sizes in place, without a new
+ * instantiation; up to 4 sequences per stream are kept, the least recently
+ * used one replaced (after its last launch has run); they live until the
+ * process ends.  Kernel faults surface at the caller's next synchronisation.
+ * One edb_exec_t must not run on two streams at once. */
 edb_status edb_execute(edb_exec_t* e, const void* const* packed_weights, const void* x,
                        void* arena_h, void* arena_c, void* stream);
+
+/* Graph reuse counters of the process (EDB_USE_GRAPH executions): the kernel
+ * sequences instantiated as new HIP graphs, and the executions that instead
+ * updated the nodes of a kept graph in place (Section 1 prices a launch;
+ * dynamic inputs change the graph every mini-batch, so a new input must not
+ * cost a new instantiation).  Host outputs; EDB_ERR_INVALID on NULL. */
+edb_status edb_graph_stats(int64_t* instantiated, int64_t* updated);
 
 /* Dataflow launches (a persistent kernel running a run of consecutive small
  * batches, each tile waiting only for the tiles that produce its operand
@@ -465,7 +477,9 @@ edb_status edb_exec_launch_times(edb_exec_t* e, float* ms, int32_t n);
  * work.  Arguments are those of the individual calls; arena_h and
  * arena_c must hold at least the plan's n_slots rows (arena_rows), which is
  * returned in *n_slots (may be NULL) also when the arena is too small
- * (EDB_ERR_INVALID).  EDB_DRYRUN is rejected.  With a frontier policy the
+ * (EDB_ERR_INVALID).  EDB_DRYRUN is rejected.  EDB_USE_GRAPH (plain path:
+ * no exec_out, no EDB_PROFILE) runs the launches through the stream's kept
+ * graph as edb_execute does.  With a frontier policy the
  * ingest leaves the acyclicity check to the schedule, which returns
  * EDB_ERR_CYCLE for a cycle as edb_build_graph would.
  * exec_out (may be NULL): on success receives the executor instead of it

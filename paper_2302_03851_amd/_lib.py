@@ -41,7 +41,7 @@ EXPORTS = [
     "edb_learn_defaults", "edb_learn_policy", "edb_learned_view", "edb_learned_q", "edb_learned_free",
     "edb_plan_memory", "edb_plan_view", "edb_plan_free",
     "edb_packed_weight_bytes", "edb_pack_weights",
-    "edb_prepare", "edb_execute", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
+    "edb_prepare", "edb_execute", "edb_graph_stats", "edb_exec_launches", "edb_exec_launch_info", "edb_exec_launch_times",
     "edb_exec_check", "edb_exec_validate", "edb_exec_free", "edb_forward", "edb_stream_release",
     "edb_forward_noalloc",
     "edb_split_phase_bytes", "edb_split_phase", "edb_probe_mfma", "edb_probe_copy",
@@ -138,6 +138,7 @@ def load():
         "edb_pack_weights": (C.c_int32, [P(Cell), P(P(C.c_float)), vp, vp]),
         "edb_prepare": (C.c_int32, [vp, vp, vp, P(Cell), C.c_int32, P(vp)]),
         "edb_execute": (C.c_int32, [vp, P(vp), vp, vp, vp, vp]),
+        "edb_graph_stats": (C.c_int32, [P(C.c_int64), P(C.c_int64)]),
         "edb_exec_launches": (C.c_int32, [vp, P(C.c_int32)]),
         "edb_exec_launch_info": (C.c_int32, [vp, C.c_int32, P(LaunchInfo)]),
         "edb_exec_launch_times": (C.c_int32, [vp, P(C.c_float), C.c_int32]),

@@ -70,9 +70,10 @@ void pq_layout(const edb_graph& g, const struct edb_schedule& s, const edb_opera
 // edb_forward's plain path (no executor handed back, no profiling): prepares
 // the launches without device memory of their own, binds them to the device
 // block cached for (current device, stream), copies the descriptors on the
-// stream and launches; the block grows in stream order when a call needs more.
+// stream and launches (with use_graph through the stream's kept HIP graph of
+// the same kernel sequence); the block grows in stream order when a call needs more.
 edb_status forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
                              const edb_cell* cells, int32_t flags, const void* const* packed_weights,
-                             const void* x, void* arena_h, void* arena_c, void* stream);
+                             const void* x, void* arena_h, void* arena_c, void* stream, bool use_graph);
 
 }  // namespace edb

@@ -8,6 +8,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <functional>
+#include <atomic>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -617,6 +618,13 @@ hipError_t ctx_streams(DeviceCtx* ctx) {
     return he;
 }
 
+namespace {
+uint64_t next_exec_id() {
+    static std::atomic<uint64_t> n{0};
+    return ++n;
+}
+}  // namespace
+
 struct edb_exec {
     int32_t flags = 0;
     int32_t T = 0, B = 0, dtype = 0;
@@ -648,10 +656,7 @@ struct edb_exec {
     hipEvent_t ready = nullptr;       // descriptors uploaded
     hipEvent_t done = nullptr;        // last execution enqueued
     bool ran = false;
-    hipStream_t cap_stream = nullptr;
-    hipGraph_t graph = nullptr;
-    hipGraphExec_t gexec = nullptr;
-    std::vector<const void*> cap_ptrs;  // pointers the captured graph was built with
+    uint64_t id = next_exec_id();       // unique per executor (graph nodes record whose calls they hold)
     std::vector<hipEvent_t> events;     // EDB_PROFILE: start and stop event of every launch
     bool profiled = false;
     int device = -1;
@@ -668,9 +673,6 @@ struct edb_exec {
         } else {
             for (hipEvent_t ev : events) (void)hipEventDestroy(ev);
         }
-        if (gexec) (void)hipGraphExecDestroy(gexec);
-        if (graph) (void)hipGraphDestroy(graph);
-        if (cap_stream) (void)hipStreamDestroy(cap_stream);
         if (dmem && dmem_owned) {
             // free in stream order after the upload and the last execution, on a
             // stream of its own so that later uploads do not queue behind this
@@ -1426,54 +1428,81 @@ BatchArgs resolve_args(const edb_exec* e, const Launch& L, const void* const* w,
     return a;
 }
 
-hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* arena_h, void* arena_c,
-                      hipStream_t st) {
-    const int esz = e->dtype == EDB_F32 ? 4 : 2;
+// One kernel call of an execution: the kernel, its launch shape and its
+// arguments by value.  The same list is issued eagerly or written into the
+// nodes of a HIP graph, so both ways run the same calls.
+struct Call {
+    const void* fn = nullptr;
+    unsigned grid = 0, block = 256;
+    size_t lds = 0;               // dynamic LDS bytes
+    int launch = 0;               // its launch record (EDB_PROFILE events)
+    int form = 0;                 // 0 (BatchArgs), 1 (BatchArgs, bf16*, float*), 2 (BatchArgs, T*), 3 staging, 4 dataflow
+    BatchArgs a{};
+    void* p0 = nullptr;
+    void* p1 = nullptr;
+    FlowArgs f{};
+    struct Stage {                // stage_kernel's parameters, in order
+        const void* x;
+        void* xs;
+        const int* src;
+        int n_x, E;
+        const int* zrow;
+        int n_zero;
+        void* arena_h;
+        float* arena_c;
+        int H;
+        int* ints;
+        int nint;
+    } s{};
+    void* argv[12];
+    // pointers to the arguments (into this object: call after it has its final address)
+    void** args() {
+        switch (form) {
+            case 0: argv[0] = &a; break;
+            case 1: argv[0] = &a; argv[1] = &p0; argv[2] = &p1; break;
+            case 2: argv[0] = &a; argv[1] = &p0; break;
+            case 3:
+                argv[0] = &s.x; argv[1] = &s.xs; argv[2] = &s.src; argv[3] = &s.n_x; argv[4] = &s.E;
+                argv[5] = &s.zrow; argv[6] = &s.n_zero; argv[7] = &s.arena_h; argv[8] = &s.arena_c;
+                argv[9] = &s.H; argv[10] = &s.ints; argv[11] = &s.nint;
+                break;
+            default: argv[0] = &f; break;
+        }
+        return argv;
+    }
+};
+
+// The calls of one execution, in launch order (records with grid 0 are not issued).
+void build_calls(const edb_exec* e, const void* const* w, const void* x, void* arena_h, void* arena_c,
+                 std::vector<Call>& out) {
+    out.clear();
+    out.reserve(e->launches.size());
     const int* db = e->dbuf;
-    const bool prof = !e->events.empty();
-    hipEvent_t* ev = prof ? e->events.data() : nullptr;
+    const bool f32 = e->dtype == EDB_F32;
     // launch 0: stage x rows, clear the zero / pad rows and the dataflow counters
-    int* cnt = e->dbuf + e->off_counters;
-    const int ncnt = (int)e->n_counters;
     {
         const Launch& L = e->launches[0];
         const bool direct = (e->flags & EDB_X_DIRECT) != 0 || e->x_in_place;
-        const int nx = direct ? 0 : e->n_x;
         if (L.info.grid > 0) {
-            if (e->dtype == EDB_F32) {
-                auto* k = stage_kernel<float>;
-                const float* xs = reinterpret_cast<const float*>(x);
-                float* xd = reinterpret_cast<float*>(e->xstaged);
-                float* ah = reinterpret_cast<float*>(arena_h);
-                float* ac = reinterpret_cast<float*>(arena_c);
-                if (prof)
-                    hipExtLaunchKernelGGL(k, dim3(L.info.grid), dim3(256), 0, st, ev[0], ev[1], 0, xs, xd,
-                                          db + e->off_xsrc, nx, e->E, db + e->off_zero, e->n_zero, ah, ac, e->H,
-                                          cnt, ncnt);
-                else
-                    hipLaunchKernelGGL(k, dim3(L.info.grid), dim3(256), 0, st, xs, xd, db + e->off_xsrc, nx, e->E,
-                                       db + e->off_zero, e->n_zero, ah, ac, e->H, cnt, ncnt);
-            } else {
-                auto* k = stage_kernel<__bf16>;
-                const __bf16* xs = reinterpret_cast<const __bf16*>(x);
-                __bf16* xd = reinterpret_cast<__bf16*>(e->xstaged);
-                __bf16* ah = reinterpret_cast<__bf16*>(arena_h);
-                float* ac = reinterpret_cast<float*>(arena_c);
-                if (prof)
-                    hipExtLaunchKernelGGL(k, dim3(L.info.grid), dim3(256), 0, st, ev[0], ev[1], 0, xs, xd,
-                                          db + e->off_xsrc, nx, e->E, db + e->off_zero, e->n_zero, ah, ac, e->H,
-                                          cnt, ncnt);
-                else
-                    hipLaunchKernelGGL(k, dim3(L.info.grid), dim3(256), 0, st, xs, xd, db + e->off_xsrc, nx, e->E,
-                                       db + e->off_zero, e->n_zero, ah, ac, e->H, cnt, ncnt);
-            }
+            Call c;
+            c.fn = f32 ? reinterpret_cast<const void*>(&stage_kernel<float>)
+                       : reinterpret_cast<const void*>(&stage_kernel<__bf16>);
+            c.grid = L.info.grid;
+            c.form = 3;
+            c.s = Call::Stage{x, e->xstaged, db + e->off_xsrc, direct ? 0 : e->n_x, e->E, db + e->off_zero,
+                              e->n_zero, arena_h, reinterpret_cast<float*>(arena_c), e->H,
+                              e->dbuf + e->off_counters, (int)e->n_counters};
+            out.push_back(c);
         }
     }
-    (void)esz;
     for (size_t i = 1; i < e->launches.size(); ++i) {
         const Launch& L = e->launches[i];
+        if (L.info.grid <= 0) continue;
+        Call c;
+        c.launch = (int)i;
+        c.grid = L.info.grid;
         if (L.flow) {
-            FlowArgs f{};
+            FlowArgs& f = c.f;
             f.ibuf = db;
             f.desc = reinterpret_cast<const BatchDesc*>(db + L.f_desc);
             f.tiles = reinterpret_cast<const int4*>(db + L.f_tiles);
@@ -1492,36 +1521,30 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
             f.arena_h = arena_h;
             f.arena_c = reinterpret_cast<float*>(arena_c);
             for (int t = 0; t < e->T && t < FLOW_MAX_TYPES; ++t) f.w[t] = w[t];
-            hipEvent_t e0 = prof ? ev[2 * i] : nullptr, e1 = prof ? ev[2 * i + 1] : nullptr;
-            if (e->dtype == EDB_F32) {
-                if (prof) hipExtLaunchKernelGGL(flow_kernel<float>, dim3(L.info.grid), dim3(256), L.lds, st, e0, e1, 0, f);
-                else hipLaunchKernelGGL(flow_kernel<float>, dim3(L.info.grid), dim3(256), L.lds, st, f);
-            } else {
-                if (prof) hipExtLaunchKernelGGL(flow_kernel<__bf16>, dim3(L.info.grid), dim3(256), L.lds, st, e0, e1, 0, f);
-                else hipLaunchKernelGGL(flow_kernel<__bf16>, dim3(L.info.grid), dim3(256), L.lds, st, f);
-            }
+            c.fn = f32 ? reinterpret_cast<const void*>(&flow_kernel<float>)
+                       : reinterpret_cast<const void*>(&flow_kernel<__bf16>);
+            c.lds = L.lds;
+            c.form = 4;
+            out.push_back(c);
             continue;
         }
-        BatchArgs a = resolve_args(e, L, w, x, arena_h, arena_c);
-        hipEvent_t e0 = prof ? ev[2 * i] : nullptr, e1 = prof ? ev[2 * i + 1] : nullptr;
-        if (L.kk == -2) {   // MV-RNN vector batch: [B a, A b] into the mvu scratch
-            const dim3 grid(L.info.grid), blk(256);
-            {   // fp32 only (cell_dims)
-                float* out = reinterpret_cast<float*>(e->mvu);
-                if (prof) hipExtLaunchKernelGGL(mv_matvec_kernel<float>, grid, blk, 0, st, e0, e1, 0, a, out);
-                else hipLaunchKernelGGL(mv_matvec_kernel<float>, grid, blk, 0, st, a, out);
-            }
+        c.a = resolve_args(e, L, w, x, arena_h, arena_c);
+        if (L.kk == -2) {   // MV-RNN vector batch: [B a, A b] into the mvu scratch (fp32 only)
+            c.fn = reinterpret_cast<const void*>(&mv_matvec_kernel<float>);
+            c.form = 2;
+            c.p0 = e->mvu;
+            out.push_back(c);
             continue;
         }
         if (L.kk < 0) {   // child-sum batch on the large tile: child sums and product sums
-            __bf16* out = reinterpret_cast<__bf16*>(e->hsum);
-            if (prof)
-                hipExtLaunchKernelGGL(child_reduce_kernel, dim3(L.info.grid), dim3(256), 0, st, e0, e1, 0, a, out,
-                                      e->racc);
-            else
-                hipLaunchKernelGGL(child_reduce_kernel, dim3(L.info.grid), dim3(256), 0, st, a, out, e->racc);
+            c.fn = reinterpret_cast<const void*>(&child_reduce_kernel);
+            c.form = 1;
+            c.p0 = e->hsum;
+            c.p1 = e->racc;
+            out.push_back(c);
             continue;
         }
+        BatchArgs& a = c.a;
         if (L.kk == K_CS_FORGET) {   // rows: the children's h; weights U_f, b_f
             a.W = a.Wr;
             a.bias = a.br;
@@ -1535,9 +1558,143 @@ hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* ar
             a.n_xrows = a.m;
             a.fc = e->racc;
         }
-        table().e[L.kk][e->dtype][L.info.variant].launch(a, L.info.grid, L.lds, st, e0, e1);
+        c.fn = table().e[L.kk][e->dtype][L.info.variant].fn;
+        c.block = L.info.block;
+        c.lds = is_large(L.info.variant) ? 0 : L.lds;   // the large tile's LDS is static
+        out.push_back(c);
+    }
+}
+
+hipError_t launch_all(edb_exec* e, const void* const* w, const void* x, void* arena_h, void* arena_c,
+                      hipStream_t st) {
+    thread_local std::vector<Call> calls;
+    build_calls(e, w, x, arena_h, arena_c, calls);
+    const bool prof = !e->events.empty();
+    hipError_t he = hipSuccess;
+    for (Call& c : calls) {
+        if (prof)
+            he = hipExtLaunchKernel(c.fn, dim3(c.grid), dim3(c.block), c.args(), c.lds, st, e->events[2 * c.launch],
+                                    e->events[2 * c.launch + 1], 0);
+        else
+            he = hipLaunchKernel(c.fn, dim3(c.grid), dim3(c.block), c.args(), c.lds, st);
+        if (he != hipSuccess) return he;
     }
     return hipGetLastError();
+}
+
+// Instantiated graphs of kernel-call sequences, kept per device and stream
+// and reused by every later execution there whose sequence has the same
+// kernels and block sizes: a new input graph updates the nodes' arguments,
+// grids and LDS in place and is not instantiated again.  Up to kTopoPerStream
+// sequences per stream; the least recently used one is replaced.  Kept for
+// the life of the process.
+constexpr int kTopoPerStream = 4;
+struct Topo {
+    std::vector<std::pair<const void*, unsigned>> sig;   // kernel and block size of each node
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    std::vector<hipGraphNode_t> nodes;
+    hipEvent_t done = nullptr;     // after its last launch
+    uint64_t used = 0;
+    uint64_t owner = 0;            // executor (id) and pointers the nodes hold now
+    std::vector<const void*> owner_ptrs;
+};
+struct TopoSet {
+    std::mutex mu;
+    std::vector<Topo> t;
+    uint64_t tick = 0;
+};
+std::mutex g_topo_mu;
+std::map<std::pair<int, hipStream_t>, TopoSet*> g_topo;
+std::atomic<int64_t> g_topo_instantiated{0}, g_topo_updated{0};
+
+hipKernelNodeParams node_params(Call& c) {
+    hipKernelNodeParams p{};
+    p.func = const_cast<void*>(c.fn);
+    p.gridDim = dim3(c.grid);
+    p.blockDim = dim3(c.block);
+    p.sharedMemBytes = (unsigned)c.lds;
+    p.kernelParams = c.args();
+    p.extra = nullptr;
+    return p;
+}
+
+// Runs the execution's calls on st through the stream's graph of the same
+// kernel sequence (instantiated on first use).
+hipError_t graph_launch(edb_exec* e, const void* const* w, const void* x, void* arena_h, void* arena_c,
+                        hipStream_t st) {
+    int dev = 0;
+    hipError_t he = hipGetDevice(&dev);
+    if (he != hipSuccess) return he;
+    TopoSet* ts = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_topo_mu);
+        TopoSet*& slot = g_topo[{dev, st}];
+        if (!slot) slot = new TopoSet;
+        ts = slot;
+    }
+    std::vector<const void*> ptrs(w, w + e->T);
+    ptrs.push_back(x);
+    ptrs.push_back(arena_h);
+    ptrs.push_back(arena_c);
+    ptrs.push_back(e->dbuf);
+    thread_local std::vector<Call> calls;
+    build_calls(e, w, x, arena_h, arena_c, calls);
+    std::vector<std::pair<const void*, unsigned>> sig;
+    sig.reserve(calls.size());
+    for (const Call& c : calls) sig.emplace_back(c.fn, c.block);
+    std::lock_guard<std::mutex> lk(ts->mu);
+    Topo* t = nullptr;
+    for (Topo& q : ts->t)
+        if (q.sig == sig) { t = &q; break; }
+    if (t) {
+        // the same executor with the same buffers: the nodes already hold its calls
+        if (t->owner != e->id || t->owner_ptrs != ptrs) {
+            for (size_t i = 0; he == hipSuccess && i < calls.size(); ++i) {
+                const hipKernelNodeParams np = node_params(calls[i]);
+                he = hipGraphExecKernelNodeSetParams(t->exec, t->nodes[i], &np);
+            }
+            if (he != hipSuccess) return he;
+            ++g_topo_updated;
+        }
+    } else {
+        if ((int)ts->t.size() >= kTopoPerStream) {
+            // replace the least recently used sequence once its last launch has run
+            size_t lru = 0;
+            for (size_t i = 1; i < ts->t.size(); ++i)
+                if (ts->t[i].used < ts->t[lru].used) lru = i;
+            Topo& old = ts->t[lru];
+            if (old.done) (void)hipEventSynchronize(old.done);
+            if (old.exec) (void)hipGraphExecDestroy(old.exec);
+            if (old.graph) (void)hipGraphDestroy(old.graph);
+            if (old.done) (void)hipEventDestroy(old.done);
+            ts->t.erase(ts->t.begin() + lru);
+        }
+        Topo n;
+        n.sig = sig;
+        he = hipGraphCreate(&n.graph, 0);
+        n.nodes.resize(calls.size());
+        for (size_t i = 0; he == hipSuccess && i < calls.size(); ++i) {
+            const hipKernelNodeParams np = node_params(calls[i]);
+            he = hipGraphAddKernelNode(&n.nodes[i], n.graph, i ? &n.nodes[i - 1] : nullptr, i ? 1 : 0, &np);
+        }
+        if (he == hipSuccess) he = hipGraphInstantiate(&n.exec, n.graph, nullptr, nullptr, 0);
+        if (he == hipSuccess) he = hipEventCreateWithFlags(&n.done, hipEventDisableTiming);
+        if (he != hipSuccess) {
+            if (n.exec) (void)hipGraphExecDestroy(n.exec);
+            if (n.graph) (void)hipGraphDestroy(n.graph);
+            return he;
+        }
+        ++g_topo_instantiated;
+        ts->t.push_back(std::move(n));
+        t = &ts->t.back();
+    }
+    t->owner = e->id;
+    t->owner_ptrs = ptrs;
+    t->used = ++ts->tick;
+    he = hipGraphLaunch(t->exec, st);
+    if (he == hipSuccess) he = hipEventRecord(t->done, st);
+    return he;
 }
 
 }  // namespace
@@ -1579,38 +1736,17 @@ extern "C" edb_status edb_execute(edb_exec_t* e, const void* const* w, const voi
         e->profiled = !e->events.empty();
         return EDB_OK;
     }
-    std::vector<const void*> ptrs(w, w + e->T);
-    ptrs.push_back(x);
-    ptrs.push_back(arena_h);
-    ptrs.push_back(arena_c);
-    if (!e->gexec || ptrs != e->cap_ptrs) {
-        if (e->gexec) { (void)hipGraphExecDestroy(e->gexec); e->gexec = nullptr; }
-        if (e->graph) { (void)hipGraphDestroy(e->graph); e->graph = nullptr; }
-        if (!e->cap_stream) {
-            he = hipStreamCreateWithFlags(&e->cap_stream, hipStreamNonBlocking);
-            if (he != hipSuccess) {
-                e->cap_stream = nullptr;
-                return fail(EDB_ERR_HIP, std::string("edb_execute: ") + hipGetErrorString(he));
-            }
-        }
-        he = hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal);
-        if (he == hipSuccess) {
-            hipError_t le = launch_all(e, w, x, arena_h, arena_c, e->cap_stream);
-            he = hipStreamEndCapture(e->cap_stream, &e->graph);
-            if (le != hipSuccess) he = le;
-        }
-        if (he == hipSuccess) he = hipGraphInstantiate(&e->gexec, e->graph, nullptr, nullptr, 0);
-        if (he != hipSuccess) {
-            if (e->graph) { (void)hipGraphDestroy(e->graph); e->graph = nullptr; }
-            e->gexec = nullptr;
-            return fail(EDB_ERR_HIP, std::string("edb_execute: graph capture: ") + hipGetErrorString(he));
-        }
-        e->cap_ptrs = ptrs;
-    }
-    he = hipGraphLaunch(e->gexec, st);
+    he = graph_launch(e, w, x, arena_h, arena_c, st);
     if (he == hipSuccess) he = hipEventRecord(e->done, st);
-    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_execute: ") + hipGetErrorString(he));
+    if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_execute: graph: ") + hipGetErrorString(he));
     e->ran = true;
+    return EDB_OK;
+}
+
+extern "C" edb_status edb_graph_stats(int64_t* instantiated, int64_t* updated) {
+    if (!instantiated || !updated) return fail(EDB_ERR_INVALID, "edb_graph_stats: NULL argument");
+    *instantiated = g_topo_instantiated.load();
+    *updated = g_topo_updated.load();
     return EDB_OK;
 }
 
@@ -1901,7 +2037,7 @@ size_t with_spare(size_t v, size_t align) { return std::max(align, (v + v / 4 + 
 
 edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s, const edb_plan_t* p,
                                   const edb_cell* cells, int32_t flags, const void* const* packed_weights,
-                                  const void* x, void* arena_h, void* arena_c, void* stream) {
+                                  const void* x, void* arena_h, void* arena_c, void* stream, bool use_graph) {
     int dev = 0;
     DeviceCtx* ctx = nullptr;
     hipError_t he = hipGetDevice(&dev);
@@ -2022,7 +2158,8 @@ edb_status edb::forward_on_stream(const edb_graph_t* g, const edb_schedule_t* s,
             e->dbuf = reinterpret_cast<int*>(sl.dev);
             e->dmem = nullptr;
             e->dmem_owned = false;
-            he = launch_all(e, packed_weights, x, arena_h, arena_c, hs);
+            he = use_graph ? graph_launch(e, packed_weights, x, arena_h, arena_c, hs)
+                           : launch_all(e, packed_weights, x, arena_h, arena_c, hs);
         }
         if (he == hipSuccess) he = hipEventRecord(sl.done, hs);
         if (he == hipSuccess) {

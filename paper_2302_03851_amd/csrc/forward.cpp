@@ -34,11 +34,12 @@ extern "C" edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_
             st = edb::fail(EDB_ERR_INVALID, "edb_forward: the arena has " + std::to_string(arena_rows) +
                                                 " rows, the plan needs " + std::to_string(p->n_slots));
     }
+    const bool use_graph = (exec_flags & EDB_USE_GRAPH) != 0;
     const int32_t flags = exec_flags & ~EDB_USE_GRAPH;
     if (st == EDB_OK && !exec_out && !(flags & EDB_PROFILE)) {
         // the plain path: the stream's cached device block, no per-call
         // allocation, upload stream, events or stream-ordered free
-        st = edb::forward_on_stream(g, s, p, cells, flags, packed_weights, x, arena_h, arena_c, stream);
+        st = edb::forward_on_stream(g, s, p, cells, flags, packed_weights, x, arena_h, arena_c, stream, use_graph);
     } else {
         if (st == EDB_OK) st = edb_prepare(g, s, p, cells, flags, &e);
         if (st == EDB_OK) st = edb_execute(e, packed_weights, x, arena_h, arena_c, stream);

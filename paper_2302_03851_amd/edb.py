@@ -376,6 +376,14 @@ class ExecRecord:
             self.handle = None
 
 
+def graph_stats() -> Tuple[int, int]:
+    """edb_graph_stats: (kernel sequences instantiated as new HIP graphs,
+    executions that updated a kept graph in place) in this process."""
+    a, b = C.c_int64(), C.c_int64()
+    L.check(L.load().edb_graph_stats(C.byref(a), C.byref(b)), "edb_graph_stats")
+    return int(a.value), int(b.value)
+
+
 def operand_shapes(w) -> List[Tuple[int, int, int]]:
     return [(nf, rg, int(KIND_SHAPE[k][2])) for (nf, rg), k in zip(w.shapes(), w.kinds)]
 

@@ -279,6 +279,24 @@ CONFIG_NAMES = {
 }
 
 
+def relabel(w: Workload, seed: int) -> Tuple[Workload, np.ndarray]:
+    """The same mini-batch with its node ids permuted: node v becomes
+    perm[v] (children keep their positions, x rows and weights are shared).
+    A different input graph whose schedule has the same batch sizes."""
+    rng = np.random.default_rng(seed)
+    V = w.n_nodes
+    perm = rng.permutation(V)
+    inv = np.argsort(perm)
+    kids = [w.children(int(v)) for v in inv]
+    ptr = np.zeros(V + 1, dtype=np.int64)
+    ptr[1:] = np.cumsum([len(c) for c in kids])
+    idx = (np.concatenate([np.where(c >= 0, perm[np.maximum(c, 0)], -1) for c in kids]).astype(np.int32)
+           if V else np.zeros(0, dtype=np.int32))
+    w2 = dataclasses.replace(w, op_type=np.ascontiguousarray(w.op_type[inv], dtype=np.int32), child_ptr=ptr,
+                             child_idx=idx, x_row=np.ascontiguousarray(w.x_row[inv], dtype=np.int32))
+    return w2, perm
+
+
 def make_config(k: int, seed: Optional[int] = None, instances: Optional[int] = None) -> Workload:
     """Build synthetic config k (1..5; 6 is the two-internal-type TreeLSTM of
     the batching study, 7 the binary TreeGRU, 8 the MV-RNN, 9 the lattice GRU).  `instances` overrides the number of

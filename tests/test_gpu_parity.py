@@ -488,6 +488,104 @@ def test_graph_replays_match_eager():
         np.testing.assert_array_equal(c, ce, err_msg=f"replay {i}")
 
 
+def _kernel_sequence(f):
+    out = []
+    for i in range(f.exec.launches()):
+        inf = f.exec.launch_info(i)
+        if inf["grid"] > 0:
+            out.append((inf["kind"], inf["variant"], inf["part"], inf["block"]))
+    return out
+
+
+@pytest.mark.parametrize("k", [2, 5])
+def test_graph_kept_per_stream_reused_by_new_inputs(k):
+    """EDB_USE_GRAPH executions share the stream's kept graphs: a new input
+    graph (the mini-batch relabelled) with the same kernel sequence updates
+    the kept graph's nodes instead of instantiating one, so does the first
+    input again, and another workload's sequence gets a graph of its own
+    without displacing the first.  Every arena is bitwise the eager one."""
+    _torch()
+    from paper_2302_03851_amd import edb
+    w = WL.make_config(k, instances=SMALL[k])
+    w2, perm = WL.relabel(w, 11)
+    eager = _fwd(w, flags=0)
+    eager.run()
+    he, ce = eager.states()
+    f1 = _fwd(w)
+    f1.run()
+    h1, c1 = f1.states()
+    np.testing.assert_array_equal(h1, he)
+    np.testing.assert_array_equal(c1, ce)
+    i0, u0 = edb.graph_stats()
+    f2 = _fwd(w2)
+    same = _kernel_sequence(f2) == _kernel_sequence(f1)
+    f2.run()
+    h2, c2 = f2.states()
+    np.testing.assert_array_equal(h2[perm], he)
+    np.testing.assert_array_equal(c2[perm], ce)
+    i1, u1 = edb.graph_stats()
+    assert same, "a relabelled mini-batch should select the same kernels"
+    assert (i1, u1) == (i0, u0 + 1), (i0, u0, i1, u1)
+    f1.arena_h.fill_(3.0)
+    f1.run()
+    h1b, c1b = f1.states()
+    np.testing.assert_array_equal(h1b, he)
+    np.testing.assert_array_equal(c1b, ce)
+    i2, u2 = edb.graph_stats()
+    assert (i2, u2) == (i1, u1 + 1), (i1, u1, i2, u2)
+    # another workload: its own graph (one instantiation at most), then the first input reuses its graph
+    w3 = WL.make_config(1, instances=SMALL[1])
+    e3 = _fwd(w3, flags=0)
+    e3.run()
+    h3e, c3e = e3.states()
+    f3 = _fwd(w3)
+    f3.run()
+    h3, c3 = f3.states()
+    np.testing.assert_array_equal(h3, h3e)
+    np.testing.assert_array_equal(c3, c3e)
+    i3, _ = edb.graph_stats()
+    assert i3 <= i2 + 1
+    f2.run()
+    h2b, _ = f2.states()
+    np.testing.assert_array_equal(h2b[perm], he)
+    i4, _ = edb.graph_stats()
+    assert i4 == i3
+
+
+def test_forward_call_graph_path_matches_eager():
+    """edb_forward with EDB_USE_GRAPH (the plain path's launches through the
+    stream's kept graph): two different mini-batches of the same kernel
+    sequence in turn, each arena bitwise the eager one."""
+    torch = _torch()
+    from paper_2302_03851_amd import edb
+    w = WL.make_config(2, instances=SMALL[2])
+    w2, perm = WL.relabel(w, 3)
+    ref = _fwd(w, flags=0)
+    ref.run()
+    h0, c0 = ref.states()
+    st = torch.cuda.Stream()
+    fcs = [edb.ForwardCall(v.op_type, v.child_ptr, v.child_idx, v.x_row, v.n_types, edb.operand_shapes(v),
+                           ref.cells, flags=L.USE_GRAPH) for v in (w, w2)]
+    g2 = edb.Graph(w2.op_type, w2.child_ptr, w2.child_idx, w2.x_row, w2.n_types)
+    plans = [ref.plan, edb.Plan(g2, edb.Schedule(g2), edb.operand_shapes(w2))]
+    for rep in range(3):
+        for j, fc in enumerate(fcs):
+            ah = torch.full((plans[j].n_slots, ref.arena_h.shape[1]), 5.0, dtype=ref.arena_h.dtype, device="cuda")
+            ac = torch.full((plans[j].n_slots, ref.arena_c.shape[1]), 5.0, dtype=torch.float32, device="cuda")
+            torch.cuda.synchronize()
+            fc.call([b.data_ptr() for b in ref.weights], ref.x.data_ptr(), ah.data_ptr(), ac.data_ptr(),
+                    ah.shape[0], st.cuda_stream)
+            st.synchronize()
+            s = plans[j].slot
+            h = ah.float().cpu().numpy()[s]
+            c = ac.cpu().numpy()[s]
+            if j == 1:
+                h, c = h[perm], c[perm]
+            np.testing.assert_array_equal(h, h0, err_msg=f"rep {rep} batch {j}")
+            np.testing.assert_array_equal(c, c0, err_msg=f"rep {rep} batch {j}")
+    edb.ForwardCall.release_stream(st.cuda_stream)
+
+
 @pytest.mark.parametrize("k", [2, 5])
 def test_forward_call_matches_handles(k):
     """edb_forward (the whole path in one call) writes bitwise the same arena

@@ -468,6 +468,36 @@ def test_forward_call_rejects_cycles_before_any_device_work(policy):
     assert ei.value.status == L.EDB_ERR_INVALID and "arena" in str(ei.value)
 
 
+
+@pytest.mark.parametrize("k", [2, 5])
+def test_relabelled_mini_batch_has_the_same_launch_sequence(k):
+    """workloads.relabel permutes node ids only: the oracle's states move with
+    the permutation, and the executor's launch sequence (kernel kind, variant,
+    part, block) is unchanged, so an EDB_USE_GRAPH execution of the relabelled
+    mini-batch can reuse a kept graph."""
+    from oracle.evaluate import evaluate
+    w = WL.make_config(k, instances=2)
+    w2, perm = WL.relabel(w, 5)
+    assert sorted(perm.tolist()) == list(range(w.n_nodes))
+    ref = evaluate(w.kinds, w.op_type, w.child_ptr, w.child_idx, w.x_row, w.x, w.weights, w.hidden,
+                   n_fixed=w.n_children, dtype=w.dtype)
+    got = evaluate(w2.kinds, w2.op_type, w2.child_ptr, w2.child_idx, w2.x_row, w2.x, w2.weights, w2.hidden,
+                   n_fixed=w2.n_children, dtype=w2.dtype)
+    for a, b in zip(ref, got):
+        np.testing.assert_array_equal(np.asarray(b)[perm], np.asarray(a))
+
+    def seq(v):
+        f = edb.Forward(v, flags=L.DRYRUN)
+        out = []
+        for i in range(f.exec.launches()):
+            inf = f.exec.launch_info(i)
+            if inf["grid"] > 0:
+                out.append((inf["kind"], inf["variant"], inf["part"], inf["block"]))
+        return out
+
+    assert seq(w) == seq(w2)
+
+
 PQ_INSTANCES = {1: 8, 2: 16, 3: 8, 4: 3, 5: 8}
 
 
