@@ -552,6 +552,65 @@ def test_graph_kept_per_stream_reused_by_new_inputs(k):
     assert i4 == i3
 
 
+def test_kept_graphs_replaced_least_recently_used_and_per_stream_threads():
+    """More kernel sequences on one stream than it keeps: the least recently
+    used graph is replaced (after its last launch) and built again when its
+    sequence returns; and four threads, each with a stream of its own, run
+    their executors through their streams' kept graphs at once.  Every arena
+    is bitwise the eager one."""
+    torch = _torch()
+    import threading
+    from paper_2302_03851_amd import edb
+    ks = [1, 2, 3, 4, 6, 7]   # six different kernel sequences
+    ws = {k: WL.make_config(k, instances=SMALL[k]) for k in ks}
+    ref = {}
+    for k in ks:
+        e = _fwd(ws[k], flags=0)
+        e.run()
+        ref[k] = e.states()
+    st = torch.cuda.Stream()
+    with torch.cuda.stream(st):
+        fs = {k: _fwd(ws[k]) for k in ks}
+    i0, _ = edb.graph_stats()
+    for rnd in range(2):
+        for k in ks:
+            with torch.cuda.stream(st):
+                fs[k].arena_h.fill_(9.0)   # on the stream, ordered before the run
+                fs[k].run()
+            h, c = fs[k].states()
+            np.testing.assert_array_equal(h, ref[k][0], err_msg=f"round {rnd} workload {k}")
+            np.testing.assert_array_equal(c, ref[k][1], err_msg=f"round {rnd} workload {k}")
+    i1, _ = edb.graph_stats()
+    assert i1 - i0 >= len(ks) + 2, (i0, i1)   # the second round rebuilds the replaced ones
+    # threads, one stream each, the same workload
+    w = ws[2]
+    streams = [torch.cuda.Stream() for _ in range(4)]
+    fwds = []
+    for sx in streams:
+        with torch.cuda.stream(sx):
+            fwds.append(_fwd(w))
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(j):
+        try:
+            for _ in range(5):
+                fwds[j].run()
+        except Exception as ex:   # reported below
+            errors.append(ex)
+
+    th = [threading.Thread(target=work, args=(j,)) for j in range(4)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    assert not errors, errors
+    for j in range(4):
+        h, c = fwds[j].states()
+        np.testing.assert_array_equal(h, ref[2][0], err_msg=f"thread {j}")
+        np.testing.assert_array_equal(c, ref[2][1], err_msg=f"thread {j}")
+
+
 def test_forward_call_graph_path_matches_eager():
     """edb_forward with EDB_USE_GRAPH (the plain path's launches through the
     stream's kept graph): two different mini-batches of the same kernel
