@@ -1654,7 +1654,10 @@ hipError_t graph_launch(edb_exec* e, const void* const* w, const void* x, void* 
                 const hipKernelNodeParams np = node_params(calls[i]);
                 he = hipGraphExecKernelNodeSetParams(t->exec, t->nodes[i], &np);
             }
-            if (he != hipSuccess) return he;
+            if (he != hipSuccess) {
+                t->owner = 0;   // nodes partly updated: whoever runs next sets them all
+                return he;
+            }
             ++g_topo_updated;
         }
     } else {
