@@ -504,10 +504,11 @@ def vendor_gemm(configs, reps=50):
 
 def study(configs, replays=100):
     """Replay study of each workload (one JSON line per workload): warm and
-    cold replays of the captured batch sequence (median, p10, p90; cold = a
+    cold replays of the batch sequence's HIP graph (median, p10, p90; cold = a
     512 MB write before every replay, twice the last-level cache), the scale
     sweep at 1x, 4x and 16x the instances, and the end-to-end time of a new
-    graph (ingest + schedule + plan + prepare + capture and first replay)."""
+    input graph (ingest + schedule + plan + prepare, then its run through the stream's kept
+    graph of the same kernel sequence and the first replay)."""
     import torch
     from paper_2302_03851_amd import _lib as L
     from paper_2302_03851_amd import edb, workloads as WL
@@ -779,7 +780,7 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     pool.close()
 
-    # device-only rate: the captured HIP graph of the same batch sequence replayed
+    # device-only rate: the HIP graph of the same batch sequence replayed
     for _ in range(10):
         base.run()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
