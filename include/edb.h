@@ -403,8 +403,8 @@ edb_status edb_prepare(const edb_graph_t* g, const edb_schedule_t* s, const edb_
  * (a new input graph of the same shape of schedule): the graph's kernel nodes
  * get the new arguments, grids and LDS sizes in place, without a new
  * instantiation; up to 4 sequences per stream are kept, the least recently
- * used one replaced (after its last launch has run); they live until the
- * process ends.  Kernel faults surface at the caller's next synchronisation.
+ * used one replaced (after its last launch has run); they live until
+ * edb_stream_release on the stream or the end of the process.  Kernel faults surface at the caller's next synchronisation.
  * One edb_exec_t must not run on two streams at once. */
 edb_status edb_execute(edb_exec_t* e, const void* const* packed_weights, const void* x,
                        void* arena_h, void* arena_c, void* stream);
@@ -497,9 +497,11 @@ edb_status edb_forward(int32_t n_nodes, int32_t n_types, const int32_t* op_type,
  * enqueued there; the call waits for the copies of the stream's descriptors
  * to have run); a later edb_forward on the stream allocates a new one.  The
  * pinned host memory of the copies comes from a pool that the library keeps
- * for the life of the process.
- * Call it before destroying a stream that edb_forward used.  No block: a
- * no-op.  Errors: EDB_ERR_HIP. */
+ * for the life of the process.  The HIP graphs kept for the stream
+ * (EDB_USE_GRAPH) are destroyed too, each after its last launch has run.
+ * Call it before destroying a stream that edb_forward or an EDB_USE_GRAPH
+ * execution used, and not while another thread enqueues work on it.  No
+ * block and no graph: a no-op.  Errors: EDB_ERR_HIP. */
 edb_status edb_stream_release(void* stream);
 
 /* For callers that cannot allocate (code under HIP graph capture, tight

@@ -2186,11 +2186,39 @@ extern "C" edb_status edb_stream_release(void* stream) {
     if (he == hipSuccess) he = device_ctx(dev, &ctx);
     if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_stream_release: ") + hipGetErrorString(he));
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    hipError_t ghe = hipSuccess;
+    {
+        // the stream's kept graphs, each after its last launch (the set itself
+        // stays: a graph launch that looked it up before keeps a valid lock)
+        TopoSet* ts = nullptr;
+        {
+            std::lock_guard<std::mutex> lk(g_topo_mu);
+            auto it = g_topo.find({dev, hs});
+            if (it != g_topo.end()) ts = it->second;
+        }
+        if (ts) {
+            std::lock_guard<std::mutex> lk(ts->mu);
+            for (Topo& t : ts->t) {
+                if (t.done) {
+                    const hipError_t we = hipEventSynchronize(t.done);
+                    if (ghe == hipSuccess) ghe = we;
+                    (void)hipEventDestroy(t.done);
+                }
+                if (t.exec) (void)hipGraphExecDestroy(t.exec);
+                if (t.graph) (void)hipGraphDestroy(t.graph);
+            }
+            ts->t.clear();
+        }
+    }
     std::shared_ptr<StreamBlock> blk;
     {
         std::lock_guard<std::mutex> lk(g_blocks_mu);
         auto it = g_blocks.find({dev, hs});
-        if (it == g_blocks.end()) return EDB_OK;
+        if (it == g_blocks.end()) {
+            if (ghe != hipSuccess)
+                return fail(EDB_ERR_HIP, std::string("edb_stream_release: ") + hipGetErrorString(ghe));
+            return EDB_OK;
+        }
         blk = std::move(it->second);
         g_blocks.erase(it);
     }
@@ -2208,6 +2236,7 @@ extern "C" edb_status edb_stream_release(void* stream) {
         if (sl.ready) (void)hipEventDestroy(sl.ready);
         if (sl.done) (void)hipEventDestroy(sl.done);
     }
+    if (he == hipSuccess) he = ghe;
     if (he != hipSuccess) return fail(EDB_ERR_HIP, std::string("edb_stream_release: ") + hipGetErrorString(he));
     return EDB_OK;
 }

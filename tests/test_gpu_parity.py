@@ -555,9 +555,9 @@ def test_graph_kept_per_stream_reused_by_new_inputs(k):
 def test_kept_graphs_replaced_least_recently_used_and_per_stream_threads():
     """More kernel sequences on one stream than it keeps: the least recently
     used graph is replaced (after its last launch) and built again when its
-    sequence returns; and four threads, each with a stream of its own, run
-    their executors through their streams' kept graphs at once.  Every arena
-    is bitwise the eager one."""
+    sequence returns; four threads, each with a stream of its own, run their
+    executors through their streams' kept graphs at once; and releasing a
+    stream drops its graphs.  Every arena is bitwise the eager one."""
     torch = _torch()
     import threading
     from paper_2302_03851_amd import edb
@@ -609,6 +609,17 @@ def test_kept_graphs_replaced_least_recently_used_and_per_stream_threads():
         h, c = fwds[j].states()
         np.testing.assert_array_equal(h, ref[2][0], err_msg=f"thread {j}")
         np.testing.assert_array_equal(c, ref[2][1], err_msg=f"thread {j}")
+    # releasing a stream drops its kept graphs: the next execution there builds its graph again
+    edb.ForwardCall.release_stream(streams[0].cuda_stream)
+    i2, _ = edb.graph_stats()
+    fwds[0].arena_h.fill_(2.0)
+    torch.cuda.synchronize()
+    fwds[0].run()
+    h, c = fwds[0].states()
+    np.testing.assert_array_equal(h, ref[2][0])
+    np.testing.assert_array_equal(c, ref[2][1])
+    i3, _ = edb.graph_stats()
+    assert i3 == i2 + 1, (i2, i3)
 
 
 def test_forward_call_graph_path_matches_eager():
