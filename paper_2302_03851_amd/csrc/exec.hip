@@ -249,19 +249,8 @@ extern "C" edb_status edb_pack_weights(const edb_cell* cell, const float* const*
 
 namespace {
 
-// Launch with optional start/stop events recorded inside the dispatch packet
-// (the kernel's own duration, as a profiler reports it).
-using LaunchFn = void (*)(const BatchArgs&, int grid, int lds, hipStream_t, hipEvent_t, hipEvent_t);
 using AttrFn = hipError_t (*)(int lds);
 
-template <int KIND, typename T, int RT, int WU, int WK>
-void launch_cell(const BatchArgs& a, int grid, int lds, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
-    if (ev0)
-        hipExtLaunchKernelGGL((cell_kernel<KIND, T, RT, WU, WK>), dim3(grid), dim3(64 * WU * WK), lds, st, ev0, ev1,
-                              0, a);
-    else
-        hipLaunchKernelGGL((cell_kernel<KIND, T, RT, WU, WK>), dim3(grid), dim3(64 * WU * WK), lds, st, a);
-}
 template <int KIND, typename T, int RT, int WU, int WK>
 hipError_t attr_cell(int lds) {
     return hipFuncSetAttribute(reinterpret_cast<const void*>(&cell_kernel<KIND, T, RT, WU, WK>),
@@ -270,27 +259,21 @@ hipError_t attr_cell(int lds) {
 template <int KIND, typename T, int RT, int WU, int WK>
 int lds_cell(int K, int Hk) { return lds_bytes<KIND, T, RT, WU, WK>(K, Hk); }
 
+// A kernel variant: its LDS attribute setter, its LDS size and the kernel
+// (null where the variant does not serve the kind).
 struct Entry {
-    LaunchFn launch;
     AttrFn attr;
     int (*lds)(int K, int Hk);   // LDS bytes for reduction length K and ragged row width Hk
-    const void* fn;   // the kernel (occupancy queries)
+    const void* fn;   // the kernel (launches, graph nodes and occupancy queries)
 };
 
 template <int KIND, typename T, int RT, int WU, int WK>
 Entry entry() {
-    return {launch_cell<KIND, T, RT, WU, WK>, attr_cell<KIND, T, RT, WU, WK>, lds_cell<KIND, T, RT, WU, WK>,
+    return {attr_cell<KIND, T, RT, WU, WK>, lds_cell<KIND, T, RT, WU, WK>,
             reinterpret_cast<const void*>(&cell_kernel<KIND, T, RT, WU, WK>)};
 }
 
 // the weight-stationary tile (bf16 leaf kinds): dynamic LDS for the weights
-template <int KIND>
-void launch_ws(const BatchArgs& a, int grid, int lds, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
-    if (ev0)
-        hipExtLaunchKernelGGL((ws_kernel<KIND>), dim3(grid), dim3(WS_NT), lds, st, ev0, ev1, 0, a);
-    else
-        hipLaunchKernelGGL((ws_kernel<KIND>), dim3(grid), dim3(WS_NT), lds, st, a);
-}
 template <int KIND>
 hipError_t attr_ws(int lds) {
     return hipFuncSetAttribute(reinterpret_cast<const void*>(&ws_kernel<KIND>),
@@ -302,18 +285,10 @@ int lds_ws(int K, int) { return ws_lds_bytes(Kind<KIND>::G, K); }
 template <int KIND, typename T>
 Entry ws_entry() {
     if constexpr (ws_kind<KIND>() && sizeof(T) == 2)
-        return {launch_ws<KIND>, attr_ws<KIND>, lds_ws<KIND>, reinterpret_cast<const void*>(&ws_kernel<KIND>)};
-    else return {nullptr, nullptr, nullptr, nullptr};
+        return {attr_ws<KIND>, lds_ws<KIND>, reinterpret_cast<const void*>(&ws_kernel<KIND>)};
+    else return {nullptr, nullptr, nullptr};
 }
 
-// the large tile's LDS is static (its two stages are distinct objects)
-template <int KIND, typename T, int VB>
-void launch_big(const BatchArgs& a, int grid, int, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
-    if (ev0)
-        hipExtLaunchKernelGGL((big_kernel<KIND, T, VB>), dim3(grid), dim3(256), 0, st, ev0, ev1, 0, a);
-    else
-        hipLaunchKernelGGL((big_kernel<KIND, T, VB>), dim3(grid), dim3(256), 0, st, a);
-}
 template <int KIND, int VB>
 hipError_t attr_big(int) { return hipSuccess; }
 template <int KIND, int VB>
@@ -322,18 +297,11 @@ int lds_big(int, int) { return big_lds_bytes<KIND, VB>(); }
 template <int KIND, typename T, int VB>
 Entry big_entry() {
     if constexpr (!Kind<KIND>::RAG && !sums_children<KIND>())
-        return {launch_big<KIND, T, VB>, attr_big<KIND, VB>, lds_big<KIND, VB>,
+        return {attr_big<KIND, VB>, lds_big<KIND, VB>,
                 reinterpret_cast<const void*>(&big_kernel<KIND, T, VB>)};
-    else return {nullptr, nullptr, nullptr, nullptr};
+    else return {nullptr, nullptr, nullptr};
 }
 
-template <int KIND, typename T, int RT, int WK>
-void launch_stream(const BatchArgs& a, int grid, int lds, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
-    if (ev0)
-        hipExtLaunchKernelGGL((stream_kernel<KIND, T, RT, WK>), dim3(grid), dim3(64 * WK), lds, st, ev0, ev1, 0, a);
-    else
-        hipLaunchKernelGGL((stream_kernel<KIND, T, RT, WK>), dim3(grid), dim3(64 * WK), lds, st, a);
-}
 template <int KIND, typename T, int RT, int WK>
 hipError_t attr_stream(int lds) {
     return hipFuncSetAttribute(reinterpret_cast<const void*>(&stream_kernel<KIND, T, RT, WK>),
@@ -345,9 +313,9 @@ int lds_stream(int, int) { return stream_lds_bytes<KIND, T, RT, WK>(); }
 // the streamed tile serves the kinds without a ragged phase
 template <int KIND, typename T, int RT, int WK>
 Entry stream_entry() {
-    if constexpr (Kind<KIND>::RAG || sums_children<KIND>()) return {nullptr, nullptr, nullptr, nullptr};
+    if constexpr (Kind<KIND>::RAG || sums_children<KIND>()) return {nullptr, nullptr, nullptr};
     else
-        return {launch_stream<KIND, T, RT, WK>, attr_stream<KIND, T, RT, WK>, lds_stream<KIND, T, RT, WK>,
+        return {attr_stream<KIND, T, RT, WK>, lds_stream<KIND, T, RT, WK>,
                 reinterpret_cast<const void*>(&stream_kernel<KIND, T, RT, WK>)};
 }
 
@@ -381,7 +349,7 @@ void fill_kind(Entry* e) {
 template <int KIND>
 void fill_internal(Entry (&e)[2][NUM_VARIANTS]) {
     for (int d = 0; d < 2; ++d)
-        for (int v = 0; v < NUM_VARIANTS; ++v) e[d][v] = {nullptr, nullptr, nullptr, nullptr};
+        for (int v = 0; v < NUM_VARIANTS; ++v) e[d][v] = {nullptr, nullptr, nullptr};
     e[1][8] = big_entry<KIND, __bf16, 0>();
     e[1][9] = big_entry<KIND, __bf16, 1>();
     e[1][10] = big_entry<KIND, __bf16, 2>();
@@ -566,7 +534,7 @@ int best_large(int kk, int dtype, int G, int m, int K, int Hu, int n_cu, int max
     est = 1e300;
     for (int vb = 0; vb < NUM_BIG_CLASSES; ++vb) {
         const Entry& en = table().e[kk][dtype][large_variant(vb)];
-        if (!en.launch) continue;
+        if (!en.fn) continue;
         const int lds = en.lds(K, 0);   // the large tile's LDS is static
         if (lds > max_lds) continue;
         const double c = large_cost(G, vb, m, K, Hu, dtype, occ(en, 256, 0, lds), n_cu) + extra_us;
@@ -975,7 +943,7 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
             for (int vi = 0; vi < NUM_VARIANTS && !large_only; ++vi) {
                 if (!is_small(vi) && !(is_stream(vi) && large_fits)) continue;
                 const Entry& en = table().e[kind_id][dtype][vi];
-                if (!en.launch) continue;
+                if (!en.fn) continue;
                 const int lds = en.lds(d.K, d.Hk);
                 if (lds > max_lds) continue;
                 if (d.rag && VAR_WU[vi] * VAR_WK[vi] > 8) continue;   // register budget of 1024 threads
@@ -989,15 +957,15 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
             // a forced streamed variant falls back to its staged counterpart
             // for kinds it does not serve (and buffers beyond 32-bit offsets)
             int fv = force_var;
-            if (is_stream(fv) && !(large_fits && table().e[kind_id][dtype][fv].launch))
+            if (is_stream(fv) && !(large_fits && table().e[kind_id][dtype][fv].fn))
                 fv = STAGED_OF[fv - FIRST_STREAM];
-            if ((is_small(fv) || is_stream(fv)) && table().e[kind_id][dtype][fv].launch &&
+            if ((is_small(fv) || is_stream(fv)) && table().e[kind_id][dtype][fv].fn &&
                 table().e[kind_id][dtype][fv].lds(d.K, d.Hk) <= max_lds)
                 var = fv;
             if (is_large(force_var) && lvar >= 0) {
                 const int fk = cs_large ? K_CS_PARENT : kind_id;
-                if (table().e[fk][dtype][force_var].launch) var = lvar = force_var;
-                if (cs_large && table().e[K_CS_FORGET][dtype][force_var].launch) fvar = force_var;
+                if (table().e[fk][dtype][force_var].fn) var = lvar = force_var;
+                if (cs_large && table().e[K_CS_FORGET][dtype][force_var].fn) fvar = force_var;
             }
             // the weight-stationary tile for the largest x-only batches (bf16):
             // the weights of its 32 units and its row table fit the LDS, the
@@ -1006,7 +974,7 @@ edb_status prepare_impl(const edb_graph_t* g, const edb_schedule_t* s, const edb
             // offsets stay 32-bit
             {
                 const Entry& wen = table().e[kind_id][dtype][WS_VARIANT];
-                const bool ws_ok = wen.launch && !cs_large && large_fits && !(flags & EDB_NO_LARGE) &&
+                const bool ws_ok = wen.fn && !cs_large && large_fits && !(flags & EDB_NO_LARGE) &&
                                    d.K % (32 * WS_D) == 0 && d.K / 32 >= 2 * WS_D &&
                                    d.Hu % WS_TU == 0 && wen.lds(d.K, d.Hk) <= max_lds;
                 if (ws_ok && ((m >= kWsMinRows && force_var < 0) || force_var == WS_VARIANT)) var = WS_VARIANT;
